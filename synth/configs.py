@@ -1,0 +1,146 @@
+"""Workload shapes for the PRISM drafting hot path.
+
+This module is shared by the oracle and the GPU path.  It only describes
+shapes and seeds; it contains none of the drafting arithmetic.
+
+The drafter follows the paper's architecture (Sec. 3.2, Table 2): a frozen
+token embedding E, a frozen LM head, and M processing modules, each a fusion
+FC plus one transformer layer.  A surjection f_map sends draft step k to the
+module that computes it.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+from typing import Optional, Tuple
+
+
+@dataclass(frozen=True)
+class DraftConfig:
+    name: str
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn: int
+    vocab: int
+    n_steps: int                 # K for a chain, D (forward passes) for a tree
+    feat_width: int              # F_t: width of the target feature fed at step 1
+    rope_theta: float
+    dtype: str                   # "f32" or "bf16": weights, embeddings, features, KV
+    batch: int
+    ctx_len: int = 0             # fixed prior context (used when ctx_range is None)
+    ctx_range: Optional[Tuple[int, int]] = None   # ragged prior context, inclusive
+    kv_block_size: int = 16
+    shuffle_blocks: bool = False  # physical KV blocks in seeded random order
+    mode: str = "chain"          # "chain" or "tree"
+    tree_width: int = 0          # w
+    tree_nodes: int = 0          # v (output nodes, root excluded)
+    rms_eps: float = 1e-5
+    seed: int = 0
+    f_map: Optional[Tuple[int, ...]] = None   # 0-based; None = identity
+    n_sets: Optional[int] = None              # M; None = n_steps
+
+    # ---- derived -------------------------------------------------------
+    @property
+    def M(self) -> int:
+        return self.n_sets if self.n_sets is not None else self.n_steps
+
+    @property
+    def fmap(self) -> Tuple[int, ...]:
+        if self.f_map is not None:
+            return tuple(self.f_map)
+        return tuple(range(self.n_steps))
+
+    @property
+    def qkv_dim(self) -> int:
+        return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    def set_feat_width(self, s: int) -> int:
+        """Feature width F_s of parameter set s.
+
+        The set that serves step 1 fuses the target feature (width F_t); sets
+        serving later steps fuse the draft's own previous hidden state
+        (width H).  A set serving both kinds needs F_t == H.
+        """
+        fm = self.fmap
+        first = fm[0] == s
+        later = any(fm[k] == s for k in range(1, len(fm)))
+        if first and later and self.feat_width != self.hidden:
+            raise ValueError("set %d serves step 1 and later steps but F_t != H" % s)
+        if first:
+            return self.feat_width
+        return self.hidden
+
+    @property
+    def n_draft_slots(self) -> int:
+        """KV slots the drafting call appends after the prior context."""
+        if self.mode == "chain":
+            return self.n_steps
+        return 1 + (self.n_steps - 1) * self.tree_width
+
+    @property
+    def max_ctx(self) -> int:
+        return self.ctx_range[1] if self.ctx_range else self.ctx_len
+
+    @property
+    def blocks_per_seq(self) -> int:
+        return -(-(self.max_ctx + self.n_draft_slots) // self.kv_block_size)
+
+    @property
+    def rows(self) -> int:
+        """Largest number of rows one forward step processes."""
+        if self.mode == "chain":
+            return self.batch
+        return self.batch * self.tree_width
+
+    @property
+    def n_candidates(self) -> int:
+        return self.tree_width + (self.n_steps - 1) * self.tree_width ** 2
+
+    def with_(self, **kw) -> "DraftConfig":
+        return replace(self, **kw)
+
+
+# The five workloads.  Shapes follow the Llama-3 8B/70B targets the paper
+# evaluates against (Sec. 4 "Target LLMs"); the tree shape follows the
+# depth/width/verified-node topology of Sec. 4.3.
+TINY_F32 = DraftConfig(
+    name="tiny_f32_chain", hidden=256, n_q_heads=4, n_kv_heads=4, head_dim=64,
+    ffn=688, vocab=4096, n_steps=3, feat_width=256, rope_theta=10000.0,
+    dtype="f32", batch=1, ctx_len=128)
+
+L3_8B_BS1 = DraftConfig(
+    name="llama3_8b_bf16_chain_bs1", hidden=4096, n_q_heads=32, n_kv_heads=8,
+    head_dim=128, ffn=14336, vocab=128256, n_steps=5, feat_width=12288,
+    rope_theta=500000.0, dtype="bf16", batch=1, ctx_len=2048)
+
+L3_8B_BS16 = L3_8B_BS1.with_(
+    name="llama3_8b_bf16_chain_bs16_paged", batch=16, ctx_len=0,
+    ctx_range=(512, 4096), shuffle_blocks=True)
+
+L3_8B_TREE = L3_8B_BS1.with_(
+    name="llama3_8b_bf16_tree_bs4", batch=4, ctx_len=1024, mode="tree",
+    n_steps=6, tree_width=8, tree_nodes=60)
+
+L3_70B_BS32 = DraftConfig(
+    name="llama3_70b_bf16_chain_bs32", hidden=8192, n_q_heads=64, n_kv_heads=8,
+    head_dim=128, ffn=28672, vocab=128256, n_steps=7, feat_width=24576,
+    rope_theta=500000.0, dtype="bf16", batch=32, ctx_len=4096)
+
+CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32)}
+
+# Reduced shapes for element-by-element parity: small enough for the oracle to
+# finish in seconds, large enough to span several tiles of every kernel and to
+# leave ragged tails (vocab not a multiple of the LM-head tile, contexts not a
+# multiple of the KV chunk or block).
+SMALL_BF16_CHAIN = DraftConfig(
+    name="small_bf16_chain", hidden=512, n_q_heads=8, n_kv_heads=2, head_dim=64,
+    ffn=1376, vocab=5008, n_steps=4, feat_width=1536, rope_theta=500000.0,
+    dtype="bf16", batch=3, ctx_len=0, ctx_range=(37, 700), shuffle_blocks=True)
+
+SMALL_BF16_TREE = SMALL_BF16_CHAIN.with_(
+    name="small_bf16_tree", batch=2, ctx_range=(200, 333), mode="tree", n_steps=4,
+    tree_width=4, tree_nodes=20)
+
+SMALL_F32_CHAIN = TINY_F32.with_(name="small_f32_chain_ragged", batch=3, ctx_len=0,
+                                 ctx_range=(1, 300), shuffle_blocks=True)
