@@ -1,0 +1,180 @@
+#!/usr/bin/env python3
+"""Benchmark of the PRISM drafting hot path on one MI355X.
+
+One benchmark step = one prism_draft_chain call: K = 5 greedy draft steps of
+the Llama-3-8B-shaped drafter (hidden 4096, 32/8 heads x 128, SwiGLU 14336,
+vocab 128256, step-1 feature 3 x 4096), batch 1, prior context 2048, bf16,
+every step with its own parameter set.  Weights and inputs are seeded
+synthetic tensors already resident in HBM when timing starts.
+
+Printed (one JSON line): drafted tokens/s, per-draft-step microseconds, the
+roofline of the dominant kernel (the LM-head GEMV with fused top-k, timed
+with HIP events inside the graph replays), and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0   # dense MFMA
+
+WORKLOADS = {
+    "8b_bs1": "llama3_8b_bf16_chain_bs1",
+    "8b_bs16": "llama3_8b_bf16_chain_bs16_paged",
+    "8b_tree": "llama3_8b_bf16_tree_bs4",
+    "70b_bs32": "llama3_70b_bf16_chain_bs32",
+}
+
+
+def lm_head_bytes(cfg, rows):
+    """Algorithmic HBM bytes of one LM-head launch: the [V, H] weight stream,
+    the normalised input rows, and the per-workgroup top-k partials."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    n_wg = (cfg.vocab // 16 + 3) // 4
+    k = max(1, cfg.tree_width)
+    return cfg.vocab * cfg.hidden * es + rows * cfg.hidden * es + rows * n_wg * (2 + 2 * k) * 4
+
+
+def step_weight_bytes(cfg, s):
+    es = 2 if cfg.dtype == "bf16" else 4
+    H, I, d = cfg.hidden, cfg.ffn, cfg.head_dim
+    F = cfg.set_feat_width(s)
+    return es * (H * (H + F) + cfg.qkv_dim * H + H * cfg.n_q_heads * d + 3 * H * I + cfg.vocab * H)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-baseline", type=int, default=1,
+                    help="time the CPU oracle on a bounded sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures the single-GPU drafting path; --gpus %d is not supported "
+              "(the path has no cross-GPU component)." % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from synth import CONFIGS, make_inputs, make_weights
+    from paper_2602_01762_amd import Drafter, binding
+
+    cfg = CONFIGS[WORKLOADS[args.workload]]
+    torch.cuda.set_device(0)
+    print("bench: %s, generating weights" % cfg.name, file=sys.stderr, flush=True)
+    w = make_weights(cfg, "cuda")
+    inp = make_inputs(cfg, "cuda")
+    dr = Drafter(cfg)
+    dr.load(w)
+    torch.cuda.synchronize()
+    tree = cfg.mode == "tree"
+    b = dr.batch(inp)
+    out = dr.tree_buffers(cfg.batch, cfg.n_steps, debug=False) if tree else \
+        dr.chain_buffers(cfg.batch, cfg.n_steps)
+    call = (lambda: dr.tree(inp, out=out, batch=b)) if tree else \
+        (lambda: dr.chain(inp, out=out, batch=b))
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    total_ms = e0.elapsed_time(e1)
+    ms_per_step = total_ms / args.steps
+    K = cfg.n_steps
+    drafted = cfg.batch * K if not tree else cfg.batch * cfg.tree_nodes
+    value = drafted * args.steps / (total_ms / 1e3)
+    assert dr.device_status() == 0
+
+    # dominant kernel: HIP events around every LM-head launch inside the graph
+    binding.prism_profile_enable(dr.ctx, True)
+    call()
+    torch.cuda.synchronize()
+    lm_ms, lm_n = 0.0, 0
+    for _ in range(args.steps):
+        call()
+        ms, n = binding.prism_profile_read(dr.ctx)
+        lm_ms += ms
+        lm_n += n
+    binding.prism_profile_enable(dr.ctx, False)
+    rows = cfg.batch if not tree else cfg.batch * cfg.tree_width
+    lm_us = lm_ms * 1e3 / max(lm_n, 1)
+    lm_b = lm_head_bytes(cfg, rows)
+    achieved = lm_b / (lm_us * 1e-6) / 1e9
+    roofline = {"kernel": "k_lmhead (LM head GEMV + fused top-k partials)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "avg_launch_us": round(lm_us, 2), "launches_timed": lm_n,
+                "algorithmic_bytes_per_launch": lm_b}
+    chain_bytes = sum(step_weight_bytes(cfg, cfg.fmap[k]) for k in range(K))
+    res = {
+        "metric": "drafted tokens/s + per-draft-step µs (8B shape, bs=1/16); % HBM/MFMA peak",
+        "value": round(value, 1), "unit": "drafted tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "data": "synthetic (seeded random-init weights N(0,0.02), features N(0,1), prior KV N(0,1))",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "draft_steps": K,
+                   "prior_context": cfg.max_ctx if cfg.ctx_range is None else list(cfg.ctx_range),
+                   "kv_block": cfg.kv_block_size, "mode": cfg.mode},
+        "per_draft_step_us": round(ms_per_step * 1e3 / K, 2),
+        "weight_bytes_per_step_call": chain_bytes,
+        "whole_call_hbm_frac_weights_only": round(chain_bytes / (ms_per_step * 1e-3) / 1e9
+                                                  / HBM_PEAK_GBS, 4),
+        "wall_s": round(t_wall, 4),
+        "roofline": roofline,
+    }
+    print("bench: gpu done %.3f ms/step" % ms_per_step, file=sys.stderr, flush=True)
+
+    if args.cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(cfg, w, inp, dr)
+    dr.close()
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(cfg, w, inp, dr):
+    """The oracle, as it is, on the host cores: full drafting calls of one
+    sequence of the same workload, repeated until about 10 s have passed."""
+    import numpy as np
+    from oracle import Oracle
+    from oracle import _native
+    from synth import host_inputs, host_weights
+    seqs = [0]
+    hw = host_weights(w)
+    hi = host_inputs(inp, cfg, seqs)
+    orc = Oracle(cfg, hw)
+    _native.lib()
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    n, t0 = 0, time.perf_counter()
+    while True:
+        if cfg.mode == "tree":
+            orc.tree(hi, seqs=seqs)
+        else:
+            orc.chain(hi, seqs=seqs)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= 10.0 or n >= 20:
+            break
+    drafted = n * (cfg.n_steps if cfg.mode == "chain" else cfg.tree_nodes)
+    return {"value": round(drafted / el, 3), "unit": "drafted tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d full %s calls of sequence 0 (%d draft steps each), fp64 with bf16 "
+                      "roundings emulated, %.1f s" % (n, cfg.mode, cfg.n_steps, el)}
+
+
+if __name__ == "__main__":
+    main()

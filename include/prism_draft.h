@@ -1,0 +1,246 @@
+/*
+ * prism_draft.h — C ABI of the PRISM drafting hot path on MI355X (gfx950).
+ *
+ * PRISM (Parametrically Refactoring Inference for Speculative sampling draft
+ * Models) drafts K tokens with a drafter made of a frozen token embedding E,
+ * a frozen LM head, and M processing modules (a fusion FC plus one
+ * transformer layer each).  A surjection f_map sends draft step k to module
+ * f_map(k); the KV cache is shared by every module.  (Paper Sec. 3.2, the
+ * architecture paragraph, Table 2 and "Draft with PRISM".)
+ *
+ * One forward pass of step k, for each of R rows:
+ *   u      = W_fc[s] . [E(x) ; f]          f = target feature (step 1) or the
+ *                                           draft's previous hidden state
+ *   a      = RMSNorm(u; g1[s])
+ *   q,k,v  = W_q,k,v[s] a ; RoPE(q, k; position)    k, v -> KV cache slot
+ *   o      = softmax(q K^T / sqrt(d)) V over the visible slots (GQA)
+ *   r1     = u + W_o[s] o
+ *   h      = r1 + W_down[s] (SiLU(W_gate[s] m) * W_up[s] m),  m = RMSNorm(r1; g2[s])
+ *   logits = LM_head . RMSNorm(h; g_final)            -> top-k / argmax
+ *
+ * Conventions for every call:
+ *   - Pointers named d_* are DEVICE pointers owned by the caller, who keeps
+ *     them alive until the work enqueued on `stream` has completed.  Other
+ *     pointers are host pointers, read before the call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Every call returns a prism_status (0 = OK, < 0 = error) and never
+ *     throws or prints.  Arguments are validated synchronously; the message
+ *     of the last error is available from prism_last_error().  Work is
+ *     enqueued asynchronously on `stream` unless stated otherwise.
+ *   - Matrices are row-major.  "dtype" below is the context's storage type
+ *     (prism_config.dtype): fp32 or bf16 (bit patterns in uint16).
+ *   - Content that only the device sees (token ids, block-table entries,
+ *     context lengths) is bounds-checked by the kernels: an out-of-range
+ *     value skips the access and raises a flag that
+ *     prism_device_status() reports.
+ *   - One context is used by one host thread at a time.  Results are
+ *     bit-identical across repeated calls with the same inputs.
+ */
+#ifndef PRISM_DRAFT_H
+#define PRISM_DRAFT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PRISM_OK = 0,
+  PRISM_ERR_INVALID_ARG = -1,   /* null pointer, value out of range          */
+  PRISM_ERR_SHAPE = -2,         /* shape not supported by the kernels         */
+  PRISM_ERR_NOT_LOADED = -3,    /* weights of a referenced set not loaded     */
+  PRISM_ERR_UNSUPPORTED = -4,   /* f_map asks one set for two feature widths  */
+  PRISM_ERR_OUT_OF_MEMORY = -5, /* device allocation failed                   */
+  PRISM_ERR_HIP = -6,           /* a HIP runtime call failed                  */
+  PRISM_ERR_CAPACITY = -7       /* KV block table / pool too small (device)   */
+} prism_status;
+
+typedef enum { PRISM_F32 = 0, PRISM_BF16 = 1 } prism_dtype;
+
+typedef struct prism_ctx prism_ctx; /* opaque */
+
+/* Model shape and capacity; fixed for the lifetime of a context. */
+typedef struct {
+  int32_t hidden;        /* H                                                */
+  int32_t n_q_heads;     /* query heads                                      */
+  int32_t n_kv_heads;    /* KV heads; n_q_heads % n_kv_heads == 0 (GQA)      */
+  int32_t head_dim;      /* d; even, 32 <= d <= 256, multiple of 8           */
+  int32_t ffn;           /* I, SwiGLU width                                  */
+  int32_t vocab;         /* V                                                */
+  int32_t n_sets;        /* M processing modules                             */
+  int32_t max_steps;     /* largest K (chain) or depth D (tree), <= 63       */
+  int32_t feat_width;    /* F_t, target feature width at step 1              */
+  float rope_theta;      /* RoPE base                                        */
+  float rms_eps;         /* RMSNorm epsilon                                  */
+  int32_t dtype;         /* prism_dtype of weights, E, features and KV       */
+  int32_t kv_block_size; /* slots per KV block                               */
+  int32_t max_batch;     /* sequences per call                               */
+  int32_t max_blocks_per_seq; /* columns of the block table                  */
+  int32_t tree_width;    /* w (0 = no tree calls)                            */
+  int32_t tree_nodes;    /* v output nodes of a tree call, <= 64             */
+} prism_config;
+/* Kernel tiling requires: H, n_q_heads*d, I multiples of 32 (bf16) or 16
+ * (fp32); H + F_t likewise; rows per pass (max_batch, or max_batch*w for
+ * trees) <= 64.  prism_create returns PRISM_ERR_SHAPE otherwise. */
+
+/* Weights of one processing module, as device tensors in the context dtype.
+ * Layouts follow y = W x with W row-major [out, in].  The call copies them
+ * into the context's own step-indexed arena, so they may be freed after
+ * prism_draft_load_params returns. */
+typedef struct {
+  const void *d_w_fc;   /* [H, H + feat_width]  input order [E(x) ; feature] */
+  const void *d_g1;     /* [H]   input RMSNorm gain                          */
+  const void *d_w_q;    /* [n_q_heads*d, H]                                  */
+  const void *d_w_k;    /* [n_kv_heads*d, H]                                 */
+  const void *d_w_v;    /* [n_kv_heads*d, H]                                 */
+  const void *d_w_o;    /* [H, n_q_heads*d]                                  */
+  const void *d_g2;     /* [H]   post-attention RMSNorm gain                 */
+  const void *d_w_gate; /* [I, H]                                            */
+  const void *d_w_up;   /* [I, H]                                            */
+  const void *d_w_down; /* [H, I]                                            */
+  int32_t feat_width;   /* F_s: F_t for a set that serves step 1, else H     */
+} prism_param_set;
+
+/* A batch of sequences and their paged draft KV cache (caller-owned, as in
+ * a serving engine).  Slot t of sequence b lives in physical block
+ * d_block_table[b*max_blocks_per_seq + t/kv_block_size] at offset
+ * t % kv_block_size.  Pools are [n_pool_blocks, n_kv_heads, kv_block_size, d]
+ * in the context dtype; slots 0..L_b-1 hold the prior context (K already
+ * rotated).  Drafting writes slots from L_b on; rejected drafts are
+ * discarded by simply not advancing L_b (paper Sec. 2, speculative
+ * decoding: KV of rejected candidates is dropped). */
+typedef struct {
+  int32_t batch;               /* B <= max_batch                            */
+  const int32_t *d_tokens;     /* [B] last accepted token per sequence      */
+  const void *d_features;      /* [B, feat_width] target hidden state (dtype) */
+  const int32_t *d_ctx_lens;   /* [B] prior context length L_b              */
+  void *d_k_pool;              /* KV pools, see above                       */
+  void *d_v_pool;
+  const int32_t *d_block_table;/* [B, max_blocks_per_seq]                   */
+  int32_t n_pool_blocks;       /* physical blocks in each pool              */
+} prism_batch;
+
+/* One forward pass on R explicit rows (the general entry point). */
+typedef struct {
+  int32_t rows;                /* R, 1..max rows                            */
+  const int32_t *d_tokens;     /* [R] input token of each row               */
+  const void *d_feat;          /* feature rows, width F_s of the step's set */
+  int32_t feat_dtype;          /* prism_dtype of d_feat (fp32 for hidden)   */
+  const int32_t *d_feat_rows;  /* [R] row of d_feat used by row r; NULL = r */
+  const int32_t *d_seq;        /* [R] sequence (index into kv arrays)       */
+  const int32_t *d_pos;        /* [R] RoPE position                         */
+  const int32_t *d_slot;       /* [R] KV slot this row writes               */
+  const uint64_t *d_tree_bits; /* [R] visible draft slots: bit j = slot
+                                  L_seq + j, plus slots 0..L_seq-1.
+                                  NULL = causal: slots 0..slot[r]          */
+  const prism_batch *kv;       /* ctx lens, pools, block table; d_seq values
+                                  must lie in 0..kv->batch-1; tokens and
+                                  features of *kv are not used            */
+  int32_t topk;                /* 1..max(1, tree_width)                     */
+  float *d_hidden_out;         /* [R, H] fp32 hidden state h                */
+  int32_t *d_topk_ids;         /* [R, topk] ids, by (logit desc, id asc)    */
+  float *d_topk_logp;          /* [R, topk] log-softmax values, or NULL     */
+  float *d_logits;             /* [R, V] fp32 logits, or NULL               */
+} prism_step_io;
+
+/* Output of a tree call.  Final arrays are [B, v]; nodes are ordered by
+ * (cumulative log-prob desc, creation order asc); the root is not a node. */
+typedef struct {
+  int32_t *d_tokens;    /* [B, v]                                          */
+  int32_t *d_parent;    /* [B, v] index of the parent node, -1 = the root  */
+  int32_t *d_depth;     /* [B, v] 1..D                                     */
+  float *d_score;       /* [B, v] cumulative log-probability               */
+  uint64_t *d_mask;     /* [B, v] bit j: node j is the node or an ancestor */
+  /* optional (NULL to skip): every candidate and every pass */
+  int32_t *d_cand_tokens; /* [B, C], C = w + (D-1) w^2, creation order     */
+  int32_t *d_cand_parent; /* [B, C] candidate index of the parent, -1 root  */
+  float *d_cand_score;    /* [B, C]                                         */
+  int32_t *d_frontier;    /* [B, D-1, w] candidate index of each expanded node */
+  float *d_logits;        /* [D, B, w, V] logits of each pass (root at r=0) */
+} prism_tree_out;
+
+/* Create a context on the current HIP device: validates the shape and
+ * allocates the workspace.  *out receives the context (NULL on error). */
+prism_status prism_create(const prism_config *cfg, prism_ctx **out);
+
+/* Release every device resource of the context.  NULL is accepted. */
+void prism_destroy(prism_ctx *ctx);
+
+/* Message of the last failed call on ctx (empty if none); valid until the
+ * next call on ctx.  With ctx == NULL: the last prism_create failure. */
+const char *prism_last_error(const prism_ctx *ctx);
+
+/* Load the frozen shared tensors (paper Table 2: E and LM_head are frozen
+ * and shared by every module) and the final RMSNorm gain:
+ * d_embed [V, H], d_lm_head [V, H], d_final_norm [H], all in the context
+ * dtype.  Copies and repacks them; synchronizes `stream` before returning. */
+prism_status prism_draft_load_shared(prism_ctx *ctx, const void *d_embed,
+                                     const void *d_lm_head,
+                                     const void *d_final_norm, void *stream);
+
+/* Load parameter set `set` (0..M-1), the weights of processing module
+ * set+1 (paper Sec. 3.2: M modules, each a fusion FC and a transformer
+ * layer).  Copies and repacks into the step-indexed arena; synchronizes
+ * `stream`.  Allocates that set's arena slot on first use. */
+prism_status prism_draft_load_params(prism_ctx *ctx, int32_t set,
+                                     const prism_param_set *params,
+                                     void *stream);
+
+/* Set the surjection f_map (paper Table 2) from draft steps to sets:
+ * f_map[k-1] is the 0-based set of step k, k = 1..K.  Host array.  Default:
+ * the identity (step k uses set k-1).  A set may serve several steps. */
+prism_status prism_set_step_map(prism_ctx *ctx, const int32_t *f_map,
+                                int32_t K);
+
+/* One forward pass of draft step k (1-based; set f_map(k)) on explicit rows
+ * (paper Sec. 3.2: one pass of the module assigned to step k). */
+prism_status prism_draft_step(prism_ctx *ctx, int32_t k,
+                              const prism_step_io *io, void *stream);
+
+/* Greedy K-step chain (paper Sec. 3.2, "Draft with PRISM"): step 1 fuses
+ * E(token) with the target feature at position L_b; step k >= 2 fuses
+ * E(x_{k-1}) with h_{k-2} at position L_b + k - 1; x_k = argmax (ties to the
+ * lowest id).  Writes KV slots L_b .. L_b+K-1.  Captured once per shape and
+ * buffer set in a HIP graph, then replayed.
+ *   d_out_tokens [B, K] int32 drafted tokens
+ *   d_out_logits [B, K, V] fp32 or NULL
+ *   d_out_hidden [B, K, H] fp32 or NULL */
+prism_status prism_draft_chain(prism_ctx *ctx, const prism_batch *batch,
+                               int32_t K, int32_t *d_out_tokens,
+                               float *d_out_logits, float *d_out_hidden,
+                               void *stream);
+
+/* Dynamic draft tree of `depth` passes and width w (paper Sec. 2, tree
+ * draft-and-verify with a tree attention mask; Sec. 3.2: PRISM works with
+ * tree drafts; Sec. 4.3: depth / width / verified-node topology).  Pass d
+ * (0-based) uses set f_map(d+1) at position L_b + d.  The root pass yields
+ * w depth-1 candidates; each later pass expands the w best nodes of the
+ * previous depth (by cumulative log-prob), attending to the prior context,
+ * the root and its ancestors only, and each expanded node contributes its w
+ * most likely children.  Output: the best v = tree_nodes candidates.  Writes
+ * KV slots L_b .. L_b + (depth-1) w. */
+prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
+                              int32_t depth, const prism_tree_out *out,
+                              void *stream);
+
+/* Synchronize `stream` and report device-side bounds flags raised since
+ * the last call: PRISM_ERR_CAPACITY (block table / pool / slot out of
+ * range), PRISM_ERR_INVALID_ARG (token id out of range), else PRISM_OK.
+ * Clears the flags. */
+prism_status prism_device_status(prism_ctx *ctx, void *stream);
+
+/* Measurement support (not part of the drafting computation).  With
+ * enable != 0, chains and trees captured afterwards record a pair of HIP
+ * events on their stream around every LM-head launch (the largest product
+ * of a step), inside the graph.  prism_profile_read() waits for the events
+ * of the last chain or tree call and returns the summed milliseconds between
+ * each pair and the number of pairs. */
+prism_status prism_profile_enable(prism_ctx *ctx, int32_t enable);
+prism_status prism_profile_read(prism_ctx *ctx, float *total_ms, int32_t *count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRISM_DRAFT_H */

@@ -1,0 +1,116 @@
+// Device helpers for the gfx950 kernels: bf16 conversion, wave64 reductions,
+// MFMA fragments.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <math.h>
+
+#include "internal.h"
+
+namespace prism {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
+
+// round-to-nearest-even fp32 -> bf16 (NaN stays NaN)
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+template <typename T> struct Ty;
+template <> struct Ty<float> {
+  static constexpr int E = 4;    // elements per 16-byte lane fragment
+  static constexpr int KB = 16;  // k per tiled k-block
+  __device__ static float ld(const float *p, size_t i) { return p[i]; }
+  __device__ static void st(float *p, size_t i, float v) { p[i] = v; }
+  // 4 MFMA 16x16x4 fp32 steps; element e of each lane is k-slot (lane>>4) of step e
+  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+  }
+};
+template <> struct Ty<bf16_t> {
+  static constexpr int E = 8;
+  static constexpr int KB = 32;
+  __device__ static float ld(const bf16_t *p, size_t i) { return bf2f(p[i]); }
+  __device__ static void st(bf16_t *p, size_t i, float v) { p[i] = (bf16_t)f2bf(v); }
+  // one MFMA 16x16x32 bf16 step: lane l holds k = 8*(l>>4) .. +7 of row/col (l & 15)
+  __device__ static f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+};
+
+// ---- wave64 reductions (butterfly; every lane ends with the same value,
+// the same operation order on every run) --------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return __shfl(v, 0, 64);
+}
+// larger value wins; equal values: lower id wins
+__device__ __forceinline__ bool better(float v, int id, float ov, int oid) {
+  return v > ov || (v == ov && id < oid);
+}
+__device__ __forceinline__ void wave_argmax(float &v, int &id) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov = __shfl_xor(v, o, 64);
+    int oid = __shfl_xor(id, o, 64);
+    if (better(ov, oid, v, id)) { v = ov; id = oid; }
+  }
+}
+
+// block-wide (256 threads = 4 waves) reductions through LDS, fixed order
+__device__ __forceinline__ float block_sum(float v, float *sh) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  const int nw = blockDim.x >> 6;
+  for (int i = 0; i < nw; ++i) t += sh[i];
+  return t;
+}
+__device__ __forceinline__ float block_max(float v, float *sh) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  float t = -INFINITY;
+  const int nw = blockDim.x >> 6;
+  for (int i = 0; i < nw; ++i) t = fmaxf(t, sh[i]);
+  return t;
+}
+__device__ __forceinline__ void block_argmax(float &v, int &id, float *shv, int *shi) {
+  wave_argmax(v, id);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) { shv[w] = v; shi[w] = id; }
+  __syncthreads();
+  const int nw = blockDim.x >> 6;
+  v = shv[0];
+  id = shi[0];
+  for (int i = 1; i < nw; ++i)
+    if (better(shv[i], shi[i], v, id)) { v = shv[i]; id = shi[i]; }
+}
+
+__device__ __forceinline__ float silu(float y) { return y / (1.0f + expf(-y)); }
+
+}  // namespace prism

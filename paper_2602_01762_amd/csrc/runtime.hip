@@ -1,0 +1,739 @@
+// Host runtime of the drafting library: context, step-indexed weight arena,
+// workspace, the per-pass launch sequence, and HIP-graph capture of the
+// chain and the tree.  Implements include/prism_draft.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "prism_draft.h"
+#include "internal.h"
+
+using namespace prism;
+
+namespace {
+
+struct Set {
+  bool loaded = false;
+  int F = 0;
+  TiledMat fc, qkv, o, gu, down;
+  void *g1 = nullptr, *g2 = nullptr;
+  void *arena = nullptr;
+};
+
+struct Plan {
+  int kw = 1, splits = 1;
+};
+
+struct Pass {            // one forward pass: where its inputs and outputs live
+  int set, R, F, topk;
+  RowsIn in;
+  float *hid_out; int ld_hid;
+  float *logits; long ld_logits;
+  int *ids; float *logp;
+  int *tok_a; int *tok_b; int ld_b;
+};
+
+std::string g_create_error;
+
+}  // namespace
+
+struct prism_ctx {
+  prism_config cfg{};
+  bool bf16 = true;
+  size_t esz = 2;
+  int dev = 0;
+  int H = 0, nq = 0, nkv = 0, d = 0, I = 0, V = 0, QKV = 0;
+  int rows_max = 0, max_slots = 0, nch = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
+  int feat_max = 0;
+
+  void *embed = nullptr, *gf = nullptr, *shared_arena = nullptr;
+  TiledMat lm;
+  bool shared_loaded = false;
+  std::vector<Set> sets;
+  std::vector<int> fmap;
+
+  // workspace
+  void *ws = nullptr;
+  void *X = nullptr, *a = nullptr, *q = nullptr, *o = nullptr, *m = nullptr, *z = nullptr,
+       *nrm = nullptr;
+  float *part = nullptr, *u = nullptr, *r1 = nullptr, *hid[2] = {nullptr, nullptr};
+  float *pm = nullptr, *pl = nullptr, *po = nullptr;
+  float *lm_max = nullptr, *lm_sum = nullptr, *lm_val = nullptr, *logp = nullptr;
+  int *lm_id = nullptr, *ids = nullptr, *tokbuf = nullptr;
+  int32_t *c_seq = nullptr, *c_pos = nullptr, *c_tok0 = nullptr;
+  int32_t *t_ctok = nullptr, *t_cpar = nullptr, *t_front = nullptr;
+  float *t_cscore = nullptr;
+  int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
+  uint64_t *t_bits[2] = {nullptr, nullptr};
+  uint32_t *err = nullptr;
+  double *inv_freq = nullptr;
+
+  hipStream_t cap = nullptr;
+  bool use_graph = true;
+  // measurement: event pairs around LM-head launches
+  bool profile = false;
+  std::vector<hipEvent_t> prof_ev;
+  int prof_used = 0;        // pairs recorded by the enqueue in progress
+  int prof_last = 0;        // pairs of the last chain/tree call
+  std::map<std::vector<uintptr_t>, int> prof_pairs;
+  std::map<std::vector<uintptr_t>, hipGraphExec_t> graphs;
+  std::string msg;
+};
+
+// ------------------------------------------------------------------ helpers
+static prism_status fail(prism_ctx *c, prism_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c) c->msg = buf;
+  else g_create_error = buf;
+  return st;
+}
+
+#define HIPCHK(c, call)                                                                  \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail((c), PRISM_ERR_HIP, "%s failed: %s", #call, hipGetErrorString(e_));    \
+  } while (0)
+
+static TiledMat make_tiled(int N, int K, bool bf16) {
+  TiledMat t;
+  t.N = N;
+  t.K = K;
+  t.n_tiles = N / 16;
+  t.nkb = K / (bf16 ? 32 : 16);
+  return t;
+}
+static size_t tiled_bytes(const TiledMat &t) { return (size_t)t.n_tiles * t.nkb * 1024; }
+
+// K-split plan for a streamed product: enough waves to cover HBM latency,
+// at least 8 k-blocks (8 KiB of W) per wave.
+static Plan plan_for(const TiledMat &t, bool allow_split) {
+  const int target_waves = 4096;
+  int slices = (target_waves + t.n_tiles - 1) / t.n_tiles;
+  const int cap = t.nkb / 8 > 0 ? t.nkb / 8 : 1;
+  if (slices > cap) slices = cap;
+  if (slices < 1) slices = 1;
+  Plan p;
+  p.kw = slices >= 4 ? 4 : (slices >= 2 ? 2 : 1);
+  p.splits = allow_split ? (slices / p.kw > 0 ? slices / p.kw : 1) : 1;
+  return p;
+}
+
+static void carve(char *&p, void **dst, size_t bytes) {
+  *dst = p;
+  p += (bytes + 255) & ~(size_t)255;
+}
+
+// ------------------------------------------------------------------ C ABI
+extern "C" {
+
+const char *prism_last_error(const prism_ctx *ctx) {
+  return ctx ? ctx->msg.c_str() : g_create_error.c_str();
+}
+
+prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
+  if (!out) return fail(nullptr, PRISM_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!cfg) return fail(nullptr, PRISM_ERR_INVALID_ARG, "cfg is NULL");
+  const prism_config &k = *cfg;
+  if (k.dtype != PRISM_F32 && k.dtype != PRISM_BF16)
+    return fail(nullptr, PRISM_ERR_INVALID_ARG, "dtype %d", k.dtype);
+  if (k.hidden <= 0 || k.n_q_heads <= 0 || k.n_kv_heads <= 0 || k.head_dim <= 0 || k.ffn <= 0 ||
+      k.vocab <= 0 || k.n_sets <= 0 || k.max_steps <= 0 || k.feat_width <= 0 ||
+      k.kv_block_size <= 0 || k.max_batch <= 0 || k.max_blocks_per_seq <= 0 || k.tree_width < 0 ||
+      k.tree_nodes < 0 || !(k.rms_eps >= 0.f) || !(k.rope_theta > 0.f))
+    return fail(nullptr, PRISM_ERR_INVALID_ARG, "non-positive size in config");
+  const bool bf16 = k.dtype == PRISM_BF16;
+  const int kq = bf16 ? 32 : 16;
+  if (k.n_q_heads % k.n_kv_heads) return fail(nullptr, PRISM_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
+  if (k.n_q_heads / k.n_kv_heads > 8) return fail(nullptr, PRISM_ERR_SHAPE, "more than 8 query heads per KV head");
+  if (k.head_dim % 8 || k.head_dim < 8 || k.head_dim > 256) return fail(nullptr, PRISM_ERR_SHAPE, "head_dim %d", k.head_dim);
+  if (k.hidden % kq || k.ffn % kq || (k.n_q_heads * k.head_dim) % kq || k.feat_width % kq)
+    return fail(nullptr, PRISM_ERR_SHAPE, "H, I, n_q*d and F_t must be multiples of %d", kq);
+  if (k.vocab % 16) return fail(nullptr, PRISM_ERR_SHAPE, "vocab must be a multiple of 16");
+  if (k.hidden > 16384) return fail(nullptr, PRISM_ERR_SHAPE, "hidden > 16384");
+  if (((k.n_q_heads + 2 * k.n_kv_heads) * k.head_dim + k.head_dim) > 16384)
+    return fail(nullptr, PRISM_ERR_SHAPE, "q/k/v width too large");
+  if (k.max_steps > 63) return fail(nullptr, PRISM_ERR_SHAPE, "max_steps > 63");
+  const int w = k.tree_width;
+  const int rows = k.max_batch * (w > 1 ? w : 1);
+  if (rows > MAX_ROWS) return fail(nullptr, PRISM_ERR_SHAPE, "rows per pass %d > %d", rows, MAX_ROWS);
+  int Cmax = 0;
+  if (w > 0) {
+    if (w > MAX_TOPK) return fail(nullptr, PRISM_ERR_SHAPE, "tree_width > %d", MAX_TOPK);
+    Cmax = w + (k.max_steps - 1) * w * w;
+    if (Cmax > MAX_TREE_CAND) return fail(nullptr, PRISM_ERR_SHAPE, "too many tree candidates");
+    if (1 + (k.max_steps - 1) * w > 64) return fail(nullptr, PRISM_ERR_SHAPE, "tree uses more than 64 draft slots");
+    if (k.tree_nodes < 1 || k.tree_nodes > 64)
+      return fail(nullptr, PRISM_ERR_SHAPE, "tree_nodes must be in 1..64");
+    if (w > k.vocab) return fail(nullptr, PRISM_ERR_SHAPE, "tree_width > vocab");
+  }
+
+  prism_ctx *c = new prism_ctx();
+  c->cfg = k;
+  c->bf16 = bf16;
+  c->esz = bf16 ? 2 : 4;
+  (void)hipGetDevice(&c->dev);
+  c->H = k.hidden; c->nq = k.n_q_heads; c->nkv = k.n_kv_heads; c->d = k.head_dim;
+  c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
+  c->rows_max = rows;
+  c->max_slots = k.max_blocks_per_seq * k.kv_block_size;
+  c->nch = (c->max_slots + 255) / 256;
+  c->kmax = w > 1 ? w : 1;
+  c->Cmax = Cmax;
+  c->feat_max = k.feat_width > k.hidden ? k.feat_width : k.hidden;
+  c->sets.resize(k.n_sets);
+  c->fmap.resize(k.max_steps);
+  for (int i = 0; i < k.max_steps; ++i) c->fmap[i] = i < k.n_sets ? i : k.n_sets - 1;
+  c->lm = make_tiled(c->V, c->H, bf16);
+  c->n_wg_lm = lm_workgroups(c->lm.n_tiles);
+  if (const char *e = getenv("PRISM_NO_GRAPH")) c->use_graph = !(e[0] == '1');
+
+  // split-K partial buffer: the largest splits x N of a streamed product
+  size_t part_n = 0;
+  auto upd = [&](int N, int K) {
+    TiledMat t = make_tiled(N, K, bf16);
+    Plan p = plan_for(t, true);
+    size_t v = (size_t)p.splits * N;
+    if (v > part_n) part_n = v;
+  };
+  upd(c->H, c->H + k.feat_width);
+  upd(c->H, 2 * c->H);
+  upd(c->QKV, c->H);
+  upd(c->H, c->nq * c->d);
+  upd(c->H, c->I);
+
+  const size_t R = rows, es = c->esz;
+  size_t total = 0;
+  std::vector<std::pair<void **, size_t>> L;
+  auto add = [&](void **p, size_t b) { L.push_back({p, b}); total += (b + 255) & ~(size_t)255; };
+  add(&c->X, R * (c->H + c->feat_max) * es);
+  add((void **)&c->part, R * part_n * 4);
+  add((void **)&c->u, R * c->H * 4);
+  add(&c->a, R * c->H * es);
+  add(&c->q, R * c->nq * c->d * es);
+  add((void **)&c->pm, R * c->nq * c->nch * 4);
+  add((void **)&c->pl, R * c->nq * c->nch * 4);
+  add((void **)&c->po, R * c->nq * c->nch * c->d * 4);
+  add(&c->o, R * c->nq * c->d * es);
+  add((void **)&c->r1, R * c->H * 4);
+  add(&c->m, R * c->H * es);
+  add(&c->z, R * c->I * es);
+  add((void **)&c->hid[0], R * c->H * 4);
+  add((void **)&c->hid[1], R * c->H * 4);
+  add(&c->nrm, R * c->H * es);
+  add((void **)&c->lm_max, R * c->n_wg_lm * 4);
+  add((void **)&c->lm_sum, R * c->n_wg_lm * 4);
+  add((void **)&c->lm_val, R * c->n_wg_lm * c->kmax * 4);
+  add((void **)&c->lm_id, R * c->n_wg_lm * c->kmax * 4);
+  add((void **)&c->ids, R * c->kmax * 4);
+  add((void **)&c->logp, R * c->kmax * 4);
+  add((void **)&c->tokbuf, R * 4);
+  add((void **)&c->c_seq, (size_t)k.max_batch * 4);
+  add((void **)&c->c_pos, (size_t)k.max_batch * k.max_steps * 4);
+  add((void **)&c->c_tok0, (size_t)k.max_batch * 4);
+  const size_t tb = (size_t)k.max_batch * (Cmax > 0 ? Cmax : 1);
+  add((void **)&c->t_ctok, tb * 4);
+  add((void **)&c->t_cpar, tb * 4);
+  add((void **)&c->t_cscore, tb * 4);
+  add((void **)&c->t_front, (size_t)k.max_batch * (k.max_steps > 1 ? k.max_steps - 1 : 1) * (w > 0 ? w : 1) * 4);
+  add((void **)&c->t_tok, R * 4);
+  add((void **)&c->t_frow, R * 4);
+  add((void **)&c->t_seq, R * 4);
+  add((void **)&c->t_pos, R * 4);
+  add((void **)&c->t_slot, R * 4);
+  add((void **)&c->t_bits[0], R * 8);
+  add((void **)&c->t_bits[1], R * 8);
+  add((void **)&c->err, 256);
+  add((void **)&c->inv_freq, (size_t)(c->d / 2) * 8);
+
+  if (hipMalloc(&c->ws, total) != hipSuccess) {
+    delete c;
+    return fail(nullptr, PRISM_ERR_OUT_OF_MEMORY, "workspace of %zu bytes", total);
+  }
+  char *p = (char *)c->ws;
+  for (auto &e : L) carve(p, e.first, e.second);
+  (void)hipMemset(c->ws, 0, total);
+  std::vector<double> inv(c->d / 2);
+  for (int i = 0; i < c->d / 2; ++i) inv[i] = std::pow((double)k.rope_theta, -2.0 * i / c->d);
+  (void)hipMemcpy(c->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice);
+  if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) {
+    (void)hipFree(c->ws);
+    delete c;
+    return fail(nullptr, PRISM_ERR_HIP, "stream creation failed");
+  }
+  *out = c;
+  return PRISM_OK;
+}
+
+static void drop_graphs(prism_ctx *c) {
+  for (auto &g : c->graphs) (void)hipGraphExecDestroy(g.second);
+  c->graphs.clear();
+  c->prof_pairs.clear();
+}
+
+void prism_destroy(prism_ctx *c) {
+  if (!c) return;
+  (void)hipDeviceSynchronize();
+  drop_graphs(c);
+  for (auto &s : c->sets)
+    if (s.arena) (void)hipFree(s.arena);
+  if (c->shared_arena) (void)hipFree(c->shared_arena);
+  if (c->ws) (void)hipFree(c->ws);
+  if (c->cap) (void)hipStreamDestroy(c->cap);
+  for (auto e : c->prof_ev) (void)hipEventDestroy(e);
+  delete c;
+}
+
+prism_status prism_draft_load_shared(prism_ctx *c, const void *d_embed, const void *d_lm_head,
+                                     const void *d_final_norm, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!d_embed || !d_lm_head || !d_final_norm)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL shared tensor");
+  hipStream_t s = (hipStream_t)stream;
+  drop_graphs(c);
+  const size_t eb = (size_t)c->V * c->H * c->esz;
+  if (!c->shared_arena) {
+    const size_t bytes = ((eb + 255) & ~(size_t)255) + ((tiled_bytes(c->lm) + 255) & ~(size_t)255) +
+                         (size_t)c->H * c->esz;
+    if (hipMalloc(&c->shared_arena, bytes) != hipSuccess)
+      return fail(c, PRISM_ERR_OUT_OF_MEMORY, "shared arena of %zu bytes", bytes);
+    char *p = (char *)c->shared_arena;
+    carve(p, &c->embed, eb);
+    carve(p, &c->lm.w, tiled_bytes(c->lm));
+    c->gf = p;
+  }
+  HIPCHK(c, hipMemcpyAsync(c->embed, d_embed, eb, hipMemcpyDeviceToDevice, s));
+  launch_repack(c->bf16, d_lm_head, c->V, c->H, 1, 0, c->lm, s);
+  HIPCHK(c, hipGetLastError());
+  HIPCHK(c, hipMemcpyAsync(c->gf, d_final_norm, (size_t)c->H * c->esz, hipMemcpyDeviceToDevice, s));
+  HIPCHK(c, hipStreamSynchronize(s));
+  c->shared_loaded = true;
+  return PRISM_OK;
+}
+
+prism_status prism_draft_load_params(prism_ctx *c, int32_t set, const prism_param_set *P,
+                                     void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!P) return fail(c, PRISM_ERR_INVALID_ARG, "params is NULL");
+  if (set < 0 || set >= c->cfg.n_sets)
+    return fail(c, PRISM_ERR_INVALID_ARG, "set %d out of range 0..%d", set, c->cfg.n_sets - 1);
+  if (!P->d_w_fc || !P->d_g1 || !P->d_w_q || !P->d_w_k || !P->d_w_v || !P->d_w_o || !P->d_g2 ||
+      !P->d_w_gate || !P->d_w_up || !P->d_w_down)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL weight tensor in set %d", set);
+  const int kq = c->bf16 ? 32 : 16;
+  if (P->feat_width <= 0 || P->feat_width % kq)
+    return fail(c, PRISM_ERR_SHAPE, "feat_width %d must be a positive multiple of %d", P->feat_width, kq);
+  if (P->feat_width != c->cfg.feat_width && P->feat_width != c->H)
+    return fail(c, PRISM_ERR_SHAPE, "feat_width %d is neither F_t nor H", P->feat_width);
+  hipStream_t s = (hipStream_t)stream;
+  drop_graphs(c);
+  Set &S = c->sets[set];
+  const int H = c->H, F = P->feat_width;
+  if (S.arena && S.F != F) {
+    (void)hipStreamSynchronize(s);
+    (void)hipFree(S.arena);
+    S.arena = nullptr;
+  }
+  if (!S.arena) {
+    S.fc = make_tiled(H, H + F, c->bf16);
+    S.qkv = make_tiled(c->QKV, H, c->bf16);
+    S.o = make_tiled(H, c->nq * c->d, c->bf16);
+    S.gu = make_tiled(2 * c->I, H, c->bf16);
+    S.down = make_tiled(H, c->I, c->bf16);
+    const size_t gb = (size_t)H * c->esz;
+    const size_t bytes = tiled_bytes(S.fc) + tiled_bytes(S.qkv) + tiled_bytes(S.o) +
+                         tiled_bytes(S.gu) + tiled_bytes(S.down) + 2 * ((gb + 255) & ~(size_t)255) + 6 * 256;
+    if (hipMalloc(&S.arena, bytes) != hipSuccess)
+      return fail(c, PRISM_ERR_OUT_OF_MEMORY, "arena of set %d (%zu bytes)", set, bytes);
+    char *p = (char *)S.arena;
+    carve(p, &S.fc.w, tiled_bytes(S.fc));
+    carve(p, &S.qkv.w, tiled_bytes(S.qkv));
+    carve(p, &S.o.w, tiled_bytes(S.o));
+    carve(p, &S.gu.w, tiled_bytes(S.gu));
+    carve(p, &S.down.w, tiled_bytes(S.down));
+    carve(p, &S.g1, gb);
+    carve(p, &S.g2, gb);
+    S.F = F;
+  }
+  S.loaded = false;
+  launch_repack(c->bf16, P->d_w_fc, H, H + F, 1, 0, S.fc, s);
+  // q, k, v rows stacked into one product
+  TiledMat qv = S.qkv;
+  launch_repack(c->bf16, P->d_w_q, c->nq * c->d, H, 1, 0, qv, s);
+  launch_repack(c->bf16, P->d_w_k, c->nkv * c->d, H, 1, c->nq * c->d, qv, s);
+  launch_repack(c->bf16, P->d_w_v, c->nkv * c->d, H, 1, (c->nq + c->nkv) * c->d, qv, s);
+  launch_repack(c->bf16, P->d_w_o, H, c->nq * c->d, 1, 0, S.o, s);
+  // gate/up interleaved row by row: gate c -> 2c, up c -> 2c + 1
+  launch_repack(c->bf16, P->d_w_gate, c->I, H, 2, 0, S.gu, s);
+  launch_repack(c->bf16, P->d_w_up, c->I, H, 2, 1, S.gu, s);
+  launch_repack(c->bf16, P->d_w_down, H, c->I, 1, 0, S.down, s);
+  HIPCHK(c, hipGetLastError());
+  HIPCHK(c, hipMemcpyAsync(S.g1, P->d_g1, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
+  HIPCHK(c, hipMemcpyAsync(S.g2, P->d_g2, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
+  HIPCHK(c, hipStreamSynchronize(s));
+  S.loaded = true;
+  return PRISM_OK;
+}
+
+prism_status prism_set_step_map(prism_ctx *c, const int32_t *f_map, int32_t K) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!f_map) return fail(c, PRISM_ERR_INVALID_ARG, "f_map is NULL");
+  if (K < 1 || K > c->cfg.max_steps) return fail(c, PRISM_ERR_INVALID_ARG, "K %d out of 1..%d", K, c->cfg.max_steps);
+  for (int i = 0; i < K; ++i)
+    if (f_map[i] < 0 || f_map[i] >= c->cfg.n_sets)
+      return fail(c, PRISM_ERR_INVALID_ARG, "f_map[%d] = %d out of range", i, f_map[i]);
+  drop_graphs(c);
+  c->fmap.assign(f_map, f_map + K);
+  return PRISM_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ passes
+static KvArgs kv_of(const prism_ctx *c, const prism_batch *b) {
+  KvArgs kv;
+  kv.k_pool = b->d_k_pool;
+  kv.v_pool = b->d_v_pool;
+  kv.block_table = b->d_block_table;
+  kv.ctx_lens = b->d_ctx_lens;
+  kv.mbps = c->cfg.max_blocks_per_seq;
+  kv.bs = c->cfg.kv_block_size;
+  kv.n_blocks = b->n_pool_blocks;
+  kv.n_seq = b->batch;
+  return kv;
+}
+
+static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
+  const Set &S = c->sets[p.set];
+  const bool bf = c->bf16;
+  const int R = p.R, H = c->H;
+  const float eps = c->cfg.rms_eps;
+  auto gemm_partial = [&](const TiledMat &m, const void *X, int ldx) {
+    Plan pl = plan_for(m, true);
+    GemmLaunch g{m, X, ldx, R, pl.kw, pl.splits, c->part, nullptr, 0};
+    launch_gemm(bf, EPI_PARTIAL, g, s);
+    return pl.splits;
+  };
+  // fusion FC: u = W_fc [E(x) ; f];  a = RMSNorm(u; g1)
+  launch_fc_prep(bf, R, p.in, c->embed, c->V, H, p.F, c->X, c->err, s);
+  int sp = gemm_partial(S.fc, c->X, H + p.F);
+  launch_rowfin(bf, R, H, c->part, sp, nullptr, 0, c->u, H, S.g1, c->a, eps, s);
+  // q, k, v; RoPE; cache append
+  sp = gemm_partial(S.qkv, c->a, H);
+  launch_qkv_fin(bf, R, c->nq, c->nkv, c->d, c->part, sp, p.in, kv, c->inv_freq, c->q, c->err, s);
+  // attention over the visible slots
+  launch_attention(bf, R, c->nq, c->nkv, c->d, c->q, p.in, kv, c->max_slots, 256, c->pm, c->pl,
+                   c->po, c->o, c->err, s);
+  // r1 = u + W_o o;  m = RMSNorm(r1; g2)
+  sp = gemm_partial(S.o, c->o, c->nq * c->d);
+  launch_rowfin(bf, R, H, c->part, sp, c->u, H, c->r1, H, S.g2, c->m, eps, s);
+  // z = SiLU(W_gate m) * (W_up m)
+  {
+    Plan pl = plan_for(S.gu, false);
+    GemmLaunch g{S.gu, c->m, H, R, pl.kw, 1, nullptr, c->z, c->I};
+    launch_gemm(bf, EPI_SWIGLU, g, s);
+  }
+  // h = r1 + W_down z;  n = RMSNorm(h; g_final)
+  sp = gemm_partial(S.down, c->z, c->I);
+  launch_rowfin(bf, R, H, c->part, sp, c->r1, H, p.hid_out, p.ld_hid, c->gf, c->nrm, eps, s);
+  // LM head + top-k
+  LmLaunch lmg{c->lm, c->nrm, H, R, c->V, p.topk, p.logits, p.ld_logits,
+               c->lm_max, c->lm_sum, c->lm_val, c->lm_id, c->n_wg_lm};
+  const bool prof = c->profile && c->prof_used * 2 + 1 < (int)c->prof_ev.size();
+  const unsigned evf = c->use_graph ? hipEventRecordExternal : hipEventRecordDefault;
+  if (prof) (void)hipEventRecordWithFlags(c->prof_ev[2 * c->prof_used], s, evf);
+  launch_lmhead(bf, lmg, s);
+  if (prof) (void)hipEventRecordWithFlags(c->prof_ev[2 * c->prof_used++ + 1], s, evf);
+  launch_lm_combine(R, c->n_wg_lm, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
+                    p.logp, p.tok_a, p.tok_b, p.ld_b, s);
+}
+
+static prism_status check_set(prism_ctx *c, int step, int want_F) {
+  if (!c->shared_loaded) return fail(c, PRISM_ERR_NOT_LOADED, "shared tensors not loaded");
+  if (step < 1 || step > (int)c->fmap.size())
+    return fail(c, PRISM_ERR_INVALID_ARG, "step %d beyond the step map (%zu steps)", step, c->fmap.size());
+  const int s = c->fmap[step - 1];
+  if (!c->sets[s].loaded) return fail(c, PRISM_ERR_NOT_LOADED, "set %d (step %d) not loaded", s, step);
+  if (want_F > 0 && c->sets[s].F != want_F)
+    return fail(c, PRISM_ERR_UNSUPPORTED,
+                "set %d serves step %d, which needs feature width %d, but was loaded with %d", s,
+                step, want_F, c->sets[s].F);
+  return PRISM_OK;
+}
+
+static prism_status check_batch(prism_ctx *c, const prism_batch *b) {
+  if (!b) return fail(c, PRISM_ERR_INVALID_ARG, "batch is NULL");
+  if (b->batch < 1 || b->batch > c->cfg.max_batch)
+    return fail(c, PRISM_ERR_INVALID_ARG, "batch %d out of 1..%d", b->batch, c->cfg.max_batch);
+  if (!b->d_tokens || !b->d_features || !b->d_ctx_lens || !b->d_k_pool || !b->d_v_pool ||
+      !b->d_block_table)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL pointer in batch");
+  if (b->n_pool_blocks < 1) return fail(c, PRISM_ERR_INVALID_ARG, "n_pool_blocks < 1");
+  return PRISM_OK;
+}
+
+// run `enqueue` directly or through a cached graph keyed by `key`
+template <typename F>
+static prism_status run_graph(prism_ctx *c, std::vector<uintptr_t> key, hipStream_t s,
+                              F enqueue) {
+  key.push_back(c->profile ? 1 : 0);
+  if (!c->use_graph) {
+    c->prof_used = 0;
+    enqueue(s);
+    c->prof_last = c->prof_used;
+    HIPCHK(c, hipGetLastError());
+    return PRISM_OK;
+  }
+  auto it = c->graphs.find(key);
+  if (it == c->graphs.end()) {
+    hipGraph_t graph;
+    HIPCHK(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal));
+    c->prof_used = 0;
+    enqueue(c->cap);
+    c->prof_last = c->prof_used;
+    hipError_t le = hipGetLastError();
+    hipError_t ee = hipStreamEndCapture(c->cap, &graph);
+    if (le != hipSuccess) return fail(c, PRISM_ERR_HIP, "launch during capture: %s", hipGetErrorString(le));
+    if (ee != hipSuccess) return fail(c, PRISM_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ee));
+    hipGraphExec_t exec;
+    hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ie != hipSuccess) return fail(c, PRISM_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
+    it = c->graphs.emplace(key, exec).first;
+    c->prof_pairs[key] = c->prof_last;
+  }
+  HIPCHK(c, hipGraphLaunch(it->second, s));
+  c->prof_last = c->prof_pairs[key];   // a replay records the pairs its capture did
+  return PRISM_OK;
+}
+
+extern "C" {
+
+prism_status prism_draft_step(prism_ctx *c, int32_t k, const prism_step_io *io, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!io) return fail(c, PRISM_ERR_INVALID_ARG, "io is NULL");
+  prism_status st = check_set(c, k, 0);
+  if (st) return st;
+  if (io->rows < 1 || io->rows > c->rows_max)
+    return fail(c, PRISM_ERR_INVALID_ARG, "rows %d out of 1..%d", io->rows, c->rows_max);
+  if (io->topk < 1 || io->topk > c->kmax || io->topk > c->V)
+    return fail(c, PRISM_ERR_INVALID_ARG, "topk %d out of 1..%d", io->topk, c->kmax);
+  if (!io->d_tokens || !io->d_feat || !io->d_seq || !io->d_pos || !io->d_slot || !io->kv ||
+      !io->d_topk_ids)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL pointer in step io");
+  if (io->feat_dtype != PRISM_F32 && io->feat_dtype != PRISM_BF16)
+    return fail(c, PRISM_ERR_INVALID_ARG, "feat_dtype %d", io->feat_dtype);
+  const prism_batch *b = io->kv;
+  if (!b->d_ctx_lens || !b->d_k_pool || !b->d_v_pool || !b->d_block_table || b->n_pool_blocks < 1 ||
+      b->batch < 1)
+    return fail(c, PRISM_ERR_INVALID_ARG, "incomplete KV description");
+  hipStream_t s = (hipStream_t)stream;
+  const int set = c->fmap[k - 1];
+  Pass p{};
+  p.set = set;
+  p.R = io->rows;
+  p.F = c->sets[set].F;
+  p.topk = io->topk;
+  p.in.tokens = io->d_tokens;
+  p.in.feat = io->d_feat;
+  p.in.feat_bf16 = io->feat_dtype == PRISM_BF16;
+  p.in.feat_ld = p.F;
+  p.in.feat_rows = io->d_feat_rows;
+  p.in.seq = io->d_seq;
+  p.in.pos = io->d_pos;
+  p.in.slot = io->d_slot;
+  p.in.bits = io->d_tree_bits;
+  p.hid_out = io->d_hidden_out ? io->d_hidden_out : c->hid[0];
+  p.ld_hid = c->H;
+  p.logits = io->d_logits;
+  p.ld_logits = c->V;
+  p.ids = io->d_topk_ids;
+  p.logp = io->d_topk_logp;
+  enqueue_pass(c, p, kv_of(c, b), s);
+  HIPCHK(c, hipGetLastError());
+  return PRISM_OK;
+}
+
+prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K,
+                               int32_t *d_out_tokens, float *d_out_logits, float *d_out_hidden,
+                               void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  prism_status st = check_batch(c, batch);
+  if (st) return st;
+  if (K < 1 || K > c->cfg.max_steps || K > (int)c->fmap.size())
+    return fail(c, PRISM_ERR_INVALID_ARG, "K %d out of 1..%zu", K, c->fmap.size());
+  if (!d_out_tokens) return fail(c, PRISM_ERR_INVALID_ARG, "d_out_tokens is NULL");
+  for (int k = 1; k <= K; ++k)
+    if ((st = check_set(c, k, k == 1 ? c->cfg.feat_width : c->H))) return st;
+  const prism_batch b = *batch;
+  const KvArgs kv = kv_of(c, &b);
+  const int B = b.batch, H = c->H, V = c->V;
+  std::vector<uintptr_t> key = {1, (uintptr_t)B, (uintptr_t)K, (uintptr_t)b.d_tokens,
+                                (uintptr_t)b.d_features, (uintptr_t)b.d_ctx_lens,
+                                (uintptr_t)b.d_k_pool, (uintptr_t)b.d_v_pool,
+                                (uintptr_t)b.d_block_table, (uintptr_t)b.n_pool_blocks,
+                                (uintptr_t)d_out_tokens, (uintptr_t)d_out_logits,
+                                (uintptr_t)d_out_hidden};
+  for (int k = 0; k < K; ++k) key.push_back((uintptr_t)c->fmap[k]);
+  auto enqueue = [&](hipStream_t s) {
+    launch_chain_setup(B, K, b.d_tokens, b.d_ctx_lens, c->c_seq, c->c_pos, c->c_tok0, s);
+    const float *prev = nullptr;
+    int ld_prev = 0;
+    for (int k = 1; k <= K; ++k) {
+      Pass p{};
+      p.set = c->fmap[k - 1];
+      p.R = B;
+      p.F = k == 1 ? c->cfg.feat_width : H;
+      p.topk = 1;
+      p.in.tokens = k == 1 ? c->c_tok0 : c->tokbuf;
+      p.in.feat = k == 1 ? b.d_features : (const void *)prev;
+      p.in.feat_bf16 = k == 1 ? (int)c->bf16 : 0;
+      p.in.feat_ld = k == 1 ? c->cfg.feat_width : ld_prev;
+      p.in.feat_rows = nullptr;
+      p.in.seq = c->c_seq;
+      p.in.pos = c->c_pos + (size_t)(k - 1) * B;
+      p.in.slot = p.in.pos;
+      p.in.bits = nullptr;
+      p.hid_out = d_out_hidden ? d_out_hidden + (size_t)(k - 1) * H : c->hid[k & 1];
+      p.ld_hid = d_out_hidden ? K * H : H;
+      p.logits = d_out_logits ? d_out_logits + (size_t)(k - 1) * V : nullptr;
+      p.ld_logits = (long)K * V;
+      p.ids = c->ids;
+      p.logp = nullptr;
+      p.tok_a = c->tokbuf;
+      p.tok_b = d_out_tokens + (k - 1);
+      p.ld_b = K;
+      enqueue_pass(c, p, kv, s);
+      prev = p.hid_out;
+      ld_prev = p.ld_hid;
+    }
+  };
+  return run_graph(c, key, (hipStream_t)stream, enqueue);
+}
+
+prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t depth,
+                              const prism_tree_out *out, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  prism_status st = check_batch(c, batch);
+  if (st) return st;
+  const int w = c->cfg.tree_width, v = c->cfg.tree_nodes;
+  if (w < 1) return fail(c, PRISM_ERR_INVALID_ARG, "context was created without tree_width");
+  if (depth < 1 || depth > c->cfg.max_steps || depth > (int)c->fmap.size())
+    return fail(c, PRISM_ERR_INVALID_ARG, "depth %d out of 1..%zu", depth, c->fmap.size());
+  if (!out || !out->d_tokens || !out->d_parent || !out->d_depth || !out->d_score || !out->d_mask)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL tree output");
+  const int C = w + (depth - 1) * w * w;
+  if (v > C) return fail(c, PRISM_ERR_SHAPE, "tree_nodes %d exceeds the %d candidates", v, C);
+  for (int k = 1; k <= depth; ++k)
+    if ((st = check_set(c, k, k == 1 ? c->cfg.feat_width : c->H))) return st;
+  const prism_batch b = *batch;
+  const prism_tree_out o = *out;
+  const KvArgs kv = kv_of(c, &b);
+  const int B = b.batch, H = c->H, V = c->V;
+  std::vector<uintptr_t> key = {2, (uintptr_t)B, (uintptr_t)depth, (uintptr_t)b.d_tokens,
+                                (uintptr_t)b.d_features, (uintptr_t)b.d_ctx_lens,
+                                (uintptr_t)b.d_k_pool, (uintptr_t)b.d_v_pool,
+                                (uintptr_t)b.d_block_table, (uintptr_t)b.n_pool_blocks,
+                                (uintptr_t)o.d_tokens, (uintptr_t)o.d_parent, (uintptr_t)o.d_depth,
+                                (uintptr_t)o.d_score, (uintptr_t)o.d_mask, (uintptr_t)o.d_cand_tokens,
+                                (uintptr_t)o.d_cand_parent, (uintptr_t)o.d_cand_score,
+                                (uintptr_t)o.d_frontier, (uintptr_t)o.d_logits};
+  for (int k = 0; k < depth; ++k) key.push_back((uintptr_t)c->fmap[k]);
+  TreeWs t{};
+  t.B = B; t.w = w; t.D = depth; t.C = C;
+  t.cand_tok = c->t_ctok; t.cand_par = c->t_cpar; t.cand_score = c->t_cscore;
+  t.front = c->t_front;
+  t.tok = c->t_tok; t.feat_row = c->t_frow; t.seq = c->t_seq; t.pos = c->t_pos; t.slot = c->t_slot;
+  auto enqueue = [&](hipStream_t s) {
+    launch_tree_setup(B, b.d_tokens, b.d_ctx_lens, c->t_tok, c->t_seq, c->t_pos, c->t_slot,
+                      c->t_bits[0], s);
+    for (int d = 0; d < depth; ++d) {
+      Pass p{};
+      p.set = c->fmap[d];
+      p.R = d == 0 ? B : B * w;
+      p.F = d == 0 ? c->cfg.feat_width : H;
+      p.topk = w;
+      p.in.tokens = c->t_tok;
+      p.in.feat = d == 0 ? b.d_features : (const void *)c->hid[(d - 1) & 1];
+      p.in.feat_bf16 = d == 0 ? (int)c->bf16 : 0;
+      p.in.feat_ld = d == 0 ? c->cfg.feat_width : H;
+      p.in.feat_rows = d == 0 ? nullptr : c->t_frow;
+      p.in.seq = c->t_seq;
+      p.in.pos = c->t_pos;
+      p.in.slot = c->t_slot;
+      p.in.bits = c->t_bits[d & 1];
+      p.hid_out = c->hid[d & 1];
+      p.ld_hid = H;
+      if (o.d_logits) {
+        p.logits = o.d_logits + (size_t)d * B * w * V;
+        p.ld_logits = d == 0 ? (long)w * V : (long)V;
+      }
+      p.ids = c->ids;
+      p.logp = c->logp;
+      enqueue_pass(c, p, kv, s);
+      TreeWs tt = t;
+      tt.bits_prev = c->t_bits[d & 1];
+      tt.bits = c->t_bits[(d + 1) & 1];
+      launch_tree_expand(d, tt, b.d_ctx_lens, c->ids, c->logp, s);
+    }
+    launch_tree_final(t, v, o.d_tokens, o.d_parent, o.d_depth, o.d_score, o.d_mask,
+                      o.d_cand_tokens, o.d_cand_parent, o.d_cand_score, o.d_frontier, s);
+  };
+  return run_graph(c, key, (hipStream_t)stream, enqueue);
+}
+
+prism_status prism_profile_enable(prism_ctx *c, int32_t enable) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  drop_graphs(c);
+  c->profile = enable != 0;
+  if (c->profile && c->prof_ev.empty()) {
+    const int pairs = c->cfg.max_steps;
+    for (int i = 0; i < 2 * pairs; ++i) {
+      hipEvent_t e;
+      HIPCHK(c, hipEventCreate(&e));
+      c->prof_ev.push_back(e);
+    }
+  }
+  c->prof_last = 0;
+  return PRISM_OK;
+}
+
+prism_status prism_profile_read(prism_ctx *c, float *total_ms, int32_t *count) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!total_ms || !count) return fail(c, PRISM_ERR_INVALID_ARG, "NULL output");
+  *total_ms = 0.f;
+  *count = 0;
+  if (!c->profile) return fail(c, PRISM_ERR_INVALID_ARG, "profiling is not enabled");
+  for (int i = 0; i < c->prof_last; ++i) {
+    HIPCHK(c, hipEventSynchronize(c->prof_ev[2 * i + 1]));
+    float ms = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&ms, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+    *total_ms += ms;
+  }
+  *count = c->prof_last;
+  return PRISM_OK;
+}
+
+prism_status prism_device_status(prism_ctx *c, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  HIPCHK(c, hipStreamSynchronize((hipStream_t)stream));
+  uint32_t flags = 0, zero = 0;
+  HIPCHK(c, hipMemcpy(&flags, c->err, 4, hipMemcpyDeviceToHost));
+  HIPCHK(c, hipMemcpy(c->err, &zero, 4, hipMemcpyHostToDevice));
+  if (flags & ERRF_CAPACITY) return fail(c, PRISM_ERR_CAPACITY, "KV slot, block or pool out of range");
+  if (flags & ERRF_TOKEN) return fail(c, PRISM_ERR_INVALID_ARG, "token id out of range");
+  return PRISM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,127 @@
+"""GPU parity: the HIP drafting path (through the C ABI) against the oracle.
+
+Small configurations are compared element by element (every sequence, every
+step); the full-size workloads are compared on sampled sequences, which the
+oracle computes exactly because sequences are independent.
+"""
+import numpy as np
+import pytest
+import torch
+
+from synth import (L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32, SMALL_BF16_CHAIN,
+                   SMALL_BF16_TREE, SMALL_F32_CHAIN, TINY_F32)
+from harness import check_chain, check_tree, gpu_setup, log, oracle_for
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def run_chain_parity(cfg, seqs=None):
+    log("chain parity", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.chain(inp, logits=True, hidden=True)
+    plain = dr.chain(inp)                      # the launch the benchmark times
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    assert torch.equal(out["tokens"], plain["tokens"])
+    seqs = list(range(cfg.batch)) if seqs is None else seqs
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    log("oracle", cfg.name, "seqs", seqs)
+    res = check_chain(cfg, out, orc, hi, seqs)
+    log(cfg.name, res)
+    dr.close()
+    return res
+
+
+@pytest.mark.parametrize("cfg", [TINY_F32, SMALL_F32_CHAIN, SMALL_BF16_CHAIN], ids=lambda c: c.name)
+def test_chain_parity_small(cfg):
+    run_chain_parity(cfg)
+
+
+def test_chain_deterministic_and_poison_free():
+    cfg = SMALL_BF16_CHAIN
+    dr, w, inp = gpu_setup(cfg)
+    a = dr.chain(inp, logits=True, hidden=True)
+    b = dr.chain(inp, logits=True, hidden=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a["tokens"], b["tokens"])
+    assert torch.equal(a["logits"], b["logits"])
+    assert torch.isfinite(a["logits"]).all() and torch.isfinite(a["hidden"]).all()
+    dr.close()
+
+
+def test_chain_fmap_surjection():
+    # the paper's evaluated instance: module 1 for step 1, module 2 for the rest
+    cfg = SMALL_BF16_CHAIN.with_(f_map=(0, 1, 1, 1), n_sets=2)
+    run_chain_parity(cfg)
+
+
+def test_step_api_matches_chain_first_step():
+    cfg = SMALL_BF16_CHAIN
+    dr, w, inp = gpu_setup(cfg)
+    ref = dr.chain(inp, K=1, logits=True, hidden=True)
+    B = cfg.batch
+    dev = inp.tokens.device
+    # the chain wrote slot L_b; the explicit step rewrites the same slot
+    rows = {"tokens": inp.tokens, "feat": inp.features,
+            "seq": torch.arange(B, dtype=torch.int32, device=dev),
+            "pos": inp.ctx_lens.clone(), "slot": inp.ctx_lens.clone()}
+    st = dr.step(1, inp, rows, topk=1, logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(st["ids"][:, 0], ref["tokens"][:, 0])
+    assert torch.equal(st["logits"], ref["logits"][:, 0])
+    assert torch.equal(st["hidden"], ref["hidden"][:, 0])
+    dr.close()
+
+
+def run_tree_parity(cfg, seqs=None):
+    log("tree parity", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.tree(inp, debug=True, logits=True)
+    plain = dr.tree(inp, debug=False)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    for k in ("tokens", "parent", "depth", "score", "mask"):
+        assert torch.equal(out[k], plain[k]), k
+    seqs = list(range(cfg.batch)) if seqs is None else seqs
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    res = check_tree(cfg, out, orc, hi, seqs, cfg.n_steps)
+    log(cfg.name, res)
+    dr.close()
+
+
+def test_tree_parity_small():
+    run_tree_parity(SMALL_BF16_TREE)
+
+
+def test_tree_width_one_equals_chain():
+    tcfg = SMALL_BF16_TREE.with_(tree_width=1, tree_nodes=SMALL_BF16_TREE.n_steps)
+    dr, w, inp = gpu_setup(tcfg)
+    t = dr.tree(inp)
+    c = dr.chain(inp, K=tcfg.n_steps)
+    torch.cuda.synchronize()
+    assert torch.equal(t["tokens"], c["tokens"])
+    dr.close()
+
+
+# ---------------------------------------------------------------- full size
+@pytest.mark.slow
+def test_full_8b_bs1_chain():
+    run_chain_parity(L3_8B_BS1)
+
+
+@pytest.mark.slow
+def test_full_8b_bs16_paged_chain():
+    from synth import ctx_lengths
+    lens = ctx_lengths(L3_8B_BS16)
+    run_chain_parity(L3_8B_BS16, seqs=[int(np.argmin(lens)), int(np.argmax(lens))])
+
+
+@pytest.mark.slow
+def test_full_8b_tree():
+    run_tree_parity(L3_8B_TREE, seqs=[0])
+
+
+@pytest.mark.slow
+def test_full_70b_bs32_chain():
+    run_chain_parity(L3_70B_BS32, seqs=[0, 31])
