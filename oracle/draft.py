@@ -21,8 +21,8 @@ What is computed (PRISM, Sec. 3.2 "Draft with PRISM"; notation of Table 2):
     (Sec. 2 "SoTA Draft Models"; Sec. 3.2 says PRISM is compatible with tree
     drafts; Sec. 4.1 and 4.3 give the depth / width / verified-node topology).
 
-Readings where the paper is silent (each is listed with its reason in the
-design notes): the decode equation is read as H_in = F(E(x_{k-1}), h_{k-2})
+Readings where the paper is silent:
+the decode equation is read as H_in = F(E(x_{k-1}), h_{k-2})
 with the transformer updating the KV; FC input order is [E(x) ; feature],
 no biases; Llama pre-norm block (RMSNorm, RoPE GQA attention, residual,
 RMSNorm, SwiGLU, residual) with the residual stream starting at the FC
@@ -31,12 +31,12 @@ rotate-half RoPE with angles in fp64 and cos/sin rounded to fp32; chain
 step k at position L+k-1; tree depth-d nodes at position L+d; ties broken by
 lowest token id.
 
-Precision: everything is fp64.  For bf16 models the storage roundings and the
-bf16 rounding of every matrix-product activation operand are emulated (FC
-input, normed attention input, q, stored k and v, attention output o, normed
-MLP input, SwiGLU output, normed LM-head input); residuals, norms, RoPE,
-softmax, h and logits stay fp64.  For fp32 models the cache stores fp32 and
-nothing else is rounded.
+Precision: the paper fixes none.  Everything here is fp64.  Stored tensors
+are exact in their storage type (bf16 or fp32 weights, embeddings, target
+features), and the one value the drafting step itself stores, the new k and
+v of the KV cache, is rounded to the cache type.  Activations that feed a
+matrix product are used exactly (the kernels carry them at fp32 precision),
+so no other rounding is emulated.
 """
 from __future__ import annotations
 
@@ -125,11 +125,6 @@ class Oracle:
         self.bf16 = cfg.dtype == "bf16"
         self.g_f = widen(hw["final_norm"])
 
-    # precision points
-    def op(self, x):
-        """A matrix-product activation operand (bf16 models round it)."""
-        return round_bf16(x) if self.bf16 else x
-
     def store(self, x):
         """A value written to the KV cache (rounded to the cache dtype)."""
         return round_bf16(x) if self.bf16 else x.astype(np.float32).astype(np.float64)
@@ -156,13 +151,13 @@ class Oracle:
         R = len(tokens)
         assert feats.shape == (R, P["feat_width"]), (feats.shape, P["feat_width"])
         e = widen(self.hw["embed"][np.asarray(tokens)])
-        u = self.lin(P["w_fc"], self.op(np.concatenate([e, feats], axis=1)))
-        a = self.op(rmsnorm(u, widen(P["g1"]), cfg.rms_eps))
+        u = self.lin(P["w_fc"], np.concatenate([e, feats], axis=1))
+        a = rmsnorm(u, widen(P["g1"]), cfg.rms_eps)
         q = self.lin(P["w_q"], a).reshape(R, nq, d)
         k = self.lin(P["w_k"], a).reshape(R, nkv, d)
         v = self.lin(P["w_v"], a).reshape(R, nkv, d)
         for r in range(R):
-            q[r] = self.op(rope(q[r], pos[r], cfg.rope_theta))
+            q[r] = rope(q[r], pos[r], cfg.rope_theta)
             k[r] = self.store(rope(k[r], pos[r], cfg.rope_theta))
             v[r] = self.store(v[r])
             caches[seq[r]]["draft"][slots[r]] = (k[r].copy(), v[r].copy())
@@ -171,13 +166,13 @@ class Oracle:
             Kv, Vv = self.gather(caches[seq[r]], visible[r])
             for h in range(nq):
                 o[r, h] = softmax_attend(q[r, h], Kv[:, h // g, :], Vv[:, h // g, :])
-        r1 = u + self.lin(P["w_o"], self.op(o.reshape(R, nq * d)))
-        m = self.op(rmsnorm(r1, widen(P["g2"]), cfg.rms_eps))
-        z = self.op(silu(self.lin(P["w_gate"], m)) * self.lin(P["w_up"], m))
+        r1 = u + self.lin(P["w_o"], o.reshape(R, nq * d))
+        m = rmsnorm(r1, widen(P["g2"]), cfg.rms_eps)
+        z = silu(self.lin(P["w_gate"], m)) * self.lin(P["w_up"], m)
         hid = r1 + self.lin(P["w_down"], z)
         logits = None
         if want_logits:
-            logits = self.lin(self.hw["lm_head"], self.op(rmsnorm(hid, self.g_f, cfg.rms_eps)))
+            logits = self.lin(self.hw["lm_head"], rmsnorm(hid, self.g_f, cfg.rms_eps))
         return hid, logits
 
     @staticmethod
@@ -389,12 +384,12 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
             for j in range(k):
                 P = orc.hw["sets"][cfg.fmap[j]]
                 e = widen(orc.hw["embed"][tok])[None]
-                u = orc.lin(P["w_fc"], orc.op(np.concatenate([e, feat[None]], 1)))
-                a = orc.op(rmsnorm(u, widen(P["g1"]), cfg.rms_eps))
+                u = orc.lin(P["w_fc"], np.concatenate([e, feat[None]], 1))
+                a = rmsnorm(u, widen(P["g1"]), cfg.rms_eps)
                 q = orc.lin(P["w_q"], a).reshape(nq, d)
                 kk = orc.lin(P["w_k"], a).reshape(nkv, d)
                 vv = orc.lin(P["w_v"], a).reshape(nkv, d)
-                q = orc.op(rope(q, L + j, cfg.rope_theta))
+                q = rope(q, L + j, cfg.rope_theta)
                 Ks[L + j] = orc.store(rope(kk, L + j, cfg.rope_theta))
                 Vs[L + j] = orc.store(vv)
                 o = np.empty((nq, d))
@@ -403,13 +398,13 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
                     sc = np.where(mask[j], sc, -np.inf)
                     p = np.exp(sc - sc.max())
                     o[hh] = (p @ Vs[:, hh // g, :]) / p.sum()
-                r1 = u + orc.lin(P["w_o"], orc.op(o.reshape(1, nq * d)))
-                m = orc.op(rmsnorm(r1, widen(P["g2"]), cfg.rms_eps))
-                z = orc.op(silu(orc.lin(P["w_gate"], m)) * orc.lin(P["w_up"], m))
+                r1 = u + orc.lin(P["w_o"], o.reshape(1, nq * d))
+                m = rmsnorm(r1, widen(P["g2"]), cfg.rms_eps)
+                z = silu(orc.lin(P["w_gate"], m)) * orc.lin(P["w_up"], m)
                 hj = (r1 + orc.lin(P["w_down"], z))[0]
                 if j == k - 1:
                     lg = orc.lin(orc.hw["lm_head"],
-                                 orc.op(rmsnorm(hj[None], orc.g_f, cfg.rms_eps)))[0]
+                                 rmsnorm(hj[None], orc.g_f, cfg.rms_eps))[0]
                     order = np.argsort(-lg, kind="stable")
                     chosen.append(int(order[0]))
                     hidden[b, k - 1] = hj
