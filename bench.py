@@ -101,7 +101,8 @@ def main():
     value = drafted * args.steps / (total_ms / 1e3)
     assert dr.device_status() == 0
 
-    # dominant kernel: HIP events around every LM-head launch inside the graph
+    # dominant kernel: HIP events around every LM-head launch (same kernels,
+    # launched directly on the stream so the events bracket each launch)
     binding.prism_profile_enable(dr.ctx, True)
     call()
     torch.cuda.synchronize()

@@ -231,11 +231,12 @@ prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
 prism_status prism_device_status(prism_ctx *ctx, void *stream);
 
 /* Measurement support (not part of the drafting computation).  With
- * enable != 0, chains and trees captured afterwards record a pair of HIP
- * events on their stream around every LM-head launch (the largest product
- * of a step), inside the graph.  prism_profile_read() waits for the events
- * of the last chain or tree call and returns the summed milliseconds between
- * each pair and the number of pairs. */
+ * enable != 0, chain and tree calls launch their kernels directly on
+ * `stream` instead of replaying a graph, and record a pair of HIP events on
+ * that stream around every LM-head launch (the largest product of a step).
+ * prism_profile_read() waits for the events of the last chain or tree call
+ * and returns the summed milliseconds between each pair and the number of
+ * pairs. */
 prism_status prism_profile_enable(prism_ctx *ctx, int32_t enable);
 prism_status prism_profile_read(prism_ctx *ctx, float *total_ms, int32_t *count);
 

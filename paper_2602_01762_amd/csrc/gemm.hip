@@ -3,207 +3,451 @@
 //
 // These products are HBM-bound (a weight byte feeds 2R flops), so the design
 // is about streaming W: W is pre-tiled so that every wave-wide load is one
-// contiguous KiB (see TiledMat), each wave keeps U such loads in flight, and
-// K is split across the waves of a workgroup (and across workgroups) until
-// the grid holds enough waves to cover HBM latency.  The MFMA treats 16 rows
-// of W as the M side and 16 rows of X as the N side; for R = 1 most of the
-// B fragment is zero, which costs MFMA cycles that are idle anyway.
+// contiguous KiB (see TiledMat), each wave keeps 8 KiB of loads in flight,
+// and up to 16 waves of one workgroup split K so that small matrices still
+// put enough bytes in flight; their partial sums meet in LDS in wave order
+// (deterministic, no second pass).  The MFMA takes 16 rows of W as its M
+// side and 16 rows of X as its N side; for R = 1 most of the B fragment is
+// zero, which costs MFMA cycles that are idle anyway.  bf16 activations come
+// as hi/lo pairs (two MFMAs per W fragment), so the products see fp32-exact
+// activations at no extra HBM traffic.
+//
+// Epilogues write whatever the next kernel needs: the fp32 residual row,
+// (y * gain) as the next operand, per-tile sums of squares for the next
+// RMSNorm, the SwiGLU product, or q and the rotated k, v cache slots.
 #include "device.h"
 
 namespace prism {
 
-constexpr int U = 8;  // k-blocks in flight per wave
-
-template <typename T, int RT>
-__device__ __forceinline__ void wave_mma(const u32x4 *__restrict__ wp, const T *__restrict__ X,
-                                         int ldx, int R, int kb0, int kb1, f32x4 (&acc)[RT]) {
+template <typename T, int RT, int NT, bool PAIR>
+__device__ __forceinline__ void mainloop(const u32x4 *__restrict__ w0, int nkb, const Act &x,
+                                         int R, int kb0, int kb1, f32x4 (&acc)[NT][RT]) {
   constexpr int E = Ty<T>::E, KB = Ty<T>::KB;
+  // k-blocks in flight: about 96 VGPRs of A and B fragments per lane
+  constexpr int U0 = 24 / (NT + (PAIR ? 2 : 1) * RT);
+  constexpr int U = U0 > 8 ? 8 : (U0 < 1 ? 1 : U0);
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, kq = lane >> 4;
-  const T *xr[RT];
+  const T *xh[RT];
+  const T *xl[RT];
   bool ok[RT];
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt) {
     const int r = col + 16 * rt;
     ok[rt] = r < R;
-    xr[rt] = X + (size_t)(ok[rt] ? r : 0) * ldx + kq * E;
+    const size_t off = (size_t)(ok[rt] ? r : 0) * x.ld + kq * E;
+    xh[rt] = (const T *)x.hi + off;
+    xl[rt] = PAIR ? (const T *)x.lo + off : nullptr;
   }
-  wp += (size_t)kb0 * 64 + lane;
+  const u32x4 *wp[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) wp[n] = w0 + ((size_t)n * nkb + kb0) * 64 + lane;
+  const u32x4 z4 = {0, 0, 0, 0};
   int kb = kb0;
   for (; kb + U <= kb1; kb += U) {
-    u32x4 a[U];
-    u32x4 b[U][RT];
-#pragma unroll
-    for (int u = 0; u < U; ++u) a[u] = __builtin_nontemporal_load(wp + u * 64);
+    u32x4 a[U][NT];
+    u32x4 bh[U][RT], bl[U][RT];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        b[u][rt] = ok[rt] ? *(const u32x4 *)(xr[rt] + (size_t)(kb + u) * KB) : u32x4{0, 0, 0, 0};
+      for (int n = 0; n < NT; ++n) a[u][n] = __builtin_nontemporal_load(wp[n] + u * 64);
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) acc[rt] = Ty<T>::mma(a[u], b[u][rt], acc[rt]);
-    wp += U * 64;
+      for (int rt = 0; rt < RT; ++rt) {
+        const size_t o = (size_t)(kb + u) * KB;
+        bh[u][rt] = ok[rt] ? *(const u32x4 *)(xh[rt] + o) : z4;
+        if (PAIR) bl[u][rt] = ok[rt] ? *(const u32x4 *)(xl[rt] + o) : z4;
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          acc[n][rt] = Ty<T>::mma(a[u][n], bh[u][rt], acc[n][rt]);
+          if (PAIR) acc[n][rt] = Ty<T>::mma(a[u][n], bl[u][rt], acc[n][rt]);
+        }
+#pragma unroll
+    for (int n = 0; n < NT; ++n) wp[n] += U * 64;
   }
   for (; kb < kb1; ++kb) {
-    const u32x4 a = __builtin_nontemporal_load(wp);
+    u32x4 a[NT];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) a[n] = __builtin_nontemporal_load(wp[n]);
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      const u32x4 b = ok[rt] ? *(const u32x4 *)(xr[rt] + (size_t)kb * KB) : u32x4{0, 0, 0, 0};
-      acc[rt] = Ty<T>::mma(a, b, acc[rt]);
+      const size_t o = (size_t)kb * KB;
+      const u32x4 bh = ok[rt] ? *(const u32x4 *)(xh[rt] + o) : z4;
+      u32x4 bl = z4;
+      if (PAIR) bl = ok[rt] ? *(const u32x4 *)(xl[rt] + o) : z4;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        acc[n][rt] = Ty<T>::mma(a[n], bh, acc[n][rt]);
+        if (PAIR) acc[n][rt] = Ty<T>::mma(a[n], bl, acc[n][rt]);
+      }
     }
-    wp += 64;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) wp[n] += 64;
   }
 }
 
-// Workgroup = 4 waves.  kw waves split the K range of one tile (summed in
-// LDS in wave order), so a workgroup covers 4/kw tiles; grid.y = splits
-// splits K further across workgroups (partials summed later in split order).
-template <typename T, int RT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmLaunch g) {
-  const TiledMat &m = g.m;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int tpw = 4 / g.kw;
-  const int tile = blockIdx.x * tpw + wave / g.kw;
-  const int ks = blockIdx.y * g.kw + wave % g.kw;
-  const int nsl = g.splits * g.kw;
-  const int kb0 = (int)((long)ks * m.nkb / nsl);
-  const int kb1 = (int)((long)(ks + 1) * m.nkb / nsl);
-  const bool live = tile < m.n_tiles;
-  f32x4 acc[RT];
+// store an fp32 value as the storage-type operand (hi/lo pair for bf16)
+template <typename T>
+__device__ __forceinline__ void put_act(const ActOut &o, size_t i, float v) {
+  if constexpr (sizeof(T) == 2) {
+    const uint32_t h = f2bf(v);
+    ((bf16_t *)o.hi)[i] = (bf16_t)h;
+    ((bf16_t *)o.lo)[i] = (bf16_t)f2bf(v - bf2f(h));
+  } else {
+    ((float *)o.hi)[i] = v;
+  }
+}
+
+// Row scales 1/sqrt(mean(x^2) + eps) from per-tile sums of squares.  Loads
+// are issued here (before the main loop) and reduced in finish_scales.
+constexpr int SS_PER_THREAD = 4;
+struct ScaleLoads {
+  float v[SS_PER_THREAD];
+};
+__device__ __forceinline__ ScaleLoads issue_scales(const RowNorm &nm, int R) {
+  ScaleLoads s;
+  const int tot = nm.n_tiles * R;
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (live)
-    wave_mma<T, RT>((const u32x4 *)m.w + (size_t)tile * m.nkb * 64, (const T *)g.X, g.ldx, g.R,
-                    kb0, kb1, acc);
-  if (g.kw > 1) {
-    __shared__ f32x4 red[4][RT][64];
-    if (wave % g.kw) {
+  for (int j = 0; j < SS_PER_THREAD; ++j) {
+    const int i = threadIdx.x + j * blockDim.x;
+    s.v[j] = i < tot ? nm.ss[i] : 0.f;
+  }
+  return s;
+}
+int own_scale_capacity(int threads) { return SS_PER_THREAD * threads; }
+
+// sums per row (ss layout [tile][R], so row = index % R): thread, then wave
+// butterfly, then waves in order through LDS.  tmp: one float per wave.
+__device__ __forceinline__ void finish_scales(const RowNorm &nm, int R, const ScaleLoads &s,
+                                              float *rowscale, float *tmp) {
+  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  for (int r = 0; r < R; ++r) {
+    float acc = 0.f;
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) red[wave][rt][lane] = acc[rt];
+    for (int j = 0; j < SS_PER_THREAD; ++j) {
+      const int i = threadIdx.x + j * blockDim.x;
+      if (i < nm.n_tiles * R && i % R == r) acc += s.v[j];
+    }
+    acc = wave_sum(acc);
+    if ((threadIdx.x & 63) == 0) tmp[wave] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = 0.f;
+      for (int i = 0; i < nw; ++i) t += tmp[i];
+      rowscale[r] = 1.0f / sqrtf(t / (float)nm.n + nm.eps);
     }
     __syncthreads();
-    if (wave % g.kw == 0) {
-      for (int j = 1; j < g.kw; ++j)
+  }
+}
+
+// batched variants (more accumulators) run at most 8 waves per workgroup,
+// which leaves them 256 VGPRs
+template <int RT, int NT>
+constexpr int gemm_max_threads() { return RT * NT >= 2 ? 512 : 1024; }
+
+template <typename T, int RT, int NT, bool PAIR, int EPI>
+__global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunch g) {
+  extern __shared__ f32x4 red[];        // [(kw - 1) * NT * RT * 64]
+  __shared__ float rowscale[MAX_ROWS];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int kw = g.kw;
+  const int t0 = blockIdx.x * NT;
+  const TiledMat &m = g.m;
+  const bool has_norm = g.norm.scale != nullptr || g.norm.n_tiles > 0;
+  const bool own_scales = g.norm.scale == nullptr && g.norm.n_tiles > 0;
+  ScaleLoads sl;
+  if (own_scales) sl = issue_scales(g.norm, g.R);
+
+  f32x4 acc[NT][RT];
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) acc[rt] += red[wave + j][rt][lane];
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int kb0 = (int)((long)wave * m.nkb / kw);
+  const int kb1 = (int)((long)(wave + 1) * m.nkb / kw);
+  mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
+                            kb1, acc);
+  if (kw > 1) {
+    if (wave > 0) {
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) red[(((wave - 1) * NT + n) * RT + rt) * 64 + lane] = acc[n][rt];
     }
   }
-  if (!live || (wave % g.kw) != 0) return;
-  // lane holds output features n0..n0+3 of batch rows (lane & 15) + 16 rt
-  const int n0 = tile * 16 + 4 * (lane >> 4);
+  if (own_scales) {
+    __syncthreads();
+    finish_scales(g.norm, g.R, sl, rowscale, (float *)&red[(kw - 1) * NT * RT * 64]);
+  } else if (kw > 1) {
+    __syncthreads();
+  }
+  if (wave != 0) return;
+  for (int j = 1; j < kw; ++j)
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = (lane & 15) + 16 * rt;
-    if (r >= g.R) continue;
-    if (EPI == EPI_PARTIAL) {
-      *(f32x4 *)(g.part + ((size_t)blockIdx.y * g.R + r) * m.N + n0) = acc[rt];
-    } else {
-      // rows are interleaved (gate c, up c, gate c+1, up c+1)
-      const int c = n0 >> 1;
-      T *z = (T *)g.Z + (size_t)r * g.ldz + c;
-      Ty<T>::st(z, 0, silu(acc[rt].x) * acc[rt].y);
-      Ty<T>::st(z, 1, silu(acc[rt].z) * acc[rt].w);
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[n][rt] += red[(((j - 1) * NT + n) * RT + rt) * 64 + lane];
+
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int tile = t0 + n;
+    const int n0 = tile * 16 + 4 * q4;   // first of this lane's 4 output rows (tiled order)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = (lane & 15) + 16 * rt;
+      const bool live = r < g.R;
+      float v[4] = {acc[n][rt].x, acc[n][rt].y, acc[n][rt].z, acc[n][rt].w};
+      if (has_norm && live) {
+        const float sc = own_scales ? rowscale[r] : g.norm.scale[r];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] *= sc;
+      }
+      if (EPI == EPI_NORM) {
+        float ss = 0.f;
+        if (live) {
+          if (g.res) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
+          }
+          *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * Ty<T>::ld((const T *)g.gain, n0 + i));
+            ss += v[i] * v[i];
+          }
+        }
+        // tile sum over the 4 lanes holding row r: fixed butterfly order
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        if (live && q4 == 0) g.ss[(size_t)tile * g.R + r] = ss;
+      } else if (EPI == EPI_SWIGLU) {
+        if (live) {
+          // rows interleave (gate c, up c, gate c + 1, up c + 1)
+          const int c = n0 >> 1;
+          put_act<T>(g.z, (size_t)r * g.z.ld + c, silu(v[0]) * v[1]);
+          put_act<T>(g.z, (size_t)r * g.z.ld + c + 1, silu(v[2]) * v[3]);
+        }
+      } else {  // EPI_QKV
+        const int d = g.d, half = d >> 1;
+        const int qd = g.nq * d, kd = g.nkv * d;
+        const int f0 = tile * 16;            // first feature of the tile (tiled order)
+        // partner values for the rotation (lanes l and l ^ 32 hold the two halves)
+        float pv[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pv[i] = __shfl_xor(v[i], 32, 64);
+        if (!live) continue;
+        if (f0 < qd + kd) {
+          const bool isq = f0 < qd;
+          const int fr = isq ? f0 : f0 - qd;
+          const int head = fr / d;
+          const int j = (fr % d) / 16;       // tile index within the head
+          const bool first = q4 < 2;
+          const int dim0 = 8 * j + 4 * (q4 & 1);   // dim within the first half
+          const int pos = g.rows.pos[r];
+          float out[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double ang = (double)pos * g.inv_freq[dim0 + i];
+            const float c = (float)cos(ang), s = (float)sin(ang);
+            // first half: y1 = x1 c - x2 s ; second half: y2 = x2 c + x1 s
+            out[i] = first ? v[i] * c - pv[i] * s : v[i] * c + pv[i] * s;
+          }
+          const int dimb = first ? dim0 : half + dim0;
+          if (isq) {
+            *(f32x4 *)(g.q + (size_t)r * qd + head * d + dimb) = f32x4{out[0], out[1], out[2], out[3]};
+          } else {
+            const int b = g.rows.seq[r], slot = g.rows.slot[r];
+            const int bi = slot / g.kv.bs;
+            long base = -1;
+            if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
+              const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
+              if (blk >= 0 && blk < g.kv.n_blocks)
+                base = ((long)blk * g.nkv + head) * g.kv.bs * d + (long)(slot % g.kv.bs) * d;
+            }
+            if (base < 0) {
+              atomicOr(g.err, ERRF_CAPACITY);
+            } else {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.k_pool, base + dimb + i, out[i]);
+            }
+          }
+        } else {
+          const int fr = f0 - qd - kd;
+          const int head = fr / d;
+          const int dim = fr % d + 4 * q4;
+          const int b = g.rows.seq[r], slot = g.rows.slot[r];
+          const int bi = slot / g.kv.bs;
+          long base = -1;
+          if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
+            const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
+            if (blk >= 0 && blk < g.kv.n_blocks)
+              base = ((long)blk * g.nkv + head) * g.kv.bs * d + (long)(slot % g.kv.bs) * d;
+          }
+          if (base < 0) {
+            atomicOr(g.err, ERRF_CAPACITY);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.v_pool, base + dim + i, v[i]);
+          }
+        }
+      }
     }
   }
 }
 
-// LM head: one wave per 16-row vocab tile over the full K, a workgroup per
-// 64 vocab ids.  The epilogue reduces the workgroup's logits of each batch
-// row to partials: max, sum of exp(logit - max), and the top-k
-// (logit desc, id asc); optional fp32 logits store.
-template <typename T, int RT>
+// LM head: each wave covers NT 16-row vocab tiles over the full K; a
+// workgroup (4 waves) covers 64*NT vocab ids.  The epilogue applies the
+// final-norm row scale and reduces the workgroup's logits of each row to
+// partials: max, sum of exp(logit - max), and the top-k (logit desc, id asc);
+// optional fp32 logits store.
+template <typename T, int RT, int NT, bool PAIR>
 __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
+  __shared__ float sl[RT * 16][64 * NT + 1];
+  __shared__ float rowscale[MAX_ROWS];
+  __shared__ float tmp[256];
   const TiledMat &m = g.m;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int tile = blockIdx.x * 4 + wave;
-  const bool live = tile < m.n_tiles;
-  f32x4 acc[RT];
+  const int t0 = (blockIdx.x * 4 + wave) * NT;
+  const bool has_norm = g.norm.scale != nullptr || g.norm.n_tiles > 0;
+  const bool own_scales = g.norm.scale == nullptr && g.norm.n_tiles > 0;
+  ScaleLoads sc;
+  if (own_scales) sc = issue_scales(g.norm, g.R);
+  f32x4 acc[NT][RT];
 #pragma unroll
-  for (int rt = 0; rt < RT; ++rt) acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bool live = t0 < m.n_tiles;    // n_tiles is a multiple of NT
   if (live)
-    wave_mma<T, RT>((const u32x4 *)m.w + (size_t)tile * m.nkb * 64, (const T *)g.X, g.ldx, g.R,
-                    0, m.nkb, acc);
-  __shared__ float sl[RT * 16][65];
-  const int q = lane >> 4;
-#pragma unroll
-  for (int rt = 0; rt < RT; ++rt) {
-    const int r = (lane & 15) + 16 * rt;
-    if (r >= g.R) continue;
-    const float v[4] = {acc[rt].x, acc[rt].y, acc[rt].z, acc[rt].w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sl[r][wave * 16 + 4 * q + i] = v[i];
-    if (live && g.logits)
-      *(f32x4 *)(g.logits + (size_t)r * g.ld_logits + tile * 16 + 4 * q) = acc[rt];
+    mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, 0,
+                              m.nkb, acc);
+  if (own_scales) {
+    __syncthreads();
+    finish_scales(g.norm, g.R, sc, rowscale, tmp);
   }
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = (lane & 15) + 16 * rt;
+      if (r >= g.R) continue;
+      const float s = has_norm ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
+      const float v[4] = {acc[n][rt].x * s, acc[n][rt].y * s, acc[n][rt].z * s, acc[n][rt].w * s};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sl[r][(wave * NT + n) * 16 + 4 * q4 + i] = v[i];
+      if (live && g.logits)
+        *(f32x4 *)(g.logits + (size_t)r * g.ld_logits + (t0 + n) * 16 + 4 * q4) =
+            f32x4{v[0], v[1], v[2], v[3]};
+    }
   __syncthreads();
+  const int base_id = blockIdx.x * 64 * NT;
   for (int r = wave; r < g.R; r += 4) {
-    const int id0 = blockIdx.x * 64 + lane;
-    const bool valid = id0 < g.V;
-    float v = valid ? sl[r][lane] : -INFINITY;
-    int id = valid ? id0 : 0x7fffffff;
-    const float mx = wave_max(v);
-    const float s = wave_sum(valid ? expf(v - mx) : 0.f);
+    float v[NT];
+    int id[NT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      const int c = n * 64 + lane;
+      id[n] = base_id + c;
+      const bool valid = id[n] < g.V;
+      v[n] = valid ? sl[r][c] : -INFINITY;
+      if (!valid) id[n] = 0x7fffffff;
+      mx = fmaxf(mx, v[n]);
+    }
+    mx = wave_max(mx);
+    float e = 0.f;
+#pragma unroll
+    for (int n = 0; n < NT; ++n) e += id[n] != 0x7fffffff ? expf(v[n] - mx) : 0.f;
+    const float s = wave_sum(e);
     const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
     if (lane == 0) {
       g.pmax[pi] = mx;
       g.psum[pi] = s;
     }
     for (int j = 0; j < g.topk; ++j) {
-      float bv = v;
-      int bid = id;
+      float bv = v[0];
+      int bid = id[0];
+#pragma unroll
+      for (int n = 1; n < NT; ++n)
+        if (better(v[n], id[n], bv, bid)) { bv = v[n]; bid = id[n]; }
       wave_argmax(bv, bid);
       if (lane == 0) {
         g.pval[pi * g.topk + j] = bv;
         g.pid[pi * g.topk + j] = bid;
       }
-      if (id == bid) { v = -INFINITY; id = 0x7fffffff; }
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+        if (id[n] == bid) { v[n] = -INFINITY; id[n] = 0x7fffffff; }
     }
   }
 }
 
-template <typename T, int EPI>
-static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
-  const int tpw = 4 / g.kw;
-  dim3 grid((g.m.n_tiles + tpw - 1) / tpw, g.splits);
-  if (g.R <= 16) hipLaunchKernelGGL((k_gemm<T, 1, EPI>), grid, dim3(256), 0, s, g);
-  else if (g.R <= 32) hipLaunchKernelGGL((k_gemm<T, 2, EPI>), grid, dim3(256), 0, s, g);
-  else hipLaunchKernelGGL((k_gemm<T, 4, EPI>), grid, dim3(256), 0, s, g);
+template <typename T, int RT, int NT, bool PAIR>
+static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
+  dim3 grid(g.m.n_tiles / NT);
+  const size_t lds = (size_t)((g.kw - 1) * NT * RT * 64) * sizeof(f32x4) +
+                     (size_t)64 * g.kw * sizeof(float);
+  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM>), grid, dim3(64 * g.kw), lds, s, g);
+  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU>), grid, dim3(64 * g.kw), lds, s, g);
+  else hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV>), grid, dim3(64 * g.kw), lds, s, g);
 }
 
-void launch_gemm(bool bf16, int epi, const GemmLaunch &g, hipStream_t s) {
-  if (bf16) {
-    if (epi == EPI_PARTIAL) gemm_rt<bf16_t, EPI_PARTIAL>(g, s);
-    else gemm_rt<bf16_t, EPI_SWIGLU>(g, s);
+template <typename T, bool PAIR>
+static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
+  if (g.nt == 2) {
+    if (g.R <= 16) gemm_epi<T, 1, 2, PAIR>(g, s);
+    else if (g.R <= 32) gemm_epi<T, 2, 2, PAIR>(g, s);
+    else gemm_epi<T, 4, 2, PAIR>(g, s);
   } else {
-    if (epi == EPI_PARTIAL) gemm_rt<float, EPI_PARTIAL>(g, s);
-    else gemm_rt<float, EPI_SWIGLU>(g, s);
+    if (g.R <= 16) gemm_epi<T, 1, 1, PAIR>(g, s);
+    else if (g.R <= 32) gemm_epi<T, 2, 1, PAIR>(g, s);
+    else gemm_epi<T, 4, 1, PAIR>(g, s);
   }
 }
 
-int lm_workgroups(int n_tiles) { return (n_tiles + 3) / 4; }
+void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s) {
+  if (bf16) gemm_rt<bf16_t, true>(g, s);
+  else gemm_rt<float, false>(g, s);
+}
 
-template <typename T>
+int lm_workgroups(int n_tiles, int nt) { return (n_tiles / nt + 3) / 4; }
+
+template <typename T, bool PAIR>
 static void lm_rt(const LmLaunch &g, hipStream_t s) {
-  dim3 grid(g.n_wg);
-  if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1>), grid, dim3(256), 0, s, g);
-  else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2>), grid, dim3(256), 0, s, g);
-  else hipLaunchKernelGGL((k_lmhead<T, 4>), grid, dim3(256), 0, s, g);
+  const dim3 grid(g.n_wg), blk(256);
+  if (g.nt == 2) {   // two tiles per wave once B fragments dominate operand traffic
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 2, PAIR>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 2, PAIR>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 2, PAIR>), grid, blk, 0, s, g);
+  } else {
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 1, PAIR>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 1, PAIR>), grid, blk, 0, s, g);
+  }
 }
 
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
-  if (bf16) lm_rt<bf16_t>(g, s);
-  else lm_rt<float>(g, s);
+  if (bf16) lm_rt<bf16_t, true>(g, s);
+  else lm_rt<float, false>(g, s);
 }
 
 // Repack a row-major [n_src_rows, K] matrix into the tiled layout: source row
 // i goes to destination row i*row_stride + row_offset (used to concatenate
-// q/k/v and to interleave gate/up).  One thread per 16-byte destination
-// fragment.
+// q/k/v and to interleave gate/up); destination rows below rot_rows belong to
+// rotated heads of size d and use the pair-aligned permutation.  One thread
+// per 16-byte destination fragment.
 template <typename T>
 __global__ void k_repack(const T *__restrict__ src, int n_src_rows, int K, int row_stride,
-                         int row_offset, u32x4 *__restrict__ dst, int n_tiles, int nkb) {
+                         int row_offset, int rot_rows, int d, u32x4 *__restrict__ dst, int n_tiles,
+                         int nkb) {
   constexpr int E = Ty<T>::E, KB = Ty<T>::KB;
   const size_t total = (size_t)n_tiles * nkb * 64;
   for (size_t f = (size_t)blockIdx.x * blockDim.x + threadIdx.x; f < total;
@@ -212,7 +456,13 @@ __global__ void k_repack(const T *__restrict__ src, int n_src_rows, int K, int r
     const size_t tj = f >> 6;
     const int j = (int)(tj % nkb);
     const int t = (int)(tj / nkb);
-    const int drow = t * 16 + (lane & 15);
+    const int i = lane & 15;
+    int drow = t * 16 + i;
+    if (drow < rot_rows) {
+      // tile jj of head h: rows 0..7 -> dims 8jj..8jj+7, rows 8..15 -> d/2 + 8jj..
+      const int h = (t * 16) / d, jj = ((t * 16) % d) / 16;
+      drow = h * d + (i < 8 ? 8 * jj + i : d / 2 + 8 * jj + (i - 8));
+    }
     const int rel = drow - row_offset;
     if (rel < 0 || rel % row_stride) continue;
     const int srow = rel / row_stride;
@@ -223,15 +473,17 @@ __global__ void k_repack(const T *__restrict__ src, int n_src_rows, int K, int r
 }
 
 void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_stride,
-                   int row_offset, TiledMat &dst, hipStream_t s) {
+                   int row_offset, int rot_rows, int d, TiledMat &dst, hipStream_t s) {
   const size_t total = (size_t)dst.n_tiles * dst.nkb * 64;
   const int blocks = (int)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
   if (bf16)
     hipLaunchKernelGGL(k_repack<bf16_t>, dim3(blocks), dim3(256), 0, s, (const bf16_t *)src,
-                       n_src_rows, K, row_stride, row_offset, (u32x4 *)dst.w, dst.n_tiles, dst.nkb);
+                       n_src_rows, K, row_stride, row_offset, rot_rows, d, (u32x4 *)dst.w,
+                       dst.n_tiles, dst.nkb);
   else
     hipLaunchKernelGGL(k_repack<float>, dim3(blocks), dim3(256), 0, s, (const float *)src,
-                       n_src_rows, K, row_stride, row_offset, (u32x4 *)dst.w, dst.n_tiles, dst.nkb);
+                       n_src_rows, K, row_stride, row_offset, rot_rows, d, (u32x4 *)dst.w,
+                       dst.n_tiles, dst.nkb);
 }
 
 }  // namespace prism

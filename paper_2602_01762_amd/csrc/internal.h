@@ -10,66 +10,52 @@ typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
 // device error flags (bit set by kernels on an out-of-range device value)
 enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u };
 
-// Tiled weight matrix W[N, K] (y = W x).  Tile t holds rows 16t..16t+15;
+constexpr int MAX_TOPK = 16;    // largest top-k of the LM-head merge
+constexpr int MAX_TREE_CAND = 2048;
+constexpr int MAX_ROWS = 64;
+constexpr int MAX_KW = 16;      // waves of one workgroup splitting K
+
+// Tiled weight matrix W[N, K] (y = W x).  Tile t holds 16 output rows;
 // k-block j holds KB consecutive k (KB = 32 for bf16, 16 for fp32).  The
 // 1 KiB of one (t, j) pair is laid out lane-major for a 64-lane wave: lane l
-// holds the 16 bytes W[16t + (l & 15)][KB*j + E*(l >> 4) + e], e < E
+// holds the 16 bytes W[row(t, l & 15)][KB*j + E*(l >> 4) + e], e < E
 // (E = 8 bf16 or 4 fp32), which is the A operand of the 16x16 MFMA.
+// row(t, i) = 16t + i, except for rotated (q, k) heads, whose tile j of a
+// head holds dims 8j..8j+7 in rows 0..7 and d/2+8j..d/2+8j+7 in rows 8..15,
+// so that the two halves of every rotation pair sit in lanes l and l ^ 32.
 struct TiledMat {
   void *w = nullptr;
   int N = 0, K = 0;
   int n_tiles = 0, nkb = 0;
 };
 
-enum Epi { EPI_PARTIAL = 0, EPI_SWIGLU = 1 };
-
-constexpr int MAX_TOPK = 16;    // largest top-k of the LM-head merge
-constexpr int MAX_TREE_CAND = 2048;
-constexpr int MAX_ROWS = 64;
-
-struct GemmLaunch {
-  TiledMat m;
-  const void *X;   // [R, ldx] activations in the storage dtype
-  int ldx;
-  int R;
-  int kw;          // waves of a workgroup splitting K for one tile (1, 2, 4)
-  int splits;      // workgroups splitting K for one tile (grid.y)
-  float *part;     // EPI_PARTIAL: [splits][R][N]
-  void *Z;         // EPI_SWIGLU: [R, ldz] storage dtype, N/2 outputs
-  int ldz;
+// An activation operand [R, ld] of a product.  fp32 models: `hi` is fp32
+// and `lo` is null.  bf16 models: the fp32 value x is carried as the pair
+// hi = bf16(x), lo = bf16(x - hi) (two planes), both fed to the MFMA, so the
+// product sees x to within 2^-17 relative.
+struct Act {
+  const void *hi = nullptr;
+  const void *lo = nullptr;
+  int ld = 0;
+};
+struct ActOut {
+  void *hi = nullptr;
+  void *lo = nullptr;
+  int ld = 0;
 };
 
-struct LmLaunch {
-  TiledMat m;
-  const void *X;
-  int ldx, R, V, topk;
-  float *logits; long ld_logits;   // optional fp32 [R, ld_logits]
-  float *pmax, *psum, *pval;       // partials [R][n_wg] / [R][n_wg][topk]
-  int *pid;
-  int n_wg;
+// Row norms: the producer of a vector x writes, per 16-feature tile t and
+// row r, ss[t * R + r] = sum of x^2 over the tile; a consumer that multiplies
+// by RMSNorm(x) * g takes x*g as its operand and scales row r of its result
+// by 1/sqrt(sum_t ss[t*R + r] / n + eps).
+struct RowNorm {
+  const float *ss = nullptr;     // partials, reduced by the consumer itself, or
+  const float *scale = nullptr;  // row scales already reduced (launch_rowscale)
+  int n_tiles = 0;
+  int n = 0;
+  float eps = 0.f;
 };
 
-// ---- launchers (gemm.hip) -------------------------------------------------
-void launch_gemm(bool bf16, int epi, const GemmLaunch &g, hipStream_t s);
-void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
-int lm_workgroups(int n_tiles);
-void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_stride,
-                   int row_offset, TiledMat &dst, hipStream_t s);
-
-// ---- launchers (misc.hip) -------------------------------------------------
-struct RowsIn {
-  const int32_t *tokens;
-  const void *feat; int feat_bf16; int feat_ld; const int32_t *feat_rows;
-  const int32_t *seq, *pos, *slot;
-  const uint64_t *bits;
-};
-
-void launch_fc_prep(bool bf16, int R, const RowsIn &in, const void *embed, int V, int H, int F,
-                    void *X, uint32_t *err, hipStream_t s);
-// sum split partials (+ residual) -> fp32 row (optional) and RMSNorm(row)*g -> storage dtype
-void launch_rowfin(bool bf16, int R, int N, const float *part, int splits, const float *res,
-                   int ldres, float *out, int ldout, const void *gain, void *normed, float eps,
-                   hipStream_t s);
 struct KvArgs {
   void *k_pool, *v_pool;
   const int32_t *block_table;
@@ -79,13 +65,72 @@ struct KvArgs {
   int n_blocks;    // pool blocks
   int n_seq;       // sequences described (valid values of a row's seq)
 };
-// sum QKV partials, RoPE q and k, write q (storage dtype) and k, v into the cache
-void launch_qkv_fin(bool bf16, int R, int nq, int nkv, int d, const float *part, int splits,
-                    const RowsIn &in, const KvArgs &kv, const double *inv_freq, void *q_out,
-                    uint32_t *err, hipStream_t s);
-void launch_attention(bool bf16, int R, int nq, int nkv, int d, const void *q, const RowsIn &in,
-                      const KvArgs &kv, int max_slots, int chunk, float *pm, float *pl, float *po,
-                      void *o_out, uint32_t *err, hipStream_t s);
+
+struct RowsIn {
+  const int32_t *tokens;
+  const void *feat; int feat_bf16; int feat_ld; const int32_t *feat_rows;
+  const int32_t *seq, *pos, *slot;
+  const uint64_t *bits;
+};
+
+enum Epi { EPI_NORM = 0, EPI_SWIGLU = 1, EPI_QKV = 2 };
+
+struct GemmLaunch {
+  TiledMat m;
+  Act x;
+  int R;
+  int kw;          // waves of the workgroup splitting K (1..16)
+  int nt;          // tiles per workgroup (1 or 2)
+  int epi;
+  RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_tiles = 0: none
+  // EPI_NORM: y = acc (+ res) -> y [R, ldy] fp32; (y * gain) -> g planes; ss
+  const float *res; int ldres;
+  float *y; int ldy;
+  const void *gain;
+  ActOut g;
+  float *ss;
+  // EPI_SWIGLU: interleaved gate/up rows -> z planes [R, N/2]
+  ActOut z;
+  // EPI_QKV: q (fp32 [R, nq*d]) and the cache slots of k, v
+  float *q;
+  int nq, nkv, d;
+  RowsIn rows;
+  KvArgs kv;
+  const double *inv_freq;
+  uint32_t *err;
+};
+
+struct LmLaunch {
+  TiledMat m;
+  Act x;
+  int R, V, topk;
+  RowNorm norm;
+  float *logits; long ld_logits;   // optional fp32 [R, ld_logits]
+  float *pmax, *psum, *pval;       // partials [R][n_wg] / [R][n_wg][topk]
+  int *pid;
+  int n_wg;
+  int nt;                          // vocab tiles per wave (1 or 2)
+};
+
+// ---- launchers (gemm.hip) -------------------------------------------------
+void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
+void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
+int lm_workgroups(int n_tiles, int nt);
+// largest number of partial entries (tiles x rows) a consumer reduces itself
+int own_scale_capacity(int threads);
+void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, float *scale,
+                     hipStream_t s);
+// rotated rows: the first rot_rows destination rows hold rotated heads of size d
+void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_stride,
+                   int row_offset, int rot_rows, int d, TiledMat &dst, hipStream_t s);
+
+// ---- launchers (misc.hip) -------------------------------------------------
+void launch_fc_prep(bool bf16, int R, const RowsIn &in, const void *embed, int V, int H, int F,
+                    ActOut X, uint32_t *err, hipStream_t s);
+void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
+                      const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
+                      ActOut o, uint32_t *err, hipStream_t s);
+int attention_chunks(int max_slots, int nsub);
 // merge LM-head partials: top-k ids, optional log-probs, and the chain's token copies
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,

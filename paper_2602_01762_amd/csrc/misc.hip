@@ -6,88 +6,88 @@
 namespace prism {
 
 // ---------------------------------------------------------------------------
-// X[r] = [E(token_r) ; feature row]  in the storage dtype.  A feature given in
-// fp32 (the draft's own hidden state) is rounded to the storage dtype, as the
-// FC consumes it as a matrix-product operand.
+// X[r] = [E(token_r) ; feature row] as the FC's operand planes.  Embeddings
+// and target features are exact in the storage type (lo = 0); a fp32 feature
+// (the draft's own hidden state) is split into its hi/lo pair.
 struct FcPrepArgs {
   RowsIn in;
   const void *embed;
   int V, H, F;
-  void *X;
+  ActOut X;
   uint32_t *err;
 };
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
-  const int r = blockIdx.x, tid = threadIdx.x;
-  const int ld = a.H + a.F;
-  T *x = (T *)a.X + (size_t)r * ld;
+  const int r = blockIdx.y;
+  const int e0 = (blockIdx.x * 256 + threadIdx.x) * 8;   // 8 consecutive columns
+  if (e0 >= a.H + a.F) return;
   int tok = a.in.tokens[r];
   if (tok < 0 || tok >= a.V) {
-    if (tid == 0) atomicOr(a.err, ERRF_TOKEN);
+    if (e0 == 0) atomicOr(a.err, ERRF_TOKEN);
     tok = -1;
   }
-  const T *e = (const T *)a.embed + (size_t)(tok < 0 ? 0 : tok) * a.H;
-  for (int i = tid; i < a.H; i += blockDim.x) x[i] = tok < 0 ? T(0) : e[i];
-  const int fr = a.in.feat_rows ? a.in.feat_rows[r] : r;
-  if (a.in.feat_bf16) {
-    const bf16_t *f = (const bf16_t *)a.in.feat + (size_t)fr * a.in.feat_ld;
-    for (int i = tid; i < a.F; i += blockDim.x) Ty<T>::st(x, a.H + i, bf2f(f[i]));
+  const size_t o = (size_t)r * a.X.ld + e0;
+  float v[8];
+  bool exact;   // value already representable in the storage type
+  if (e0 < a.H) {
+    exact = true;
+    const T *e = (const T *)a.embed + (size_t)(tok < 0 ? 0 : tok) * a.H + e0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = tok < 0 ? 0.f : Ty<T>::ld(e, i);
   } else {
-    const float *f = (const float *)a.in.feat + (size_t)fr * a.in.feat_ld;
-    for (int i = tid; i < a.F; i += blockDim.x) Ty<T>::st(x, a.H + i, f[i]);
+    const int fr = a.in.feat_rows ? a.in.feat_rows[r] : r;
+    const int c = e0 - a.H;
+    if (a.in.feat_bf16) {
+      exact = sizeof(T) == 2;
+      const bf16_t *f = (const bf16_t *)a.in.feat + (size_t)fr * a.in.feat_ld + c;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = bf2f(f[i]);
+    } else {
+      exact = sizeof(T) == 4;
+      const float *f = (const float *)a.in.feat + (size_t)fr * a.in.feat_ld + c;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = f[i];
+    }
+  }
+  if constexpr (sizeof(T) == 2) {
+    bf16_t *hi = (bf16_t *)a.X.hi + o, *lo = (bf16_t *)a.X.lo + o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t h = f2bf(v[i]);
+      hi[i] = (bf16_t)h;
+      lo[i] = exact ? (bf16_t)0 : (bf16_t)f2bf(v[i] - bf2f(h));
+    }
+  } else {
+    float *hi = (float *)a.X.hi + o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) hi[i] = v[i];
   }
 }
 
 void launch_fc_prep(bool bf16, int R, const RowsIn &in, const void *embed, int V, int H, int F,
-                    void *X, uint32_t *err, hipStream_t s) {
+                    ActOut X, uint32_t *err, hipStream_t s) {
   FcPrepArgs a{in, embed, V, H, F, X, err};
-  if (bf16) hipLaunchKernelGGL(k_fc_prep<bf16_t>, dim3(R), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_fc_prep<float>, dim3(R), dim3(256), 0, s, a);
+  dim3 grid((H + F + 2047) / 2048, R);
+  if (bf16) hipLaunchKernelGGL(k_fc_prep<bf16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_fc_prep<float>, grid, dim3(256), 0, s, a);
 }
 
 // ---------------------------------------------------------------------------
-// v = sum_s part[s][r] (+ res[r]);  out[r] = v (fp32, optional);
-// normed[r] = v / sqrt(mean(v^2) + eps) * g  (storage dtype, optional)
-struct RowFinArgs {
-  const float *part;
-  int splits, R, N;
-  const float *res; int ldres;
-  float *out; int ldout;
-  const void *gain;
-  void *normed;
-  float eps;
-};
-
-template <typename T>
-__global__ __launch_bounds__(256) void k_rowfin(RowFinArgs a) {
-  extern __shared__ float row[];
-  __shared__ float red[8];
-  const int r = blockIdx.x, tid = threadIdx.x;
-  float ss = 0.f;
-  for (int n = tid; n < a.N; n += blockDim.x) {
-    float v = 0.f;
-    for (int sp = 0; sp < a.splits; ++sp) v += a.part[((size_t)sp * a.R + r) * a.N + n];
-    if (a.res) v += a.res[(size_t)r * a.ldres + n];
-    row[n] = v;
-    if (a.out) a.out[(size_t)r * a.ldout + n] = v;
-    ss += v * v;
-  }
-  if (!a.normed) return;
-  const float tot = block_sum(ss, red);
-  const float scale = 1.0f / sqrtf(tot / (float)a.N + a.eps);
-  const T *g = (const T *)a.gain;
-  for (int n = tid; n < a.N; n += blockDim.x)
-    Ty<T>::st((T *)a.normed, (size_t)r * a.N + n, row[n] * scale * Ty<T>::ld(g, n));
+// Row scales for batched consumers: scale[r] = 1/sqrt(sum_t ss[t*R + r]/n + eps)
+__global__ __launch_bounds__(256) void k_rowscale(int R, const float *ss, int n_tiles, int n,
+                                                  float eps, float *scale) {
+  __shared__ float sh[8];
+  const int r = blockIdx.x;
+  float acc = 0.f;
+  for (int t = threadIdx.x; t < n_tiles; t += blockDim.x) acc += ss[(size_t)t * R + r];
+  const float tot = block_sum(acc, sh);
+  if (threadIdx.x == 0) scale[r] = 1.0f / sqrtf(tot / (float)n + eps);
 }
 
-void launch_rowfin(bool bf16, int R, int N, const float *part, int splits, const float *res,
-                   int ldres, float *out, int ldout, const void *gain, void *normed, float eps,
-                   hipStream_t s) {
-  RowFinArgs a{part, splits, R, N, res, ldres, out, ldout, gain, normed, eps};
-  const size_t lds = (size_t)N * sizeof(float);
-  if (bf16) hipLaunchKernelGGL(k_rowfin<bf16_t>, dim3(R), dim3(256), lds, s, a);
-  else hipLaunchKernelGGL(k_rowfin<float>, dim3(R), dim3(256), lds, s, a);
+void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, float *scale,
+                     hipStream_t s) {
+  hipLaunchKernelGGL(k_rowscale, dim3(R), dim3(256), 0, s, R, ss, n_tiles, n, eps, scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -95,6 +95,7 @@ void launch_rowfin(bool bf16, int R, int N, const float *part, int splits, const
 //   lse = M + log(sum_i s_i exp(m_i - M)),  top-k by (logit desc, id asc),
 //   log-prob = logit - lse.
 constexpr int MAXK = MAX_TOPK;
+constexpr int CMB_UNROLL = 8;
 struct LmCombArgs {
   int R, n_wg, topk, V;
   const float *pmax, *psum, *pval;
@@ -111,12 +112,29 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   const int r = blockIdx.x, tid = threadIdx.x;
   const float *pm = a.pmax + (size_t)r * a.n_wg;
   const float *ps = a.psum + (size_t)r * a.n_wg;
-  float m = -INFINITY;
-  for (int i = tid; i < a.n_wg; i += blockDim.x) m = fmaxf(m, pm[i]);
+  float m = -INFINITY, s = 0.f;
+  for (int i0 = 0; i0 < a.n_wg; i0 += 256 * CMB_UNROLL) {
+    float vm[CMB_UNROLL], vs[CMB_UNROLL];
+#pragma unroll
+    for (int u = 0; u < CMB_UNROLL; ++u) {
+      const int i = i0 + u * 256 + tid;
+      vm[u] = i < a.n_wg ? pm[i] : -INFINITY;
+      vs[u] = i < a.n_wg ? ps[i] : 0.f;
+    }
+    // online merge of this thread's partials, in index order
+#pragma unroll
+    for (int u = 0; u < CMB_UNROLL; ++u) {
+      if (vm[u] == -INFINITY) continue;
+      if (vm[u] > m) {
+        s = s * expf(m - vm[u]) + vs[u];
+        m = vm[u];
+      } else {
+        s += vs[u] * expf(vm[u] - m);
+      }
+    }
+  }
   const float M = block_max(m, shv);
-  float s = 0.f;
-  for (int i = tid; i < a.n_wg; i += blockDim.x) s += ps[i] * expf(pm[i] - M);
-  const float S = block_sum(s, shv);
+  const float S = block_sum(m == -INFINITY ? 0.f : s * expf(m - M), shv);
   const float lse = M + logf(S);
 
   const int k = a.topk;
@@ -127,18 +145,29 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   float lv[MAXK];
   int li[MAXK];
   for (int j = 0; j < MAXK; ++j) { lv[j] = -INFINITY; li[j] = 0x7fffffff; }
-  for (int i = tid; i < nc; i += blockDim.x) {
-    float v = pv[i];
-    int id = pi[i];
-    if (!better(v, id, lv[k - 1], li[k - 1])) continue;
-    int j = k - 1;
-    while (j > 0 && better(v, id, lv[j - 1], li[j - 1])) {
-      lv[j] = lv[j - 1];
-      li[j] = li[j - 1];
-      --j;
+  for (int i0 = 0; i0 < nc; i0 += 256 * CMB_UNROLL) {
+    float cv[CMB_UNROLL];
+    int ci[CMB_UNROLL];
+#pragma unroll
+    for (int u = 0; u < CMB_UNROLL; ++u) {
+      const int i = i0 + u * 256 + tid;
+      cv[u] = i < nc ? pv[i] : -INFINITY;
+      ci[u] = i < nc ? pi[i] : 0x7fffffff;
     }
-    lv[j] = v;
-    li[j] = id;
+#pragma unroll
+    for (int u = 0; u < CMB_UNROLL; ++u) {
+      const float v = cv[u];
+      const int id = ci[u];
+      if (!better(v, id, lv[k - 1], li[k - 1])) continue;
+      int j = k - 1;
+      while (j > 0 && better(v, id, lv[j - 1], li[j - 1])) {
+        lv[j] = lv[j - 1];
+        li[j] = li[j - 1];
+        --j;
+      }
+      lv[j] = v;
+      li[j] = id;
+    }
   }
   int head = 0;
   for (int j = 0; j < k; ++j) {

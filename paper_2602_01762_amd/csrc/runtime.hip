@@ -27,7 +27,7 @@ struct Set {
 };
 
 struct Plan {
-  int kw = 1, splits = 1;
+  int kw = 1, nt = 1;
 };
 
 struct Pass {            // one forward pass: where its inputs and outputs live
@@ -60,10 +60,16 @@ struct prism_ctx {
 
   // workspace
   void *ws = nullptr;
-  void *X = nullptr, *a = nullptr, *q = nullptr, *o = nullptr, *m = nullptr, *z = nullptr,
-       *nrm = nullptr;
-  float *part = nullptr, *u = nullptr, *r1 = nullptr, *hid[2] = {nullptr, nullptr};
-  float *pm = nullptr, *pl = nullptr, *po = nullptr;
+  ActOut xfc;                       // FC operand planes [R, H + feat_max]
+  float *u = nullptr, *r1 = nullptr;  // residual stream rows [R, H]
+  ActOut ug, r1g, hg;               // (x * gain) operand planes [R, H]
+  float *ss_u = nullptr, *ss_r1 = nullptr, *ss_h = nullptr;  // [H/16][R]
+  float *sc_u = nullptr, *sc_r1 = nullptr, *sc_h = nullptr;  // row scales [R]
+  float *q = nullptr;               // [R, nq*d] fp32
+  float *pm = nullptr, *pl = nullptr, *po = nullptr;         // attention partials
+  ActOut o;                         // attention output planes [R, nq*d]
+  ActOut z;                         // SwiGLU planes [R, I]
+  float *hid[2] = {nullptr, nullptr};
   float *lm_max = nullptr, *lm_sum = nullptr, *lm_val = nullptr, *logp = nullptr;
   int *lm_id = nullptr, *ids = nullptr, *tokbuf = nullptr;
   int32_t *c_seq = nullptr, *c_pos = nullptr, *c_tok0 = nullptr;
@@ -71,6 +77,7 @@ struct prism_ctx {
   float *t_cscore = nullptr;
   int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
   uint64_t *t_bits[2] = {nullptr, nullptr};
+  int nsub = 1;                     // attention: 64-slot steps per workgroup
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
 
@@ -81,7 +88,6 @@ struct prism_ctx {
   std::vector<hipEvent_t> prof_ev;
   int prof_used = 0;        // pairs recorded by the enqueue in progress
   int prof_last = 0;        // pairs of the last chain/tree call
-  std::map<std::vector<uintptr_t>, int> prof_pairs;
   std::map<std::vector<uintptr_t>, hipGraphExec_t> graphs;
   std::string msg;
 };
@@ -115,17 +121,22 @@ static TiledMat make_tiled(int N, int K, bool bf16) {
 }
 static size_t tiled_bytes(const TiledMat &t) { return (size_t)t.n_tiles * t.nkb * 1024; }
 
-// K-split plan for a streamed product: enough waves to cover HBM latency,
-// at least 8 k-blocks (8 KiB of W) per wave.
-static Plan plan_for(const TiledMat &t, bool allow_split) {
-  const int target_waves = 4096;
-  int slices = (target_waves + t.n_tiles - 1) / t.n_tiles;
-  const int cap = t.nkb / 8 > 0 ? t.nkb / 8 : 1;
-  if (slices > cap) slices = cap;
-  if (slices < 1) slices = 1;
+// Launch plan of a streamed product: enough waves to cover HBM latency
+// (about 16 per CU), at least 4 k-blocks (4 KiB of W) per wave, and two tiles
+// per wave once batched rows make the B fragments the larger operand stream.
+static Plan plan_for(const TiledMat &t, int R) {
   Plan p;
-  p.kw = slices >= 4 ? 4 : (slices >= 2 ? 2 : 1);
-  p.splits = allow_split ? (slices / p.kw > 0 ? slices / p.kw : 1) : 1;
+  const int rt = R <= 16 ? 1 : (R <= 32 ? 2 : 4);
+  if (R > 16 && t.n_tiles % 2 == 0 && t.n_tiles >= 1024) p.nt = 2;
+  const int groups = t.n_tiles / p.nt;
+  int kw = (4096 + groups - 1) / groups;
+  const int max_kw = rt * p.nt >= 2 ? MAX_KW / 2 : MAX_KW;   // see gemm_max_threads
+  if (kw > max_kw) kw = max_kw;
+  if (kw > t.nkb / 4) kw = t.nkb / 4;
+  if (kw < 1) kw = 1;
+  // LDS for the cross-wave sum: (kw - 1) * nt * rt KiB
+  while (kw > 1 && (kw - 1) * p.nt * rt > 48) --kw;
+  p.kw = kw;
   return p;
 }
 
@@ -157,7 +168,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   const int kq = bf16 ? 32 : 16;
   if (k.n_q_heads % k.n_kv_heads) return fail(nullptr, PRISM_ERR_SHAPE, "n_q_heads %% n_kv_heads != 0");
   if (k.n_q_heads / k.n_kv_heads > 8) return fail(nullptr, PRISM_ERR_SHAPE, "more than 8 query heads per KV head");
-  if (k.head_dim % 8 || k.head_dim < 8 || k.head_dim > 256) return fail(nullptr, PRISM_ERR_SHAPE, "head_dim %d", k.head_dim);
+  if (k.head_dim < 32 || k.head_dim > 256 || (k.head_dim & (k.head_dim - 1)))
+    return fail(nullptr, PRISM_ERR_SHAPE, "head_dim %d must be a power of two in 32..256", k.head_dim);
+  if ((k.n_q_heads / k.n_kv_heads) * k.head_dim > 1024)
+    return fail(nullptr, PRISM_ERR_SHAPE, "query heads per KV head x head_dim > 1024");
   if (k.hidden % kq || k.ffn % kq || (k.n_q_heads * k.head_dim) % kq || k.feat_width % kq)
     return fail(nullptr, PRISM_ERR_SHAPE, "H, I, n_q*d and F_t must be multiples of %d", kq);
   if (k.vocab % 16) return fail(nullptr, PRISM_ERR_SHAPE, "vocab must be a multiple of 16");
@@ -188,7 +202,11 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
   c->rows_max = rows;
   c->max_slots = k.max_blocks_per_seq * k.kv_block_size;
-  c->nch = (c->max_slots + 255) / 256;
+  // attention steps per workgroup: keep the grid near 8K workgroups
+  c->nsub = 1;
+  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 8192)
+    c->nsub *= 2;
+  c->nch = attention_chunks(c->max_slots, c->nsub);
   c->kmax = w > 1 ? w : 1;
   c->Cmax = Cmax;
   c->feat_max = k.feat_width > k.hidden ? k.feat_width : k.hidden;
@@ -196,42 +214,38 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->fmap.resize(k.max_steps);
   for (int i = 0; i < k.max_steps; ++i) c->fmap[i] = i < k.n_sets ? i : k.n_sets - 1;
   c->lm = make_tiled(c->V, c->H, bf16);
-  c->n_wg_lm = lm_workgroups(c->lm.n_tiles);
+  c->n_wg_lm = lm_workgroups(c->lm.n_tiles, 1);
   if (const char *e = getenv("PRISM_NO_GRAPH")) c->use_graph = !(e[0] == '1');
-
-  // split-K partial buffer: the largest splits x N of a streamed product
-  size_t part_n = 0;
-  auto upd = [&](int N, int K) {
-    TiledMat t = make_tiled(N, K, bf16);
-    Plan p = plan_for(t, true);
-    size_t v = (size_t)p.splits * N;
-    if (v > part_n) part_n = v;
-  };
-  upd(c->H, c->H + k.feat_width);
-  upd(c->H, 2 * c->H);
-  upd(c->QKV, c->H);
-  upd(c->H, c->nq * c->d);
-  upd(c->H, c->I);
 
   const size_t R = rows, es = c->esz;
   size_t total = 0;
   std::vector<std::pair<void **, size_t>> L;
   auto add = [&](void **p, size_t b) { L.push_back({p, b}); total += (b + 255) & ~(size_t)255; };
-  add(&c->X, R * (c->H + c->feat_max) * es);
-  add((void **)&c->part, R * part_n * 4);
+  auto planes = [&](ActOut &a, size_t n) {   // hi (and lo for bf16) planes of n values
+    add(&a.hi, n * es);
+    if (bf16) add(&a.lo, n * es);
+  };
+  const size_t nth = (size_t)c->H / 16;
+  planes(c->xfc, R * (c->H + c->feat_max));
   add((void **)&c->u, R * c->H * 4);
-  add(&c->a, R * c->H * es);
-  add(&c->q, R * c->nq * c->d * es);
+  add((void **)&c->r1, R * c->H * 4);
+  planes(c->ug, R * c->H);
+  planes(c->r1g, R * c->H);
+  planes(c->hg, R * c->H);
+  add((void **)&c->ss_u, nth * R * 4);
+  add((void **)&c->ss_r1, nth * R * 4);
+  add((void **)&c->ss_h, nth * R * 4);
+  add((void **)&c->sc_u, R * 4);
+  add((void **)&c->sc_r1, R * 4);
+  add((void **)&c->sc_h, R * 4);
+  add((void **)&c->q, R * c->nq * c->d * 4);
   add((void **)&c->pm, R * c->nq * c->nch * 4);
   add((void **)&c->pl, R * c->nq * c->nch * 4);
   add((void **)&c->po, R * c->nq * c->nch * c->d * 4);
-  add(&c->o, R * c->nq * c->d * es);
-  add((void **)&c->r1, R * c->H * 4);
-  add(&c->m, R * c->H * es);
-  add(&c->z, R * c->I * es);
+  planes(c->o, R * c->nq * c->d);
+  planes(c->z, R * c->I);
   add((void **)&c->hid[0], R * c->H * 4);
   add((void **)&c->hid[1], R * c->H * 4);
-  add(&c->nrm, R * c->H * es);
   add((void **)&c->lm_max, R * c->n_wg_lm * 4);
   add((void **)&c->lm_sum, R * c->n_wg_lm * 4);
   add((void **)&c->lm_val, R * c->n_wg_lm * c->kmax * 4);
@@ -279,7 +293,6 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
 static void drop_graphs(prism_ctx *c) {
   for (auto &g : c->graphs) (void)hipGraphExecDestroy(g.second);
   c->graphs.clear();
-  c->prof_pairs.clear();
 }
 
 void prism_destroy(prism_ctx *c) {
@@ -314,7 +327,7 @@ prism_status prism_draft_load_shared(prism_ctx *c, const void *d_embed, const vo
     c->gf = p;
   }
   HIPCHK(c, hipMemcpyAsync(c->embed, d_embed, eb, hipMemcpyDeviceToDevice, s));
-  launch_repack(c->bf16, d_lm_head, c->V, c->H, 1, 0, c->lm, s);
+  launch_repack(c->bf16, d_lm_head, c->V, c->H, 1, 0, 0, c->d, c->lm, s);
   HIPCHK(c, hipGetLastError());
   HIPCHK(c, hipMemcpyAsync(c->gf, d_final_norm, (size_t)c->H * c->esz, hipMemcpyDeviceToDevice, s));
   HIPCHK(c, hipStreamSynchronize(s));
@@ -367,17 +380,18 @@ prism_status prism_draft_load_params(prism_ctx *c, int32_t set, const prism_para
     S.F = F;
   }
   S.loaded = false;
-  launch_repack(c->bf16, P->d_w_fc, H, H + F, 1, 0, S.fc, s);
-  // q, k, v rows stacked into one product
+  launch_repack(c->bf16, P->d_w_fc, H, H + F, 1, 0, 0, c->d, S.fc, s);
+  // q, k, v rows stacked into one product; q and k heads pair-permuted for RoPE
   TiledMat qv = S.qkv;
-  launch_repack(c->bf16, P->d_w_q, c->nq * c->d, H, 1, 0, qv, s);
-  launch_repack(c->bf16, P->d_w_k, c->nkv * c->d, H, 1, c->nq * c->d, qv, s);
-  launch_repack(c->bf16, P->d_w_v, c->nkv * c->d, H, 1, (c->nq + c->nkv) * c->d, qv, s);
-  launch_repack(c->bf16, P->d_w_o, H, c->nq * c->d, 1, 0, S.o, s);
+  const int rot = (c->nq + c->nkv) * c->d;
+  launch_repack(c->bf16, P->d_w_q, c->nq * c->d, H, 1, 0, rot, c->d, qv, s);
+  launch_repack(c->bf16, P->d_w_k, c->nkv * c->d, H, 1, c->nq * c->d, rot, c->d, qv, s);
+  launch_repack(c->bf16, P->d_w_v, c->nkv * c->d, H, 1, rot, rot, c->d, qv, s);
+  launch_repack(c->bf16, P->d_w_o, H, c->nq * c->d, 1, 0, 0, c->d, S.o, s);
   // gate/up interleaved row by row: gate c -> 2c, up c -> 2c + 1
-  launch_repack(c->bf16, P->d_w_gate, c->I, H, 2, 0, S.gu, s);
-  launch_repack(c->bf16, P->d_w_up, c->I, H, 2, 1, S.gu, s);
-  launch_repack(c->bf16, P->d_w_down, H, c->I, 1, 0, S.down, s);
+  launch_repack(c->bf16, P->d_w_gate, c->I, H, 2, 0, 0, c->d, S.gu, s);
+  launch_repack(c->bf16, P->d_w_up, c->I, H, 2, 1, 0, c->d, S.gu, s);
+  launch_repack(c->bf16, P->d_w_down, H, c->I, 1, 0, 0, c->d, S.down, s);
   HIPCHK(c, hipGetLastError());
   HIPCHK(c, hipMemcpyAsync(S.g1, P->d_g1, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
   HIPCHK(c, hipMemcpyAsync(S.g2, P->d_g2, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
@@ -414,48 +428,98 @@ static KvArgs kv_of(const prism_ctx *c, const prism_batch *b) {
   return kv;
 }
 
+static Act act_of(const ActOut &o, int ld) {
+  Act a;
+  a.hi = o.hi;
+  a.lo = o.lo;
+  a.ld = ld;
+  return a;
+}
+
+// RMSNorm row scales for a consumer: reduced by the consumer itself when
+// its threads can hold all partials, else by a small kernel first.
+static RowNorm norm_for(prism_ctx *c, const float *ss, float *scale, int R, int threads,
+                        hipStream_t s) {
+  RowNorm n;
+  n.n_tiles = c->H / 16;
+  n.n = c->H;
+  n.eps = c->cfg.rms_eps;
+  if (n.n_tiles * R <= own_scale_capacity(threads)) {
+    n.ss = ss;
+  } else {
+    launch_rowscale(R, ss, n.n_tiles, c->H, n.eps, scale, s);
+    n.scale = scale;
+  }
+  return n;
+}
+
+static GemmLaunch gemm_of(const TiledMat &m, const Act &x, int R, int epi) {
+  GemmLaunch g{};
+  g.m = m;
+  g.x = x;
+  g.R = R;
+  g.epi = epi;
+  Plan pl = plan_for(m, R);
+  g.kw = pl.kw;
+  g.nt = pl.nt;
+  return g;
+}
+
 static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
   const Set &S = c->sets[p.set];
   const bool bf = c->bf16;
   const int R = p.R, H = c->H;
-  const float eps = c->cfg.rms_eps;
-  auto gemm_partial = [&](const TiledMat &m, const void *X, int ldx) {
-    Plan pl = plan_for(m, true);
-    GemmLaunch g{m, X, ldx, R, pl.kw, pl.splits, c->part, nullptr, 0};
-    launch_gemm(bf, EPI_PARTIAL, g, s);
-    return pl.splits;
-  };
-  // fusion FC: u = W_fc [E(x) ; f];  a = RMSNorm(u; g1)
-  launch_fc_prep(bf, R, p.in, c->embed, c->V, H, p.F, c->X, c->err, s);
-  int sp = gemm_partial(S.fc, c->X, H + p.F);
-  launch_rowfin(bf, R, H, c->part, sp, nullptr, 0, c->u, H, S.g1, c->a, eps, s);
-  // q, k, v; RoPE; cache append
-  sp = gemm_partial(S.qkv, c->a, H);
-  launch_qkv_fin(bf, R, c->nq, c->nkv, c->d, c->part, sp, p.in, kv, c->inv_freq, c->q, c->err, s);
-  // attention over the visible slots
-  launch_attention(bf, R, c->nq, c->nkv, c->d, c->q, p.in, kv, c->max_slots, 256, c->pm, c->pl,
-                   c->po, c->o, c->err, s);
-  // r1 = u + W_o o;  m = RMSNorm(r1; g2)
-  sp = gemm_partial(S.o, c->o, c->nq * c->d);
-  launch_rowfin(bf, R, H, c->part, sp, c->u, H, c->r1, H, S.g2, c->m, eps, s);
-  // z = SiLU(W_gate m) * (W_up m)
-  {
-    Plan pl = plan_for(S.gu, false);
-    GemmLaunch g{S.gu, c->m, H, R, pl.kw, 1, nullptr, c->z, c->I};
-    launch_gemm(bf, EPI_SWIGLU, g, s);
-  }
-  // h = r1 + W_down z;  n = RMSNorm(h; g_final)
-  sp = gemm_partial(S.down, c->z, c->I);
-  launch_rowfin(bf, R, H, c->part, sp, c->r1, H, p.hid_out, p.ld_hid, c->gf, c->nrm, eps, s);
-  // LM head + top-k
-  LmLaunch lmg{c->lm, c->nrm, H, R, c->V, p.topk, p.logits, p.ld_logits,
-               c->lm_max, c->lm_sum, c->lm_val, c->lm_id, c->n_wg_lm};
+  // fusion FC: u = W_fc [E(x) ; f]  ->  u, (u * g1), sums of squares
+  ActOut X = c->xfc;
+  X.ld = H + p.F;
+  launch_fc_prep(bf, R, p.in, c->embed, c->V, H, p.F, X, c->err, s);
+  GemmLaunch g = gemm_of(S.fc, act_of(X, H + p.F), R, EPI_NORM);
+  g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
+  launch_gemm(bf, g, s);
+  // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
+  g = gemm_of(S.qkv, act_of(c->ug, H), R, EPI_QKV);
+  g.norm = norm_for(c, c->ss_u, c->sc_u, R, 64 * g.kw, s);
+  g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
+  g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
+  launch_gemm(bf, g, s);
+  // attention over the visible slots -> o
+  ActOut o = c->o;
+  o.ld = c->nq * c->d;
+  launch_attention(bf, R, c->nq, c->nkv, c->d, c->q, p.in, kv, c->max_slots, c->nsub, c->pm,
+                   c->pl, c->po, o, c->err, s);
+  // r1 = u + W_o o  ->  r1, (r1 * g2), sums of squares
+  g = gemm_of(S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
+  g.res = c->u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
+  g.ss = c->ss_r1;
+  launch_gemm(bf, g, s);
+  // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
+  g = gemm_of(S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
+  g.norm = norm_for(c, c->ss_r1, c->sc_r1, R, 64 * g.kw, s);
+  g.z = c->z; g.z.ld = c->I;
+  launch_gemm(bf, g, s);
+  // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
+  g = gemm_of(S.down, act_of(c->z, c->I), R, EPI_NORM);
+  g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
+  g.g.ld = H; g.ss = c->ss_h;
+  launch_gemm(bf, g, s);
+  // logits = LM_head RMSNorm(h; g_final)  ->  top-k partials
+  LmLaunch lmg{};
+  lmg.m = c->lm;
+  lmg.x = act_of(c->hg, H);
+  lmg.R = R;
+  lmg.V = c->V;
+  lmg.topk = p.topk;
+  lmg.nt = (R > 16 && c->lm.n_tiles % 2 == 0) ? 2 : 1;
+  lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);
+  lmg.norm = norm_for(c, c->ss_h, c->sc_h, R, 256, s);
+  lmg.logits = p.logits;
+  lmg.ld_logits = p.ld_logits;
+  lmg.pmax = c->lm_max; lmg.psum = c->lm_sum; lmg.pval = c->lm_val; lmg.pid = c->lm_id;
   const bool prof = c->profile && c->prof_used * 2 + 1 < (int)c->prof_ev.size();
-  const unsigned evf = c->use_graph ? hipEventRecordExternal : hipEventRecordDefault;
-  if (prof) (void)hipEventRecordWithFlags(c->prof_ev[2 * c->prof_used], s, evf);
+  if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
   launch_lmhead(bf, lmg, s);
-  if (prof) (void)hipEventRecordWithFlags(c->prof_ev[2 * c->prof_used++ + 1], s, evf);
-  launch_lm_combine(R, c->n_wg_lm, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
+  if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used++ + 1], s);
+  launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
                     p.logp, p.tok_a, p.tok_b, p.ld_b, s);
 }
 
@@ -485,10 +549,10 @@ static prism_status check_batch(prism_ctx *c, const prism_batch *b) {
 
 // run `enqueue` directly or through a cached graph keyed by `key`
 template <typename F>
-static prism_status run_graph(prism_ctx *c, std::vector<uintptr_t> key, hipStream_t s,
+static prism_status run_graph(prism_ctx *c, const std::vector<uintptr_t> &key, hipStream_t s,
                               F enqueue) {
-  key.push_back(c->profile ? 1 : 0);
-  if (!c->use_graph) {
+  // profiled calls run eagerly: event pairs bracket each LM-head launch on `s`
+  if (!c->use_graph || c->profile) {
     c->prof_used = 0;
     enqueue(s);
     c->prof_last = c->prof_used;
@@ -511,10 +575,8 @@ static prism_status run_graph(prism_ctx *c, std::vector<uintptr_t> key, hipStrea
     (void)hipGraphDestroy(graph);
     if (ie != hipSuccess) return fail(c, PRISM_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
     it = c->graphs.emplace(key, exec).first;
-    c->prof_pairs[key] = c->prof_last;
   }
   HIPCHK(c, hipGraphLaunch(it->second, s));
-  c->prof_last = c->prof_pairs[key];   // a replay records the pairs its capture did
   return PRISM_OK;
 }
 
