@@ -18,6 +18,8 @@ namespace prism {
 constexpr int ATT_S = 64;        // slots per step
 constexpr int ATT_MAXG = 8;      // query heads per KV head
 constexpr int ATT_MAXGD = 1024;  // g * d
+constexpr int ATT_MAXVS = 8;     // slots per thread in P.V: 64 / (256 / (d / 8)) for d <= 256
+constexpr int ATT_MAXCH = 1024;  // chunks per row merged by the combine kernel
 
 struct AttnArgs {
   const float *q;             // [R, nq*d] fp32, RoPE applied
@@ -118,6 +120,20 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       offs[tid] = off;
     }
     __syncthreads();
+    // V rows of this thread's slots, fetched together with the K rows
+    u32x4 vraw[ATT_MAXVS][sizeof(T) == 2 ? 1 : 2];
+    if (tg < G) {
+#pragma unroll
+      for (int i = 0; i < ATT_MAXVS; ++i) {
+        const int ts = tg + i * G;
+        const long off = ts < n_here ? offs[ts] : -1;
+        if (off >= 0) {
+          const u32x4 *vp = (const u32x4 *)((const T *)a.kv.v_pool + off + dg * 8);
+          vraw[i][0] = vp[0];
+          if (sizeof(T) == 4) vraw[i][sizeof(T) == 2 ? 0 : 1] = vp[1];
+        }
+      }
+    }
     // scores: 4 threads per slot, d/4 dims each
     {
       const int ts = tid >> 2, part = tid & 3;
@@ -177,11 +193,25 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
         for (int i = 0; i < 8; ++i) acc[h][i] *= al;
       }
     if (tg < G) {
-      for (int ts = tg; ts < n_here; ts += G) {
-        const long off = offs[ts];
-        if (off < 0) continue;
+#pragma unroll
+      for (int vi = 0; vi < ATT_MAXVS; ++vi) {
+        const int ts = tg + vi * G;
+        if (ts >= n_here || offs[ts] < 0) continue;
         float vv[8];
-        load8<T>((const T *)a.kv.v_pool + off + dg * 8, vv);
+        if constexpr (sizeof(T) == 2) {
+          const uint32_t w4[4] = {vraw[vi][0].x, vraw[vi][0].y, vraw[vi][0].z, vraw[vi][0].w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            vv[2 * i] = __uint_as_float(w4[i] << 16);
+            vv[2 * i + 1] = __uint_as_float(w4[i] & 0xffff0000u);
+          }
+        } else {
+          const u32x4 x0 = vraw[vi][0], x1 = vraw[vi][sizeof(T) == 2 ? 0 : 1];
+          vv[0] = __uint_as_float(x0.x); vv[1] = __uint_as_float(x0.y);
+          vv[2] = __uint_as_float(x0.z); vv[3] = __uint_as_float(x0.w);
+          vv[4] = __uint_as_float(x1.x); vv[5] = __uint_as_float(x1.y);
+          vv[6] = __uint_as_float(x1.z); vv[7] = __uint_as_float(x1.w);
+        }
 #pragma unroll
         for (int h = 0; h < ATT_MAXG; ++h)
           if (h < g) {
@@ -223,28 +253,51 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 }
 
 template <typename T>
-__global__ void k_attn_combine(AttnArgs a) {
-  const int h = blockIdx.x, r = blockIdx.y, dim = threadIdx.x;
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  __shared__ float wch[ATT_MAXCH];
+  __shared__ float red[256];
+  __shared__ float sh[8];
+  const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
   int b, L, prefix, total;
   uint64_t bits;
   row_range(a, r, b, L, prefix, total, bits);
   const int span = ATT_S * a.nsub;
-  if (total > a.nch * span && h == 0 && dim == 0) atomicOr(a.err, ERRF_CAPACITY);
+  if (total > a.nch * span && h == 0 && tid == 0) atomicOr(a.err, ERRF_CAPACITY);
   const int nch = min((total + span - 1) / span, a.nch);
   const size_t base = ((size_t)r * a.nq + h) * a.nch;
-  float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, a.pm[base + c]);
-  float lsum = 0.f, o = 0.f;
-  for (int c = 0; c < nch; ++c) {
+  // chunk weights exp(m_c - M) and the total sum, in fixed order
+  float m = -INFINITY;
+  for (int c = tid; c < nch; c += 256)
+    if (a.pl[base + c] > 0.f) m = fmaxf(m, a.pm[base + c]);
+  const float M = block_max(m, sh);
+  float lp = 0.f;
+  for (int c = tid; c < nch; c += 256) {
     const float l = a.pl[base + c];
-    if (l == 0.f) continue;
-    const float w = expf(a.pm[base + c] - M);
-    lsum += l * w;
-    if (dim < a.d) o += a.po[(base + c) * a.d + dim] * w;
+    const float w = l > 0.f ? expf(a.pm[base + c] - M) : 0.f;
+    wch[c] = w;
+    lp += l * w;
   }
-  if (dim >= a.d) return;
-  const float v = lsum > 0.f ? o / lsum : 0.f;
-  const size_t i = (size_t)r * a.o.ld + (size_t)h * a.d + dim;
+  const float lsum = block_sum(lp, sh);   // ends with a barrier: wch is visible
+  // output dims: thread = (dim, chunk group)
+  const int d = a.d, G = 256 / d;
+  const int dim = tid % d, grp = tid / d;
+  float o = 0.f;
+  if (grp < G) {
+    int c = grp;
+    for (; c + 3 * G < nch; c += 4 * G) {
+      const float p0 = a.po[(base + c) * d + dim], p1 = a.po[(base + c + G) * d + dim];
+      const float p2 = a.po[(base + c + 2 * G) * d + dim], p3 = a.po[(base + c + 3 * G) * d + dim];
+      o += p0 * wch[c] + p1 * wch[c + G] + p2 * wch[c + 2 * G] + p3 * wch[c + 3 * G];
+    }
+    for (; c < nch; c += G) o += a.po[(base + c) * d + dim] * wch[c];
+  }
+  red[tid] = o;
+  __syncthreads();
+  if (grp != 0) return;
+  float sum = 0.f;
+  for (int gg = 0; gg < G; ++gg) sum += red[gg * d + dim];
+  const float v = lsum > 0.f ? sum / lsum : 0.f;
+  const size_t i = (size_t)r * a.o.ld + (size_t)h * d + dim;
   if constexpr (sizeof(T) == 2) {
     const uint32_t hb = f2bf(v);
     ((bf16_t *)a.o.hi)[i] = (bf16_t)hb;
@@ -280,13 +333,12 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   a.o = o;
   a.err = err;
   dim3 g1(a.nch, nkv, R), g2(nq, R);
-  const int th = d <= 64 ? 64 : (d <= 128 ? 128 : 256);
   if (bf16) {
     hipLaunchKernelGGL(k_attn_partial<bf16_t>, g1, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_attn_combine<bf16_t>, g2, dim3(th), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<bf16_t>, g2, dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL(k_attn_partial<float>, g1, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_attn_combine<float>, g2, dim3(th), 0, s, a);
+    hipLaunchKernelGGL(k_attn_combine<float>, g2, dim3(256), 0, s, a);
   }
 }
 

@@ -254,8 +254,11 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
           float out[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
+            // angle in fp64, reduced to [-pi, pi] in fp64, cos/sin in fp32
             const double ang = (double)pos * g.inv_freq[dim0 + i];
-            const float c = (float)cos(ang), s = (float)sin(ang);
+            const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+            float s, c;
+            sincosf((float)red, &s, &c);
             // first half: y1 = x1 c - x2 s ; second half: y2 = x2 c + x1 s
             out[i] = first ? v[i] * c - pv[i] * s : v[i] * c + pv[i] * s;
           }

@@ -207,6 +207,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 8192)
     c->nsub *= 2;
   c->nch = attention_chunks(c->max_slots, c->nsub);
+  if (c->nch > 1024) {
+    delete c;
+    return fail(nullptr, PRISM_ERR_SHAPE, "KV capacity per sequence too large for the attention merge");
+  }
   c->kmax = w > 1 ? w : 1;
   c->Cmax = Cmax;
   c->feat_max = k.feat_width > k.hidden ? k.feat_width : k.hidden;
