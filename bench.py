@@ -9,7 +9,7 @@ synthetic tensors already resident in HBM when timing starts.
 
 Printed (one JSON line): drafted tokens/s, per-draft-step microseconds, the
 roofline of the dominant kernel (the LM-head GEMV with fused top-k, timed
-with HIP events inside the graph replays), and the CPU oracle timed on a
+with HIP events around each of its launches), and the CPU oracle timed on a
 bounded sample of the same workload.
 """
 import argparse
@@ -23,6 +23,31 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0   # dense MFMA
+COPY_BYTES = 256 << 20      # counter-calibration copy
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lmhead_traffic.json")
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "device.h", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2602_01762_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def lm_traffic(cfg):
+    """HBM bytes per LM-head launch measured with FETCH_SIZE / WRITE_SIZE
+    counter runs (profiles/k_lmhead_traffic.json), or None when they were
+    taken on other kernel sources or another workload."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_digest") != kernel_source_digest() or t.get("workload") != cfg.name:
+        return None
+    return t.get("bytes_per_launch")
 
 WORKLOADS = {
     "8b_bs1": "llama3_8b_bf16_chain_bs1",
@@ -56,6 +81,8 @@ def main():
     ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-baseline", type=int, default=1,
                     help="time the CPU oracle on a bounded sample (0 = skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="also run a plain 256 MiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures the single-GPU drafting path; --gpus %d is not supported "
@@ -140,6 +167,15 @@ def main():
         "roofline": roofline,
     }
     print("bench: gpu done %.3f ms/step" % ms_per_step, file=sys.stderr, flush=True)
+    if args.calibrate_copy:
+        # a copy of known size: its FETCH_SIZE / WRITE_SIZE counters give the
+        # KiB-per-byte scale of the same counters on the LM-head kernel
+        src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda").normal_()
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+    res["roofline"]["traffic"] = lm_traffic(cfg)
 
     if args.cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(cfg, w, inp, dr)
@@ -168,7 +204,7 @@ def cpu_baseline(cfg, w, inp, dr):
             orc.chain(hi, seqs=seqs)
         n += 1
         el = time.perf_counter() - t0
-        if el >= 10.0 or n >= 20:
+        if el >= 10.0 or n >= 200:
             break
     drafted = n * (cfg.n_steps if cfg.mode == "chain" else cfg.tree_nodes)
     return {"value": round(drafted / el, 3), "unit": "drafted tokens/s", "cores": threads,

@@ -39,12 +39,12 @@ __device__ __forceinline__ bool row_range(const AttnArgs &a, int r, int &b, int 
   L = prefix = total = 0;
   bits = 0ull;
   if (b < 0 || b >= a.kv.n_seq) return false;
-  L = a.kv.ctx_lens[b];
-  bits = a.bits ? a.bits[r] : 0ull;
   if (a.bits) {
+    L = a.kv.ctx_lens[b];
+    bits = a.bits[r];
     prefix = L;
     total = L + (bits ? 64 - __clzll((long long)bits) : 0);
-  } else {
+  } else {   // causal: the slot alone bounds the range (no context-length load)
     prefix = a.slot[r] + 1;
     total = prefix;
   }

@@ -43,53 +43,140 @@ __device__ __forceinline__ void mainloop(const u32x4 *__restrict__ w0, int nkb, 
 #pragma unroll
   for (int n = 0; n < NT; ++n) wp[n] = w0 + ((size_t)n * nkb + kb0) * 64 + lane;
   const u32x4 z4 = {0, 0, 0, 0};
-  int kb = kb0;
-  for (; kb + U <= kb1; kb += U) {
+  // batches of U k-blocks; the last batch is partial (n < U) but its loads
+  // are still issued together, so no k-block waits for another
+  for (int kb = kb0; kb < kb1; kb += U) {
+    const int nb = kb1 - kb;
     u32x4 a[U][NT];
     u32x4 bh[U][RT], bl[U][RT];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int n = 0; n < NT; ++n) a[u][n] = __builtin_nontemporal_load(wp[n] + u * 64);
+      for (int n = 0; n < NT; ++n) a[u][n] = u < nb ? __builtin_nontemporal_load(wp[n] + u * 64) : z4;
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
         const size_t o = (size_t)(kb + u) * KB;
-        bh[u][rt] = ok[rt] ? *(const u32x4 *)(xh[rt] + o) : z4;
-        if (PAIR) bl[u][rt] = ok[rt] ? *(const u32x4 *)(xl[rt] + o) : z4;
+        const bool ld = ok[rt] && u < nb;
+        bh[u][rt] = ld ? *(const u32x4 *)(xh[rt] + o) : z4;
+        if (PAIR) bl[u][rt] = ld ? *(const u32x4 *)(xl[rt] + o) : z4;
       }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      if (u < nb) {
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n)
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-          acc[n][rt] = Ty<T>::mma(a[u][n], bh[u][rt], acc[n][rt]);
-          if (PAIR) acc[n][rt] = Ty<T>::mma(a[u][n], bl[u][rt], acc[n][rt]);
-        }
-#pragma unroll
-    for (int n = 0; n < NT; ++n) wp[n] += U * 64;
-  }
-  for (; kb < kb1; ++kb) {
-    u32x4 a[NT];
-#pragma unroll
-    for (int n = 0; n < NT; ++n) a[n] = __builtin_nontemporal_load(wp[n]);
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      const size_t o = (size_t)kb * KB;
-      const u32x4 bh = ok[rt] ? *(const u32x4 *)(xh[rt] + o) : z4;
-      u32x4 bl = z4;
-      if (PAIR) bl = ok[rt] ? *(const u32x4 *)(xl[rt] + o) : z4;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        acc[n][rt] = Ty<T>::mma(a[n], bh, acc[n][rt]);
-        if (PAIR) acc[n][rt] = Ty<T>::mma(a[n], bl, acc[n][rt]);
+          for (int rt = 0; rt < RT; ++rt) {
+            acc[n][rt] = Ty<T>::mma(a[u][n], bh[u][rt], acc[n][rt]);
+            if (PAIR) acc[n][rt] = Ty<T>::mma(a[u][n], bl[u][rt], acc[n][rt]);
+          }
       }
     }
 #pragma unroll
-    for (int n = 0; n < NT; ++n) wp[n] += 64;
+    for (int n = 0; n < NT; ++n) wp[n] += U * 64;
   }
+}
+
+// GEMV main loop for a few rows (R <= RR <= 4) of a bf16 matrix: the
+// workgroup first stages the activation rows in LDS as fp32 (hi + lo), then
+// each lane multiplies its 8 weights of a k-block by the matching fp32
+// activations (an LDS broadcast: the 16 lanes of a k-quarter read the same
+// address).  Only weight fragments occupy registers, so 16 k-blocks
+// (16 KiB) stay in flight per wave, and the products are fp32-exact.  The
+// first batch of weight loads is issued before the staging so the two
+// overlap.  Every wave of the workgroup must call this (it contains a
+// barrier); waves without work pass kb0 == kb1.  Leaves the result in the
+// MFMA accumulator layout so that all epilogues are shared.
+constexpr int UV = 16;
+
+__device__ __forceinline__ float lo_bf(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+template <int RR>
+__device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
+                                              int K, float *xs, int kb0, int kb1, f32x4 &out) {
+  const int lane = threadIdx.x & 63, kq = lane >> 4;
+  const u32x4 z4 = {0, 0, 0, 0};
+  const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
+  u32x4 a[UV];
+  {
+    const int nb = kb1 - kb0;
+#pragma unroll
+    for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
+  }
+  // stage x rows (8 columns per thread step) as fp32
+  for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
+    const int r = i / K, k = i % K;
+    float v[8];
+    if (r < R) {
+      const u32x4 h = *(const u32x4 *)((const bf16_t *)x.hi + (size_t)r * x.ld + k);
+      const u32x4 l = *(const u32x4 *)((const bf16_t *)x.lo + (size_t)r * x.ld + k);
+      const uint32_t hw[4] = {h.x, h.y, h.z, h.w}, lw[4] = {l.x, l.y, l.z, l.w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        v[2 * m] = lo_bf(hw[m]) + lo_bf(lw[m]);
+        v[2 * m + 1] = hi_bf(hw[m]) + hi_bf(lw[m]);
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 8; ++m) v[m] = 0.f;
+    }
+    *(f32x4 *)(xs + i) = f32x4{v[0], v[1], v[2], v[3]};
+    *(f32x4 *)(xs + i + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+  __syncthreads();
+  float acc[RR];
+#pragma unroll
+  for (int r = 0; r < RR; ++r) acc[r] = 0.f;
+  for (int kb = kb0; kb < kb1; kb += UV) {
+    const int nb = kb1 - kb;
+    if (kb > kb0) {
+#pragma unroll
+      for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
+    }
+#pragma unroll
+    for (int u = 0; u < UV; ++u) {
+      if (u < nb) {
+      const int k0 = (kb + u) * 32 + kq * 8;
+      const uint32_t w[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
+#pragma unroll
+      for (int r = 0; r < RR; ++r) {
+        const f32x4 x0 = *(const f32x4 *)(xs + r * K + k0);
+        const f32x4 x1 = *(const f32x4 *)(xs + r * K + k0 + 4);
+        float t = acc[r];
+        t += lo_bf(w[0]) * x0.x; t += hi_bf(w[0]) * x0.y;
+        t += lo_bf(w[1]) * x0.z; t += hi_bf(w[1]) * x0.w;
+        t += lo_bf(w[2]) * x1.x; t += hi_bf(w[2]) * x1.y;
+        t += lo_bf(w[3]) * x1.z; t += hi_bf(w[3]) * x1.w;
+        acc[r] = t;
+      }
+      }
+    }
+    wp += UV * 64;
+  }
+  // sum the 4 k-quarters of each tile row (lanes l, l^16, l^32, l^48)
+#pragma unroll
+  for (int r = 0; r < RR; ++r) {
+    acc[r] += __shfl_xor(acc[r], 16, 64);
+    acc[r] += __shfl_xor(acc[r], 32, 64);
+  }
+  // lane l now holds tile row (l & 15); the MFMA layout wants, in lane L,
+  // tile rows 4 (L >> 4) + i of batch row (L & 15)
+  const int col = lane & 15, rq = lane >> 4;
+  float v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float t = 0.f;
+#pragma unroll
+    for (int r = 0; r < RR; ++r) {
+      const float sv = __shfl(acc[r], 4 * rq + i, 64);
+      if (col == r) t = sv;
+    }
+    v[i] = t;
+  }
+  out = f32x4{v[0], v[1], v[2], v[3]};
 }
 
 // store an fp32 value as the storage-type operand (hi/lo pair for bf16)
@@ -151,9 +238,11 @@ __device__ __forceinline__ void finish_scales(const RowNorm &nm, int R, const Sc
 template <int RT, int NT>
 constexpr int gemm_max_threads() { return RT * NT >= 2 ? 512 : 1024; }
 
-template <typename T, int RT, int NT, bool PAIR, int EPI>
+template <typename T, int RT, int NT, bool PAIR, int EPI, int VR>
 __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunch g) {
-  extern __shared__ f32x4 red[];        // [(kw - 1) * NT * RT * 64]
+  // dynamic LDS: [(kw - 1) * NT * RT * 64] f32x4 partial sums, kw floats,
+  // then (GEMV path, VR > 0) VR * K floats of staged activations
+  extern __shared__ f32x4 red[];
   __shared__ float rowscale[MAX_ROWS];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int kw = g.kw;
@@ -164,6 +253,28 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   ScaleLoads sl;
   if (own_scales) sl = issue_scales(g.norm, g.R);
 
+  // QKV: wave 0 looks up its rows' cache slots and positions before the
+  // main loop, so these dependent loads overlap the weight stream
+  long cbase[RT];
+  int rpos[RT];
+  if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      cbase[rt] = -1;
+      rpos[rt] = 0;
+      const int r = (lane & 15) + 16 * rt;
+      if (wave == 0 && r < g.R) {
+        rpos[rt] = g.rows.pos[r];
+        const int b = g.rows.seq[r], slot = g.rows.slot[r];
+        const int bi = slot / g.kv.bs;
+        if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
+          const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
+          if (blk >= 0 && blk < g.kv.n_blocks)
+            cbase[rt] = (long)blk * g.nkv * g.kv.bs * g.d + (long)(slot % g.kv.bs) * g.d;
+        }
+      }
+    }
+  }
   f32x4 acc[NT][RT];
 #pragma unroll
   for (int n = 0; n < NT; ++n)
@@ -171,8 +282,14 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int kb0 = (int)((long)wave * m.nkb / kw);
   const int kb1 = (int)((long)(wave + 1) * m.nkb / kw);
-  mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
-                            kb1, acc);
+  if constexpr (VR > 0) {
+    float *xs = (float *)&red[(kw - 1) * NT * RT * 64] + 64 * kw;
+    mainloop_valu<VR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0, kb1,
+                      acc[0][0]);
+  } else {
+    mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
+                              kb1, acc);
+  }
   if (kw > 1) {
     if (wave > 0) {
 #pragma unroll
@@ -250,7 +367,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
           const int j = (fr % d) / 16;       // tile index within the head
           const bool first = q4 < 2;
           const int dim0 = 8 * j + 4 * (q4 & 1);   // dim within the first half
-          const int pos = g.rows.pos[r];
+          const int pos = rpos[rt];
           float out[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -266,14 +383,8 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
           if (isq) {
             *(f32x4 *)(g.q + (size_t)r * qd + head * d + dimb) = f32x4{out[0], out[1], out[2], out[3]};
           } else {
-            const int b = g.rows.seq[r], slot = g.rows.slot[r];
-            const int bi = slot / g.kv.bs;
-            long base = -1;
-            if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
-              const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
-              if (blk >= 0 && blk < g.kv.n_blocks)
-                base = ((long)blk * g.nkv + head) * g.kv.bs * d + (long)(slot % g.kv.bs) * d;
-            }
+            // pool layout [block, kv head, slot in block, d]
+            const long base = cbase[rt] < 0 ? -1 : cbase[rt] + (long)head * g.kv.bs * d;
             if (base < 0) {
               atomicOr(g.err, ERRF_CAPACITY);
             } else {
@@ -285,14 +396,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
           const int fr = f0 - qd - kd;
           const int head = fr / d;
           const int dim = fr % d + 4 * q4;
-          const int b = g.rows.seq[r], slot = g.rows.slot[r];
-          const int bi = slot / g.kv.bs;
-          long base = -1;
-          if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
-            const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
-            if (blk >= 0 && blk < g.kv.n_blocks)
-              base = ((long)blk * g.nkv + head) * g.kv.bs * d + (long)(slot % g.kv.bs) * d;
-          }
+          const long base = cbase[rt] < 0 ? -1 : cbase[rt] + (long)head * g.kv.bs * d;
           if (base < 0) {
             atomicOr(g.err, ERRF_CAPACITY);
           } else {
@@ -310,8 +414,9 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
 // final-norm row scale and reduces the workgroup's logits of each row to
 // partials: max, sum of exp(logit - max), and the top-k (logit desc, id asc);
 // optional fp32 logits store.
-template <typename T, int RT, int NT, bool PAIR>
+template <typename T, int RT, int NT, bool PAIR, int VR>
 __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
+  extern __shared__ float xs_lm[];   // GEMV path: VR * K staged activations
   __shared__ float sl[RT * 16][64 * NT + 1];
   __shared__ float rowscale[MAX_ROWS];
   __shared__ float tmp[256];
@@ -328,9 +433,14 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bool live = t0 < m.n_tiles;    // n_tiles is a multiple of NT
-  if (live)
+  if constexpr (VR > 0) {
+    // every wave takes part (staging barrier); idle waves stream nothing
+    mainloop_valu<VR>((const u32x4 *)m.w + (size_t)(live ? t0 : 0) * m.nkb * 64, g.x, g.R, m.K,
+                      xs_lm, 0, live ? m.nkb : 0, acc[0][0]);
+  } else if (live) {
     mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, 0,
                               m.nkb, acc);
+  }
   if (own_scales) {
     __syncthreads();
     finish_scales(g.norm, g.R, sc, rowscale, tmp);
@@ -393,26 +503,40 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   }
 }
 
-template <typename T, int RT, int NT, bool PAIR>
+size_t gemv_lds_bytes(int R, int K) {
+  const int vr = R <= 1 ? 1 : (R <= 2 ? 2 : 4);
+  return (size_t)vr * K * sizeof(float);
+}
+
+template <typename T, int RT, int NT, bool PAIR, int VR>
 static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
   dim3 grid(g.m.n_tiles / NT);
-  const size_t lds = (size_t)((g.kw - 1) * NT * RT * 64) * sizeof(f32x4) +
-                     (size_t)64 * g.kw * sizeof(float);
-  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM>), grid, dim3(64 * g.kw), lds, s, g);
-  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU>), grid, dim3(64 * g.kw), lds, s, g);
-  else hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV>), grid, dim3(64 * g.kw), lds, s, g);
+  size_t lds = (size_t)((g.kw - 1) * NT * RT * 64) * sizeof(f32x4) +
+               (size_t)64 * g.kw * sizeof(float);
+  if (VR > 0) lds += (size_t)VR * g.m.K * sizeof(float);
+  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM, VR>), grid, dim3(64 * g.kw), lds, s, g);
+  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU, VR>), grid, dim3(64 * g.kw), lds, s, g);
+  else hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
 }
 
 template <typename T, bool PAIR>
 static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    if (g.gemv) {
+      if (g.R <= 1) gemm_epi<T, 1, 1, PAIR, 1>(g, s);
+      else if (g.R <= 2) gemm_epi<T, 1, 1, PAIR, 2>(g, s);
+      else gemm_epi<T, 1, 1, PAIR, 4>(g, s);
+      return;
+    }
+  }
   if (g.nt == 2) {
-    if (g.R <= 16) gemm_epi<T, 1, 2, PAIR>(g, s);
-    else if (g.R <= 32) gemm_epi<T, 2, 2, PAIR>(g, s);
-    else gemm_epi<T, 4, 2, PAIR>(g, s);
+    if (g.R <= 16) gemm_epi<T, 1, 2, PAIR, 0>(g, s);
+    else if (g.R <= 32) gemm_epi<T, 2, 2, PAIR, 0>(g, s);
+    else gemm_epi<T, 4, 2, PAIR, 0>(g, s);
   } else {
-    if (g.R <= 16) gemm_epi<T, 1, 1, PAIR>(g, s);
-    else if (g.R <= 32) gemm_epi<T, 2, 1, PAIR>(g, s);
-    else gemm_epi<T, 4, 1, PAIR>(g, s);
+    if (g.R <= 16) gemm_epi<T, 1, 1, PAIR, 0>(g, s);
+    else if (g.R <= 32) gemm_epi<T, 2, 1, PAIR, 0>(g, s);
+    else gemm_epi<T, 4, 1, PAIR, 0>(g, s);
   }
 }
 
@@ -426,14 +550,23 @@ int lm_workgroups(int n_tiles, int nt) { return (n_tiles / nt + 3) / 4; }
 template <typename T, bool PAIR>
 static void lm_rt(const LmLaunch &g, hipStream_t s) {
   const dim3 grid(g.n_wg), blk(256);
+  if constexpr (sizeof(T) == 2) {
+    if (g.gemv) {
+      const size_t lds = gemv_lds_bytes(g.R, g.m.K);
+      if (g.R <= 1) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 1>), grid, blk, lds, s, g);
+      else if (g.R <= 2) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 2>), grid, blk, lds, s, g);
+      else hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 4>), grid, blk, lds, s, g);
+      return;
+    }
+  }
   if (g.nt == 2) {   // two tiles per wave once B fragments dominate operand traffic
-    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 2, PAIR>), grid, blk, 0, s, g);
-    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 2, PAIR>), grid, blk, 0, s, g);
-    else hipLaunchKernelGGL((k_lmhead<T, 4, 2, PAIR>), grid, blk, 0, s, g);
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 2, PAIR, 0>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 2, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 2, PAIR, 0>), grid, blk, 0, s, g);
   } else {
-    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR>), grid, blk, 0, s, g);
-    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 1, PAIR>), grid, blk, 0, s, g);
-    else hipLaunchKernelGGL((k_lmhead<T, 4, 1, PAIR>), grid, blk, 0, s, g);
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 0>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 1, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 1, PAIR, 0>), grid, blk, 0, s, g);
   }
 }
 

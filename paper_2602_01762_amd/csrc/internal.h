@@ -81,6 +81,7 @@ struct GemmLaunch {
   int R;
   int kw;          // waves of the workgroup splitting K (1..16)
   int nt;          // tiles per workgroup (1 or 2)
+  int gemv;        // 1: VALU GEMV main loop (bf16, R <= 4, staged fp32 activations)
   int epi;
   RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_tiles = 0: none
   // EPI_NORM: y = acc (+ res) -> y [R, ldy] fp32; (y * gain) -> g planes; ss
@@ -110,12 +111,15 @@ struct LmLaunch {
   int *pid;
   int n_wg;
   int nt;                          // vocab tiles per wave (1 or 2)
+  int gemv;                        // 1: VALU GEMV main loop (bf16, R <= 4)
 };
 
 // ---- launchers (gemm.hip) -------------------------------------------------
 void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
 int lm_workgroups(int n_tiles, int nt);
+// LDS of the staged activations of the GEMV main loop
+size_t gemv_lds_bytes(int R, int K);
 // largest number of partial entries (tiles x rows) a consumer reduces itself
 int own_scale_capacity(int threads);
 void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, float *scale,

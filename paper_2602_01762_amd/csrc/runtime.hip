@@ -78,6 +78,7 @@ struct prism_ctx {
   int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
   uint64_t *t_bits[2] = {nullptr, nullptr};
   int nsub = 1;                     // attention: 64-slot steps per workgroup
+  size_t lds_limit = 65536;         // LDS bytes one workgroup may use
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
 
@@ -198,6 +199,12 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->bf16 = bf16;
   c->esz = bf16 ? 2 : 4;
   (void)hipGetDevice(&c->dev);
+  {
+    int lds = 0;
+    if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, c->dev) == hipSuccess &&
+        lds > 0)
+      c->lds_limit = (size_t)lds;
+  }
   c->H = k.hidden; c->nq = k.n_q_heads; c->nkv = k.n_kv_heads; c->d = k.head_dim;
   c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
   c->rows_max = rows;
@@ -457,7 +464,15 @@ static RowNorm norm_for(prism_ctx *c, const float *ss, float *scale, int R, int 
   return n;
 }
 
-static GemmLaunch gemm_of(const TiledMat &m, const Act &x, int R, int epi) {
+// GEMV main loop (bf16, at most 4 rows) when the staged activations fit in
+// the workgroup's LDS next to the cross-wave partial sums
+static bool use_gemv(const prism_ctx *c, int R, int K, int kw) {
+  if (!c->bf16 || R > 4) return false;
+  const size_t lds = gemv_lds_bytes(R, K) + (size_t)(kw - 1) * 64 * 16 + (size_t)64 * kw * 4;
+  return lds <= c->lds_limit;
+}
+
+static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, int R, int epi) {
   GemmLaunch g{};
   g.m = m;
   g.x = x;
@@ -466,6 +481,8 @@ static GemmLaunch gemm_of(const TiledMat &m, const Act &x, int R, int epi) {
   Plan pl = plan_for(m, R);
   g.kw = pl.kw;
   g.nt = pl.nt;
+  g.gemv = use_gemv(c, R, m.K, g.kw) ? 1 : 0;
+  if (g.gemv) g.nt = 1;
   return g;
 }
 
@@ -477,11 +494,11 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   ActOut X = c->xfc;
   X.ld = H + p.F;
   launch_fc_prep(bf, R, p.in, c->embed, c->V, H, p.F, X, c->err, s);
-  GemmLaunch g = gemm_of(S.fc, act_of(X, H + p.F), R, EPI_NORM);
+  GemmLaunch g = gemm_of(c, S.fc, act_of(X, H + p.F), R, EPI_NORM);
   g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
   launch_gemm(bf, g, s);
   // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
-  g = gemm_of(S.qkv, act_of(c->ug, H), R, EPI_QKV);
+  g = gemm_of(c, S.qkv, act_of(c->ug, H), R, EPI_QKV);
   g.norm = norm_for(c, c->ss_u, c->sc_u, R, 64 * g.kw, s);
   g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
   g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
@@ -492,17 +509,17 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   launch_attention(bf, R, c->nq, c->nkv, c->d, c->q, p.in, kv, c->max_slots, c->nsub, c->pm,
                    c->pl, c->po, o, c->err, s);
   // r1 = u + W_o o  ->  r1, (r1 * g2), sums of squares
-  g = gemm_of(S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
+  g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
   g.res = c->u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
   g.ss = c->ss_r1;
   launch_gemm(bf, g, s);
   // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
-  g = gemm_of(S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
+  g = gemm_of(c, S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
   g.norm = norm_for(c, c->ss_r1, c->sc_r1, R, 64 * g.kw, s);
   g.z = c->z; g.z.ld = c->I;
   launch_gemm(bf, g, s);
   // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
-  g = gemm_of(S.down, act_of(c->z, c->I), R, EPI_NORM);
+  g = gemm_of(c, S.down, act_of(c->z, c->I), R, EPI_NORM);
   g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
   g.g.ld = H; g.ss = c->ss_h;
   launch_gemm(bf, g, s);
@@ -513,7 +530,8 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   lmg.R = R;
   lmg.V = c->V;
   lmg.topk = p.topk;
-  lmg.nt = (R > 16 && c->lm.n_tiles % 2 == 0) ? 2 : 1;
+  lmg.gemv = (c->bf16 && R <= 4 && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
+  lmg.nt = (!lmg.gemv && R > 16 && c->lm.n_tiles % 2 == 0) ? 2 : 1;
   lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);
   lmg.norm = norm_for(c, c->ss_h, c->sc_h, R, 256, s);
   lmg.logits = p.logits;
