@@ -233,6 +233,111 @@ __device__ __forceinline__ void finish_scales(const RowNorm &nm, int R, const Sc
   }
 }
 
+// Epilogue of one 16x16 accumulator tile in the MFMA layout: the lane holds
+// output rows n0..n0+3 (tiled order) of batch row r = (lane & 15) + 16 rt.
+// Every lane of the wave must call it (it shuffles).  scale: the row's
+// RMSNorm scale (1 if none); cbase / rpos: the row's cache slot and position
+// (QKV only).
+template <typename T, int EPI>
+__device__ __forceinline__ void epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
+                                              float scale, long cbase, int rpos) {
+  const int lane = threadIdx.x & 63, q4 = lane >> 4;
+  const int n0 = tile * 16 + 4 * q4;
+  const bool live = r < g.R;
+  float v[4] = {a.x * scale, a.y * scale, a.z * scale, a.w * scale};
+  if (EPI == EPI_NORM) {
+    float ss = 0.f;
+    if (live) {
+      if (g.res) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
+      }
+      *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * Ty<T>::ld((const T *)g.gain, n0 + i));
+        ss += v[i] * v[i];
+      }
+    }
+    // tile sum over the 4 lanes holding row r: fixed butterfly order
+    ss += __shfl_xor(ss, 16, 64);
+    ss += __shfl_xor(ss, 32, 64);
+    if (live && q4 == 0) g.ss[(size_t)tile * g.R + r] = ss;
+  } else if (EPI == EPI_SWIGLU) {
+    if (live) {
+      // rows interleave (gate c, up c, gate c + 1, up c + 1)
+      const int c = n0 >> 1;
+      put_act<T>(g.z, (size_t)r * g.z.ld + c, silu(v[0]) * v[1]);
+      put_act<T>(g.z, (size_t)r * g.z.ld + c + 1, silu(v[2]) * v[3]);
+    }
+  } else {  // EPI_QKV
+    const int d = g.d, half = d >> 1;
+    const int qd = g.nq * d, kd = g.nkv * d;
+    const int f0 = tile * 16;            // first feature of the tile (tiled order)
+    // partner values for the rotation (lanes l and l ^ 32 hold the two halves)
+    float pv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pv[i] = __shfl_xor(v[i], 32, 64);
+    if (!live) return;
+    if (f0 < qd + kd) {
+      const bool isq = f0 < qd;
+      const int fr = isq ? f0 : f0 - qd;
+      const int head = fr / d;
+      const int j = (fr % d) / 16;       // tile index within the head
+      const bool first = q4 < 2;
+      const int dim0 = 8 * j + 4 * (q4 & 1);   // dim within the first half
+      float out[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // angle in fp64, reduced to [-pi, pi] in fp64, cos/sin in fp32
+        const double ang = (double)rpos * g.inv_freq[dim0 + i];
+        const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+        float sn, cs;
+        sincosf((float)red, &sn, &cs);
+        // first half: y1 = x1 c - x2 s ; second half: y2 = x2 c + x1 s
+        out[i] = first ? v[i] * cs - pv[i] * sn : v[i] * cs + pv[i] * sn;
+      }
+      const int dimb = first ? dim0 : half + dim0;
+      if (isq) {
+        *(f32x4 *)(g.q + (size_t)r * qd + head * d + dimb) = f32x4{out[0], out[1], out[2], out[3]};
+      } else {
+        // pool layout [block, kv head, slot in block, d]
+        const long base = cbase < 0 ? -1 : cbase + (long)head * g.kv.bs * d;
+        if (base < 0) {
+          atomicOr(g.err, ERRF_CAPACITY);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.k_pool, base + dimb + i, out[i]);
+        }
+      }
+    } else {
+      const int fr = f0 - qd - kd;
+      const int head = fr / d;
+      const int dim = fr % d + 4 * q4;
+      const long base = cbase < 0 ? -1 : cbase + (long)head * g.kv.bs * d;
+      if (base < 0) {
+        atomicOr(g.err, ERRF_CAPACITY);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.v_pool, base + dim + i, v[i]);
+      }
+    }
+  }
+}
+
+// cache slot (block, head 0, offset) and position of row r, or -1
+__device__ __forceinline__ long cache_base(const GemmLaunch &g, int r, int &pos) {
+  pos = g.rows.pos[r];
+  const int b = g.rows.seq[r], slot = g.rows.slot[r];
+  const int bi = slot / g.kv.bs;
+  if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
+    const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
+    if (blk >= 0 && blk < g.kv.n_blocks)
+      return (long)blk * g.nkv * g.kv.bs * g.d + (long)(slot % g.kv.bs) * g.d;
+  }
+  return -1;
+}
+
 // batched variants (more accumulators) run at most 8 waves per workgroup,
 // which leaves them 256 VGPRs
 template <int RT, int NT>
@@ -257,22 +362,16 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   // main loop, so these dependent loads overlap the weight stream
   long cbase[RT];
   int rpos[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    cbase[rt] = -1;
+    rpos[rt] = 0;
+  }
   if constexpr (EPI == EPI_QKV) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      cbase[rt] = -1;
-      rpos[rt] = 0;
       const int r = (lane & 15) + 16 * rt;
-      if (wave == 0 && r < g.R) {
-        rpos[rt] = g.rows.pos[r];
-        const int b = g.rows.seq[r], slot = g.rows.slot[r];
-        const int bi = slot / g.kv.bs;
-        if (b >= 0 && b < g.kv.n_seq && slot >= 0 && bi < g.kv.mbps) {
-          const int blk = g.kv.block_table[(size_t)b * g.kv.mbps + bi];
-          if (blk >= 0 && blk < g.kv.n_blocks)
-            cbase[rt] = (long)blk * g.nkv * g.kv.bs * g.d + (long)(slot % g.kv.bs) * g.d;
-        }
-      }
+      if (wave == 0 && r < g.R) cbase[rt] = cache_base(g, r, rpos[rt]);
     }
   }
   f32x4 acc[NT][RT];
@@ -311,102 +410,65 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) acc[n][rt] += red[(((j - 1) * NT + n) * RT + rt) * 64 + lane];
 
-  const int q4 = lane >> 4;
 #pragma unroll
-  for (int n = 0; n < NT; ++n) {
-    const int tile = t0 + n;
-    const int n0 = tile * 16 + 4 * q4;   // first of this lane's 4 output rows (tiled order)
+  for (int n = 0; n < NT; ++n)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       const int r = (lane & 15) + 16 * rt;
-      const bool live = r < g.R;
-      float v[4] = {acc[n][rt].x, acc[n][rt].y, acc[n][rt].z, acc[n][rt].w};
-      if (has_norm && live) {
-        const float sc = own_scales ? rowscale[r] : g.norm.scale[r];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] *= sc;
-      }
-      if (EPI == EPI_NORM) {
-        float ss = 0.f;
-        if (live) {
-          if (g.res) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
-          }
-          *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * Ty<T>::ld((const T *)g.gain, n0 + i));
-            ss += v[i] * v[i];
-          }
-        }
-        // tile sum over the 4 lanes holding row r: fixed butterfly order
-        ss += __shfl_xor(ss, 16, 64);
-        ss += __shfl_xor(ss, 32, 64);
-        if (live && q4 == 0) g.ss[(size_t)tile * g.R + r] = ss;
-      } else if (EPI == EPI_SWIGLU) {
-        if (live) {
-          // rows interleave (gate c, up c, gate c + 1, up c + 1)
-          const int c = n0 >> 1;
-          put_act<T>(g.z, (size_t)r * g.z.ld + c, silu(v[0]) * v[1]);
-          put_act<T>(g.z, (size_t)r * g.z.ld + c + 1, silu(v[2]) * v[3]);
-        }
-      } else {  // EPI_QKV
-        const int d = g.d, half = d >> 1;
-        const int qd = g.nq * d, kd = g.nkv * d;
-        const int f0 = tile * 16;            // first feature of the tile (tiled order)
-        // partner values for the rotation (lanes l and l ^ 32 hold the two halves)
-        float pv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pv[i] = __shfl_xor(v[i], 32, 64);
-        if (!live) continue;
-        if (f0 < qd + kd) {
-          const bool isq = f0 < qd;
-          const int fr = isq ? f0 : f0 - qd;
-          const int head = fr / d;
-          const int j = (fr % d) / 16;       // tile index within the head
-          const bool first = q4 < 2;
-          const int dim0 = 8 * j + 4 * (q4 & 1);   // dim within the first half
-          const int pos = rpos[rt];
-          float out[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // angle in fp64, reduced to [-pi, pi] in fp64, cos/sin in fp32
-            const double ang = (double)pos * g.inv_freq[dim0 + i];
-            const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
-            float s, c;
-            sincosf((float)red, &s, &c);
-            // first half: y1 = x1 c - x2 s ; second half: y2 = x2 c + x1 s
-            out[i] = first ? v[i] * c - pv[i] * s : v[i] * c + pv[i] * s;
-          }
-          const int dimb = first ? dim0 : half + dim0;
-          if (isq) {
-            *(f32x4 *)(g.q + (size_t)r * qd + head * d + dimb) = f32x4{out[0], out[1], out[2], out[3]};
-          } else {
-            // pool layout [block, kv head, slot in block, d]
-            const long base = cbase[rt] < 0 ? -1 : cbase[rt] + (long)head * g.kv.bs * d;
-            if (base < 0) {
-              atomicOr(g.err, ERRF_CAPACITY);
-            } else {
-#pragma unroll
-              for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.k_pool, base + dimb + i, out[i]);
-            }
-          }
-        } else {
-          const int fr = f0 - qd - kd;
-          const int head = fr / d;
-          const int dim = fr % d + 4 * q4;
-          const long base = cbase[rt] < 0 ? -1 : cbase[rt] + (long)head * g.kv.bs * d;
-          if (base < 0) {
-            atomicOr(g.err, ERRF_CAPACITY);
-          } else {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) Ty<T>::st((T *)g.kv.v_pool, base + dim + i, v[i]);
-          }
-        }
-      }
+      const float sc = has_norm && r < g.R ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
+      epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt]);
     }
+}
+
+// Batched products (R > 4 rows): the 4 waves of a workgroup take 4
+// consecutive groups of NT tiles over the same K slice (slice blockIdx.y of
+// gridDim.y), so the B fragments a wave loads are the ones its neighbours
+// load at about the same time (L1 hits), and each fragment feeds NT tiles.
+// Slice partial sums go to part[s][r][n]; k_gemm_finish adds the slices in
+// order and applies the epilogue.
+template <typename T, int RT, int NT, bool PAIR>
+__global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const TiledMat &m = g.m;
+  const int t0 = (blockIdx.x * 4 + wave) * NT;
+  if (t0 >= m.n_tiles) return;   // n_tiles is a multiple of NT; no barriers below
+  const int S = gridDim.y, sl = blockIdx.y;
+  const int kb0 = (int)((long)sl * m.nkb / S), kb1 = (int)((long)(sl + 1) * m.nkb / S);
+  f32x4 acc[NT][RT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0, kb1,
+                            acc);
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = (lane & 15) + 16 * rt;
+      if (r < g.R)
+        *(f32x4 *)(g.part + ((size_t)sl * g.R + r) * m.N + (t0 + n) * 16 + 4 * q4) = acc[n][rt];
+    }
+}
+
+// One wave per (tile, 16-row group): the slices' partial sums in slice
+// order, then the shared epilogue.  Row scales come precomputed.
+template <typename T, int EPI>
+__global__ __launch_bounds__(64) void k_gemm_finish(GemmLaunch g) {
+  const int tile = blockIdx.x, lane = threadIdx.x;
+  const int r = (lane & 15) + 16 * blockIdx.y;
+  const int n0 = tile * 16 + 4 * (lane >> 4);
+  f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+  long cbase = -1;
+  int rpos = 0;
+  float sc = 1.f;
+  if (r < g.R) {
+    for (int sl = 0; sl < g.split; ++sl) a += *(const f32x4 *)(g.part + ((size_t)sl * g.R + r) * g.m.N + n0);
+    if (g.norm.scale) sc = g.norm.scale[r];
+    if (EPI == EPI_QKV) cbase = cache_base(g, r, rpos);
   }
+  epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos);
 }
 
 // LM head: each wave covers NT 16-row vocab tiles over the full K; a
@@ -519,8 +581,35 @@ static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
   else hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
 }
 
+template <typename T, int RT, int NT, bool PAIR>
+static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
+  const int groups = g.m.n_tiles / NT;
+  hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), dim3((groups + 3) / 4, g.split), dim3(256), 0,
+                     s, g);
+  const dim3 fg(g.m.n_tiles, (g.R + 15) / 16);
+  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, dim3(64), 0, s, g);
+  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, dim3(64), 0, s, g);
+  else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, dim3(64), 0, s, g);
+}
+
 template <typename T, bool PAIR>
 static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
+  if (g.split > 0) {
+    if (g.nt == 4) {
+      if (g.R <= 16) gemm_split_launch<T, 1, 4, PAIR>(g, s);
+      else if (g.R <= 32) gemm_split_launch<T, 2, 4, PAIR>(g, s);
+      else gemm_split_launch<T, 4, 2, PAIR>(g, s);
+    } else if (g.nt == 2) {
+      if (g.R <= 16) gemm_split_launch<T, 1, 2, PAIR>(g, s);
+      else if (g.R <= 32) gemm_split_launch<T, 2, 2, PAIR>(g, s);
+      else gemm_split_launch<T, 4, 2, PAIR>(g, s);
+    } else {
+      if (g.R <= 16) gemm_split_launch<T, 1, 1, PAIR>(g, s);
+      else if (g.R <= 32) gemm_split_launch<T, 2, 1, PAIR>(g, s);
+      else gemm_split_launch<T, 4, 1, PAIR>(g, s);
+    }
+    return;
+  }
   if constexpr (sizeof(T) == 2) {
     if (g.gemv) {
       if (g.R <= 1) gemm_epi<T, 1, 1, PAIR, 1>(g, s);
@@ -559,7 +648,12 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
       return;
     }
   }
-  if (g.nt == 2) {   // two tiles per wave once B fragments dominate operand traffic
+  if (g.nt == 4) {   // four tiles per wave share each B fragment (batched rows)
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 4, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 2, 4, PAIR, 0>), grid, blk, 0, s, g);
+    return;
+  }
+  if (g.nt == 2) {
     if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 2, PAIR, 0>), grid, blk, 0, s, g);
     else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 2, PAIR, 0>), grid, blk, 0, s, g);
     else hipLaunchKernelGGL((k_lmhead<T, 4, 2, PAIR, 0>), grid, blk, 0, s, g);

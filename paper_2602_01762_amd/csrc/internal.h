@@ -82,6 +82,8 @@ struct GemmLaunch {
   int kw;          // waves of the workgroup splitting K (1..16)
   int nt;          // tiles per workgroup (1 or 2)
   int gemv;        // 1: VALU GEMV main loop (bf16, R <= 4, staged fp32 activations)
+  int split;       // > 0: batched path, K split over `split` workgroup slices
+  float *part;     // batched path: slice partial sums [split][R][N]
   int epi;
   RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_tiles = 0: none
   // EPI_NORM: y = acc (+ res) -> y [R, ldy] fp32; (y * gain) -> g planes; ss

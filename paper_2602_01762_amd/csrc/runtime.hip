@@ -70,6 +70,7 @@ struct prism_ctx {
   ActOut o;                         // attention output planes [R, nq*d]
   ActOut z;                         // SwiGLU planes [R, I]
   float *hid[2] = {nullptr, nullptr};
+  float *part = nullptr;            // batched products: K-slice partial sums
   float *lm_max = nullptr, *lm_sum = nullptr, *lm_val = nullptr, *logp = nullptr;
   int *lm_id = nullptr, *ids = nullptr, *tokbuf = nullptr;
   int32_t *c_seq = nullptr, *c_pos = nullptr, *c_tok0 = nullptr;
@@ -139,6 +140,18 @@ static Plan plan_for(const TiledMat &t, int R) {
   while (kw > 1 && (kw - 1) * p.nt * rt > 48) --kw;
   p.kw = kw;
   return p;
+}
+
+// Batched products (more than 4 rows): tiles per wave (B fragment reuse) and
+// K slices across workgroups (about 512 workgroups of 4 waves, at least 4
+// k-blocks per slice).
+static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
+  nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
+  if (R > 32 && nt == 4) nt = 2;
+  const int wgs = (t.n_tiles / nt + 3) / 4;
+  int sp = (512 + wgs - 1) / wgs;
+  if (sp > t.nkb / 4) sp = t.nkb / 4;
+  split = sp < 1 ? 1 : sp;
 }
 
 static void carve(char *&p, void **dst, size_t bytes) {
@@ -257,6 +270,23 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   planes(c->z, R * c->I);
   add((void **)&c->hid[0], R * c->H * 4);
   add((void **)&c->hid[1], R * c->H * 4);
+  if (rows > 4) {   // batched products: K-slice partial sums
+    size_t pn = 0;
+    auto upd = [&](int N, int K) {   // the plan depends on the row count: take both regimes
+      for (int rr : {5, rows}) {
+        int nt, sp;
+        plan_batched(make_tiled(N, K, bf16), rr, nt, sp);
+        if ((size_t)sp * N > pn) pn = (size_t)sp * N;
+      }
+    };
+    upd(c->H, c->H + k.feat_width);
+    upd(c->H, 2 * c->H);
+    upd(c->QKV, c->H);
+    upd(c->H, c->nq * c->d);
+    upd(2 * c->I, c->H);
+    upd(c->H, c->I);
+    add((void **)&c->part, R * pn * 4);
+  }
   add((void **)&c->lm_max, R * c->n_wg_lm * 4);
   add((void **)&c->lm_sum, R * c->n_wg_lm * 4);
   add((void **)&c->lm_val, R * c->n_wg_lm * c->kmax * 4);
@@ -478,6 +508,12 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   g.x = x;
   g.R = R;
   g.epi = epi;
+  if (R > 4) {
+    plan_batched(m, R, g.nt, g.split);
+    g.kw = 1;
+    g.part = c->part;
+    return g;
+  }
   Plan pl = plan_for(m, R);
   g.kw = pl.kw;
   g.nt = pl.nt;
@@ -485,6 +521,10 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   if (g.gemv) g.nt = 1;
   return g;
 }
+
+// threads of a consumer that reduces its own row scales (0: batched path,
+// which takes precomputed scales)
+static int scale_threads(const GemmLaunch &g) { return g.split > 0 ? 0 : 64 * g.kw; }
 
 static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
   const Set &S = c->sets[p.set];
@@ -499,7 +539,7 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   launch_gemm(bf, g, s);
   // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
   g = gemm_of(c, S.qkv, act_of(c->ug, H), R, EPI_QKV);
-  g.norm = norm_for(c, c->ss_u, c->sc_u, R, 64 * g.kw, s);
+  g.norm = norm_for(c, c->ss_u, c->sc_u, R, scale_threads(g), s);
   g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
   g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
   launch_gemm(bf, g, s);
@@ -515,7 +555,7 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   launch_gemm(bf, g, s);
   // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
   g = gemm_of(c, S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
-  g.norm = norm_for(c, c->ss_r1, c->sc_r1, R, 64 * g.kw, s);
+  g.norm = norm_for(c, c->ss_r1, c->sc_r1, R, scale_threads(g), s);
   g.z = c->z; g.z.ld = c->I;
   launch_gemm(bf, g, s);
   // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
@@ -531,7 +571,11 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   lmg.V = c->V;
   lmg.topk = p.topk;
   lmg.gemv = (c->bf16 && R <= 4 && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
-  lmg.nt = (!lmg.gemv && R > 16 && c->lm.n_tiles % 2 == 0) ? 2 : 1;
+  lmg.nt = 1;
+  if (!lmg.gemv && R > 4) {   // batched rows: several vocab tiles per wave share B fragments
+    if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
+    else if (c->lm.n_tiles % 2 == 0) lmg.nt = 2;
+  }
   lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);
   lmg.norm = norm_for(c, c->ss_h, c->sc_h, R, 256, s);
   lmg.logits = p.logits;
