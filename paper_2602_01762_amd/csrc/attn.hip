@@ -18,6 +18,7 @@ namespace prism {
 constexpr int ATT_S = 64;        // slots per step
 constexpr int ATT_MAXG = 8;      // query heads per KV head
 constexpr int ATT_MAXGD = 1024;  // g * d
+constexpr int ATT_MAXD = 256;    // head_dim
 constexpr int ATT_MAXVS = 8;     // slots per thread in P.V: 64 / (256 / (d / 8)) for d <= 256
 constexpr int ATT_MAXCH = 1024;  // chunks per row merged by the combine kernel
 
@@ -252,6 +253,190 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
+
+// MFMA variant for bf16 caches.  Each wave takes 16 slots of every 64-slot
+// step: the scores of those slots against all g query heads are one 16x16
+// MFMA tile (K rows as the A operand, q as the B operand carried as a
+// hi/lo bf16 pair), the online softmax runs per head with lane shuffles, and
+// P.V is a 16x16x16 MFMA per 16 dims with P (hi/lo pair) straight from the
+// score layout and V transposed through a small per-wave LDS tile.  Each
+// wave keeps its own softmax state; the 4 waves merge in LDS at the end and
+// write the same per-chunk partials as the VALU kernel.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return f2bf(lo) | (f2bf(hi) << 16);
+}
+
+template <int DK>   // head_dim / 32
+__global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
+  constexpr int ATT_MAXDK = DK, ATT_MAXDT = 2 * DK;
+  const int c = blockIdx.x, j = blockIdx.y, r = blockIdx.z;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 15, q4 = lane >> 4;
+  int b, L, prefix, total;
+  uint64_t bits;
+  if (!row_range(a, r, b, L, prefix, total, bits)) {
+    if (c == 0 && j == 0 && tid == 0) atomicOr(a.err, ERRF_CAPACITY);
+    return;
+  }
+  const int tbeg = c * ATT_S * a.nsub;
+  if (tbeg >= total) return;                 // uniform across the workgroup
+  const int d = a.d, g = a.nq / a.nkv, ndk = d >> 5, ndt = d >> 4;
+
+  __shared__ bf16_t vt[4][32 * DK][16];     // per wave: V tile as [dim][slot]
+  __shared__ float mg_m[4][16], mg_l[4][16];
+  __shared__ float mg_o[4][ATT_MAXGD];
+
+  // q of head `col` as the B operand (k = dims 32 kk + 8 q4 .. +7), hi/lo
+  u32x4 qh[ATT_MAXDK], ql[ATT_MAXDK];
+#pragma unroll
+  for (int kk = 0; kk < ATT_MAXDK; ++kk) {
+    qh[kk] = ql[kk] = u32x4{0, 0, 0, 0};
+    if (kk < ndk && col < g) {
+      const float *qp = a.q + (size_t)r * a.nq * d + (size_t)(j * g + col) * d + 32 * kk + 8 * q4;
+      const f32x4 x0 = *(const f32x4 *)qp, x1 = *(const f32x4 *)(qp + 4);
+      const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      float hi[8], lo[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        hi[e] = bf2f(f2bf(x[e]));
+        lo[e] = x[e] - hi[e];
+      }
+      qh[kk] = u32x4{pack2(hi[0], hi[1]), pack2(hi[2], hi[3]), pack2(hi[4], hi[5]), pack2(hi[6], hi[7])};
+      ql[kk] = u32x4{pack2(lo[0], lo[1]), pack2(lo[2], lo[3]), pack2(lo[4], lo[5]), pack2(lo[6], lo[7])};
+    }
+  }
+  float m_run = -INFINITY, l_run = 0.f;      // softmax state of head `col`
+  f32x4 o[ATT_MAXDT];                         // O[head 4 q4 + i][dim 16 dt + col]
+#pragma unroll
+  for (int dt = 0; dt < ATT_MAXDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int sub = 0; sub < a.nsub; ++sub) {
+    const int t0 = tbeg + sub * ATT_S;
+    if (t0 >= total) break;                   // uniform
+    // this lane's slot: row `col` of the wave's 16-slot tile
+    const int t = t0 + 16 * wave + col;
+    long off = -1;
+    if (t < total && (t < prefix || (a.bits && t >= L && ((bits >> (t - L)) & 1ull)))) {
+      const int bi = t / a.kv.bs;
+      const int blk = bi < a.kv.mbps ? a.kv.block_table[(size_t)b * a.kv.mbps + bi] : -1;
+      // pool layout [block, kv head, slot in block, d]
+      if (blk < 0 || blk >= a.kv.n_blocks) atomicOr(a.err, ERRF_CAPACITY);
+      else off = ((long)blk * a.nkv + j) * a.kv.bs * d + (long)(t % a.kv.bs) * d;
+    }
+    u32x4 ka[ATT_MAXDK], va[ATT_MAXDK];
+#pragma unroll
+    for (int kk = 0; kk < ATT_MAXDK; ++kk) {
+      ka[kk] = va[kk] = u32x4{0, 0, 0, 0};
+      if (kk < ndk && off >= 0) {
+        ka[kk] = *(const u32x4 *)((const bf16_t *)a.kv.k_pool + off + 32 * kk + 8 * q4);
+        va[kk] = *(const u32x4 *)((const bf16_t *)a.kv.v_pool + off + 32 * kk + 8 * q4);
+      }
+    }
+    // scores S[slot 4 q4 + i][head col]
+    f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < ATT_MAXDK; ++kk) {
+      if (kk < ndk) {
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
+                                                      __builtin_bit_cast(bf16x8, qh[kk]), sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
+                                                      __builtin_bit_cast(bf16x8, ql[kk]), sc, 0, 0, 0);
+      }
+    }
+    const int vis = off >= 0 ? 1 : 0;
+    float sv[4] = {sc.x, sc.y, sc.z, sc.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int vi = __shfl(vis, 4 * q4 + i, 64);
+      sv[i] = vi ? sv[i] * a.scale : -INFINITY;
+    }
+    // online softmax of head col over these 16 slots (lanes col, col^16, ...)
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m_run, mx);
+    const float al = m_run == -INFINITY ? 0.f : expf(m_run - mn);
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = sv[i] == -INFINITY ? 0.f : expf(sv[i] - mn);
+    float ps = (p[0] + p[1]) + (p[2] + p[3]);
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * al + ps;
+    m_run = mn;
+    // V tile -> LDS as [dim][slot]
+#pragma unroll
+    for (int kk = 0; kk < ATT_MAXDK; ++kk) {
+      if (kk < ndk) {
+        const uint32_t w4[4] = {va[kk].x, va[kk].y, va[kk].z, va[kk].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vt[wave][32 * kk + 8 * q4 + 2 * e][col] = (bf16_t)(w4[e] & 0xffffu);
+          vt[wave][32 * kk + 8 * q4 + 2 * e + 1][col] = (bf16_t)(w4[e] >> 16);
+        }
+      }
+    }
+    __syncthreads();
+    // rescale O rows (heads 4 q4 + i) by their alpha, then O += P V
+    float ah[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ah[i] = __shfl(al, 4 * q4 + i, 64);
+    float ph[4], pl[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ph[i] = bf2f(f2bf(p[i]));
+      pl[i] = p[i] - ph[i];
+    }
+    const s16x4 pah = __builtin_bit_cast(s16x4, uint2{pack2(ph[0], ph[1]), pack2(ph[2], ph[3])});
+    const s16x4 pal = __builtin_bit_cast(s16x4, uint2{pack2(pl[0], pl[1]), pack2(pl[2], pl[3])});
+#pragma unroll
+    for (int dt = 0; dt < ATT_MAXDT; ++dt) {
+      if (dt < ndt) {
+        o[dt].x *= ah[0]; o[dt].y *= ah[1]; o[dt].z *= ah[2]; o[dt].w *= ah[3];
+        const s16x4 vb = *(const s16x4 *)&vt[wave][16 * dt + col][4 * q4];
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pah, vb, o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pal, vb, o[dt], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+  // merge the 4 waves' states and write this chunk's partials
+  if (q4 == 0) {
+    mg_m[wave][col] = m_run;
+    mg_l[wave][col] = l_run;
+  }
+#pragma unroll
+  for (int dt = 0; dt < ATT_MAXDT; ++dt)
+    if (dt < ndt) {
+      const float ov[4] = {o[dt].x, o[dt].y, o[dt].z, o[dt].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int h = 4 * q4 + i;
+        if (h < g) mg_o[wave][h * d + 16 * dt + col] = ov[i];
+      }
+    }
+  __syncthreads();
+  for (int e = tid; e < g * d; e += 256) {
+    const int h = e / d, dim = e % d;
+    float M = -INFINITY;
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, mg_m[w][h]);
+    float lsum = 0.f, osum = 0.f;
+    for (int w = 0; w < 4; ++w) {
+      const float wt = mg_m[w][h] == -INFINITY ? 0.f : expf(mg_m[w][h] - M);
+      lsum += mg_l[w][h] * wt;
+      osum += mg_o[w][e] * wt;
+    }
+    const size_t pi = ((size_t)r * a.nq + j * g + h) * a.nch + c;
+    a.po[pi * d + dim] = osum;
+    if (dim == 0) {
+      a.pm[pi] = M;
+      a.pl[pi] = lsum;
+    }
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   __shared__ float wch[ATT_MAXCH];
@@ -334,7 +519,10 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   a.err = err;
   dim3 g1(a.nch, nkv, R), g2(nq, R);
   if (bf16) {
-    hipLaunchKernelGGL(k_attn_partial<bf16_t>, g1, dim3(256), 0, s, a);
+    if (d == 64) hipLaunchKernelGGL(k_attn_mfma<2>, g1, dim3(256), 0, s, a);
+    else if (d == 128) hipLaunchKernelGGL(k_attn_mfma<4>, g1, dim3(256), 0, s, a);
+    else if (d == 256) hipLaunchKernelGGL(k_attn_mfma<8>, g1, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_attn_partial<bf16_t>, g1, dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_attn_combine<bf16_t>, g2, dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL(k_attn_partial<float>, g1, dim3(256), 0, s, a);

@@ -1,0 +1,135 @@
+"""Boundary behaviour of the C ABI on the GPU: status codes, device-side
+bounds flags, isolation of unused parameter sets, graph replay with new
+device data.  Every error here is caught by host validation or by the
+kernels' own bounds checks (no out-of-range access is ever issued)."""
+import numpy as np
+import pytest
+import torch
+
+from synth import SMALL_BF16_CHAIN, make_inputs, make_weights
+from harness import gpu_setup
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+CFG = SMALL_BF16_CHAIN
+
+
+def _drafter(cfg, **kw):
+    from paper_2602_01762_amd import Drafter
+    return Drafter(cfg, **kw)
+
+
+def test_unloaded_set_is_reported():
+    from paper_2602_01762_amd import PrismError
+    w = make_weights(CFG, "cuda")
+    inp = make_inputs(CFG, "cuda")
+    dr = _drafter(CFG)
+    dr.load(w, sets=[0, 1])            # sets 2 and 3 missing (weights list truncated below)
+    with pytest.raises(PrismError) as e:
+        dr.chain(inp)
+    assert e.value.status == -3        # PRISM_ERR_NOT_LOADED
+    # a chain that only reaches loaded sets works
+    out = dr.chain(inp, K=2)
+    torch.cuda.synchronize()
+    assert (out["tokens"] >= 0).all()
+    dr.close()
+
+
+def test_set_serving_two_feature_widths_is_unsupported():
+    from paper_2602_01762_amd import PrismError
+    cfg = CFG.with_(f_map=(0, 0, 0, 0), n_sets=1)   # F_t = 1536 != H = 512
+    w = make_weights(CFG, "cuda", sets=[0])
+    inp = make_inputs(cfg, "cuda")
+    dr = _drafter(cfg)
+    dr.set_step_map(cfg.fmap)
+    dr.load(w)
+    with pytest.raises(PrismError) as e:
+        dr.chain(inp)
+    assert e.value.status == -4        # PRISM_ERR_UNSUPPORTED
+    assert dr.chain(inp, K=1)["tokens"].shape == (CFG.batch, 1)
+    dr.close()
+
+
+def test_short_block_table_raises_capacity_flag():
+    cfg = CFG.with_(ctx_range=None, ctx_len=32 * 16)      # context fills whole blocks
+    w = make_weights(cfg, "cuda")
+    inp = make_inputs(cfg, "cuda")
+    mbps = 32                                              # no block left for draft slots
+    dr = _drafter(cfg, max_blocks_per_seq=mbps)
+    dr.load(w)
+    inp.block_table = inp.block_table[:, :mbps].contiguous()
+    dr.chain(inp)
+    torch.cuda.synchronize()
+    assert dr.device_status() == -7    # PRISM_ERR_CAPACITY
+    assert dr.device_status() == 0     # flags are cleared by the read
+    dr.close()
+
+
+def test_out_of_range_token_raises_flag():
+    dr, w, inp = gpu_setup(CFG)
+    bad = inp.tokens.clone()
+    bad[0] = CFG.vocab + 5
+    inp.tokens = bad
+    dr.chain(inp)
+    torch.cuda.synchronize()
+    assert dr.device_status() == -1    # PRISM_ERR_INVALID_ARG
+    dr.close()
+
+
+def test_unused_sets_with_nan_do_not_leak():
+    dr, w, inp = gpu_setup(CFG)
+    ref = dr.chain(inp, K=2, logits=True)
+    torch.cuda.synchronize()
+    for s in (2, 3):
+        ps = w.sets[s]
+        for name in ("w_fc", "w_q", "w_k", "w_v", "w_o", "w_gate", "w_up", "w_down", "g1", "g2"):
+            getattr(ps, name).fill_(float("nan"))
+        dr.load_set(s, ps)
+    out = dr.chain(inp, K=2, logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out["tokens"], ref["tokens"])
+    assert torch.equal(out["logits"], ref["logits"])
+    dr.close()
+
+
+def test_graph_replay_reads_new_context_lengths():
+    dr, w, inp = gpu_setup(CFG)
+    out = dr.chain_buffers(CFG.batch, CFG.n_steps, logits=True)
+    b = dr.batch(inp)
+    dr.chain(inp, out=out, batch=b)               # captures the graph
+    lens = inp.ctx_lens.clone()
+    inp.ctx_lens.sub_(3)                           # same buffer, shorter contexts
+    dr.chain(inp, out=out, batch=b)               # replays the same graph
+    torch.cuda.synchronize()
+    got = {k: v.clone() for k, v in out.items() if v is not None}
+    fresh = _drafter(CFG)
+    fresh.load(w)
+    ref = fresh.chain(inp, logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(got["tokens"], ref["tokens"])
+    assert torch.equal(got["logits"], ref["logits"])
+    inp.ctx_lens.copy_(lens)
+    fresh.close()
+    dr.close()
+
+
+def test_bad_host_arguments():
+    from paper_2602_01762_amd import PrismError, binding as B
+    dr, w, inp = gpu_setup(CFG)
+    b = dr.batch(inp)
+    b.batch = CFG.batch + 1                        # above max_batch
+    with pytest.raises(PrismError) as e:
+        B.prism_draft_chain(dr.ctx, b, 2, torch.empty((8, 2), dtype=torch.int32, device="cuda"))
+    assert e.value.status == -1
+    b = dr.batch(inp)
+    with pytest.raises(PrismError) as e:
+        B.prism_draft_chain(dr.ctx, b, CFG.n_steps + 1, torch.empty((8, 9), dtype=torch.int32, device="cuda"))
+    assert e.value.status == -1
+    with pytest.raises(PrismError) as e:
+        B.prism_set_step_map(dr.ctx, [0, 7])       # set out of range
+    assert e.value.status == -1
+    with pytest.raises(PrismError) as e:
+        dr.tree(inp)                               # context created without a tree width
+    assert e.value.status == -1
+    dr.close()
