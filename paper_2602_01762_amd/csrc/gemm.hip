@@ -595,7 +595,10 @@ static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
 template <typename T, bool PAIR>
 static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
   if (g.split > 0) {
-    if (g.nt == 4) {
+    if (g.nt == 8) {
+      if (g.R <= 16) gemm_split_launch<T, 1, 8, PAIR>(g, s);
+      else gemm_split_launch<T, 2, 8, PAIR>(g, s);
+    } else if (g.nt == 4) {
       if (g.R <= 16) gemm_split_launch<T, 1, 4, PAIR>(g, s);
       else if (g.R <= 32) gemm_split_launch<T, 2, 4, PAIR>(g, s);
       else gemm_split_launch<T, 4, 2, PAIR>(g, s);
@@ -647,6 +650,11 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
       else hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 4>), grid, blk, lds, s, g);
       return;
     }
+  }
+  if (g.nt == 8) {   // eight tiles per wave share each B fragment (up to 32 rows)
+    if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 8, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 2, 8, PAIR, 0>), grid, blk, 0, s, g);
+    return;
   }
   if (g.nt == 4) {   // four tiles per wave share each B fragment (batched rows)
     if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 4, PAIR, 0>), grid, blk, 0, s, g);

@@ -147,6 +147,7 @@ static Plan plan_for(const TiledMat &t, int R) {
 // k-blocks per slice).
 static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
+  if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
   if (R > 32 && nt == 4) nt = 2;
   const int wgs = (t.n_tiles / nt + 3) / 4;
   int sp = (512 + wgs - 1) / wgs;
@@ -273,7 +274,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   if (rows > 4) {   // batched products: K-slice partial sums
     size_t pn = 0;
     auto upd = [&](int N, int K) {   // the plan depends on the row count: take both regimes
-      for (int rr : {5, rows}) {
+      for (int rr = 5; rr <= rows; ++rr) {
         int nt, sp;
         plan_batched(make_tiled(N, K, bf16), rr, nt, sp);
         if ((size_t)sp * N > pn) pn = (size_t)sp * N;
@@ -573,7 +574,8 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   lmg.gemv = (c->bf16 && R <= 4 && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
   lmg.nt = 1;
   if (!lmg.gemv && R > 4) {   // batched rows: several vocab tiles per wave share B fragments
-    if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
+    if (R > 16 && R <= 32 && c->lm.n_tiles % 8 == 0) lmg.nt = 8;
+    else if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
     else if (c->lm.n_tiles % 2 == 0) lmg.nt = 2;
   }
   lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);

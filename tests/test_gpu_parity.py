@@ -38,6 +38,17 @@ def test_chain_parity_small(cfg):
     run_chain_parity(cfg)
 
 
+# Batched row counts: 17-32 rows take two 16-row groups and eight tiles per
+# wave where the tile count allows (vocabulary 5120 = 320 tiles), more than 32
+# rows take four groups; every sequence is compared.
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24", batch=24, vocab=5120),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs40", batch=40, ctx_range=(20, 300)),
+], ids=lambda c: c.name)
+def test_chain_parity_batched_rows(cfg):
+    run_chain_parity(cfg)
+
+
 def test_chain_deterministic_and_poison_free():
     cfg = SMALL_BF16_CHAIN
     dr, w, inp = gpu_setup(cfg)
