@@ -113,4 +113,30 @@ __device__ __forceinline__ void block_argmax(float &v, int &id, float *shv, int 
 
 __device__ __forceinline__ float silu(float y) { return y / (1.0f + expf(-y)); }
 
+// Token of row r from the LM head's top-1 partials (larger logit wins, ties
+// -> lower id).  Every thread of the block calls it (block reduction) and
+// gets the result; shv / shi hold one entry per wave.
+constexpr int TOK_UNROLL = 4;
+__device__ __forceinline__ int token_from_lm(const TokFromLm &t, int r, float *shv, int *shi) {
+  float bv = -INFINITY;
+  int bid = 0x7fffffff;
+  const float *pv = t.pval + (size_t)r * t.n_wg;
+  const int *pi = t.pid + (size_t)r * t.n_wg;
+  for (int i0 = 0; i0 < t.n_wg; i0 += TOK_UNROLL * (int)blockDim.x) {
+    float v[TOK_UNROLL];
+    int id[TOK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < TOK_UNROLL; ++u) {   // all loads first, then the compares
+      const int i = i0 + u * blockDim.x + threadIdx.x;
+      v[u] = i < t.n_wg ? pv[i] : -INFINITY;
+      id[u] = i < t.n_wg ? pi[i] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int u = 0; u < TOK_UNROLL; ++u)
+      if (better(v[u], id[u], bv, bid)) { bv = v[u]; bid = id[u]; }
+  }
+  block_argmax(bv, bid, shv, shi);
+  return bid;
+}
+
 }  // namespace prism

@@ -94,9 +94,78 @@ constexpr int UV = 16;
 __device__ __forceinline__ float lo_bf(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Staging of gathered fusion-FC rows x_r = [E(token_r) ; feature row] (K =
+// H + F columns) as fp32: the tokens come from the rows or from the previous
+// LM head's partials; an out-of-range token flags ERRF_TOKEN and reads as a
+// zero embedding.
+template <int RR>
+__device__ __forceinline__ void stage_gather(const Gather &gx, int R, int K, float *xs,
+                                             uint32_t *err) {
+  __shared__ int s_tok[RR];
+  __shared__ float s_v[16];
+  __shared__ int s_i[16];
+  const bool lead = blockIdx.x == 0 && threadIdx.x == 0;
+  for (int r = 0; r < R; ++r) {
+    int tok;
+    if (gx.lm.pval) {
+      tok = token_from_lm(gx.lm, r, s_v, s_i);
+      if (lead && gx.lm.rec) gx.lm.rec[(size_t)r * gx.lm.ld_rec] = tok;
+    } else {
+      tok = gx.in.tokens[r];
+    }
+    if (tok < 0 || tok >= gx.V) {
+      if (lead) atomicOr(err, ERRF_TOKEN);
+      tok = -1;
+    }
+    if (threadIdx.x == 0) s_tok[r] = tok;
+  }
+  __syncthreads();
+  const int H = gx.H;
+  for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
+    const int r = i / K, k = i % K;
+    float v[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) v[m] = 0.f;
+    if (r < R) {
+      if (k < H) {
+        const int tok = s_tok[r];
+        if (tok >= 0) {
+          const u32x4 e = *(const u32x4 *)((const bf16_t *)gx.embed + (size_t)tok * H + k);
+          const uint32_t ew[4] = {e.x, e.y, e.z, e.w};
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            v[2 * m] = lo_bf(ew[m]);
+            v[2 * m + 1] = hi_bf(ew[m]);
+          }
+        }
+      } else {
+        const int fr = gx.in.feat_rows ? gx.in.feat_rows[r] : r;
+        const size_t o = (size_t)fr * gx.in.feat_ld + (k - H);
+        if (gx.in.feat_bf16) {
+          const u32x4 f = *(const u32x4 *)((const bf16_t *)gx.in.feat + o);
+          const uint32_t fw[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            v[2 * m] = lo_bf(fw[m]);
+            v[2 * m + 1] = hi_bf(fw[m]);
+          }
+        } else {
+          const f32x4 f0 = *(const f32x4 *)((const float *)gx.in.feat + o);
+          const f32x4 f1 = *(const f32x4 *)((const float *)gx.in.feat + o + 4);
+          v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+          v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
+        }
+      }
+    }
+    *(f32x4 *)(xs + i) = f32x4{v[0], v[1], v[2], v[3]};
+    *(f32x4 *)(xs + i + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+}
+
 template <int RR>
 __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
-                                              int K, float *xs, int kb0, int kb1, f32x4 &out) {
+                                              int K, float *xs, int kb0, int kb1, f32x4 &out,
+                                              const Gather *gx = nullptr, uint32_t *err = nullptr) {
   const int lane = threadIdx.x & 63, kq = lane >> 4;
   const u32x4 z4 = {0, 0, 0, 0};
   const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
@@ -107,7 +176,8 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
     for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
   }
   // stage x rows (8 columns per thread step) as fp32
-  for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
+  if (gx && gx->embed) stage_gather<RR>(*gx, R, K, xs, err);
+  else for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
     const int r = i / K, k = i % K;
     float v[8];
     if (r < R) {
@@ -384,7 +454,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   if constexpr (VR > 0) {
     float *xs = (float *)&red[(kw - 1) * NT * RT * 64] + 64 * kw;
     mainloop_valu<VR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0, kb1,
-                      acc[0][0]);
+                      acc[0][0], &g.gx, g.err);
   } else {
     mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
                               kb1, acc);

@@ -75,6 +75,26 @@ struct RowsIn {
 
 enum Epi { EPI_NORM = 0, EPI_SWIGLU = 1, EPI_QKV = 2 };
 
+// Token of each row taken straight from the previous LM head's top-1
+// partials ([R][n_wg] values and ids; larger value wins, ties -> lower id),
+// so that no separate merge kernel runs between two chain steps.  The chosen
+// token is also recorded at rec[r * ld_rec] (one writer).
+struct TokFromLm {
+  const float *pval;   // NULL: tokens come from RowsIn::tokens
+  const int *pid;
+  int n_wg;
+  int32_t *rec; int ld_rec;
+};
+
+// Fusion-FC operand rows gathered by the product kernel itself:
+// x_r = [E(token_r) ; feature row], the GEMV path's staging step.
+struct Gather {
+  const void *embed;   // NULL: the operand comes as planes (GemmLaunch::x)
+  int V, H;
+  RowsIn in;           // tokens and feature rows
+  TokFromLm lm;
+};
+
 struct GemmLaunch {
   TiledMat m;
   Act x;
@@ -101,6 +121,7 @@ struct GemmLaunch {
   KvArgs kv;
   const double *inv_freq;
   uint32_t *err;
+  Gather gx;       // GEMV fusion FC: rows gathered from E and the features
 };
 
 struct LmLaunch {
@@ -131,8 +152,8 @@ void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_st
                    int row_offset, int rot_rows, int d, TiledMat &dst, hipStream_t s);
 
 // ---- launchers (misc.hip) -------------------------------------------------
-void launch_fc_prep(bool bf16, int R, const RowsIn &in, const void *embed, int V, int H, int F,
-                    ActOut X, uint32_t *err, hipStream_t s);
+void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
+                    int V, int H, int F, ActOut X, uint32_t *err, hipStream_t s);
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
                       const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
                       ActOut o, uint32_t *err, hipStream_t s);

@@ -9,8 +9,11 @@ namespace prism {
 // X[r] = [E(token_r) ; feature row] as the FC's operand planes.  Embeddings
 // and target features are exact in the storage type (lo = 0); a fp32 feature
 // (the draft's own hidden state) is split into its hi/lo pair.
+// The row's token is RowsIn::tokens[r], or the argmax of the previous LM
+// head's top-1 partials (then recorded by one workgroup).
 struct FcPrepArgs {
   RowsIn in;
+  TokFromLm lm;
   const void *embed;
   int V, H, F;
   ActOut X;
@@ -19,10 +22,18 @@ struct FcPrepArgs {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
+  __shared__ float shv[4];
+  __shared__ int shi[4];
   const int r = blockIdx.y;
+  int tok;
+  if (a.lm.pval) {
+    tok = token_from_lm(a.lm, r, shv, shi);
+    if (a.lm.rec && blockIdx.x == 0 && threadIdx.x == 0) a.lm.rec[(size_t)r * a.lm.ld_rec] = tok;
+  } else {
+    tok = a.in.tokens[r];
+  }
   const int e0 = (blockIdx.x * 256 + threadIdx.x) * 8;   // 8 consecutive columns
   if (e0 >= a.H + a.F) return;
-  int tok = a.in.tokens[r];
   if (tok < 0 || tok >= a.V) {
     if (e0 == 0) atomicOr(a.err, ERRF_TOKEN);
     tok = -1;
@@ -65,9 +76,9 @@ __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
   }
 }
 
-void launch_fc_prep(bool bf16, int R, const RowsIn &in, const void *embed, int V, int H, int F,
-                    ActOut X, uint32_t *err, hipStream_t s) {
-  FcPrepArgs a{in, embed, V, H, F, X, err};
+void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
+                    int V, int H, int F, ActOut X, uint32_t *err, hipStream_t s) {
+  FcPrepArgs a{in, lm, embed, V, H, F, X, err};
   dim3 grid((H + F + 2047) / 2048, R);
   if (bf16) hipLaunchKernelGGL(k_fc_prep<bf16_t>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(k_fc_prep<float>, grid, dim3(256), 0, s, a);

@@ -33,6 +33,8 @@ struct Plan {
 struct Pass {            // one forward pass: where its inputs and outputs live
   int set, R, F, topk;
   RowsIn in;
+  TokFromLm lm_in;        // tokens from the previous pass's LM partials (pval != NULL)
+  bool defer_merge;       // leave the LM partials to the next pass (chain, top-1)
   float *hid_out; int ld_hid;
   float *logits; long ld_logits;
   int *ids; float *logp;
@@ -79,6 +81,7 @@ struct prism_ctx {
   int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
   uint64_t *t_bits[2] = {nullptr, nullptr};
   int nsub = 1;                     // attention: 64-slot steps per workgroup
+  int lm_nwg_last = 0;              // LM-head partial count of the pass last enqueued
   size_t lds_limit = 65536;         // LDS bytes one workgroup may use
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
@@ -134,6 +137,9 @@ static Plan plan_for(const TiledMat &t, int R) {
   int kw = (4096 + groups - 1) / groups;
   const int max_kw = rt * p.nt >= 2 ? MAX_KW / 2 : MAX_KW;   // see gemm_max_threads
   if (kw > max_kw) kw = max_kw;
+  // up to 2 workgroups per CU: keep them co-resident (16 waves per CU) so
+  // that a grid of, e.g., 1.5 workgroups per CU runs in one round
+  if (groups <= 512 && groups > 256 && kw > 8) kw = 8;
   if (kw > t.nkb / 4) kw = t.nkb / 4;
   if (kw < 1) kw = 1;
   // LDS for the cross-wave sum: (kw - 1) * nt * rt KiB
@@ -534,8 +540,13 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   // fusion FC: u = W_fc [E(x) ; f]  ->  u, (u * g1), sums of squares
   ActOut X = c->xfc;
   X.ld = H + p.F;
-  launch_fc_prep(bf, R, p.in, c->embed, c->V, H, p.F, X, c->err, s);
   GemmLaunch g = gemm_of(c, S.fc, act_of(X, H + p.F), R, EPI_NORM);
+  if (g.gemv) {   // the GEMV stages [E(x) ; f] itself
+    g.gx.embed = c->embed; g.gx.V = c->V; g.gx.H = H; g.gx.in = p.in; g.gx.lm = p.lm_in;
+    g.err = c->err;
+  } else {
+    launch_fc_prep(bf, R, p.in, p.lm_in, c->embed, c->V, H, p.F, X, c->err, s);
+  }
   g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
   launch_gemm(bf, g, s);
   // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
@@ -587,8 +598,10 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
   launch_lmhead(bf, lmg, s);
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used++ + 1], s);
-  launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
-                    p.logp, p.tok_a, p.tok_b, p.ld_b, s);
+  c->lm_nwg_last = lmg.n_wg;
+  if (!p.defer_merge)
+    launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
+                      p.logp, p.tok_a, p.tok_b, p.ld_b, s);
 }
 
 static prism_status check_set(prism_ctx *c, int step, int want_F) {
@@ -726,7 +739,12 @@ prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K
       p.R = B;
       p.F = k == 1 ? c->cfg.feat_width : H;
       p.topk = 1;
-      p.in.tokens = k == 1 ? c->c_tok0 : c->tokbuf;
+      p.in.tokens = c->c_tok0;      // step 1; later steps take the previous LM partials
+      if (k > 1) {
+        p.lm_in.pval = c->lm_val; p.lm_in.pid = c->lm_id; p.lm_in.n_wg = c->lm_nwg_last;
+        p.lm_in.rec = d_out_tokens + (k - 2); p.lm_in.ld_rec = K;
+      }
+      p.defer_merge = k < K;
       p.in.feat = k == 1 ? b.d_features : (const void *)prev;
       p.in.feat_bf16 = k == 1 ? (int)c->bf16 : 0;
       p.in.feat_ld = k == 1 ? c->cfg.feat_width : ld_prev;
