@@ -36,17 +36,21 @@ struct AttnArgs {
 
 __device__ __forceinline__ bool row_range(const AttnArgs &a, int r, int &b, int &L, int &prefix,
                                           int &total, uint64_t &bits) {
+  // the row's own entries are loaded together; only the tree's context
+  // length depends on the sequence index
   b = a.seq[r];
+  const int slot = a.bits ? 0 : a.slot[r];
+  const uint64_t bw = a.bits ? a.bits[r] : 0ull;
   L = prefix = total = 0;
   bits = 0ull;
   if (b < 0 || b >= a.kv.n_seq) return false;
   if (a.bits) {
     L = a.kv.ctx_lens[b];
-    bits = a.bits[r];
+    bits = bw;
     prefix = L;
     total = L + (bits ? 64 - __clzll((long long)bits) : 0);
   } else {   // causal: the slot alone bounds the range (no context-length load)
-    prefix = a.slot[r] + 1;
+    prefix = slot + 1;
     total = prefix;
   }
   return true;
@@ -259,14 +263,27 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 // MFMA tile (K rows as the A operand, q as the B operand carried as a
 // hi/lo bf16 pair), the online softmax runs per head with lane shuffles, and
 // P.V is a 16x16x16 MFMA per 16 dims with P (hi/lo pair) straight from the
-// score layout and V transposed through a small per-wave LDS tile.  Each
-// wave keeps its own softmax state; the 4 waves merge in LDS at the end and
-// write the same per-chunk partials as the VALU kernel.
+// score layout and V transposed through the wave's own LDS tile.  The
+// chunk's block-table entries are staged in LDS once, and each wave loads
+// the K/V rows of its next step before it computes the current one, so the
+// waves stream independently.  Each wave keeps its own softmax state; the 4
+// waves merge in LDS at the end and write the same per-chunk partials as the
+// VALU kernel.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return f2bf(lo) | (f2bf(hi) << 16);
 }
+
+// order the wave's LDS writes before its later reads (and the reverse): the
+// tile is private to the wave, so no workgroup barrier is needed
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+constexpr int ATT_MAXSUB = 8;    // 64-slot steps per workgroup
 
 template <int DK>   // head_dim / 32
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
@@ -280,13 +297,25 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     if (c == 0 && j == 0 && tid == 0) atomicOr(a.err, ERRF_CAPACITY);
     return;
   }
-  const int tbeg = c * ATT_S * a.nsub;
+  const int span = ATT_S * a.nsub;
+  const int tbeg = c * span;
   if (tbeg >= total) return;                 // uniform across the workgroup
   const int d = a.d, g = a.nq / a.nkv, ndk = d >> 5, ndt = d >> 4;
+  const int bs = a.kv.bs;
 
   __shared__ bf16_t vt[4][32 * DK][16];     // per wave: V tile as [dim][slot]
   __shared__ float mg_m[4][16], mg_l[4][16];
   __shared__ float mg_o[4][ATT_MAXGD];
+  __shared__ int s_blk[ATT_S * ATT_MAXSUB];  // physical blocks of the chunk's slots
+
+  // block-table entries of the chunk (at most one per slot)
+  const int tend = min(total, tbeg + span);
+  const int bfirst = tbeg / bs;
+  const int nblk = (tend - 1) / bs - bfirst + 1;
+  for (int i = tid; i < nblk; i += 256) {
+    const int bi = bfirst + i;
+    s_blk[i] = bi < a.kv.mbps ? a.kv.block_table[(size_t)b * a.kv.mbps + bi] : -1;
+  }
 
   // q of head `col` as the B operand (k = dims 32 kk + 8 q4 .. +7), hi/lo
   u32x4 qh[ATT_MAXDK], ql[ATT_MAXDK];
@@ -307,25 +336,20 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       ql[kk] = u32x4{pack2(lo[0], lo[1]), pack2(lo[2], lo[3]), pack2(lo[4], lo[5]), pack2(lo[6], lo[7])};
     }
   }
-  float m_run = -INFINITY, l_run = 0.f;      // softmax state of head `col`
-  f32x4 o[ATT_MAXDT];                         // O[head 4 q4 + i][dim 16 dt + col]
-#pragma unroll
-  for (int dt = 0; dt < ATT_MAXDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();                            // s_blk
 
-  for (int sub = 0; sub < a.nsub; ++sub) {
-    const int t0 = tbeg + sub * ATT_S;
-    if (t0 >= total) break;                   // uniform
-    // this lane's slot: row `col` of the wave's 16-slot tile
-    const int t = t0 + 16 * wave + col;
-    long off = -1;
-    if (t < total && (t < prefix || (a.bits && t >= L && ((bits >> (t - L)) & 1ull)))) {
-      const int bi = t / a.kv.bs;
-      const int blk = bi < a.kv.mbps ? a.kv.block_table[(size_t)b * a.kv.mbps + bi] : -1;
-      // pool layout [block, kv head, slot in block, d]
-      if (blk < 0 || blk >= a.kv.n_blocks) atomicOr(a.err, ERRF_CAPACITY);
-      else off = ((long)blk * a.nkv + j) * a.kv.bs * d + (long)(t % a.kv.bs) * d;
+  // cache offset of slot t for this KV head, or -1 (not visible / no block)
+  auto slot_off = [&](int t) -> long {
+    if (t >= tend || !(t < prefix || (a.bits && t >= L && ((bits >> (t - L)) & 1ull)))) return -1;
+    const int blk = s_blk[t / bs - bfirst];
+    // pool layout [block, kv head, slot in block, d]
+    if (blk < 0 || blk >= a.kv.n_blocks) {
+      atomicOr(a.err, ERRF_CAPACITY);
+      return -1;
     }
-    u32x4 ka[ATT_MAXDK], va[ATT_MAXDK];
+    return ((long)blk * a.nkv + j) * bs * d + (long)(t % bs) * d;
+  };
+  auto load_kv = [&](long off, u32x4 (&ka)[ATT_MAXDK], u32x4 (&va)[ATT_MAXDK]) {
 #pragma unroll
     for (int kk = 0; kk < ATT_MAXDK; ++kk) {
       ka[kk] = va[kk] = u32x4{0, 0, 0, 0};
@@ -334,6 +358,24 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         va[kk] = *(const u32x4 *)((const bf16_t *)a.kv.v_pool + off + 32 * kk + 8 * q4);
       }
     }
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;      // softmax state of head `col`
+  f32x4 o[ATT_MAXDT];                         // O[head 4 q4 + i][dim 16 dt + col]
+#pragma unroll
+  for (int dt = 0; dt < ATT_MAXDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // this lane's slot of a step: row `col` of the wave's 16-slot tile
+  long off = slot_off(tbeg + 16 * wave + col);
+  u32x4 ka[ATT_MAXDK], va[ATT_MAXDK];
+  load_kv(off, ka, va);
+  for (int sub = 0; sub < a.nsub; ++sub) {
+    const int t0 = tbeg + sub * ATT_S;
+    if (t0 >= tend) break;                    // uniform
+    // next step's rows, in flight while this step computes
+    const long off_n = sub + 1 < a.nsub ? slot_off(t0 + ATT_S + 16 * wave + col) : -1;
+    u32x4 kn[ATT_MAXDK], vn[ATT_MAXDK];
+    load_kv(off_n, kn, vn);
     // scores S[slot 4 q4 + i][head col]
     f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -378,7 +420,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         }
       }
     }
-    __syncthreads();
+    wave_lds_sync();
     // rescale O rows (heads 4 q4 + i) by their alpha, then O += P V
     float ah[4];
 #pragma unroll
@@ -400,7 +442,13 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pal, vb, o[dt], 0, 0, 0);
       }
     }
-    __syncthreads();
+    wave_lds_sync();                          // reads done before the next step's writes
+    off = off_n;
+#pragma unroll
+    for (int kk = 0; kk < ATT_MAXDK; ++kk) {
+      ka[kk] = kn[kk];
+      va[kk] = vn[kk];
+    }
   }
   // merge the 4 waves' states and write this chunk's partials
   if (q4 == 0) {

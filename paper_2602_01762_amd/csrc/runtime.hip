@@ -149,15 +149,18 @@ static Plan plan_for(const TiledMat &t, int R) {
 }
 
 // Batched products (more than 4 rows): tiles per wave (B fragment reuse) and
-// K slices across workgroups (about 512 workgroups of 4 waves, at least 4
-// k-blocks per slice).
+// K slices across workgroups: about one workgroup of 4 waves per CU (longer
+// slices stream better than more of them), at least 4 k-blocks per slice,
+// and fp32 slice partials of at most 1/8 of the weight bytes
+// (split * R * N * 4 <= N * K * 2 / 8).
 static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
   if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
   if (R > 32 && nt == 4) nt = 2;
   const int wgs = (t.n_tiles / nt + 3) / 4;
-  int sp = (512 + wgs - 1) / wgs;
+  int sp = (256 + wgs - 1) / wgs;
   if (sp > t.nkb / 4) sp = t.nkb / 4;
+  if (sp > t.K / (16 * R)) sp = t.K / (16 * R);
   split = sp < 1 ? 1 : sp;
 }
 
@@ -229,9 +232,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
   c->rows_max = rows;
   c->max_slots = k.max_blocks_per_seq * k.kv_block_size;
-  // attention steps per workgroup: keep the grid near 8K workgroups
+  // attention steps per workgroup: at most about 2K (row, head, chunk) units,
+  // so that each workgroup streams several steps after its lookups
   c->nsub = 1;
-  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 8192)
+  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 2048)
     c->nsub *= 2;
   c->nch = attention_chunks(c->max_slots, c->nsub);
   if (c->nch > 1024) {
