@@ -105,7 +105,6 @@ void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, floa
 // Merge the LM-head partials of row r:
 //   lse = M + log(sum_i s_i exp(m_i - M)),  top-k by (logit desc, id asc),
 //   log-prob = logit - lse.
-constexpr int MAXK = MAX_TOPK;
 constexpr int CMB_UNROLL = 8;
 struct LmCombArgs {
   int R, n_wg, topk, V;
@@ -117,6 +116,10 @@ struct LmCombArgs {
   int *tok_b; int ld_b; // optional [R * ld_b]: ids[r][0]
 };
 
+// KB: a power of two >= topk; each thread keeps a sorted list of KB
+// candidates in registers (fixed indices, so no dynamic register indexing),
+// and the block then takes k rounds of arg-max over the list heads.
+template <int KB>
 __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   __shared__ float shv[8];
   __shared__ int shi[8];
@@ -152,10 +155,11 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   const int nc = a.n_wg * k;
   const float *pv = a.pval + (size_t)r * nc;
   const int *pi = a.pid + (size_t)r * nc;
-  // thread-local sorted top-k of a strided subset
-  float lv[MAXK];
-  int li[MAXK];
-  for (int j = 0; j < MAXK; ++j) { lv[j] = -INFINITY; li[j] = 0x7fffffff; }
+  // thread-local sorted list (best first) of a strided subset
+  float lv[KB];
+  int li[KB];
+#pragma unroll
+  for (int j = 0; j < KB; ++j) { lv[j] = -INFINITY; li[j] = 0x7fffffff; }
   for (int i0 = 0; i0 < nc; i0 += 256 * CMB_UNROLL) {
     float cv[CMB_UNROLL];
     int ci[CMB_UNROLL];
@@ -167,25 +171,27 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < CMB_UNROLL; ++u) {
-      const float v = cv[u];
-      const int id = ci[u];
-      if (!better(v, id, lv[k - 1], li[k - 1])) continue;
-      int j = k - 1;
-      while (j > 0 && better(v, id, lv[j - 1], li[j - 1])) {
-        lv[j] = lv[j - 1];
-        li[j] = li[j - 1];
-        --j;
-      }
-      lv[j] = v;
-      li[j] = id;
+      if (!better(cv[u], ci[u], lv[KB - 1], li[KB - 1])) continue;
+      lv[KB - 1] = cv[u];
+      li[KB - 1] = ci[u];
+#pragma unroll
+      for (int j = KB - 1; j > 0; --j)   // bubble the new entry to its place
+        if (better(lv[j], li[j], lv[j - 1], li[j - 1])) {
+          const float tv = lv[j]; lv[j] = lv[j - 1]; lv[j - 1] = tv;
+          const int ti = li[j]; li[j] = li[j - 1]; li[j - 1] = ti;
+        }
     }
   }
-  int head = 0;
   for (int j = 0; j < k; ++j) {
-    float v = head < k ? lv[head] : -INFINITY;
-    int id = head < k ? li[head] : 0x7fffffff;
+    float v = lv[0];
+    int id = li[0];
     block_argmax(v, id, shv, shi);
-    if (head < k && li[head] == id) ++head;
+    if (li[0] == id) {   // ids are distinct: exactly one thread owns the winner
+#pragma unroll
+      for (int q = 0; q < KB - 1; ++q) { lv[q] = lv[q + 1]; li[q] = li[q + 1]; }
+      lv[KB - 1] = -INFINITY;
+      li[KB - 1] = 0x7fffffff;
+    }
     if (tid == 0) {
       a.ids[(size_t)r * k + j] = id;
       if (a.logp) a.logp[(size_t)r * k + j] = v - lse;
@@ -201,7 +207,11 @@ void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, cons
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
                        int *tok_b, int ld_b, hipStream_t s) {
   LmCombArgs a{R, n_wg, topk, V, pmax, psum, pval, pid, ids, logp, tok_a, tok_b, ld_b};
-  hipLaunchKernelGGL(k_lm_combine, dim3(R), dim3(256), 0, s, a);
+  if (topk <= 1) hipLaunchKernelGGL(k_lm_combine<1>, dim3(R), dim3(256), 0, s, a);
+  else if (topk <= 2) hipLaunchKernelGGL(k_lm_combine<2>, dim3(R), dim3(256), 0, s, a);
+  else if (topk <= 4) hipLaunchKernelGGL(k_lm_combine<4>, dim3(R), dim3(256), 0, s, a);
+  else if (topk <= 8) hipLaunchKernelGGL(k_lm_combine<8>, dim3(R), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_lm_combine<16>, dim3(R), dim3(256), 0, s, a);
 }
 
 // ---------------------------------------------------------------------------
