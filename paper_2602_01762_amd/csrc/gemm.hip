@@ -635,8 +635,10 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   }
 }
 
+static_assert(GEMV_MAX_ROWS == 2, "GEMV variants cover 1 and 2 rows");
+
 size_t gemv_lds_bytes(int R, int K) {
-  const int vr = R <= 1 ? 1 : (R <= 2 ? 2 : 4);
+  const int vr = R <= 1 ? 1 : 2;
   return (size_t)vr * K * sizeof(float);
 }
 
@@ -686,8 +688,7 @@ static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
     if (g.gemv) {
       if (g.R <= 1) gemm_epi<T, 1, 1, PAIR, 1>(g, s);
-      else if (g.R <= 2) gemm_epi<T, 1, 1, PAIR, 2>(g, s);
-      else gemm_epi<T, 1, 1, PAIR, 4>(g, s);
+      else gemm_epi<T, 1, 1, PAIR, 2>(g, s);   // R <= GEMV_MAX_ROWS
       return;
     }
   }
@@ -715,9 +716,8 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
     if (g.gemv) {
       const size_t lds = gemv_lds_bytes(g.R, g.m.K);
-      if (g.R <= 1) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 1>), grid, blk, lds, s, g);
-      else if (g.R <= 2) hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 2>), grid, blk, lds, s, g);
-      else hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 4>), grid, blk, lds, s, g);
+      // one row (LM_GEMV_MAX_ROWS): more rows take the MFMA tiles
+      hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 1>), grid, blk, lds, s, g);
       return;
     }
   }

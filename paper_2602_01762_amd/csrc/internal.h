@@ -10,6 +10,11 @@ typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
 // device error flags (bit set by kernels on an out-of-range device value)
 enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u };
 
+// Rows up to which bf16 products (LM head) take the VALU GEMV main loop;
+// above it the staged-activation LDS reads, which grow with the rows, cost
+// more than the MFMA path's fixed 16-row tiles.
+constexpr int GEMV_MAX_ROWS = 2;
+constexpr int LM_GEMV_MAX_ROWS = 1;
 constexpr int MAX_TOPK = 16;    // largest top-k of the LM-head merge
 constexpr int MAX_TREE_CAND = 2048;
 constexpr int MAX_ROWS = 64;

@@ -148,11 +148,11 @@ static Plan plan_for(const TiledMat &t, int R) {
   return p;
 }
 
-// Batched products (more than 4 rows): tiles per wave (B fragment reuse) and
-// K slices across workgroups: about one workgroup of 4 waves per CU (longer
-// slices stream better than more of them), at least 4 k-blocks per slice,
-// and fp32 slice partials of at most 1/8 of the weight bytes
-// (split * R * N * 4 <= N * K * 2 / 8).
+// Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
+// fragment reuse) and K slices across workgroups: about one workgroup of 4
+// waves per CU (longer slices stream better than more of them), at least 4
+// k-blocks per slice, and fp32 slice partials of at most 1/8 of the weight
+// bytes (split * R * N * 4 <= N * K * 2 / 8).
 static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
   if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
@@ -281,10 +281,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   planes(c->z, R * c->I);
   add((void **)&c->hid[0], R * c->H * 4);
   add((void **)&c->hid[1], R * c->H * 4);
-  if (rows > 4) {   // batched products: K-slice partial sums
+  if (rows > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums
     size_t pn = 0;
     auto upd = [&](int N, int K) {   // the plan depends on the row count: take both regimes
-      for (int rr = 5; rr <= rows; ++rr) {
+      for (int rr = GEMV_MAX_ROWS + 1; rr <= rows; ++rr) {
         int nt, sp;
         plan_batched(make_tiled(N, K, bf16), rr, nt, sp);
         if ((size_t)sp * N > pn) pn = (size_t)sp * N;
@@ -508,7 +508,7 @@ static RowNorm norm_for(prism_ctx *c, const float *ss, float *scale, int R, int 
 // GEMV main loop (bf16, at most 4 rows) when the staged activations fit in
 // the workgroup's LDS next to the cross-wave partial sums
 static bool use_gemv(const prism_ctx *c, int R, int K, int kw) {
-  if (!c->bf16 || R > 4) return false;
+  if (!c->bf16 || R > GEMV_MAX_ROWS) return false;
   const size_t lds = gemv_lds_bytes(R, K) + (size_t)(kw - 1) * 64 * 16 + (size_t)64 * kw * 4;
   return lds <= c->lds_limit;
 }
@@ -519,7 +519,7 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   g.x = x;
   g.R = R;
   g.epi = epi;
-  if (R > 4) {
+  if (R > GEMV_MAX_ROWS) {
     plan_batched(m, R, g.nt, g.split);
     g.kw = 1;
     g.part = c->part;
@@ -586,9 +586,9 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   lmg.R = R;
   lmg.V = c->V;
   lmg.topk = p.topk;
-  lmg.gemv = (c->bf16 && R <= 4 && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
+  lmg.gemv = (c->bf16 && R <= LM_GEMV_MAX_ROWS && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
   lmg.nt = 1;
-  if (!lmg.gemv && R > 4) {   // batched rows: several vocab tiles per wave share B fragments
+  if (!lmg.gemv && R > LM_GEMV_MAX_ROWS) {   // batched rows: several vocab tiles per wave share B fragments
     if (R > 16 && R <= 32 && c->lm.n_tiles % 8 == 0) lmg.nt = 8;
     else if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
     else if (c->lm.n_tiles % 2 == 0) lmg.nt = 2;

@@ -38,14 +38,18 @@ def test_chain_parity_small(cfg):
     run_chain_parity(cfg)
 
 
-# Batched row counts: 17-32 rows take two 16-row groups and eight tiles per
-# wave where the tile count allows (vocabulary 5120 = 320 tiles), more than 32
-# rows take four groups; every sequence is compared.
+# Row counts that select different product paths: 1 and 2 rows take the
+# VALU GEMV main loop (1 row also the GEMV LM head), 3-16 rows one 16-row
+# MFMA group, 17-32 rows two groups and eight tiles per wave where the tile
+# count allows (vocabulary 5120 = 320 tiles), more than 32 rows four groups;
+# every sequence is compared.
 @pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs1", batch=1),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs2", batch=2),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24", batch=24, vocab=5120),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs40", batch=40, ctx_range=(20, 300)),
 ], ids=lambda c: c.name)
-def test_chain_parity_batched_rows(cfg):
+def test_chain_parity_row_counts(cfg):
     run_chain_parity(cfg)
 
 
