@@ -650,7 +650,8 @@ static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
   if (VR > 0) lds += (size_t)VR * g.m.K * sizeof(float);
   if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM, VR>), grid, dim3(64 * g.kw), lds, s, g);
   else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU, VR>), grid, dim3(64 * g.kw), lds, s, g);
-  else hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
+  else if constexpr (NT <= 2) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
+  // (the planner keeps QKV off the 4- and 8-tile unsplit variants)
 }
 
 template <typename T, int RT, int NT, bool PAIR>
@@ -692,7 +693,13 @@ static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
       return;
     }
   }
-  if (g.nt == 2) {
+  if (g.nt == 8) {          // batched rows, many tiles: no K slices
+    if (g.R <= 16) gemm_epi<T, 1, 8, PAIR, 0>(g, s);
+    else gemm_epi<T, 2, 8, PAIR, 0>(g, s);
+  } else if (g.nt == 4) {
+    if (g.R <= 16) gemm_epi<T, 1, 4, PAIR, 0>(g, s);
+    else gemm_epi<T, 2, 4, PAIR, 0>(g, s);
+  } else if (g.nt == 2) {
     if (g.R <= 16) gemm_epi<T, 1, 2, PAIR, 0>(g, s);
     else if (g.R <= 32) gemm_epi<T, 2, 2, PAIR, 0>(g, s);
     else gemm_epi<T, 4, 2, PAIR, 0>(g, s);

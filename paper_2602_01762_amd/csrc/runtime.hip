@@ -523,6 +523,17 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
     plan_batched(m, R, g.nt, g.split);
     g.kw = 1;
     g.part = c->part;
+    const int rt = R <= 16 ? 1 : (R <= 32 ? 2 : 4);
+    const int groups = m.n_tiles / g.nt;
+    if (groups >= 200 && (g.nt == 4 || g.nt == 8) && rt <= 2 && epi != EPI_QKV) {
+      // enough tile groups to fill the chip: K split across the waves of a
+      // workgroup (LDS reduction, epilogue in the kernel), no finish pass;
+      // about 1024 waves in all
+      g.split = 0;
+      int kw = 1024 / groups;
+      while (kw > 1 && ((kw - 1) * g.nt * rt > 48 || kw > m.nkb / 4)) --kw;
+      g.kw = kw < 1 ? 1 : kw;
+    }
     return g;
   }
   Plan pl = plan_for(m, R);

@@ -53,6 +53,17 @@ def test_chain_parity_row_counts(cfg):
     run_chain_parity(cfg)
 
 
+# A wide FFN gives the gate/up product at least 200 groups of 4 (16 rows) or
+# 8 (24 rows) tiles, which takes the unsplit batched path (K shared by the
+# waves of a workgroup, epilogue in the kernel).
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs16_ffn6400", batch=16, ffn=6400),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24_ffn12800", batch=24, ffn=12800, vocab=5120),
+], ids=lambda c: c.name)
+def test_chain_parity_unsplit_products(cfg):
+    run_chain_parity(cfg)
+
+
 def test_chain_deterministic_and_poison_free():
     cfg = SMALL_BF16_CHAIN
     dr, w, inp = gpu_setup(cfg)
