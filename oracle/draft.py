@@ -10,9 +10,11 @@ What is computed (PRISM, Sec. 3.2 "Draft with PRISM"; notation of Table 2):
     (Sec. 3.2 architecture paragraph, Table 2);
   * M processing modules, each a fusion FC F_i and one transformer layer L_i;
     draft step k runs module f_map(k) (Sec. 3.2, the surjection paragraph);
-  * step 1 fuses E(x) of the last accepted token with the target's hidden
-    state for it, runs L_{f(1)}, and predicts x_1 = argmax LM_head(h_0)
-    (Sec. 3.2, the prefill equations with one new token);
+  * step 1 fuses E(x_i) of every accepted token with the target's hidden
+    state for it, runs L_{f(1)} over the fused rows in one pass (causal
+    among them), and predicts x_1 = argmax LM_head(h_0) from the last row
+    (Sec. 3.2, the prefill equations); the plain chain has one accepted
+    token per sequence;
   * step k >= 2 fuses E(x_{k-1}) with the draft's own previous hidden state
     h_{k-2}, runs L_{f(k)} against the KV cache shared by all modules, and
     predicts x_k = argmax LM_head(h_{k-1}) (Sec. 3.2, decoding equations;
@@ -197,13 +199,26 @@ class Oracle:
 
     # chain ------------------------------------------------------------------
     def chain(self, hi: dict, K: Optional[int] = None, forced: Optional[np.ndarray] = None,
-              seqs: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+              seqs: Optional[Sequence[int]] = None, catchup: bool = False) -> Dict[str, np.ndarray]:
         """Greedy K-step chain for the sequences in `seqs` (default all).
+
+        Step 1 is the drafter's prefill (Sec. 3.2, "Draft with PRISM"): each
+        accepted token x_i of the sequence is fused with the target's hidden
+        state h_{i-1}, and the fused rows run through module f_map(1) in one
+        pass at positions L_b .. L_b + n_b - 1, each attending to the prior
+        context and to the new rows up to itself.  The last row's output is
+        h_0 and x_1 = argmax LM_head(h_0).  Without `catchup` the accepted
+        tokens are just the last one (hi["tokens"] / hi["features"], n_b = 1);
+        with it they are the rows of hi["new_tokens"] / hi["new_features"]
+        delimited by hi["new_offsets"].  Step k >= 2 fuses E(x_{k-1}) with
+        h_{k-2} at position L_b + n_b + k - 2.
 
         forced[b, k]: token fed to step k+2 instead of the oracle's own
         argmax of step k+1 (teacher forcing on another drafter's choices).
         Returns tokens [B,K], logits [B,K,V], hidden [B,K,H] (rows of
-        sequences not computed are left at -1 / NaN).
+        sequences not computed are left at -1 / NaN; step 1 holds the last
+        row's values) and, per computed sequence, the draft KV it wrote
+        ("draft_kv": {b: {slot: (k, v)}}).
         """
         cfg = self.cfg
         K = cfg.n_steps if K is None else K
@@ -214,11 +229,40 @@ class Oracle:
         logits = np.full((B, K, cfg.vocab), np.nan)
         hidden = np.full((B, K, cfg.hidden), np.nan)
         caches = {b: self.new_cache(hi, b) for b in seqs}
-        x_in = {b: int(hi["tokens"][b]) for b in seqs}
-        f_in = {b: widen(hi["features"][b]) for b in seqs}
-        for k in range(1, K + 1):
+        # the accepted rows of each sequence, oldest first
+        acc = {}
+        for b in seqs:
+            if catchup:
+                o0, o1 = int(hi["new_offsets"][b]), int(hi["new_offsets"][b + 1])
+                acc[b] = ([int(t) for t in hi["new_tokens"][o0:o1]],
+                          [widen(hi["new_features"][i]) for i in range(o0, o1)])
+            else:
+                acc[b] = ([int(hi["tokens"][b])], [widen(hi["features"][b])])
+        # step 1: one pass of set f_map(1) over every accepted row
+        rows_b, tk, ft, pos = [], [], [], []
+        for b in seqs:
+            L = caches[b]["L"]
+            for i, (t, f) in enumerate(zip(*acc[b])):
+                rows_b.append(b)
+                tk.append(t)
+                ft.append(f)
+                pos.append(L + i)
+        h, lg = self.forward(fm[0], tk, np.stack(ft), pos, caches, rows_b, pos,
+                             [list(range(p + 1)) for p in pos])
+        last = {b: max(i for i, rb in enumerate(rows_b) if rb == b) for b in seqs}
+        x_in, f_in, start = {}, {}, {}
+        for b in seqs:
+            i = last[b]
+            toks[b, 0] = int(np.argmax(lg[i]))
+            logits[b, 0] = lg[i]
+            hidden[b, 0] = h[i]
+            x_in[b] = int(forced[b, 0]) if forced is not None else toks[b, 0]
+            f_in[b] = h[i]
+            start[b] = pos[i] + 1          # position of step 2
+        # steps k >= 2: decoding
+        for k in range(2, K + 1):
             s = fm[k - 1]
-            pos = [caches[b]["L"] + k - 1 for b in seqs]
+            pos = [start[b] + k - 2 for b in seqs]
             h, lg = self.forward(s, [x_in[b] for b in seqs], np.stack([f_in[b] for b in seqs]),
                                  pos, caches, seqs, pos, [list(range(p + 1)) for p in pos])
             for i, b in enumerate(seqs):
@@ -227,7 +271,8 @@ class Oracle:
                 hidden[b, k - 1] = h[i]
                 x_in[b] = int(forced[b, k - 1]) if forced is not None else toks[b, k - 1]
                 f_in[b] = h[i]
-        return {"tokens": toks, "logits": logits, "hidden": hidden}
+        return {"tokens": toks, "logits": logits, "hidden": hidden,
+                "draft_kv": {b: caches[b]["draft"] for b in seqs}}
 
     # tree -------------------------------------------------------------------
     def tree(self, hi: dict, forced: Optional[dict] = None,
@@ -353,14 +398,18 @@ class Oracle:
 
 
 # ------------------------------------------------------------ brute force
-def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = None):
+def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = None,
+                catchup: bool = False):
     """Greedy chain recomputed from scratch at every step, for tiny shapes.
 
-    No cache object survives between steps: for step k the k draft positions
-    are all re-run (position j with set f(j), its token, and the hidden state
-    this same recomputation produced for j-1), attention is an explicit
-    [k, L+k] causal mask over the full key matrix, and the token is the first
-    entry of a full sort of the logits.  Returns tokens [B,K] and hidden [B,K,H].
+    No cache object survives between steps: for step k all draft positions
+    are re-run in order -- the n_b - 1 earlier accepted tokens (with
+    `catchup`; set f(1), their own tokens and target features), then the k
+    chain positions (set f(j), its token, and the hidden state this same
+    recomputation produced for the position before) -- attention is an
+    explicit causal mask over the full key matrix, and the token is the
+    first entry of a full sort of the logits.  Returns tokens [B,K] and
+    hidden [B,K,H].
     """
     cfg = orc.cfg
     H, d, nq, nkv = cfg.hidden, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
@@ -372,17 +421,26 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
     for b in seqs:
         L = int(hi["ctx_lens"][b])
         Kp, Vp = widen(hi["prior_k"][b]), widen(hi["prior_v"][b])
+        if catchup:
+            o0, o1 = int(hi["new_offsets"][b]), int(hi["new_offsets"][b + 1])
+            pre = [(int(hi["new_tokens"][i]), widen(hi["new_features"][i])) for i in range(o0, o1 - 1)]
+            first = (int(hi["new_tokens"][o1 - 1]), widen(hi["new_features"][o1 - 1]))
+        else:
+            pre, first = [], (int(hi["tokens"][b]), widen(hi["features"][b]))
+        n0 = len(pre)
         chosen: List[int] = []
         for k in range(1, K + 1):
-            Ks = np.zeros((L + k, nkv, d))
-            Vs = np.zeros((L + k, nkv, d))
+            n = n0 + k                      # draft positions recomputed for this step
+            Ks = np.zeros((L + n, nkv, d))
+            Vs = np.zeros((L + n, nkv, d))
             Ks[:L], Vs[:L] = Kp, Vp
-            mask = np.zeros((k, L + k), dtype=bool)
-            for j in range(k):
+            mask = np.zeros((n, L + n), dtype=bool)
+            for j in range(n):
                 mask[j, : L + j + 1] = True
-            tok, feat = int(hi["tokens"][b]), widen(hi["features"][b])
-            for j in range(k):
-                P = orc.hw["sets"][cfg.fmap[j]]
+            tok, feat = pre[0] if n0 else first
+            for j in range(n):
+                step = max(j - n0, 0)       # 0-based chain step of position j
+                P = orc.hw["sets"][cfg.fmap[step]]
                 e = widen(orc.hw["embed"][tok])[None]
                 u = orc.lin(P["w_fc"], np.concatenate([e, feat[None]], 1))
                 a = rmsnorm(u, widen(P["g1"]), cfg.rms_eps)
@@ -402,13 +460,17 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
                 m = rmsnorm(r1, widen(P["g2"]), cfg.rms_eps)
                 z = silu(orc.lin(P["w_gate"], m)) * orc.lin(P["w_up"], m)
                 hj = (r1 + orc.lin(P["w_down"], z))[0]
-                if j == k - 1:
+                if j == n - 1:
                     lg = orc.lin(orc.hw["lm_head"],
                                  rmsnorm(hj[None], orc.g_f, cfg.rms_eps))[0]
                     order = np.argsort(-lg, kind="stable")
                     chosen.append(int(order[0]))
                     hidden[b, k - 1] = hj
+                elif j < n0 - 1:
+                    tok, feat = pre[j + 1]  # the next accepted token, its target feature
+                elif j == n0 - 1:
+                    tok, feat = first
                 else:
-                    tok, feat = chosen[j], hj
+                    tok, feat = chosen[j - n0], hj
         toks[b] = chosen
     return {"tokens": toks, "hidden": hidden}

@@ -39,6 +39,9 @@ class DraftConfig:
     seed: int = 0
     f_map: Optional[Tuple[int, ...]] = None   # 0-based; None = identity
     n_sets: Optional[int] = None              # M; None = n_steps
+    # chain whose step 1 catches up on n_b accepted tokens per sequence,
+    # n_b uniform on this inclusive range (None: step 1 takes the last one)
+    n_new: Optional[Tuple[int, int]] = None
 
     # ---- derived -------------------------------------------------------
     @property
@@ -75,8 +78,13 @@ class DraftConfig:
     def n_draft_slots(self) -> int:
         """KV slots the drafting call appends after the prior context."""
         if self.mode == "chain":
-            return self.n_steps
+            return self.n_steps + (self.n_new[1] - 1 if self.n_new else 0)
         return 1 + (self.n_steps - 1) * self.tree_width
+
+    @property
+    def max_new_rows(self) -> int:
+        """Largest total of catch-up rows (0 without catch-up)."""
+        return self.batch * self.n_new[1] if self.n_new else 0
 
     @property
     def max_ctx(self) -> int:

@@ -16,6 +16,10 @@ tensor is synthetic):
   * paged KV: blocks of `kv_block_size` slots; the block table is a seeded
     permutation of the physical blocks when `shuffle_blocks` is set; slots that
     hold no prior context are NaN so that a read of them shows up.
+  * catch-up chains: n_b accepted tokens per sequence, uniform on the
+    configured inclusive range; the earlier n_b - 1 tokens uniform on [0, V)
+    and their target features N(0, 1); the newest one is the sequence's
+    `tokens[b]` / `features[b]`, so n_b = 1 is the plain chain.
 """
 from __future__ import annotations
 
@@ -30,7 +34,7 @@ from .configs import DraftConfig
 # tensor ids used to derive per-tensor seeds
 T_EMBED, T_LMHEAD, T_FNORM = 0, 1, 2
 T_FC, T_G1, T_WQ, T_WK, T_WV, T_WO, T_G2, T_WGATE, T_WUP, T_WDOWN = range(10, 20)
-T_TOK, T_FEAT, T_CTX, T_KPOOL, T_VPOOL, T_BTAB = range(100, 106)
+T_TOK, T_FEAT, T_CTX, T_KPOOL, T_VPOOL, T_BTAB, T_NNEW, T_NTOK, T_NFEAT = range(100, 109)
 
 SET_TENSORS = ("w_fc", "g1", "w_q", "w_k", "w_v", "w_o", "g2", "w_gate", "w_up", "w_down")
 
@@ -90,6 +94,11 @@ class Inputs:
     k_pool: torch.Tensor        # [n_blocks, n_kv, block, d]
     v_pool: torch.Tensor        # [n_blocks, n_kv, block, d]
     block_table: torch.Tensor   # int32 [B, blocks_per_seq]
+    # catch-up chains only: rows new_offsets[b] .. new_offsets[b+1]-1 of
+    # new_tokens / new_features are sequence b's accepted tokens, oldest first
+    new_offsets: Optional[torch.Tensor] = None   # int32 [B + 1]
+    new_tokens: Optional[torch.Tensor] = None    # int32 [T]
+    new_features: Optional[torch.Tensor] = None  # [T, F_t]
 
 
 def make_param_set(cfg: DraftConfig, s: int, device="cpu") -> ParamSet:
@@ -126,6 +135,16 @@ def ctx_lengths(cfg: DraftConfig) -> np.ndarray:
     out = np.empty(cfg.batch, dtype=np.int32)
     for b in range(cfg.batch):
         rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, T_CTX, b])))
+        out[b] = rng.integers(lo, hi + 1)
+    return out
+
+
+def new_counts(cfg: DraftConfig) -> np.ndarray:
+    """Accepted tokens n_b per sequence of a catch-up chain."""
+    lo, hi = cfg.n_new
+    out = np.empty(cfg.batch, dtype=np.int32)
+    for b in range(cfg.batch):
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([cfg.seed, T_NNEW, b])))
         out[b] = rng.integers(lo, hi + 1)
     return out
 
@@ -168,10 +187,26 @@ def make_inputs(cfg: DraftConfig, device="cpu", extra_blocks: int = 0) -> Inputs
     dead = (~live).to(device)[:, None, :, None].expand(shape)
     k_pool.masked_fill_(dead, float("nan"))
     v_pool.masked_fill_(dead, float("nan"))
-    return Inputs(tokens=tokens, features=features,
-                  ctx_lens=torch.from_numpy(lens).to(device),
-                  k_pool=k_pool, v_pool=v_pool,
-                  block_table=torch.from_numpy(btab).to(device))
+    inp = Inputs(tokens=tokens, features=features,
+                 ctx_lens=torch.from_numpy(lens).to(device),
+                 k_pool=k_pool, v_pool=v_pool,
+                 block_table=torch.from_numpy(btab).to(device))
+    if cfg.n_new:
+        counts = new_counts(cfg)
+        nt, nf = [], []
+        for b in range(B):
+            n = int(counts[b])
+            if n > 1:
+                nt.append(torch.randint(0, cfg.vocab, (n - 1,), generator=_gen(device, sd, T_NTOK, b),
+                                        device=device, dtype=torch.int64).to(torch.int32))
+                nf.append(_normal((n - 1, cfg.feat_width), 1.0, 0.0, dt, device, sd, T_NFEAT, b))
+            nt.append(tokens[b:b + 1])
+            nf.append(features[b:b + 1])
+        offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+        inp.new_offsets = torch.from_numpy(offs).to(device)
+        inp.new_tokens = torch.cat(nt).contiguous()
+        inp.new_features = torch.cat(nf, 0).contiguous()
+    return inp
 
 
 def logical_prior_kv(kp: torch.Tensor, vp: torch.Tensor, btab: torch.Tensor, L: int,
@@ -225,5 +260,10 @@ def host_inputs(inp: Inputs, cfg: DraftConfig, seqs=None) -> dict:
         k, v = logical_prior_kv(kp, vp, btab[b], int(lens[b]), cfg)
         ks.append(k)
         vs.append(v)
-    return {"tokens": to_host(inp.tokens), "features": to_host(inp.features),
-            "ctx_lens": to_host(inp.ctx_lens), "prior_k": ks, "prior_v": vs}
+    out = {"tokens": to_host(inp.tokens), "features": to_host(inp.features),
+           "ctx_lens": to_host(inp.ctx_lens), "prior_k": ks, "prior_v": vs}
+    if inp.new_offsets is not None:
+        out["new_offsets"] = to_host(inp.new_offsets)
+        out["new_tokens"] = to_host(inp.new_tokens)
+        out["new_features"] = to_host(inp.new_features)
+    return out

@@ -151,6 +151,61 @@ def test_chain_equals_brute_force(cfg):
     assert np.max(np.abs(inc["hidden"] - bf["hidden"])) < 1e-12
 
 
+# ------------------------------------------------------------------ T1b catch-up prefill
+TINY_CU = TINY.with_(name="pin_tiny_catchup", batch=4, n_new=(1, 4))
+
+
+@pytest.mark.parametrize("cfg", [TINY_CU, TINY_CU.with_(dtype="bf16")], ids=lambda c: c.dtype)
+def test_catchup_chain_equals_brute_force(cfg):
+    hw, hi = build(cfg)
+    n = np.diff(hi["new_offsets"])
+    assert n.min() == 1 and n.max() > 2        # ragged, including a single-token sequence
+    orc = Oracle(cfg, hw)
+    inc = orc.chain(hi, catchup=True)
+    bf = brute_chain(orc, hi, cfg.n_steps, catchup=True)
+    assert np.array_equal(inc["tokens"], bf["tokens"])
+    assert np.max(np.abs(inc["hidden"] - bf["hidden"])) < 1e-12
+
+
+def test_catchup_of_one_token_is_plain_chain():
+    cfg = TINY_CU.with_(n_new=(1, 1))
+    hw, hi = build(cfg)
+    orc = Oracle(cfg, hw)
+    a, b = orc.chain(hi, catchup=True), orc.chain(hi)
+    assert np.array_equal(a["tokens"], b["tokens"])
+    assert np.array_equal(a["logits"], b["logits"])
+
+
+def test_catchup_block_prefill_equals_row_by_row():
+    # one pass over all accepted rows (causal among them) equals feeding the
+    # rows one at a time, each after the previous one's KV is written
+    cfg = TINY_CU
+    hw, hi = build(cfg)
+    orc = Oracle(cfg, hw)
+    ref = orc.chain(hi, catchup=True)
+    s1 = cfg.fmap[0]
+    for b in range(cfg.batch):
+        cache = {b: orc.new_cache(hi, b)}
+        L = cache[b]["L"]
+        o0, o1 = int(hi["new_offsets"][b]), int(hi["new_offsets"][b + 1])
+        for i in range(o1 - o0):
+            f = widen(hi["new_features"][o0 + i])[None]
+            h, lg = orc.forward(s1, [int(hi["new_tokens"][o0 + i])], f, [L + i], cache, [b],
+                                [L + i], [list(range(L + i + 1))])
+        p = L + o1 - o0
+        for k in range(1, cfg.n_steps + 1):
+            if k > 1:
+                h, lg = orc.forward(cfg.fmap[k - 1], [x], h, [p], cache, [b], [p],
+                                    [list(range(p + 1))])
+                p += 1
+            assert np.max(np.abs(lg[0] - ref["logits"][b, k - 1])) < 1e-12
+            x = int(np.argmax(lg[0]))
+        assert sorted(cache[b]["draft"]) == sorted(ref["draft_kv"][b])
+        for slot, (kk, vv) in cache[b]["draft"].items():
+            rk, rv = ref["draft_kv"][b][slot]
+            assert np.array_equal(kk, rk) and np.array_equal(vv, rv)
+
+
 # ------------------------------------------------------------------ T2 tree = chains
 @pytest.mark.parametrize("cfg", [TINY, TINY_BF16], ids=lambda c: c.dtype)
 def test_tree_nodes_equal_forced_chains(cfg):
