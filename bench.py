@@ -54,6 +54,8 @@ WORKLOADS = {
     "8b_bs16": "llama3_8b_bf16_chain_bs16_paged",
     "8b_tree": "llama3_8b_bf16_tree_bs4",
     "70b_bs32": "llama3_70b_bf16_chain_bs32",
+    "8b_bs1_catchup": "llama3_8b_bf16_chain_bs1_catchup4",
+    "8b_bs16_catchup": "llama3_8b_bf16_chain_bs16_paged_catchup",
 }
 
 
@@ -106,8 +108,12 @@ def main():
     b = dr.batch(inp)
     out = dr.tree_buffers(cfg.batch, cfg.n_steps, debug=False) if tree else \
         dr.chain_buffers(cfg.batch, cfg.n_steps)
-    call = (lambda: dr.tree(inp, out=out, batch=b)) if tree else \
-        (lambda: dr.chain(inp, out=out, batch=b))
+    if tree:
+        call = lambda: dr.tree(inp, out=out, batch=b)
+    elif cfg.n_new:      # step 1 prefills every accepted token
+        call = lambda: dr.chain_catchup(inp, out=out, batch=b)
+    else:
+        call = lambda: dr.chain(inp, out=out, batch=b)
 
     for _ in range(args.warmup):
         call()
@@ -158,7 +164,8 @@ def main():
         "data": "synthetic (seeded random-init weights N(0,0.02), features N(0,1), prior KV N(0,1))",
         "config": {"workload": cfg.name, "batch": cfg.batch, "draft_steps": K,
                    "prior_context": cfg.max_ctx if cfg.ctx_range is None else list(cfg.ctx_range),
-                   "kv_block": cfg.kv_block_size, "mode": cfg.mode},
+                   "kv_block": cfg.kv_block_size, "mode": cfg.mode,
+                   "accepted_tokens_step1": list(cfg.n_new) if cfg.n_new else 1},
         "per_draft_step_us": round(ms_per_step * 1e3 / K, 2),
         "weight_bytes_per_step_call": chain_bytes,
         "whole_call_hbm_frac_weights_only": round(chain_bytes / (ms_per_step * 1e-3) / 1e9
@@ -201,7 +208,7 @@ def cpu_baseline(cfg, w, inp, dr):
         if cfg.mode == "tree":
             orc.tree(hi, seqs=seqs)
         else:
-            orc.chain(hi, seqs=seqs)
+            orc.chain(hi, seqs=seqs, catchup=bool(cfg.n_new))
         n += 1
         el = time.perf_counter() - t0
         if el >= 10.0 or n >= 200:

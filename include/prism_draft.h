@@ -79,10 +79,14 @@ typedef struct {
   int32_t max_blocks_per_seq; /* columns of the block table                  */
   int32_t tree_width;    /* w (0 = no tree calls)                            */
   int32_t tree_nodes;    /* v output nodes of a tree call, <= 64             */
+  int32_t max_new_rows;  /* largest total of new accepted tokens in one
+                            prism_draft_chain_catchup call (0 = no such
+                            calls), <= 64                                   */
 } prism_config;
 /* Kernel tiling requires: H, n_q_heads*d, I multiples of 32 (bf16) or 16
  * (fp32); H + F_t likewise; rows per pass (max_batch, or max_batch*w for
- * trees) <= 64.  prism_create returns PRISM_ERR_SHAPE otherwise. */
+ * trees, or max_new_rows) <= 64.  prism_create returns PRISM_ERR_SHAPE
+ * otherwise. */
 
 /* Weights of one processing module, as device tensors in the context dtype.
  * Layouts follow y = W x with W row-major [out, in].  The call copies them
@@ -120,6 +124,22 @@ typedef struct {
   const int32_t *d_block_table;/* [B, max_blocks_per_seq]                   */
   int32_t n_pool_blocks;       /* physical blocks in each pool              */
 } prism_batch;
+
+/* The tokens accepted since the last drafting call, for a chain whose first
+ * step is the drafter's prefill over all of them (paper Sec. 3.2, "Draft
+ * with PRISM": every accepted token x_i is fused with the target's hidden
+ * state h_{i-1} and the fused sequence runs through module f_map(1) in one
+ * pass).  Sequence b owns rows d_offsets[b] .. d_offsets[b+1]-1 (n_b >= 1
+ * rows, the last one is its newest token), which take positions and KV slots
+ * L_b .. L_b + n_b - 1 after its prior context L_b = d_ctx_lens[b]. */
+typedef struct {
+  int32_t total_rows;          /* T = sum of n_b, 1..max_new_rows (host)    */
+  const int32_t *d_offsets;    /* [B + 1] row offsets, d_offsets[0] = 0,
+                                  d_offsets[B] = T, increasing             */
+  const int32_t *d_tokens;     /* [T] accepted tokens, sequence by sequence */
+  const void *d_features;      /* [T, feat_width] target hidden states of
+                                  those tokens (dtype)                      */
+} prism_catchup;
 
 /* One forward pass on R explicit rows (the general entry point). */
 typedef struct {
@@ -211,6 +231,22 @@ prism_status prism_draft_chain(prism_ctx *ctx, const prism_batch *batch,
                                float *d_out_logits, float *d_out_hidden,
                                void *stream);
 
+/* Greedy K-step chain whose first step catches up on several accepted
+ * tokens per sequence (paper Sec. 3.2: the prefill over S_acc with H_base,
+ * then h_0 = the last row's output and x_1 = argmax LM_head(h_0)).  Step 1
+ * writes KV slots L_b .. L_b + n_b - 1 (each new row attends causally to the
+ * prior context and the new rows up to itself); step k >= 2 runs at position
+ * L_b + n_b + k - 2.  Writes KV slots L_b .. L_b + n_b + K - 2.  The tokens
+ * and features of *batch are not used; catchup->d_offsets must describe
+ * batch->batch sequences (a malformed table raises PRISM_ERR_INVALID_ARG in
+ * prism_device_status and leaves the outputs unspecified).  Outputs as in
+ * prism_draft_chain; d_out_logits and d_out_hidden hold the last row's
+ * values for step 1.  Requires max_new_rows >= total_rows. */
+prism_status prism_draft_chain_catchup(prism_ctx *ctx, const prism_batch *batch,
+                                       const prism_catchup *catchup, int32_t K,
+                                       int32_t *d_out_tokens, float *d_out_logits,
+                                       float *d_out_hidden, void *stream);
+
 /* Dynamic draft tree of `depth` passes and width w (paper Sec. 2, tree
  * draft-and-verify with a tree attention mask; Sec. 3.2: PRISM works with
  * tree drafts; Sec. 4.3: depth / width / verified-node topology).  Pass d
@@ -226,7 +262,8 @@ prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
 
 /* Synchronize `stream` and report device-side bounds flags raised since
  * the last call: PRISM_ERR_CAPACITY (block table / pool / slot out of
- * range), PRISM_ERR_INVALID_ARG (token id out of range), else PRISM_OK.
+ * range), PRISM_ERR_INVALID_ARG (token id out of range, malformed catch-up
+ * offsets), else PRISM_OK.
  * Clears the flags. */
 prism_status prism_device_status(prism_ctx *ctx, void *stream);
 

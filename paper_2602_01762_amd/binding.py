@@ -18,7 +18,8 @@ STATUS = {0: "PRISM_OK", -1: "PRISM_ERR_INVALID_ARG", -2: "PRISM_ERR_SHAPE",
           -5: "PRISM_ERR_OUT_OF_MEMORY", -6: "PRISM_ERR_HIP", -7: "PRISM_ERR_CAPACITY"}
 EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_load_shared",
            "prism_draft_load_params", "prism_set_step_map", "prism_draft_step",
-           "prism_draft_chain", "prism_draft_tree", "prism_device_status",
+           "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_tree",
+           "prism_device_status",
            "prism_profile_enable", "prism_profile_read")
 
 c_i32, c_u64, c_f32, c_vp = ctypes.c_int32, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p
@@ -30,7 +31,7 @@ class prism_config(ctypes.Structure):
                 ("max_steps", c_i32), ("feat_width", c_i32), ("rope_theta", c_f32),
                 ("rms_eps", c_f32), ("dtype", c_i32), ("kv_block_size", c_i32),
                 ("max_batch", c_i32), ("max_blocks_per_seq", c_i32), ("tree_width", c_i32),
-                ("tree_nodes", c_i32)]
+                ("tree_nodes", c_i32), ("max_new_rows", c_i32)]
 
 
 class prism_param_set(ctypes.Structure):
@@ -43,6 +44,11 @@ class prism_batch(ctypes.Structure):
     _fields_ = [("batch", c_i32), ("d_tokens", c_vp), ("d_features", c_vp),
                 ("d_ctx_lens", c_vp), ("d_k_pool", c_vp), ("d_v_pool", c_vp),
                 ("d_block_table", c_vp), ("n_pool_blocks", c_i32)]
+
+
+class prism_catchup(ctypes.Structure):
+    _fields_ = [("total_rows", c_i32), ("d_offsets", c_vp), ("d_tokens", c_vp),
+                ("d_features", c_vp)]
 
 
 class prism_step_io(ctypes.Structure):
@@ -87,6 +93,8 @@ def lib():
         L.prism_set_step_map.argtypes = [c_vp, P(c_i32), c_i32]
         L.prism_draft_step.argtypes = [c_vp, c_i32, P(prism_step_io), c_vp]
         L.prism_draft_chain.argtypes = [c_vp, P(prism_batch), c_i32, c_vp, c_vp, c_vp, c_vp]
+        L.prism_draft_chain_catchup.argtypes = [c_vp, P(prism_batch), P(prism_catchup), c_i32,
+                                                c_vp, c_vp, c_vp, c_vp]
         L.prism_draft_tree.argtypes = [c_vp, P(prism_batch), c_i32, P(prism_tree_out), c_vp]
         L.prism_device_status.argtypes = [c_vp, c_vp]
         L.prism_profile_enable.argtypes = [c_vp, c_i32]
@@ -154,6 +162,13 @@ def prism_draft_chain(ctx, batch: prism_batch, K: int, out_tokens, out_logits=No
                       out_hidden=None, stream=None):
     _check(lib().prism_draft_chain(ctx, ctypes.byref(batch), K, ptr(out_tokens), ptr(out_logits),
                                    ptr(out_hidden), cur_stream() if stream is None else stream), ctx)
+
+
+def prism_draft_chain_catchup(ctx, batch: prism_batch, catchup: prism_catchup, K: int,
+                              out_tokens, out_logits=None, out_hidden=None, stream=None):
+    _check(lib().prism_draft_chain_catchup(ctx, ctypes.byref(batch), ctypes.byref(catchup), K,
+                                           ptr(out_tokens), ptr(out_logits), ptr(out_hidden),
+                                           cur_stream() if stream is None else stream), ctx)
 
 
 def prism_draft_tree(ctx, batch: prism_batch, depth: int, out: prism_tree_out, stream=None):

@@ -8,7 +8,7 @@ namespace prism {
 typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
 
 // device error flags (bit set by kernels on an out-of-range device value)
-enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u };
+enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u, ERRF_ROWS = 4u };
 
 // Rows up to which bf16 products (LM head) take the VALU GEMV main loop;
 // above it the staged-activation LDS reads, which grow with the rows, cost
@@ -169,6 +169,18 @@ void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, cons
                        int *tok_b, int ld_b, hipStream_t s);
 void launch_chain_setup(int B, int K, const int32_t *tokens, const int32_t *ctx_lens, int32_t *seq,
                         int32_t *pos, int32_t *tok0, hipStream_t s);
+// catch-up chain: per accepted row its sequence and position; per sequence
+// its last row and the chain's positions [K][B]
+void launch_catchup_setup(int B, int T, int K, const int32_t *offsets, const int32_t *ctx_lens,
+                          int32_t *rseq, int32_t *rpos, int32_t *last, int32_t *seq, int32_t *pos,
+                          uint32_t *err, hipStream_t s);
+struct RowsGather {              // two dense fp32 matrices [*, n[m]]
+  const int32_t *idx;            // [rows] source row of each destination row, -1: zeros
+  const float *src[2];
+  float *dst[2];
+  int n[2];
+};
+void launch_rows_gather(int rows, const RowsGather &a, hipStream_t s);
 // tree bookkeeping
 struct TreeWs {
   int B, w, D, C;                 // batch, width, depth, candidates per sequence

@@ -236,6 +236,60 @@ void launch_chain_setup(int B, int K, const int32_t *tokens, const int32_t *ctx_
 }
 
 // ---------------------------------------------------------------------------
+// Catch-up chain rows.  Accepted row r (of T) belongs to the sequence b with
+// offsets[b] <= r < offsets[b+1] and sits at position and slot
+// L_b + r - offsets[b]; step k (0-based) of the chain then runs at
+// L_b + n_b - 1 + k, step 0 being the prefill's last row.  A malformed table
+// (offsets[0] != 0, offsets[B] != T, or an empty sequence) raises ERRF_ROWS;
+// rows that fall in no sequence get seq -1, which every later kernel skips.
+__global__ void k_catchup_setup(int B, int T, int K, const int32_t *offsets,
+                                const int32_t *ctx_lens, int32_t *rseq, int32_t *rpos,
+                                int32_t *last, int32_t *seq, int32_t *pos, uint32_t *err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < T) {
+    int lo = 0, hi = B;   // largest b with offsets[b] <= i (bounded search)
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (offsets[mid] <= i) lo = mid; else hi = mid;
+    }
+    const bool ok = offsets[lo] <= i && i < offsets[lo + 1];
+    rseq[i] = ok ? lo : -1;
+    rpos[i] = ok ? ctx_lens[lo] + (i - offsets[lo]) : 0;
+  }
+  if (i < B) {
+    const int o0 = offsets[i], o1 = offsets[i + 1];
+    const bool bad = o1 <= o0 || (i == 0 && o0 != 0) || (i == B - 1 && o1 != T);
+    if (bad) atomicOr(err, ERRF_ROWS);
+    last[i] = bad || o1 - 1 >= T ? -1 : o1 - 1;
+    seq[i] = bad ? -1 : i;
+    for (int k = 0; k < K; ++k) pos[(size_t)k * B + i] = ctx_lens[i] + (o1 - o0 - 1) + k;
+  }
+}
+
+void launch_catchup_setup(int B, int T, int K, const int32_t *offsets, const int32_t *ctx_lens,
+                          int32_t *rseq, int32_t *rpos, int32_t *last, int32_t *seq, int32_t *pos,
+                          uint32_t *err, hipStream_t s) {
+  const int n = T > B ? T : B;
+  hipLaunchKernelGGL(k_catchup_setup, dim3((n + 255) / 256), dim3(256), 0, s, B, T, K, offsets,
+                     ctx_lens, rseq, rpos, last, seq, pos, err);
+}
+
+// For each of two dense fp32 matrices m (blockIdx.z): dst_m[b][0..n_m) =
+// src_m[idx[b]][0..n_m) for b < rows; idx -1 gives zeros.
+__global__ void k_rows_gather(RowsGather a) {
+  const int b = blockIdx.y, m = blockIdx.z;
+  const int r = a.idx[b];
+  const int n = a.n[m];
+  for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < n; c += gridDim.x * blockDim.x)
+    a.dst[m][(size_t)b * n + c] = r >= 0 ? a.src[m][(size_t)r * n + c] : 0.f;
+}
+
+void launch_rows_gather(int rows, const RowsGather &a, hipStream_t s) {
+  const int n = a.n[0] > a.n[1] ? a.n[0] : a.n[1];
+  hipLaunchKernelGGL(k_rows_gather, dim3((n + 255) / 256, rows, 2), dim3(256), 0, s, a);
+}
+
+// ---------------------------------------------------------------------------
 // Draft tree.  Candidate c of a sequence is created in order: the root's w
 // children first (depth 1), then for each later pass the w children of each
 // of the w frontier nodes (frontier rank major, child rank minor).  A score

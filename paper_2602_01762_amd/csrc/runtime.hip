@@ -82,6 +82,9 @@ struct prism_ctx {
   uint64_t *t_bits[2] = {nullptr, nullptr};
   int nsub = 1;                     // attention: 64-slot steps per workgroup
   int lm_nwg_last = 0;              // LM-head partial count of the pass last enqueued
+  int new_max = 0;                  // catch-up rows capacity
+  int32_t *c_rseq = nullptr, *c_rpos = nullptr, *c_last = nullptr;   // catch-up rows
+  float *q2 = nullptr, *u2 = nullptr;   // q and u of each sequence's last accepted row
   size_t lds_limit = 65536;         // LDS bytes one workgroup may use
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
@@ -203,6 +206,8 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   if (((k.n_q_heads + 2 * k.n_kv_heads) * k.head_dim + k.head_dim) > 16384)
     return fail(nullptr, PRISM_ERR_SHAPE, "q/k/v width too large");
   if (k.max_steps > 63) return fail(nullptr, PRISM_ERR_SHAPE, "max_steps > 63");
+  if (k.max_new_rows < 0 || k.max_new_rows > MAX_ROWS)
+    return fail(nullptr, PRISM_ERR_SHAPE, "max_new_rows %d out of 0..%d", k.max_new_rows, MAX_ROWS);
   const int w = k.tree_width;
   const int rows = k.max_batch * (w > 1 ? w : 1);
   if (rows > MAX_ROWS) return fail(nullptr, PRISM_ERR_SHAPE, "rows per pass %d > %d", rows, MAX_ROWS);
@@ -252,7 +257,11 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->n_wg_lm = lm_workgroups(c->lm.n_tiles, 1);
   if (const char *e = getenv("PRISM_NO_GRAPH")) c->use_graph = !(e[0] == '1');
 
+  // rows of a full pass (R) and of the fusion FC / QKV front of a catch-up
+  // step (RF: every accepted token)
   const size_t R = rows, es = c->esz;
+  const size_t RF = rows > k.max_new_rows ? rows : k.max_new_rows;
+  c->new_max = k.max_new_rows;
   size_t total = 0;
   std::vector<std::pair<void **, size_t>> L;
   auto add = [&](void **p, size_t b) { L.push_back({p, b}); total += (b + 255) & ~(size_t)255; };
@@ -261,19 +270,19 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
     if (bf16) add(&a.lo, n * es);
   };
   const size_t nth = (size_t)c->H / 16;
-  planes(c->xfc, R * (c->H + c->feat_max));
-  add((void **)&c->u, R * c->H * 4);
+  planes(c->xfc, RF * (c->H + c->feat_max));
+  add((void **)&c->u, RF * c->H * 4);
   add((void **)&c->r1, R * c->H * 4);
-  planes(c->ug, R * c->H);
+  planes(c->ug, RF * c->H);
   planes(c->r1g, R * c->H);
   planes(c->hg, R * c->H);
-  add((void **)&c->ss_u, nth * R * 4);
+  add((void **)&c->ss_u, nth * RF * 4);
   add((void **)&c->ss_r1, nth * R * 4);
   add((void **)&c->ss_h, nth * R * 4);
-  add((void **)&c->sc_u, R * 4);
+  add((void **)&c->sc_u, RF * 4);
   add((void **)&c->sc_r1, R * 4);
   add((void **)&c->sc_h, R * 4);
-  add((void **)&c->q, R * c->nq * c->d * 4);
+  add((void **)&c->q, RF * c->nq * c->d * 4);
   add((void **)&c->pm, R * c->nq * c->nch * 4);
   add((void **)&c->pl, R * c->nq * c->nch * 4);
   add((void **)&c->po, R * c->nq * c->nch * c->d * 4);
@@ -281,10 +290,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   planes(c->z, R * c->I);
   add((void **)&c->hid[0], R * c->H * 4);
   add((void **)&c->hid[1], R * c->H * 4);
-  if (rows > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums
+  if ((int)RF > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums
     size_t pn = 0;
-    auto upd = [&](int N, int K) {   // the plan depends on the row count: take both regimes
-      for (int rr = GEMV_MAX_ROWS + 1; rr <= rows; ++rr) {
+    auto upd = [&](int N, int K) {   // the plan depends on the row count: take every count
+      for (int rr = GEMV_MAX_ROWS + 1; rr <= (int)RF; ++rr) {
         int nt, sp;
         plan_batched(make_tiled(N, K, bf16), rr, nt, sp);
         if ((size_t)sp * N > pn) pn = (size_t)sp * N;
@@ -296,7 +305,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
     upd(c->H, c->nq * c->d);
     upd(2 * c->I, c->H);
     upd(c->H, c->I);
-    add((void **)&c->part, R * pn * 4);
+    add((void **)&c->part, RF * pn * 4);
   }
   add((void **)&c->lm_max, R * c->n_wg_lm * 4);
   add((void **)&c->lm_sum, R * c->n_wg_lm * 4);
@@ -308,6 +317,13 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->c_seq, (size_t)k.max_batch * 4);
   add((void **)&c->c_pos, (size_t)k.max_batch * k.max_steps * 4);
   add((void **)&c->c_tok0, (size_t)k.max_batch * 4);
+  if (k.max_new_rows > 0) {   // catch-up: accepted rows and each sequence's last one
+    add((void **)&c->c_rseq, (size_t)k.max_new_rows * 4);
+    add((void **)&c->c_rpos, (size_t)k.max_new_rows * 4);
+    add((void **)&c->c_last, (size_t)k.max_batch * 4);
+    add((void **)&c->q2, (size_t)k.max_batch * c->nq * c->d * 4);
+    add((void **)&c->u2, (size_t)k.max_batch * c->H * 4);
+  }
   const size_t tb = (size_t)k.max_batch * (Cmax > 0 ? Cmax : 1);
   add((void **)&c->t_ctok, tb * 4);
   add((void **)&c->t_cpar, tb * 4);
@@ -548,7 +564,9 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
 // which takes precomputed scales)
 static int scale_threads(const GemmLaunch &g) { return g.split > 0 ? 0 : 64 * g.kw; }
 
-static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
+// Front of a pass: fusion FC and QKV (RoPE, KV append) for p.R rows -> u
+// and q in the workspace.
+static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
   const Set &S = c->sets[p.set];
   const bool bf = c->bf16;
   const int R = p.R, H = c->H;
@@ -570,14 +588,23 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
   g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
   launch_gemm(bf, g, s);
+}
+
+// Back of a pass, for p.R rows whose q and FC output u are given: attention,
+// O, MLP, LM head (and the top-k merge unless deferred).
+static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const float *q,
+                         const float *u, hipStream_t s) {
+  const Set &S = c->sets[p.set];
+  const bool bf = c->bf16;
+  const int R = p.R, H = c->H;
   // attention over the visible slots -> o
   ActOut o = c->o;
   o.ld = c->nq * c->d;
-  launch_attention(bf, R, c->nq, c->nkv, c->d, c->q, p.in, kv, c->max_slots, c->nsub, c->pm,
+  launch_attention(bf, R, c->nq, c->nkv, c->d, q, p.in, kv, c->max_slots, c->nsub, c->pm,
                    c->pl, c->po, o, c->err, s);
   // r1 = u + W_o o  ->  r1, (r1 * g2), sums of squares
-  g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
-  g.res = c->u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
+  GemmLaunch g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
+  g.res = u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
   g.ss = c->ss_r1;
   launch_gemm(bf, g, s);
   // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
@@ -617,6 +644,11 @@ static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStrea
   if (!p.defer_merge)
     launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
                       p.logp, p.tok_a, p.tok_b, p.ld_b, s);
+}
+
+static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
+  enqueue_front(c, p, kv, s);
+  enqueue_back(c, p, kv, c->q, c->u, s);
 }
 
 static prism_status check_set(prism_ctx *c, int step, int want_F) {
@@ -723,10 +755,78 @@ prism_status prism_draft_step(prism_ctx *c, int32_t k, const prism_step_io *io, 
   return PRISM_OK;
 }
 
-prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K,
-                               int32_t *d_out_tokens, float *d_out_logits, float *d_out_hidden,
-                               void *stream) {
-  if (!c) return PRISM_ERR_INVALID_ARG;
+// K greedy steps for B sequences.  Step 1 fuses each sequence's last
+// accepted token with its target feature, or (cu != NULL) is the prefill over
+// all accepted rows: the FC / QKV front runs on the T rows (writing their
+// KV), then the back of the pass continues from each sequence's last row.
+// Step k >= 2 takes its token from the previous LM head's partials.
+static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, int K,
+                          const prism_catchup *cu, int32_t *d_out_tokens, float *d_out_logits,
+                          float *d_out_hidden, hipStream_t s) {
+  const int B = b.batch, H = c->H, V = c->V;
+  if (cu)
+    launch_catchup_setup(B, cu->total_rows, K, cu->d_offsets, b.d_ctx_lens, c->c_rseq, c->c_rpos,
+                         c->c_last, c->c_seq, c->c_pos, c->err, s);
+  else
+    launch_chain_setup(B, K, b.d_tokens, b.d_ctx_lens, c->c_seq, c->c_pos, c->c_tok0, s);
+  const float *prev = nullptr;
+  int ld_prev = 0;
+  for (int k = 1; k <= K; ++k) {
+    Pass p{};
+    p.set = c->fmap[k - 1];
+    p.R = B;
+    p.F = k == 1 ? c->cfg.feat_width : H;
+    p.topk = 1;
+    p.in.tokens = c->c_tok0;      // step 1; later steps take the previous LM partials
+    if (k > 1) {
+      p.lm_in.pval = c->lm_val; p.lm_in.pid = c->lm_id; p.lm_in.n_wg = c->lm_nwg_last;
+      p.lm_in.rec = d_out_tokens + (k - 2); p.lm_in.ld_rec = K;
+    }
+    p.defer_merge = k < K;
+    p.in.feat = k == 1 ? b.d_features : (const void *)prev;
+    p.in.feat_bf16 = k == 1 ? (int)c->bf16 : 0;
+    p.in.feat_ld = k == 1 ? c->cfg.feat_width : ld_prev;
+    p.in.feat_rows = nullptr;
+    p.in.seq = c->c_seq;
+    p.in.pos = c->c_pos + (size_t)(k - 1) * B;
+    p.in.slot = p.in.pos;
+    p.in.bits = nullptr;
+    p.hid_out = d_out_hidden ? d_out_hidden + (size_t)(k - 1) * H : c->hid[k & 1];
+    p.ld_hid = d_out_hidden ? K * H : H;
+    p.logits = d_out_logits ? d_out_logits + (size_t)(k - 1) * V : nullptr;
+    p.ld_logits = (long)K * V;
+    p.ids = c->ids;
+    p.logp = nullptr;
+    p.tok_a = c->tokbuf;
+    p.tok_b = d_out_tokens + (k - 1);
+    p.ld_b = K;
+    if (k == 1 && cu) {
+      Pass f = p;                 // front over every accepted row
+      f.R = cu->total_rows;
+      f.in.tokens = cu->d_tokens;
+      f.in.feat = cu->d_features;
+      f.in.feat_bf16 = (int)c->bf16;
+      f.in.feat_ld = c->cfg.feat_width;
+      f.in.seq = c->c_rseq;
+      f.in.pos = c->c_rpos;
+      f.in.slot = c->c_rpos;
+      enqueue_front(c, f, kv, s);
+      RowsGather rg{};
+      rg.idx = c->c_last;
+      rg.src[0] = c->q; rg.dst[0] = c->q2; rg.n[0] = c->nq * c->d;
+      rg.src[1] = c->u; rg.dst[1] = c->u2; rg.n[1] = H;
+      launch_rows_gather(B, rg, s);
+      enqueue_back(c, p, kv, c->q2, c->u2, s);
+    } else {
+      enqueue_pass(c, p, kv, s);
+    }
+    prev = p.hid_out;
+    ld_prev = p.ld_hid;
+  }
+}
+
+static prism_status check_chain(prism_ctx *c, const prism_batch *batch, int32_t K,
+                                const int32_t *d_out_tokens) {
   prism_status st = check_batch(c, batch);
   if (st) return st;
   if (K < 1 || K > c->cfg.max_steps || K > (int)c->fmap.size())
@@ -734,55 +834,65 @@ prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K
   if (!d_out_tokens) return fail(c, PRISM_ERR_INVALID_ARG, "d_out_tokens is NULL");
   for (int k = 1; k <= K; ++k)
     if ((st = check_set(c, k, k == 1 ? c->cfg.feat_width : c->H))) return st;
-  const prism_batch b = *batch;
-  const KvArgs kv = kv_of(c, &b);
-  const int B = b.batch, H = c->H, V = c->V;
-  std::vector<uintptr_t> key = {1, (uintptr_t)B, (uintptr_t)K, (uintptr_t)b.d_tokens,
+  return PRISM_OK;
+}
+
+static std::vector<uintptr_t> chain_key(prism_ctx *c, uintptr_t kind, const prism_batch &b, int K,
+                                        int32_t *d_out_tokens, float *d_out_logits,
+                                        float *d_out_hidden) {
+  std::vector<uintptr_t> key = {kind, (uintptr_t)b.batch, (uintptr_t)K, (uintptr_t)b.d_tokens,
                                 (uintptr_t)b.d_features, (uintptr_t)b.d_ctx_lens,
                                 (uintptr_t)b.d_k_pool, (uintptr_t)b.d_v_pool,
                                 (uintptr_t)b.d_block_table, (uintptr_t)b.n_pool_blocks,
                                 (uintptr_t)d_out_tokens, (uintptr_t)d_out_logits,
                                 (uintptr_t)d_out_hidden};
   for (int k = 0; k < K; ++k) key.push_back((uintptr_t)c->fmap[k]);
-  auto enqueue = [&](hipStream_t s) {
-    launch_chain_setup(B, K, b.d_tokens, b.d_ctx_lens, c->c_seq, c->c_pos, c->c_tok0, s);
-    const float *prev = nullptr;
-    int ld_prev = 0;
-    for (int k = 1; k <= K; ++k) {
-      Pass p{};
-      p.set = c->fmap[k - 1];
-      p.R = B;
-      p.F = k == 1 ? c->cfg.feat_width : H;
-      p.topk = 1;
-      p.in.tokens = c->c_tok0;      // step 1; later steps take the previous LM partials
-      if (k > 1) {
-        p.lm_in.pval = c->lm_val; p.lm_in.pid = c->lm_id; p.lm_in.n_wg = c->lm_nwg_last;
-        p.lm_in.rec = d_out_tokens + (k - 2); p.lm_in.ld_rec = K;
-      }
-      p.defer_merge = k < K;
-      p.in.feat = k == 1 ? b.d_features : (const void *)prev;
-      p.in.feat_bf16 = k == 1 ? (int)c->bf16 : 0;
-      p.in.feat_ld = k == 1 ? c->cfg.feat_width : ld_prev;
-      p.in.feat_rows = nullptr;
-      p.in.seq = c->c_seq;
-      p.in.pos = c->c_pos + (size_t)(k - 1) * B;
-      p.in.slot = p.in.pos;
-      p.in.bits = nullptr;
-      p.hid_out = d_out_hidden ? d_out_hidden + (size_t)(k - 1) * H : c->hid[k & 1];
-      p.ld_hid = d_out_hidden ? K * H : H;
-      p.logits = d_out_logits ? d_out_logits + (size_t)(k - 1) * V : nullptr;
-      p.ld_logits = (long)K * V;
-      p.ids = c->ids;
-      p.logp = nullptr;
-      p.tok_a = c->tokbuf;
-      p.tok_b = d_out_tokens + (k - 1);
-      p.ld_b = K;
-      enqueue_pass(c, p, kv, s);
-      prev = p.hid_out;
-      ld_prev = p.ld_hid;
-    }
-  };
-  return run_graph(c, key, (hipStream_t)stream, enqueue);
+  return key;
+}
+
+prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K,
+                               int32_t *d_out_tokens, float *d_out_logits, float *d_out_hidden,
+                               void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  prism_status st = check_chain(c, batch, K, d_out_tokens);
+  if (st) return st;
+  const prism_batch b = *batch;
+  const KvArgs kv = kv_of(c, &b);
+  auto key = chain_key(c, 1, b, K, d_out_tokens, d_out_logits, d_out_hidden);
+  return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
+    enqueue_chain(c, b, kv, K, nullptr, d_out_tokens, d_out_logits, d_out_hidden, s);
+  });
+}
+
+prism_status prism_draft_chain_catchup(prism_ctx *c, const prism_batch *batch,
+                                       const prism_catchup *catchup, int32_t K,
+                                       int32_t *d_out_tokens, float *d_out_logits,
+                                       float *d_out_hidden, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!batch) return fail(c, PRISM_ERR_INVALID_ARG, "batch is NULL");
+  if (!catchup) return fail(c, PRISM_ERR_INVALID_ARG, "catchup is NULL");
+  if (c->new_max < 1) return fail(c, PRISM_ERR_INVALID_ARG, "context was created without max_new_rows");
+  // the batch's own tokens and features are not used here
+  prism_batch b = *batch;
+  if (!b.d_tokens) b.d_tokens = catchup->d_tokens;
+  if (!b.d_features) b.d_features = catchup->d_features;
+  prism_status st = check_chain(c, &b, K, d_out_tokens);
+  if (st) return st;
+  const prism_catchup cu = *catchup;
+  if (cu.total_rows < b.batch || cu.total_rows > c->new_max)
+    return fail(c, PRISM_ERR_INVALID_ARG, "total_rows %d out of %d..%d", cu.total_rows, b.batch,
+                c->new_max);
+  if (!cu.d_offsets || !cu.d_tokens || !cu.d_features)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL pointer in catchup");
+  const KvArgs kv = kv_of(c, &b);
+  auto key = chain_key(c, 3, b, K, d_out_tokens, d_out_logits, d_out_hidden);
+  key.push_back((uintptr_t)cu.total_rows);
+  key.push_back((uintptr_t)cu.d_offsets);
+  key.push_back((uintptr_t)cu.d_tokens);
+  key.push_back((uintptr_t)cu.d_features);
+  return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
+    enqueue_chain(c, b, kv, K, &cu, d_out_tokens, d_out_logits, d_out_hidden, s);
+  });
 }
 
 prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t depth,
@@ -894,6 +1004,7 @@ prism_status prism_device_status(prism_ctx *c, void *stream) {
   uint32_t flags = 0, zero = 0;
   HIPCHK(c, hipMemcpy(&flags, c->err, 4, hipMemcpyDeviceToHost));
   HIPCHK(c, hipMemcpy(c->err, &zero, 4, hipMemcpyHostToDevice));
+  if (flags & ERRF_ROWS) return fail(c, PRISM_ERR_INVALID_ARG, "malformed catch-up offsets");
   if (flags & ERRF_CAPACITY) return fail(c, PRISM_ERR_CAPACITY, "KV slot, block or pool out of range");
   if (flags & ERRF_TOKEN) return fail(c, PRISM_ERR_INVALID_ARG, "token id out of range");
   return PRISM_OK;

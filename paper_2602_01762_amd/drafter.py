@@ -27,7 +27,7 @@ class Drafter:
     """
 
     def __init__(self, shape, max_batch: Optional[int] = None, max_steps: Optional[int] = None,
-                 max_blocks_per_seq: Optional[int] = None):
+                 max_blocks_per_seq: Optional[int] = None, max_new_rows: Optional[int] = None):
         self.shape = shape
         cfg = B.prism_config()
         cfg.hidden = shape.hidden
@@ -47,6 +47,8 @@ class Drafter:
         cfg.max_blocks_per_seq = max_blocks_per_seq or shape.blocks_per_seq
         cfg.tree_width = shape.tree_width
         cfg.tree_nodes = shape.tree_nodes
+        cfg.max_new_rows = (max_new_rows if max_new_rows is not None
+                            else getattr(shape, "max_new_rows", 0))
         self.cfg = cfg
         self.ctx = B.prism_create(cfg)
         self.device = torch.device("cuda", torch.cuda.current_device())
@@ -109,6 +111,23 @@ class Drafter:
         if out is None:
             out = self.chain_buffers(b.batch, K, logits, hidden)
         B.prism_draft_chain(self.ctx, b, K, out["tokens"], out["logits"], out["hidden"])
+        return out
+
+    def chain_catchup(self, inp, K: Optional[int] = None, logits=False, hidden=False, out=None,
+                      batch=None):
+        """Chain whose step 1 is the prefill over inp.new_tokens / new_features
+        (rows delimited by inp.new_offsets)."""
+        K = K or self.shape.n_steps
+        b = batch if batch is not None else self.batch(inp)
+        if out is None:
+            out = self.chain_buffers(b.batch, K, logits, hidden)
+        cu = B.prism_catchup()
+        cu.total_rows = int(inp.new_tokens.shape[0])
+        cu.d_offsets = B.ptr(inp.new_offsets)
+        cu.d_tokens = B.ptr(inp.new_tokens)
+        cu.d_features = B.ptr(inp.new_features)
+        B.prism_draft_chain_catchup(self.ctx, b, cu, K, out["tokens"], out["logits"],
+                                    out["hidden"])
         return out
 
     def tree_buffers(self, nb: int, depth: int, debug=True, logits=False):

@@ -135,7 +135,16 @@ L3_70B_BS32 = DraftConfig(
     head_dim=128, ffn=28672, vocab=128256, n_steps=7, feat_width=24576,
     rope_theta=500000.0, dtype="bf16", batch=32, ctx_len=4096)
 
-CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32)}
+# Catch-up chains: step 1 prefills every token accepted in the last
+# verification (the paper's S_acc; with K = 5 drafts, up to K + 1 = 6 tokens
+# can be accepted per cycle; the batch-16 shape keeps the total within the
+# 64-row pass capacity).
+L3_8B_BS1_CATCHUP = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_catchup4", n_new=(4, 4))
+L3_8B_BS16_CATCHUP = L3_8B_BS16.with_(name="llama3_8b_bf16_chain_bs16_paged_catchup",
+                                      n_new=(1, 4))
+
+CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32,
+                               L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP)}
 
 # Reduced shapes for element-by-element parity: small enough for the oracle to
 # finish in seconds, large enough to span several tiles of every kernel and to

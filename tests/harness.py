@@ -55,12 +55,17 @@ def check_token(lg_oracle: np.ndarray, tok: int, what: str):
             what, tok, lg_oracle[tok], top1)
 
 
-def check_chain(cfg, out: dict, orc: Oracle, hi: dict, seqs, hidden_tol=None):
+def check_chain(cfg, out: dict, orc: Oracle, hi: dict, seqs, hidden_tol=None, catchup=False,
+                inp=None):
+    """Teacher-forced comparison of a GPU chain; with `inp` also the draft KV
+    the chain wrote into the paged pools."""
     tol = LOGIT_TOL[cfg.dtype]
     hidden_tol = tol if hidden_tol is None else hidden_tol
     toks = out["tokens"].cpu().numpy().astype(np.int64)
     K = toks.shape[1]
-    ref = orc.chain(hi, K=K, forced=toks, seqs=seqs)
+    ref = orc.chain(hi, K=K, forced=toks, seqs=seqs, catchup=catchup)
+    if inp is not None:
+        check_draft_kv(cfg, inp, ref["draft_kv"], seqs)
     lg = out["logits"].cpu().numpy() if out.get("logits") is not None else None
     hd = out["hidden"].cpu().numpy() if out.get("hidden") is not None else None
     worst = 0.0
@@ -78,6 +83,32 @@ def check_chain(cfg, out: dict, orc: Oracle, hi: dict, seqs, hidden_tol=None):
                 assert e <= hidden_tol, "%s: hidden max-abs %.3g" % (what, e)
     agree = np.mean([toks[b, k] == np.argmax(ref["logits"][b, k]) for b in seqs for k in range(K)])
     return {"max_logit_err": worst, "argmax_agreement": float(agree)}
+
+
+def check_draft_kv(cfg, inp, draft_kv: dict, seqs):
+    """The K and V rows the GPU stored at every draft slot equal the oracle's
+    stored values.  fp32 caches: to fp32 accumulation order.  bf16: within one
+    rounding step of the value plus 2^-12 of the row's RMS; the two sides
+    round an fp32 (activations carried to 2^-17) and an fp64 value of the
+    same quantity, whose difference scales with the row, not the element."""
+    from synth import to_host
+    from oracle import widen
+    bs = cfg.kv_block_size
+    kp, vp = inp.k_pool.cpu(), inp.v_pool.cpu()
+    btab = inp.block_table.cpu().numpy()
+    for b in seqs:
+        for slot, (kr, vr) in sorted(draft_kv[b].items()):
+            blk = int(btab[b, slot // bs])
+            kg = widen(to_host(kp[blk, :, slot % bs, :]))
+            vg = widen(to_host(vp[blk, :, slot % bs, :]))
+            for got, want, what in ((kg, kr, "k"), (vg, vr, "v")):
+                if cfg.dtype == "f32":
+                    assert np.max(np.abs(got - want)) <= 1e-5 * (1 + np.max(np.abs(want))), (b, slot, what)
+                else:
+                    rms = np.sqrt(np.mean(want * want, axis=-1, keepdims=True))
+                    lim = 2.0 ** -7 * np.abs(want) + 2.0 ** -12 * rms
+                    assert np.all(np.abs(got - want) <= lim), (
+                        "seq %d slot %d %s: max diff %.3g" % (b, slot, what, np.max(np.abs(got - want))))
 
 
 def _valid_cut(chosen_vals: np.ndarray, all_vals: np.ndarray, slack: float, what: str):

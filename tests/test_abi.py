@@ -21,7 +21,7 @@ def declared_functions():
     return sorted(set(re.findall(r"\b(prism_\w+)\s*\(", src)))
 
 
-def test_header_declares_north_star_calls():
+def test_header_declares_drafting_calls():
     fns = declared_functions()
     for name in ("prism_draft_load_params", "prism_draft_step", "prism_draft_chain",
                  "prism_draft_tree"):
@@ -39,16 +39,34 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
-def _struct_sizes_from_header():
-    return {"prism_config": 17 * 4, "prism_param_set": 10 * 8 + 8,
-            "prism_batch": 8 + 6 * 8 + 8}
+STRUCTS = ("prism_config", "prism_param_set", "prism_batch", "prism_catchup", "prism_step_io",
+           "prism_tree_out")
 
 
-def test_struct_layouts():
-    s = _struct_sizes_from_header()
-    assert ctypes.sizeof(B.prism_config) == s["prism_config"]
-    assert ctypes.sizeof(B.prism_param_set) == s["prism_param_set"]
-    assert ctypes.sizeof(B.prism_batch) == s["prism_batch"]
+def _layouts_from_header(tmp_path):
+    """sizeof and field offsets of the header's structs, from a C compiler."""
+    import subprocess
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "prism_draft.h"', "int main(void) {"]
+    for st in STRUCTS:
+        lines.append('  printf("%s %%zu\\n", sizeof(%s));' % (st, st))
+        for f, _ in getattr(B, st)._fields_:
+            lines.append('  printf("%s.%s %%zu\\n", offsetof(%s, %s));' % (st, f, st, f))
+    lines.append("  return 0;\n}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    return {k: int(v) for k, v in (ln.split() for ln in out.splitlines())}
+
+
+def test_struct_layouts(tmp_path):
+    ref = _layouts_from_header(tmp_path)
+    for st in STRUCTS:
+        cls = getattr(B, st)
+        assert ctypes.sizeof(cls) == ref[st], st
+        for f, _ in cls._fields_:
+            assert getattr(cls, f).offset == ref["%s.%s" % (st, f)], (st, f)
 
 
 def _cfg(**kw):
@@ -74,6 +92,8 @@ def _cfg(**kw):
     (dict(max_batch=65), -2),            # more than 64 rows per pass
     (dict(tree_width=8, tree_nodes=0, max_steps=3), -2),
     (dict(tree_width=8, tree_nodes=60, max_steps=9, max_batch=1), -2),  # > 64 draft slots
+    (dict(max_new_rows=65), -2),         # more than 64 catch-up rows
+    (dict(max_new_rows=-1), -2),
 ])
 def test_create_rejects_bad_config(bad, code):
     L = B.lib()

@@ -66,6 +66,34 @@ def test_short_block_table_raises_capacity_flag():
     dr.close()
 
 
+def test_malformed_catchup_offsets_raise_flag():
+    from paper_2602_01762_amd import PrismError
+    cfg = CFG.with_(n_new=(1, 3))
+    dr, w, inp = gpu_setup(cfg)
+    good = inp.new_offsets.clone()
+    bad = good.clone()
+    bad[1] = bad[0]                                # an empty sequence
+    inp.new_offsets = bad
+    dr.chain_catchup(inp)
+    torch.cuda.synchronize()
+    assert dr.device_status() == -1    # PRISM_ERR_INVALID_ARG
+    inp.new_offsets = good
+    dr.chain_catchup(inp)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    # host-side checks: too many rows for the context, no catch-up capacity
+    inp.new_tokens = torch.cat([inp.new_tokens] * 8)
+    with pytest.raises(PrismError) as e:
+        dr.chain_catchup(inp)
+    assert e.value.status == -1
+    dr.close()
+    plain = _drafter(CFG)
+    with pytest.raises(PrismError) as e:
+        plain.chain_catchup(make_inputs(cfg, "cuda"))
+    assert e.value.status == -1
+    plain.close()
+
+
 def test_out_of_range_token_raises_flag():
     dr, w, inp = gpu_setup(CFG)
     bad = inp.tokens.clone()

@@ -8,8 +8,8 @@ import numpy as np
 import pytest
 import torch
 
-from synth import (L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32, SMALL_BF16_CHAIN,
-                   SMALL_BF16_TREE, SMALL_F32_CHAIN, TINY_F32)
+from synth import (L3_8B_BS1, L3_8B_BS1_CATCHUP, L3_8B_BS16, L3_8B_BS16_CATCHUP, L3_8B_TREE,
+                   L3_70B_BS32, SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN, TINY_F32)
 from harness import check_chain, check_tree, gpu_setup, log, oracle_for
 
 pytestmark = [pytest.mark.gpu,
@@ -27,7 +27,7 @@ def run_chain_parity(cfg, seqs=None):
     seqs = list(range(cfg.batch)) if seqs is None else seqs
     orc, hi = oracle_for(cfg, w, inp, seqs)
     log("oracle", cfg.name, "seqs", seqs)
-    res = check_chain(cfg, out, orc, hi, seqs)
+    res = check_chain(cfg, out, orc, hi, seqs, inp=inp)
     log(cfg.name, res)
     dr.close()
     return res
@@ -62,6 +62,43 @@ def test_chain_parity_row_counts(cfg):
 ], ids=lambda c: c.name)
 def test_chain_parity_unsplit_products(cfg):
     run_chain_parity(cfg)
+
+
+# Catch-up chains: step 1 is the prefill over every accepted token of a
+# sequence (ragged n_b), then the chain continues from the last one.  The
+# draft KV written for the accepted rows and the chain steps is compared slot
+# by slot.  n_b = 2 at one sequence keeps the front on the GEMV path; larger
+# totals take the MFMA path, and the back of step 1 runs on B rows.
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs1_n2", batch=1, n_new=(2, 2)),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs1_n5", batch=1, n_new=(5, 5)),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs3", batch=3, n_new=(1, 5)),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs12", batch=12, n_new=(1, 4)),
+    SMALL_F32_CHAIN.with_(name="small_f32_catchup", n_new=(1, 4)),
+], ids=lambda c: c.name)
+def test_chain_catchup_parity(cfg):
+    log("catch-up parity", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.chain_catchup(inp, logits=True, hidden=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    seqs = list(range(cfg.batch))
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    res = check_chain(cfg, out, orc, hi, seqs, catchup=True, inp=inp)
+    log(cfg.name, "n_b", np.diff(hi["new_offsets"]).tolist(), res)
+    dr.close()
+
+
+def test_catchup_of_one_token_equals_chain():
+    cfg = SMALL_BF16_CHAIN.with_(n_new=(1, 1))
+    dr, w, inp = gpu_setup(cfg)
+    a = dr.chain_catchup(inp, logits=True, hidden=True)
+    b = dr.chain(inp, logits=True, hidden=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a["tokens"], b["tokens"])
+    assert torch.equal(a["logits"], b["logits"])
+    assert torch.equal(a["hidden"], b["hidden"])
+    dr.close()
 
 
 def test_chain_deterministic_and_poison_free():
@@ -151,3 +188,29 @@ def test_full_8b_tree():
 @pytest.mark.slow
 def test_full_70b_bs32_chain():
     run_chain_parity(L3_70B_BS32, seqs=[0, 31])
+
+
+def run_catchup_parity(cfg, seqs):
+    log("catch-up parity", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.chain_catchup(inp, logits=True, hidden=True)
+    plain = dr.chain_catchup(inp)                # the launch the benchmark times
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    assert torch.equal(out["tokens"], plain["tokens"])
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    res = check_chain(cfg, out, orc, hi, seqs, catchup=True, inp=inp)
+    log(cfg.name, "seqs", seqs, res)
+    dr.close()
+
+
+@pytest.mark.slow
+def test_full_8b_bs1_catchup():
+    run_catchup_parity(L3_8B_BS1_CATCHUP, [0])
+
+
+@pytest.mark.slow
+def test_full_8b_bs16_catchup():
+    from synth import new_counts
+    n = new_counts(L3_8B_BS16_CATCHUP)
+    run_catchup_parity(L3_8B_BS16_CATCHUP, sorted({int(np.argmin(n)), int(np.argmax(n)), 15}))
