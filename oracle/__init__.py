@@ -9,5 +9,5 @@ Parity status of each function (what pins it) is listed in the test module
 tests/test_oracle_pins.py; no function here is "parity unpinned".
 """
 from .draft import (Oracle, brute_chain, round_bf16, rmsnorm, silu, rope, rope_cos_sin,
-                    softmax_attend, logsumexp, topk_ids)
+                    softmax_attend, logsumexp, topk_ids, sample_inverse_cdf)
 from ._native import linear, widen, build as build_native

@@ -116,6 +116,22 @@ def topk_ids(v: np.ndarray, k: int) -> np.ndarray:
     return np.argsort(-v, kind="stable")[:k]
 
 
+def sample_inverse_cdf(logits: np.ndarray, temperature: float, u: float):
+    """Draw from p = softmax(logits / T) with the uniform u in [0, 1): the
+    smallest token id t whose cumulative probability (ids 0..t, in id order)
+    exceeds u.  Returns (t, log p_t).  This is the draft distribution whose
+    probabilities the rejection rule of Sec. 2 compares with the target's.
+    """
+    z = logits / temperature
+    m = z.max()
+    e = np.exp(z - m)
+    S = e.sum()
+    cdf = np.cumsum(e) / S
+    t = int(np.searchsorted(cdf, u, side="right"))
+    t = min(t, len(cdf) - 1)
+    return t, float(z[t] - m - np.log(S))
+
+
 # --------------------------------------------------------------------- model
 class Oracle:
     """The drafter on host arrays (see module docstring)."""
@@ -199,7 +215,9 @@ class Oracle:
 
     # chain ------------------------------------------------------------------
     def chain(self, hi: dict, K: Optional[int] = None, forced: Optional[np.ndarray] = None,
-              seqs: Optional[Sequence[int]] = None, catchup: bool = False) -> Dict[str, np.ndarray]:
+              seqs: Optional[Sequence[int]] = None, catchup: bool = False,
+              temperature: Optional[float] = None,
+              uniforms: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
         """Greedy K-step chain for the sequences in `seqs` (default all).
 
         Step 1 is the drafter's prefill (Sec. 3.2, "Draft with PRISM"): each
@@ -213,8 +231,14 @@ class Oracle:
         delimited by hi["new_offsets"].  Step k >= 2 fuses E(x_{k-1}) with
         h_{k-2} at position L_b + n_b + k - 2.
 
+        Greedy by default (x_k = argmax, ties to the lowest id).  With a
+        `temperature` T > 0, x_k is drawn from softmax(logits / T) by
+        sample_inverse_cdf with the uniform uniforms[b, k-1] (stochastic
+        drafting, Sec. 2; Sec. 3.2 notes PRISM works with it), and
+        "logp"[b, k-1] holds log p_draft(x_k).
+
         forced[b, k]: token fed to step k+2 instead of the oracle's own
-        argmax of step k+1 (teacher forcing on another drafter's choices).
+        choice at step k+1 (teacher forcing on another drafter's choices).
         Returns tokens [B,K], logits [B,K,V], hidden [B,K,H] (rows of
         sequences not computed are left at -1 / NaN; step 1 holds the last
         row's values) and, per computed sequence, the draft KV it wrote
@@ -228,6 +252,15 @@ class Oracle:
         toks = np.full((B, K), -1, dtype=np.int64)
         logits = np.full((B, K, cfg.vocab), np.nan)
         hidden = np.full((B, K, cfg.hidden), np.nan)
+        logp = np.full((B, K), np.nan)
+
+        def choose(b, k, lg):       # the token of step k (1-based) from its logits
+            if temperature is None:
+                return int(np.argmax(lg))
+            t, lp = sample_inverse_cdf(lg, temperature, float(uniforms[b, k - 1]))
+            logp[b, k - 1] = lp
+            return t
+
         caches = {b: self.new_cache(hi, b) for b in seqs}
         # the accepted rows of each sequence, oldest first
         acc = {}
@@ -253,7 +286,7 @@ class Oracle:
         x_in, f_in, start = {}, {}, {}
         for b in seqs:
             i = last[b]
-            toks[b, 0] = int(np.argmax(lg[i]))
+            toks[b, 0] = choose(b, 1, lg[i])
             logits[b, 0] = lg[i]
             hidden[b, 0] = h[i]
             x_in[b] = int(forced[b, 0]) if forced is not None else toks[b, 0]
@@ -266,12 +299,12 @@ class Oracle:
             h, lg = self.forward(s, [x_in[b] for b in seqs], np.stack([f_in[b] for b in seqs]),
                                  pos, caches, seqs, pos, [list(range(p + 1)) for p in pos])
             for i, b in enumerate(seqs):
-                toks[b, k - 1] = int(np.argmax(lg[i]))
+                toks[b, k - 1] = choose(b, k, lg[i])
                 logits[b, k - 1] = lg[i]
                 hidden[b, k - 1] = h[i]
                 x_in[b] = int(forced[b, k - 1]) if forced is not None else toks[b, k - 1]
                 f_in[b] = h[i]
-        return {"tokens": toks, "logits": logits, "hidden": hidden,
+        return {"tokens": toks, "logits": logits, "hidden": hidden, "logp": logp,
                 "draft_kv": {b: caches[b]["draft"] for b in seqs}}
 
     # tree -------------------------------------------------------------------
@@ -399,7 +432,8 @@ class Oracle:
 
 # ------------------------------------------------------------ brute force
 def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = None,
-                catchup: bool = False):
+                catchup: bool = False, temperature: Optional[float] = None,
+                uniforms: Optional[np.ndarray] = None):
     """Greedy chain recomputed from scratch at every step, for tiny shapes.
 
     No cache object survives between steps: for step k all draft positions
@@ -408,8 +442,9 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
     chain positions (set f(j), its token, and the hidden state this same
     recomputation produced for the position before) -- attention is an
     explicit causal mask over the full key matrix, and the token is the
-    first entry of a full sort of the logits.  Returns tokens [B,K] and
-    hidden [B,K,H].
+    first entry of a full sort of the logits, or with a temperature the
+    first id at which a running sum of exp(logit / T - max) passes u times
+    the total.  Returns tokens [B,K] and hidden [B,K,H].
     """
     cfg = orc.cfg
     H, d, nq, nkv = cfg.hidden, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
@@ -463,8 +498,18 @@ def brute_chain(orc: Oracle, hi: dict, K: int, seqs: Optional[Sequence[int]] = N
                 if j == n - 1:
                     lg = orc.lin(orc.hw["lm_head"],
                                  rmsnorm(hj[None], orc.g_f, cfg.rms_eps))[0]
-                    order = np.argsort(-lg, kind="stable")
-                    chosen.append(int(order[0]))
+                    if temperature is None:
+                        order = np.argsort(-lg, kind="stable")
+                        chosen.append(int(order[0]))
+                    else:
+                        w = [float(np.exp((x - lg.max()) / temperature)) for x in lg]
+                        goal, run, pick = float(uniforms[b, k - 1]) * sum(w), 0.0, len(w) - 1
+                        for t, wt in enumerate(w):
+                            run += wt
+                            if run > goal:
+                                pick = t
+                                break
+                        chosen.append(pick)
                     hidden[b, k - 1] = hj
                 elif j < n0 - 1:
                     tok, feat = pre[j + 1]  # the next accepted token, its target feature

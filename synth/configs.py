@@ -42,6 +42,9 @@ class DraftConfig:
     # chain whose step 1 catches up on n_b accepted tokens per sequence,
     # n_b uniform on this inclusive range (None: step 1 takes the last one)
     n_new: Optional[Tuple[int, int]] = None
+    # stochastic drafting: tokens drawn from softmax(logits / T) with seeded
+    # uniforms (None: greedy)
+    temperature: Optional[float] = None
 
     # ---- derived -------------------------------------------------------
     @property

@@ -16,6 +16,8 @@ tensor is synthetic):
   * paged KV: blocks of `kv_block_size` slots; the block table is a seeded
     permutation of the physical blocks when `shuffle_blocks` is set; slots that
     hold no prior context are NaN so that a read of them shows up.
+  * stochastic drafting: one uniform on [0, 1) per (sequence, step), the
+    draw that picks the token by inverse CDF
   * catch-up chains: n_b accepted tokens per sequence, uniform on the
     configured inclusive range; the earlier n_b - 1 tokens uniform on [0, V)
     and their target features N(0, 1); the newest one is the sequence's
@@ -34,7 +36,7 @@ from .configs import DraftConfig
 # tensor ids used to derive per-tensor seeds
 T_EMBED, T_LMHEAD, T_FNORM = 0, 1, 2
 T_FC, T_G1, T_WQ, T_WK, T_WV, T_WO, T_G2, T_WGATE, T_WUP, T_WDOWN = range(10, 20)
-T_TOK, T_FEAT, T_CTX, T_KPOOL, T_VPOOL, T_BTAB, T_NNEW, T_NTOK, T_NFEAT = range(100, 109)
+T_TOK, T_FEAT, T_CTX, T_KPOOL, T_VPOOL, T_BTAB, T_NNEW, T_NTOK, T_NFEAT, T_UNIF = range(100, 110)
 
 SET_TENSORS = ("w_fc", "g1", "w_q", "w_k", "w_v", "w_o", "g2", "w_gate", "w_up", "w_down")
 
@@ -99,6 +101,8 @@ class Inputs:
     new_offsets: Optional[torch.Tensor] = None   # int32 [B + 1]
     new_tokens: Optional[torch.Tensor] = None    # int32 [T]
     new_features: Optional[torch.Tensor] = None  # [T, F_t]
+    # stochastic drafting only: the uniform in [0, 1) of each (sequence, step)
+    uniforms: Optional[torch.Tensor] = None      # fp32 [B, K]
 
 
 def make_param_set(cfg: DraftConfig, s: int, device="cpu") -> ParamSet:
@@ -206,6 +210,9 @@ def make_inputs(cfg: DraftConfig, device="cpu", extra_blocks: int = 0) -> Inputs
         inp.new_offsets = torch.from_numpy(offs).to(device)
         inp.new_tokens = torch.cat(nt).contiguous()
         inp.new_features = torch.cat(nf, 0).contiguous()
+    if cfg.temperature is not None:
+        inp.uniforms = torch.rand((B, cfg.n_steps), generator=_gen(device, sd, T_UNIF),
+                                  device=device, dtype=torch.float32)
     return inp
 
 
@@ -266,4 +273,6 @@ def host_inputs(inp: Inputs, cfg: DraftConfig, seqs=None) -> dict:
         out["new_offsets"] = to_host(inp.new_offsets)
         out["new_tokens"] = to_host(inp.new_tokens)
         out["new_features"] = to_host(inp.new_features)
+    if inp.uniforms is not None:
+        out["uniforms"] = to_host(inp.uniforms).astype(np.float64)
     return out

@@ -15,7 +15,7 @@ import torch
 
 import oracle
 from oracle import Oracle, brute_chain, round_bf16, rmsnorm, silu, rope, softmax_attend
-from oracle import logsumexp, topk_ids, widen
+from oracle import logsumexp, topk_ids, widen, sample_inverse_cdf
 from synth import DraftConfig, make_weights, make_inputs, host_weights, host_inputs
 
 pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
@@ -204,6 +204,48 @@ def test_catchup_block_prefill_equals_row_by_row():
         for slot, (kk, vv) in cache[b]["draft"].items():
             rk, rv = ref["draft_kv"][b][slot]
             assert np.array_equal(kk, rk) and np.array_equal(vv, rv)
+
+
+# ------------------------------------------------------------------ T1c stochastic drafting
+def test_inverse_cdf_frequencies_match_softmax():
+    # u on a regular grid: the share of grid points mapped to token t is its
+    # probability up to the grid step; the returned log-prob is log p_t
+    lg = np.random.default_rng(3).standard_normal(7) * 2.0
+    N = 20000
+    for T in (0.5, 1.0, 2.0):
+        p = np.exp(lg / T - (lg / T).max())
+        p /= p.sum()
+        counts = np.zeros(len(lg))
+        for i in range(N):
+            t, lp = sample_inverse_cdf(lg, T, (i + 0.5) / N)
+            counts[t] += 1
+            assert abs(lp - np.log(p[t])) < 1e-12
+        assert np.max(np.abs(counts / N - p)) <= 1.0 / N + 1e-12
+
+
+def test_inverse_cdf_edges():
+    lg = np.array([0.3, -1.0, 2.0, 0.5])
+    assert sample_inverse_cdf(lg, 1.0, 0.0)[0] == 0
+    assert sample_inverse_cdf(lg, 1.0, float(np.nextafter(1.0, 0.0)))[0] == 3
+    for u in (0.01, 0.5, 0.99):      # a cold temperature puts the mass on the argmax
+        assert sample_inverse_cdf(lg, 1e-3, u)[0] == 2
+
+
+@pytest.mark.parametrize("cfg", [TINY, TINY_BF16], ids=lambda c: c.dtype)
+def test_sampled_chain_equals_brute_force(cfg):
+    scfg = cfg.with_(temperature=1.0)
+    hw, hi = build(scfg)
+    orc = Oracle(scfg, hw)
+    inc = orc.chain(hi, temperature=1.0, uniforms=hi["uniforms"])
+    bf = brute_chain(orc, hi, scfg.n_steps, temperature=1.0, uniforms=hi["uniforms"])
+    assert np.array_equal(inc["tokens"], bf["tokens"])
+    assert np.max(np.abs(inc["hidden"] - bf["hidden"])) < 1e-12
+    greedy = orc.chain(hi)
+    assert not np.array_equal(inc["tokens"], greedy["tokens"])   # the draws matter
+    lse = np.array([[logsumexp(inc["logits"][b, k]) for k in range(scfg.n_steps)]
+                    for b in range(scfg.batch)])
+    picked = np.take_along_axis(inc["logits"], inc["tokens"][..., None], axis=2)[..., 0]
+    assert np.max(np.abs(inc["logp"] - (picked - lse))) < 1e-12
 
 
 # ------------------------------------------------------------------ T2 tree = chains
