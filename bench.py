@@ -56,6 +56,7 @@ WORKLOADS = {
     "70b_bs32": "llama3_70b_bf16_chain_bs32",
     "8b_bs1_catchup": "llama3_8b_bf16_chain_bs1_catchup4",
     "8b_bs16_catchup": "llama3_8b_bf16_chain_bs16_paged_catchup",
+    "8b_bs1_t1": "llama3_8b_bf16_chain_bs1_t1",
 }
 
 
@@ -112,6 +113,9 @@ def main():
         call = lambda: dr.tree(inp, out=out, batch=b)
     elif cfg.n_new:      # step 1 prefills every accepted token
         call = lambda: dr.chain_catchup(inp, out=out, batch=b)
+    elif cfg.temperature:    # stochastic drafting: draws and their log p_draft
+        out["logp"] = torch.empty((cfg.batch, cfg.n_steps), dtype=torch.float32, device="cuda")
+        call = lambda: dr.chain_sample(inp, cfg.temperature, out=out, batch=b)
     else:
         call = lambda: dr.chain(inp, out=out, batch=b)
 
@@ -165,7 +169,8 @@ def main():
         "config": {"workload": cfg.name, "batch": cfg.batch, "draft_steps": K,
                    "prior_context": cfg.max_ctx if cfg.ctx_range is None else list(cfg.ctx_range),
                    "kv_block": cfg.kv_block_size, "mode": cfg.mode,
-                   "accepted_tokens_step1": list(cfg.n_new) if cfg.n_new else 1},
+                   "accepted_tokens_step1": list(cfg.n_new) if cfg.n_new else 1,
+                   "temperature": cfg.temperature or 0.0},
         "per_draft_step_us": round(ms_per_step * 1e3 / K, 2),
         "weight_bytes_per_step_call": chain_bytes,
         "whole_call_hbm_frac_weights_only": round(chain_bytes / (ms_per_step * 1e-3) / 1e9
@@ -208,7 +213,8 @@ def cpu_baseline(cfg, w, inp, dr):
         if cfg.mode == "tree":
             orc.tree(hi, seqs=seqs)
         else:
-            orc.chain(hi, seqs=seqs, catchup=bool(cfg.n_new))
+            orc.chain(hi, seqs=seqs, catchup=bool(cfg.n_new), temperature=cfg.temperature,
+                      uniforms=hi.get("uniforms"))
         n += 1
         el = time.perf_counter() - t0
         if el >= 10.0 or n >= 200:

@@ -231,6 +231,27 @@ prism_status prism_draft_chain(prism_ctx *ctx, const prism_batch *batch,
                                float *d_out_logits, float *d_out_hidden,
                                void *stream);
 
+/* K-step chain with stochastic drafting (paper Sec. 2: draft tokens are
+ * drawn from p_draft and verified by a rejection rule on the ratio
+ * p_target / p_draft; Sec. 3.2: PRISM works with stochastic sampling; the T =
+ * 1 rows of Tables 4-5).  Steps, positions and KV slots as in
+ * prism_draft_chain; x_k is drawn from softmax(logits / temperature) by
+ * inverse CDF in token-id order: the smallest id whose cumulative
+ * probability exceeds u = d_uniforms[b*K + k-1].  The caller draws the
+ * uniforms (so a call is reproducible); values are clamped to [0, 1].
+ *   temperature   > 0 (finite 1/temperature)
+ *   d_uniforms    [B, K] fp32
+ *   d_out_tokens  [B, K] int32 drawn tokens
+ *   d_out_logp    [B, K] fp32 log p_draft(x_k) of the drawn tokens, or NULL
+ *   d_out_logits  [B, K, V] fp32 raw logits, or NULL
+ *   d_out_hidden  [B, K, H] fp32, or NULL */
+prism_status prism_draft_chain_sample(prism_ctx *ctx, const prism_batch *batch,
+                                      int32_t K, float temperature,
+                                      const float *d_uniforms,
+                                      int32_t *d_out_tokens, float *d_out_logp,
+                                      float *d_out_logits, float *d_out_hidden,
+                                      void *stream);
+
 /* Greedy K-step chain whose first step catches up on several accepted
  * tokens per sequence (paper Sec. 3.2: the prefill over S_acc with H_base,
  * then h_0 = the last row's output and x_1 = argmax LM_head(h_0)).  Step 1

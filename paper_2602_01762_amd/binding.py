@@ -18,7 +18,8 @@ STATUS = {0: "PRISM_OK", -1: "PRISM_ERR_INVALID_ARG", -2: "PRISM_ERR_SHAPE",
           -5: "PRISM_ERR_OUT_OF_MEMORY", -6: "PRISM_ERR_HIP", -7: "PRISM_ERR_CAPACITY"}
 EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_load_shared",
            "prism_draft_load_params", "prism_set_step_map", "prism_draft_step",
-           "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_tree",
+           "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_chain_sample",
+           "prism_draft_tree",
            "prism_device_status",
            "prism_profile_enable", "prism_profile_read")
 
@@ -95,6 +96,8 @@ def lib():
         L.prism_draft_chain.argtypes = [c_vp, P(prism_batch), c_i32, c_vp, c_vp, c_vp, c_vp]
         L.prism_draft_chain_catchup.argtypes = [c_vp, P(prism_batch), P(prism_catchup), c_i32,
                                                 c_vp, c_vp, c_vp, c_vp]
+        L.prism_draft_chain_sample.argtypes = [c_vp, P(prism_batch), c_i32, c_f32, c_vp, c_vp,
+                                               c_vp, c_vp, c_vp, c_vp]
         L.prism_draft_tree.argtypes = [c_vp, P(prism_batch), c_i32, P(prism_tree_out), c_vp]
         L.prism_device_status.argtypes = [c_vp, c_vp]
         L.prism_profile_enable.argtypes = [c_vp, c_i32]
@@ -169,6 +172,15 @@ def prism_draft_chain_catchup(ctx, batch: prism_batch, catchup: prism_catchup, K
     _check(lib().prism_draft_chain_catchup(ctx, ctypes.byref(batch), ctypes.byref(catchup), K,
                                            ptr(out_tokens), ptr(out_logits), ptr(out_hidden),
                                            cur_stream() if stream is None else stream), ctx)
+
+
+def prism_draft_chain_sample(ctx, batch: prism_batch, K: int, temperature: float, uniforms,
+                             out_tokens, out_logp=None, out_logits=None, out_hidden=None,
+                             stream=None):
+    _check(lib().prism_draft_chain_sample(ctx, ctypes.byref(batch), K, float(temperature),
+                                          ptr(uniforms), ptr(out_tokens), ptr(out_logp),
+                                          ptr(out_logits), ptr(out_hidden),
+                                          cur_stream() if stream is None else stream), ctx)
 
 
 def prism_draft_tree(ctx, batch: prism_batch, depth: int, out: prism_tree_out, stream=None):

@@ -608,13 +608,15 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
       mx = fmaxf(mx, v[n]);
     }
     mx = wave_max(mx);
+    // max and sum of exp over the scaled logits z = v * inv_temp (inv_temp > 0)
+    const float mz = mx * g.inv_temp;
     float e = 0.f;
 #pragma unroll
-    for (int n = 0; n < NT; ++n) e += id[n] != 0x7fffffff ? expf(v[n] - mx) : 0.f;
+    for (int n = 0; n < NT; ++n) e += id[n] != 0x7fffffff ? expf(v[n] * g.inv_temp - mz) : 0.f;
     const float s = wave_sum(e);
     const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
     if (lane == 0) {
-      g.pmax[pi] = mx;
+      g.pmax[pi] = mz;
       g.psum[pi] = s;
     }
     for (int j = 0; j < g.topk; ++j) {

@@ -138,8 +138,9 @@ struct LmLaunch {
   float *pmax, *psum, *pval;       // partials [R][n_wg] / [R][n_wg][topk]
   int *pid;
   int n_wg;
-  int nt;                          // vocab tiles per wave (1 or 2)
-  int gemv;                        // 1: VALU GEMV main loop (bf16, R <= 4)
+  int nt;                          // vocab tiles per wave (1, 2, 4 or 8)
+  int gemv;                        // 1: VALU GEMV main loop (bf16, one row)
+  float inv_temp;                  // pmax / psum describe logits * inv_temp (1: greedy)
 };
 
 // ---- launchers (gemm.hip) -------------------------------------------------
@@ -163,6 +164,22 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
                       const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
                       ActOut o, uint32_t *err, hipStream_t s);
 int attention_chunks(int max_slots, int nsub);
+// Draw each row's token from softmax(logits * inv_temp) by inverse CDF in
+// id order with the row's uniform u[r * ld_u]: the LM head's per-group
+// (max, sum) of the scaled logits locate the group where the running sum
+// passes u * total, and the row's stored fp32 logits locate the id inside it.
+struct LmSampleArgs {
+  int R, n_wg, V, group;           // group: vocab ids per LM-head workgroup
+  float inv_temp;
+  const float *pmax, *psum;        // [R][n_wg], scaled logits
+  const float *logits; long ld_logits;
+  const float *u; int ld_u;
+  int *ids;                        // [R] drawn token
+  float *logp; int ld_logp;        // [R * ld_logp] its log-probability, or NULL
+  int *tok_a;                      // optional [R] copy
+  int *tok_b; int ld_b;            // optional [R * ld_b] copy
+};
+void launch_lm_sample(const LmSampleArgs &a, hipStream_t s);
 // merge LM-head partials: top-k ids, optional log-probs, and the chain's token copies
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,

@@ -203,6 +203,134 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Stochastic drafting: inverse-CDF draw of row r (one workgroup).  Groups
+// are contiguous vocab ranges in id order; thread t owns a contiguous run of
+// groups, so the exclusive prefix of the per-thread sums (taken in thread
+// order) orders the whole vocabulary.  The first group whose running sum
+// passes u * S holds the token; wave 0 then scans that group's ids with a
+// fixed-order wave prefix sum.  A draw that rounding pushes past the last
+// group takes the highest id of nonzero probability.
+__global__ __launch_bounds__(256) void k_lm_sample(LmSampleArgs a) {
+  __shared__ float shv[8];
+  __shared__ float s_pre[256];
+  __shared__ int s_cg[256];
+  __shared__ float s_cb[256];
+  __shared__ float s_S;
+  __shared__ int s_g;
+  __shared__ float s_base;
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const float *pm = a.pmax + (size_t)r * a.n_wg;
+  const float *ps = a.psum + (size_t)r * a.n_wg;
+  float m = -INFINITY;
+  for (int g = tid; g < a.n_wg; g += 256) m = fmaxf(m, pm[g]);
+  const float M = block_max(m, shv);
+  const int per = (a.n_wg + 255) / 256;
+  const int g0 = tid * per < a.n_wg ? tid * per : a.n_wg;
+  const int g1 = g0 + per < a.n_wg ? g0 + per : a.n_wg;
+  auto weight = [&](int g) { return pm[g] == -INFINITY ? 0.f : ps[g] * expf(pm[g] - M); };
+  float loc = 0.f;
+  for (int g = g0; g < g1; ++g) loc += weight(g);
+  s_pre[tid] = loc;
+  __syncthreads();
+  if (tid == 0) {   // exclusive prefix in thread (= id) order
+    float run = 0.f;
+    for (int i = 0; i < 256; ++i) {
+      const float t = s_pre[i];
+      s_pre[i] = run;
+      run += t;
+    }
+    s_S = run;
+  }
+  __syncthreads();
+  const float S = s_S;
+  const float u = fminf(fmaxf(a.u[(size_t)r * a.ld_u], 0.f), 1.f);
+  const float goal = u * S;
+  {
+    float run = s_pre[tid];
+    int cg = 0x7fffffff;
+    float cb = 0.f;
+    for (int g = g0; g < g1; ++g) {
+      const float w = weight(g);
+      if (w > 0.f && run + w > goal) {
+        cg = g;
+        cb = run;
+        break;
+      }
+      run += w;
+    }
+    s_cg[tid] = cg;
+    s_cb[tid] = cb;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int g = -1;
+    float base = 0.f;
+    for (int i = 0; i < 256; ++i)
+      if (s_cg[i] != 0x7fffffff) {
+        g = s_cg[i];
+        base = s_cb[i];
+        break;
+      }
+    if (g < 0) {    // past the end by rounding: the last group of nonzero weight
+      float run = S;
+      for (int q = a.n_wg - 1; q >= 0; --q) {
+        const float w = weight(q);
+        run -= w;
+        if (w > 0.f) {
+          g = q;
+          base = run;
+          break;
+        }
+      }
+    }
+    s_g = g;
+    s_base = base;
+  }
+  __syncthreads();
+  if (tid >= 64) return;
+  const int g = s_g;
+  int tok = -1;
+  if (g >= 0) {
+    const float *lg = a.logits + (size_t)r * a.ld_logits;
+    const int id0 = g * a.group;
+    float run = s_base;
+    int last_nz = -1;
+    for (int i0 = 0; i0 < a.group; i0 += 64) {
+      const int id = id0 + i0 + lane;
+      const float e = id < a.V ? expf(lg[id] * a.inv_temp - M) : 0.f;
+      float x = e;   // inclusive prefix over the wave, fixed order
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float t = __shfl_up(x, o, 64);
+        if (lane >= o) x += t;
+      }
+      const unsigned long long hit = __ballot(e > 0.f && run + x > goal);
+      const unsigned long long nz = __ballot(e > 0.f);
+      if (nz) last_nz = id0 + i0 + 63 - __clzll((long long)nz);
+      if (hit) {
+        tok = id0 + i0 + __ffsll((long long)hit) - 1;
+        break;
+      }
+      run += __shfl(x, 63, 64);
+    }
+    if (tok < 0) tok = last_nz;
+  }
+  if (lane == 0) {
+    a.ids[r] = tok;
+    if (a.logp) {
+      const float lt = tok >= 0 ? a.logits[(size_t)r * a.ld_logits + tok] * a.inv_temp : -INFINITY;
+      a.logp[(size_t)r * a.ld_logp] = lt - M - logf(S);
+    }
+    if (a.tok_a) a.tok_a[r] = tok;
+    if (a.tok_b) a.tok_b[(size_t)r * a.ld_b] = tok;
+  }
+}
+
+void launch_lm_sample(const LmSampleArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(k_lm_sample, dim3(a.R), dim3(256), 0, s, a);
+}
+
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
                        int *tok_b, int ld_b, hipStream_t s) {

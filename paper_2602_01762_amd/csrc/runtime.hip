@@ -35,6 +35,10 @@ struct Pass {            // one forward pass: where its inputs and outputs live
   RowsIn in;
   TokFromLm lm_in;        // tokens from the previous pass's LM partials (pval != NULL)
   bool defer_merge;       // leave the LM partials to the next pass (chain, top-1)
+  // stochastic drafting (u != NULL): draw from softmax(logits * inv_temp)
+  const float *u; int ld_u;
+  float inv_temp;
+  float *logp_out; int ld_logp;
   float *hid_out; int ld_hid;
   float *logits; long ld_logits;
   int *ids; float *logp;
@@ -85,6 +89,7 @@ struct prism_ctx {
   int new_max = 0;                  // catch-up rows capacity
   int32_t *c_rseq = nullptr, *c_rpos = nullptr, *c_last = nullptr;   // catch-up rows
   float *q2 = nullptr, *u2 = nullptr;   // q and u of each sequence's last accepted row
+  float *samp_logits = nullptr;     // [rows, V] fp32 logits kept for the sampler
   size_t lds_limit = 65536;         // LDS bytes one workgroup may use
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
@@ -314,6 +319,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->ids, R * c->kmax * 4);
   add((void **)&c->logp, R * c->kmax * 4);
   add((void **)&c->tokbuf, R * 4);
+  add((void **)&c->samp_logits, R * c->V * 4);
   add((void **)&c->c_seq, (size_t)k.max_batch * 4);
   add((void **)&c->c_pos, (size_t)k.max_batch * k.max_steps * 4);
   add((void **)&c->c_tok0, (size_t)k.max_batch * 4);
@@ -624,6 +630,7 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   lmg.R = R;
   lmg.V = c->V;
   lmg.topk = p.topk;
+  lmg.inv_temp = p.u ? p.inv_temp : 1.f;
   lmg.gemv = (c->bf16 && R <= LM_GEMV_MAX_ROWS && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
   lmg.nt = 1;
   if (!lmg.gemv && R > LM_GEMV_MAX_ROWS) {   // batched rows: several vocab tiles per wave share B fragments
@@ -635,15 +642,30 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   lmg.norm = norm_for(c, c->ss_h, c->sc_h, R, 256, s);
   lmg.logits = p.logits;
   lmg.ld_logits = p.ld_logits;
+  if (p.u && !lmg.logits) {   // the sampler reads the draw's group back from the logits
+    lmg.logits = c->samp_logits;
+    lmg.ld_logits = c->V;
+  }
   lmg.pmax = c->lm_max; lmg.psum = c->lm_sum; lmg.pval = c->lm_val; lmg.pid = c->lm_id;
   const bool prof = c->profile && c->prof_used * 2 + 1 < (int)c->prof_ev.size();
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
   launch_lmhead(bf, lmg, s);
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used++ + 1], s);
   c->lm_nwg_last = lmg.n_wg;
-  if (!p.defer_merge)
+  if (p.u) {
+    LmSampleArgs sa{};
+    sa.R = R; sa.n_wg = lmg.n_wg; sa.V = c->V; sa.group = 64 * lmg.nt;
+    sa.inv_temp = p.inv_temp;
+    sa.pmax = c->lm_max; sa.psum = c->lm_sum;
+    sa.logits = lmg.logits; sa.ld_logits = lmg.ld_logits;
+    sa.u = p.u; sa.ld_u = p.ld_u;
+    sa.ids = p.ids; sa.logp = p.logp_out; sa.ld_logp = p.ld_logp;
+    sa.tok_a = p.tok_a; sa.tok_b = p.tok_b; sa.ld_b = p.ld_b;
+    launch_lm_sample(sa, s);
+  } else if (!p.defer_merge) {
     launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
                       p.logp, p.tok_a, p.tok_b, p.ld_b, s);
+  }
 }
 
 static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
@@ -760,9 +782,12 @@ prism_status prism_draft_step(prism_ctx *c, int32_t k, const prism_step_io *io, 
 // all accepted rows: the FC / QKV front runs on the T rows (writing their
 // KV), then the back of the pass continues from each sequence's last row.
 // Step k >= 2 takes its token from the previous LM head's partials.
+// With uniforms u [B, K] the tokens are drawn from softmax(logits / T)
+// (inv_temp = 1/T) and their log-probabilities go to d_out_logp.
 static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, int K,
                           const prism_catchup *cu, int32_t *d_out_tokens, float *d_out_logits,
-                          float *d_out_hidden, hipStream_t s) {
+                          float *d_out_hidden, hipStream_t s, const float *u = nullptr,
+                          float inv_temp = 1.f, float *d_out_logp = nullptr) {
   const int B = b.batch, H = c->H, V = c->V;
   if (cu)
     launch_catchup_setup(B, cu->total_rows, K, cu->d_offsets, b.d_ctx_lens, c->c_rseq, c->c_rpos,
@@ -778,11 +803,15 @@ static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, 
     p.F = k == 1 ? c->cfg.feat_width : H;
     p.topk = 1;
     p.in.tokens = c->c_tok0;      // step 1; later steps take the previous LM partials
-    if (k > 1) {
+    if (u) {                      // drawn tokens: the sampler writes them for the next step
+      if (k > 1) p.in.tokens = c->tokbuf;
+      p.u = u + (k - 1); p.ld_u = K; p.inv_temp = inv_temp;
+      p.logp_out = d_out_logp ? d_out_logp + (k - 1) : nullptr; p.ld_logp = K;
+    } else if (k > 1) {
       p.lm_in.pval = c->lm_val; p.lm_in.pid = c->lm_id; p.lm_in.n_wg = c->lm_nwg_last;
       p.lm_in.rec = d_out_tokens + (k - 2); p.lm_in.ld_rec = K;
     }
-    p.defer_merge = k < K;
+    p.defer_merge = !u && k < K;
     p.in.feat = k == 1 ? b.d_features : (const void *)prev;
     p.in.feat_bf16 = k == 1 ? (int)c->bf16 : 0;
     p.in.feat_ld = k == 1 ? c->cfg.feat_width : ld_prev;
@@ -861,6 +890,31 @@ prism_status prism_draft_chain(prism_ctx *c, const prism_batch *batch, int32_t K
   auto key = chain_key(c, 1, b, K, d_out_tokens, d_out_logits, d_out_hidden);
   return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
     enqueue_chain(c, b, kv, K, nullptr, d_out_tokens, d_out_logits, d_out_hidden, s);
+  });
+}
+
+prism_status prism_draft_chain_sample(prism_ctx *c, const prism_batch *batch, int32_t K,
+                                      float temperature, const float *d_uniforms,
+                                      int32_t *d_out_tokens, float *d_out_logp,
+                                      float *d_out_logits, float *d_out_hidden, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  prism_status st = check_chain(c, batch, K, d_out_tokens);
+  if (st) return st;
+  if (!(temperature > 0.f) || !std::isfinite(1.f / temperature))
+    return fail(c, PRISM_ERR_INVALID_ARG, "temperature %g must be positive", (double)temperature);
+  if (!d_uniforms) return fail(c, PRISM_ERR_INVALID_ARG, "d_uniforms is NULL");
+  const prism_batch b = *batch;
+  const KvArgs kv = kv_of(c, &b);
+  const float inv_temp = 1.f / temperature;
+  auto key = chain_key(c, 4, b, K, d_out_tokens, d_out_logits, d_out_hidden);
+  uint32_t tb;
+  std::memcpy(&tb, &inv_temp, 4);
+  key.push_back((uintptr_t)tb);
+  key.push_back((uintptr_t)d_uniforms);
+  key.push_back((uintptr_t)d_out_logp);
+  return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
+    enqueue_chain(c, b, kv, K, nullptr, d_out_tokens, d_out_logits, d_out_hidden, s, d_uniforms,
+                  inv_temp, d_out_logp);
   });
 }
 

@@ -113,6 +113,20 @@ class Drafter:
         B.prism_draft_chain(self.ctx, b, K, out["tokens"], out["logits"], out["hidden"])
         return out
 
+    def chain_sample(self, inp, temperature: float, K: Optional[int] = None, logits=False,
+                     hidden=False, out=None, batch=None):
+        """Stochastic chain: tokens drawn from softmax(logits / T) with the
+        uniforms inp.uniforms [B, K]; out["logp"] holds log p_draft."""
+        K = K or self.shape.n_steps
+        b = batch if batch is not None else self.batch(inp)
+        if out is None:
+            out = self.chain_buffers(b.batch, K, logits, hidden)
+            out["logp"] = torch.full((b.batch, K), float("nan"), dtype=torch.float32,
+                                     device=self.device)
+        B.prism_draft_chain_sample(self.ctx, b, K, temperature, inp.uniforms, out["tokens"],
+                                   out.get("logp"), out["logits"], out["hidden"])
+        return out
+
     def chain_catchup(self, inp, K: Optional[int] = None, logits=False, hidden=False, out=None,
                       batch=None):
         """Chain whose step 1 is the prefill over inp.new_tokens / new_features

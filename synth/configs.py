@@ -146,8 +146,11 @@ L3_8B_BS1_CATCHUP = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_catchup4", n_
 L3_8B_BS16_CATCHUP = L3_8B_BS16.with_(name="llama3_8b_bf16_chain_bs16_paged_catchup",
                                       n_new=(1, 4))
 
+# Stochastic drafting at T = 1 (the paper's T = 1 rows, Tables 4-5).
+L3_8B_BS1_T1 = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_t1", temperature=1.0)
+
 CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32,
-                               L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP)}
+                               L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP, L3_8B_BS1_T1)}
 
 # Reduced shapes for element-by-element parity: small enough for the oracle to
 # finish in seconds, large enough to span several tiles of every kernel and to

@@ -85,6 +85,44 @@ def check_chain(cfg, out: dict, orc: Oracle, hi: dict, seqs, hidden_tol=None, ca
     return {"max_logit_err": worst, "argmax_agreement": float(agree)}
 
 
+CDF_SLACK = {"bf16": 1e-4, "f32": 1e-6}
+
+
+def check_sampled_chain(cfg, out: dict, orc: Oracle, hi: dict, seqs, temperature: float):
+    """Stochastic chain: with the oracle replayed on the GPU's draws, each
+    drawn token's cumulative-probability interval [F(t-1), F(t)) (oracle, id
+    order) contains its uniform up to a slack for the logit error, and the
+    returned log p_draft matches the oracle's."""
+    tol = LOGIT_TOL[cfg.dtype]
+    toks = out["tokens"].cpu().numpy().astype(np.int64)
+    K = toks.shape[1]
+    u = hi["uniforms"]
+    ref = orc.chain(hi, K=K, forced=toks, seqs=seqs, temperature=temperature, uniforms=u)
+    lp = out["logp"].cpu().numpy()
+    lg = out["logits"].cpu().numpy() if out.get("logits") is not None else None
+    worst, same = 0.0, []
+    for b in seqs:
+        for k in range(K):
+            what = "seq %d step %d" % (b, k + 1)
+            t = int(toks[b, k])
+            assert 0 <= t < cfg.vocab, what
+            z = ref["logits"][b, k] / temperature
+            p = np.exp(z - z.max())
+            p /= p.sum()
+            lo = float(p[:t].sum())
+            hi_ = lo + float(p[t])
+            sl = CDF_SLACK[cfg.dtype] / temperature
+            assert lo - sl <= u[b, k] < hi_ + sl, "%s: u %.7f outside [%.7f, %.7f)" % (
+                what, u[b, k], lo, hi_)
+            e = abs(float(lp[b, k]) - float(np.log(p[t])))
+            assert e <= tol / temperature, "%s: log p %.5f vs %.5f" % (what, lp[b, k], np.log(p[t]))
+            if lg is not None:
+                worst = max(worst, float(np.max(np.abs(lg[b, k] - ref["logits"][b, k]))))
+                assert worst <= tol, "%s: logits max-abs %.3g" % (what, worst)
+            same.append(t == int(ref["tokens"][b, k]))
+    return {"max_logit_err": worst, "draw_agreement": float(np.mean(same))}
+
+
 def check_draft_kv(cfg, inp, draft_kv: dict, seqs):
     """The K and V rows the GPU stored at every draft slot equal the oracle's
     stored values.  fp32 caches: to fp32 accumulation order.  bf16: within one

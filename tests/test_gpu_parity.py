@@ -8,9 +8,10 @@ import numpy as np
 import pytest
 import torch
 
-from synth import (L3_8B_BS1, L3_8B_BS1_CATCHUP, L3_8B_BS16, L3_8B_BS16_CATCHUP, L3_8B_TREE,
+from synth import (L3_8B_BS1, L3_8B_BS1_CATCHUP, L3_8B_BS1_T1, L3_8B_BS16, L3_8B_BS16_CATCHUP, L3_8B_TREE,
                    L3_70B_BS32, SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN, TINY_F32)
-from harness import check_chain, check_tree, gpu_setup, log, oracle_for
+from harness import (check_chain, check_draft_kv, check_sampled_chain, check_tree, gpu_setup,
+                     log, oracle_for)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -86,6 +87,34 @@ def test_chain_catchup_parity(cfg):
     orc, hi = oracle_for(cfg, w, inp, seqs)
     res = check_chain(cfg, out, orc, hi, seqs, catchup=True, inp=inp)
     log(cfg.name, "n_b", np.diff(hi["new_offsets"]).tolist(), res)
+    dr.close()
+
+
+# Stochastic drafting: tokens drawn from softmax(logits / T) by inverse CDF
+# with seeded uniforms, through the MFMA LM head (batch 3) and the GEMV one
+# (batch 1), in bf16 and fp32.
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_sample_t1", temperature=1.0),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_sample_bs1_t07", batch=1, temperature=0.7),
+    SMALL_F32_CHAIN.with_(name="small_f32_sample_t15", temperature=1.5),
+], ids=lambda c: c.name)
+def test_chain_sample_parity(cfg):
+    log("sampled chain parity", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.chain_sample(inp, cfg.temperature, logits=True, hidden=True)
+    again = dr.chain_sample(inp, cfg.temperature)        # the launch the benchmark times
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    assert torch.equal(out["tokens"], again["tokens"])
+    assert torch.equal(out["logp"], again["logp"])
+    seqs = list(range(cfg.batch))
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    res = check_sampled_chain(cfg, out, orc, hi, seqs, cfg.temperature)
+    check_draft_kv(cfg, inp, orc.chain(hi, forced=out["tokens"].cpu().numpy().astype(np.int64),
+                                       temperature=cfg.temperature,
+                                       uniforms=hi["uniforms"])["draft_kv"], seqs)
+    log(cfg.name, res)
+    assert res["draw_agreement"] == 1.0
     dr.close()
 
 
@@ -201,6 +230,19 @@ def run_catchup_parity(cfg, seqs):
     orc, hi = oracle_for(cfg, w, inp, seqs)
     res = check_chain(cfg, out, orc, hi, seqs, catchup=True, inp=inp)
     log(cfg.name, "seqs", seqs, res)
+    dr.close()
+
+
+@pytest.mark.slow
+def test_full_8b_bs1_sample():
+    cfg = L3_8B_BS1_T1
+    dr, w, inp = gpu_setup(cfg)
+    out = dr.chain_sample(inp, 1.0, logits=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    orc, hi = oracle_for(cfg, w, inp, [0])
+    res = check_sampled_chain(cfg, out, orc, hi, [0], 1.0)
+    log(cfg.name, res)
     dr.close()
 
 
