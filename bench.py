@@ -57,6 +57,9 @@ WORKLOADS = {
     "8b_bs1_catchup": "llama3_8b_bf16_chain_bs1_catchup4",
     "8b_bs16_catchup": "llama3_8b_bf16_chain_bs16_paged_catchup",
     "8b_bs1_t1": "llama3_8b_bf16_chain_bs1_t1",
+    "l2_7b_bs1": "llama2_7b_bf16_chain_bs1",
+    "l2_7b_bs1_m1": "llama2_7b_bf16_chain_bs1_m1",
+    "l2_7b_bs1_m2": "llama2_7b_bf16_chain_bs1_m2",
 }
 
 
@@ -103,6 +106,8 @@ def main():
     w = make_weights(cfg, "cuda")
     inp = make_inputs(cfg, "cuda")
     dr = Drafter(cfg)
+    if cfg.f_map is not None:
+        dr.set_step_map(cfg.fmap)
     dr.load(w)
     torch.cuda.synchronize()
     tree = cfg.mode == "tree"

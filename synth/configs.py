@@ -146,11 +146,24 @@ L3_8B_BS1_CATCHUP = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_catchup4", n_
 L3_8B_BS16_CATCHUP = L3_8B_BS16.with_(name="llama3_8b_bf16_chain_bs16_paged_catchup",
                                       n_new=(1, 4))
 
+# The paper's second target family (Sec. 4 "Target LLMs": Llama-2 7B; MHA,
+# vocabulary 32000).  The draft fuses only the target's last-layer hidden
+# state here (F_t = H, the paper's own design), so one parameter set can
+# serve every step: M = 1, 2 (the paper's evaluated instance: module 1 for
+# step 1, module 2 for the rest) and 5 are all valid step maps.
+L2_7B_BS1 = DraftConfig(
+    name="llama2_7b_bf16_chain_bs1", hidden=4096, n_q_heads=32, n_kv_heads=32,
+    head_dim=128, ffn=11008, vocab=32000, n_steps=5, feat_width=4096,
+    rope_theta=10000.0, dtype="bf16", batch=1, ctx_len=2048)
+L2_7B_BS1_M1 = L2_7B_BS1.with_(name="llama2_7b_bf16_chain_bs1_m1", f_map=(0, 0, 0, 0, 0), n_sets=1)
+L2_7B_BS1_M2 = L2_7B_BS1.with_(name="llama2_7b_bf16_chain_bs1_m2", f_map=(0, 1, 1, 1, 1), n_sets=2)
+
 # Stochastic drafting at T = 1 (the paper's T = 1 rows, Tables 4-5).
 L3_8B_BS1_T1 = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_t1", temperature=1.0)
 
 CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32,
-                               L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP, L3_8B_BS1_T1)}
+                               L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP, L3_8B_BS1_T1,
+                               L2_7B_BS1, L2_7B_BS1_M1, L2_7B_BS1_M2)}
 
 # Reduced shapes for element-by-element parity: small enough for the oracle to
 # finish in seconds, large enough to span several tiles of every kernel and to

@@ -8,7 +8,8 @@ import numpy as np
 import pytest
 import torch
 
-from synth import (L3_8B_BS1, L3_8B_BS1_CATCHUP, L3_8B_BS1_T1, L3_8B_BS16, L3_8B_BS16_CATCHUP, L3_8B_TREE,
+from synth import (L2_7B_BS1, L2_7B_BS1_M1, L2_7B_BS1_M2, L3_8B_BS1, L3_8B_BS1_CATCHUP,
+                   L3_8B_BS1_T1, L3_8B_BS16, L3_8B_BS16_CATCHUP, L3_8B_TREE,
                    L3_70B_BS32, SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN, TINY_F32)
 from harness import (check_chain, check_draft_kv, check_sampled_chain, check_tree, gpu_setup,
                      log, oracle_for)
@@ -231,6 +232,12 @@ def run_catchup_parity(cfg, seqs):
     res = check_chain(cfg, out, orc, hi, seqs, catchup=True, inp=inp)
     log(cfg.name, "seqs", seqs, res)
     dr.close()
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cfg", [L2_7B_BS1, L2_7B_BS1_M1, L2_7B_BS1_M2], ids=lambda c: c.name)
+def test_full_llama2_7b_chain(cfg):
+    run_chain_parity(cfg)
 
 
 @pytest.mark.slow
