@@ -242,10 +242,11 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
   c->rows_max = rows;
   c->max_slots = k.max_blocks_per_seq * k.kv_block_size;
-  // attention steps per workgroup: at most about 2K (row, head, chunk) units,
-  // so that each workgroup streams several steps after its lookups
+  // attention steps per workgroup: at most about 512 (row, head, chunk)
+  // units (two resident workgroups per CU), so that each workgroup streams
+  // several steps after its dependent lookups
   c->nsub = 1;
-  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 2048)
+  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 512)
     c->nsub *= 2;
   c->nch = attention_chunks(c->max_slots, c->nsub);
   if (c->nch > 1024) {
