@@ -11,3 +11,5 @@ tests/test_oracle_pins.py; no function here is "parity unpinned".
 from .draft import (Oracle, brute_chain, round_bf16, rmsnorm, silu, rope, rope_cos_sin,
                     softmax_attend, logsumexp, topk_ids, sample_inverse_cdf)
 from ._native import linear, widen, build as build_native
+from .verify import (verify_chain_greedy, verify_chain_sample, verify_tree_greedy, softmax_t,
+                     draw_from)
