@@ -79,12 +79,74 @@ def step_weight_bytes(cfg, s):
     return es * (H * (H + F) + cfg.qkv_dim * H + H * cfg.n_q_heads * d + 3 * H * I + cfg.vocab * H)
 
 
+VERIFY_WORKLOADS = {
+    # the verification step of Sec. 2 on synthetic target logits, 8B vocabulary
+    "verify_bs16": dict(mode="chain", batch=16, K=5, temperature=1.0),
+    "verify_bs16_greedy": dict(mode="chain", batch=16, K=5, temperature=0.0),
+    "verify_tree_bs4": dict(mode="tree", batch=4, nodes=60),
+}
+
+
+def verify_bench(args):
+    """Time the verification call and report it against the HBM roofline of
+    its logits stream (every logits row read once)."""
+    import torch
+    from synth import L3_8B_BS16, make_verify_chain, make_verify_tree_targets
+    from paper_2602_01762_amd import Drafter
+    spec = VERIFY_WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    cfg = L3_8B_BS16          # context of the 8B vocabulary (verification needs no weights)
+    dr = Drafter(cfg)
+    V, B = cfg.vocab, spec["batch"]
+    if spec["mode"] == "chain":
+        K, T = spec["K"], spec["temperature"]
+        d = make_verify_chain(V, B, K, seed=0, device="cuda")
+        dlg, uni = (d["draft_logits"], d["uniforms"]) if T > 0 else (None, None)
+        call = lambda: dr.verify_chain(d["target_logits"], d["draft_tokens"], T, dlg, uni)
+        rows = B * (K + 1) + (B * K if T > 0 else 0)
+        name = "verify_chain_8b_vocab_bs%d_k%d_t%g" % (B, K, T)
+    else:
+        v = spec["nodes"]
+        g = torch.Generator(device="cuda")
+        g.manual_seed(0)
+        tokens = torch.randint(0, V, (B, v), generator=g, device="cuda", dtype=torch.int32)
+        parent = torch.tensor([[j - 1 for j in range(v)]] * B, dtype=torch.int32, device="cuda")
+        tl = make_verify_tree_targets(tokens, parent, V, seed=0)
+        call = lambda: dr.verify_tree(tl, tokens, parent)
+        rows = B * (v + 1)
+        name = "verify_tree_8b_vocab_bs%d_nodes%d" % (B, v)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    us = e0.elapsed_time(e1) * 1e3 / args.steps
+    nbytes = rows * V * 4
+    gbs = nbytes / (us * 1e-6) / 1e9
+    res = {"metric": "verification call latency", "value": round(us, 2), "unit": "us",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(us / 1e3, 5), "higher_is_better": False, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic target / draft logits",
+           "config": {"workload": name, "batch": B, "vocab": V},
+           "roofline": {"kernel": "k_rows_stats + k_verify_* (logits stream)", "bound": "hbm",
+                        "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                        "algorithmic_bytes_per_launch": nbytes}}
+    dr.close()
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS) + sorted(VERIFY_WORKLOADS))
     ap.add_argument("--cpu-baseline", type=int, default=1,
                     help="time the CPU oracle on a bounded sample (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0,
@@ -94,6 +156,9 @@ def main():
         print("bench.py measures the single-GPU drafting path; --gpus %d is not supported "
               "(the path has no cross-GPU component)." % args.gpus, file=sys.stderr)
         sys.exit(2)
+
+    if args.workload in VERIFY_WORKLOADS:
+        return verify_bench(args)
 
     import numpy as np
     import torch

@@ -281,6 +281,47 @@ prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
                               int32_t depth, const prism_tree_out *out,
                               void *stream);
 
+/* Verification of drafted chains (paper Sec. 2, speculative decoding): the
+ * target model has scored the K drafts of each sequence in one pass, giving
+ * logits row i for the token after i drafts (i = 0..K).  Greedy
+ * (temperature == 0): drafts are kept while each equals the arg-max of its
+ * target row (ties to the lowest id); the next token is the arg-max of the
+ * row after the last kept draft.  Sampled (temperature > 0): draft i is kept
+ * when r_i < min(1, p_target(x_i) / p_draft(x_i)) with p = softmax(logits /
+ * T) of the target row and of the draft's own row; at the first rejection
+ * the next token is drawn from max(0, p_target - p_draft) at that position,
+ * and when all K are kept it is drawn from p_target of row K (draws by
+ * inverse CDF in token-id order with u = r_K).  Vocabulary V of the context.
+ *   d_target_logits [B, K+1, V] fp32      d_draft_logits [B, K, V] fp32
+ *                                         (sampled only, else NULL)
+ *   d_draft_tokens  [B, K] int32          d_uniforms [B, K+1] fp32
+ *                                         (sampled only, else NULL)
+ *   d_n_accepted    [B] int32 kept drafts 0..K
+ *   d_next_token    [B] int32 the token that follows them
+ * B <= max_batch, K <= max_steps.  A draft id outside 0..V-1 is not kept and
+ * raises PRISM_ERR_INVALID_ARG in prism_device_status. */
+prism_status prism_verify_chain(prism_ctx *ctx, int32_t batch, int32_t K, float temperature,
+                                const float *d_target_logits, const float *d_draft_logits,
+                                const int32_t *d_draft_tokens, const float *d_uniforms,
+                                int32_t *d_n_accepted, int32_t *d_next_token, void *stream);
+
+/* Greedy verification of a draft tree (paper Sec. 2, tree verification
+ * under a tree attention mask): target logits row 0 is for the token after
+ * the root (the last accepted token), row 1+j for the token after node j.
+ * Starting at the root, the child whose token is the arg-max of the current
+ * position's row is kept (the first in node order if several), until no
+ * child matches.  Nodes as prism_draft_tree outputs them (parent -1 = the
+ * root).
+ *   d_target_logits [B, n_nodes+1, V] fp32
+ *   d_tokens, d_parent [B, n_nodes] int32
+ *   d_n_accepted [B]; d_path [B, n_nodes] kept node indices in depth order,
+ *   then -1; d_next_token [B] the arg-max after the last kept node.
+ * B <= max_batch, n_nodes <= 64. */
+prism_status prism_verify_tree(prism_ctx *ctx, int32_t batch, int32_t n_nodes,
+                               const float *d_target_logits, const int32_t *d_tokens,
+                               const int32_t *d_parent, int32_t *d_n_accepted,
+                               int32_t *d_path, int32_t *d_next_token, void *stream);
+
 /* Synchronize `stream` and report device-side bounds flags raised since
  * the last call: PRISM_ERR_CAPACITY (block table / pool / slot out of
  * range), PRISM_ERR_INVALID_ARG (token id out of range, malformed catch-up

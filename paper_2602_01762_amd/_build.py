@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libprism_draft.so")
-SOURCES = ["gemm.hip", "attn.hip", "misc.hip", "runtime.hip"]
+SOURCES = ["gemm.hip", "attn.hip", "misc.hip", "verify.hip", "runtime.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # keep the compiler from emitting packed fp32 arithmetic

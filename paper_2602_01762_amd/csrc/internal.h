@@ -15,7 +15,8 @@ enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u, ERRF_ROWS = 4u };
 // more than the MFMA path's fixed 16-row tiles.
 constexpr int GEMV_MAX_ROWS = 2;
 constexpr int LM_GEMV_MAX_ROWS = 1;
-constexpr int MAX_TOPK = 16;    // largest top-k of the LM-head merge
+constexpr int MAX_TOPK = 16;
+constexpr int MAX_VERIFY_NODES = 64;   // tree nodes one verification call takes    // largest top-k of the LM-head merge
 constexpr int MAX_TREE_CAND = 2048;
 constexpr int MAX_ROWS = 64;
 constexpr int MAX_KW = 16;      // waves of one workgroup splitting K
@@ -180,6 +181,15 @@ struct LmSampleArgs {
   int *tok_b; int ld_b;            // optional [R * ld_b] copy
 };
 void launch_lm_sample(const LmSampleArgs &a, hipStream_t s);
+// ---- launchers (verify.hip) -----------------------------------------------
+// workspace for the per-slice statistics of `rows` logits rows
+size_t verify_stats_bytes(int rows);
+void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, const float *dl,
+                         const int32_t *drafts, const float *u, int32_t *n_acc, int32_t *next,
+                         void *stats, uint32_t *err, hipStream_t s);
+void launch_verify_tree(int B, int nodes, int V, const float *tl, const int32_t *tokens,
+                        const int32_t *parent, int32_t *n_acc, int32_t *path, int32_t *next,
+                        void *stats, hipStream_t s);
 // merge LM-head partials: top-k ids, optional log-probs, and the chain's token copies
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,

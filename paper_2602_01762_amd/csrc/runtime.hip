@@ -90,6 +90,8 @@ struct prism_ctx {
   int32_t *c_rseq = nullptr, *c_rpos = nullptr, *c_last = nullptr;   // catch-up rows
   float *q2 = nullptr, *u2 = nullptr;   // q and u of each sequence's last accepted row
   float *samp_logits = nullptr;     // [rows, V] fp32 logits kept for the sampler
+  void *vstats = nullptr;           // verification: per-slice statistics of logits rows
+  int vrows_max = 0;
   size_t lds_limit = 65536;         // LDS bytes one workgroup may use
   uint32_t *err = nullptr;
   double *inv_freq = nullptr;
@@ -321,6 +323,12 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->logp, R * c->kmax * 4);
   add((void **)&c->tokbuf, R * 4);
   add((void **)&c->samp_logits, R * c->V * 4);
+  {   // verification rows: target and draft rows of a chain, or every node of a tree
+    const int chain_rows = k.max_batch * (2 * k.max_steps + 1);
+    const int tree_rows = k.max_batch * (MAX_VERIFY_NODES + 1);
+    c->vrows_max = chain_rows > tree_rows ? chain_rows : tree_rows;
+    add(&c->vstats, verify_stats_bytes(c->vrows_max));
+  }
   add((void **)&c->c_seq, (size_t)k.max_batch * 4);
   add((void **)&c->c_pos, (size_t)k.max_batch * k.max_steps * 4);
   add((void **)&c->c_tok0, (size_t)k.max_batch * 4);
@@ -917,6 +925,46 @@ prism_status prism_draft_chain_sample(prism_ctx *c, const prism_batch *batch, in
     enqueue_chain(c, b, kv, K, nullptr, d_out_tokens, d_out_logits, d_out_hidden, s, d_uniforms,
                   inv_temp, d_out_logp);
   });
+}
+
+prism_status prism_verify_chain(prism_ctx *c, int32_t batch, int32_t K, float temperature,
+                                const float *d_target_logits, const float *d_draft_logits,
+                                const int32_t *d_draft_tokens, const float *d_uniforms,
+                                int32_t *d_n_accepted, int32_t *d_next_token, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (batch < 1 || batch > c->cfg.max_batch)
+    return fail(c, PRISM_ERR_INVALID_ARG, "batch %d out of 1..%d", batch, c->cfg.max_batch);
+  if (K < 1 || K > c->cfg.max_steps)
+    return fail(c, PRISM_ERR_INVALID_ARG, "K %d out of 1..%d", K, c->cfg.max_steps);
+  if (!(temperature >= 0.f) || (temperature > 0.f && !std::isfinite(1.f / temperature)))
+    return fail(c, PRISM_ERR_INVALID_ARG, "temperature %g", (double)temperature);
+  const bool sampled = temperature > 0.f;
+  if (!d_target_logits || !d_draft_tokens || !d_n_accepted || !d_next_token ||
+      (sampled && (!d_draft_logits || !d_uniforms)))
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL pointer");
+  hipStream_t s = (hipStream_t)stream;
+  launch_verify_chain(batch, K, c->V, sampled ? 1.f / temperature : 0.f, d_target_logits,
+                      d_draft_logits, d_draft_tokens, d_uniforms, d_n_accepted, d_next_token,
+                      c->vstats, c->err, s);
+  HIPCHK(c, hipGetLastError());
+  return PRISM_OK;
+}
+
+prism_status prism_verify_tree(prism_ctx *c, int32_t batch, int32_t n_nodes,
+                               const float *d_target_logits, const int32_t *d_tokens,
+                               const int32_t *d_parent, int32_t *d_n_accepted, int32_t *d_path,
+                               int32_t *d_next_token, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (batch < 1 || batch > c->cfg.max_batch)
+    return fail(c, PRISM_ERR_INVALID_ARG, "batch %d out of 1..%d", batch, c->cfg.max_batch);
+  if (n_nodes < 1 || n_nodes > MAX_VERIFY_NODES)
+    return fail(c, PRISM_ERR_INVALID_ARG, "n_nodes %d out of 1..%d", n_nodes, MAX_VERIFY_NODES);
+  if (!d_target_logits || !d_tokens || !d_parent || !d_n_accepted || !d_path || !d_next_token)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL pointer");
+  launch_verify_tree(batch, n_nodes, c->V, d_target_logits, d_tokens, d_parent, d_n_accepted,
+                     d_path, d_next_token, c->vstats, (hipStream_t)stream);
+  HIPCHK(c, hipGetLastError());
+  return PRISM_OK;
 }
 
 prism_status prism_draft_chain_catchup(prism_ctx *c, const prism_batch *batch,

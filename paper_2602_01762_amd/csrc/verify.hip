@@ -1,0 +1,348 @@
+// Verification step that follows drafting (paper Sec. 2): the target model
+// scores the drafted tokens in one pass, and the drafts are kept while they
+// pass the test -- greedy: the target's own arg-max equals the draft;
+// sampled: the rejection rule r < min(1, p_target(x) / p_draft(x)), with the
+// replacement drawn from max(0, p_target - p_draft) at the first rejection,
+// or one extra token from p_target when all pass.  Trees (greedy): the
+// longest root path whose every node is the target's choice at its parent.
+//
+// Logits rows are V-wide fp32 (0.5 MB at V = 128256), so the work is a
+// stream over them: k_rows_stats splits each row over VSPLIT workgroups,
+// each reducing its slice to (max z, sum exp(z - max), arg-max of the raw
+// logits), z = logit / T; one workgroup per sequence then merges the slices
+// in order and takes the decisions.  Draws use the drafter's inverse CDF
+// in token-id order.
+#include "device.h"
+
+namespace prism {
+
+constexpr int VSPLIT = 8;
+constexpr int VER_UNROLL = 4;
+
+struct RowStat {      // one slice of one row
+  float mx, sum, best;
+  int arg;
+};
+
+// slice of a row: ids [lo, hi) with lo a multiple of 4 (16-byte loads)
+__device__ __forceinline__ void slice_of(int V, int part, int &lo, int &hi) {
+  const int per = (((V + VSPLIT - 1) / VSPLIT) + 3) & ~3;
+  lo = min(V, part * per);
+  hi = min(V, lo + per);
+}
+
+__global__ __launch_bounds__(256) void k_rows_stats(const float *__restrict__ x, int V,
+                                                    float inv_t, RowStat *out) {
+  __shared__ float shv[8];
+  __shared__ int shi[8];
+  const int row = blockIdx.y, part = blockIdx.x, tid = threadIdx.x;
+  int lo, hi;
+  slice_of(V, part, lo, hi);
+  const float *r = x + (size_t)row * V;   // V % 4 == 0: rows are 16-byte aligned
+  float mz = -INFINITY, s = 0.f, bv = -INFINITY;
+  int bi = 0x7fffffff;
+  auto take = [&](float v, int i) {
+    if (better(v, i, bv, bi)) { bv = v; bi = i; }
+    const float z = v * inv_t;            // online max / sum of exp(z - max)
+    if (z > mz) {
+      s = s * expf(mz - z) + 1.f;
+      mz = z;
+    } else {
+      s += expf(z - mz);
+    }
+  };
+  for (int i0 = lo + 4 * tid; i0 < hi; i0 += 4 * 256 * VER_UNROLL) {
+    f32x4 v[VER_UNROLL];
+#pragma unroll
+    for (int u = 0; u < VER_UNROLL; ++u) {   // all loads first
+      const int i = i0 + u * 4 * 256;
+      v[u] = i + 3 < hi ? *(const f32x4 *)(r + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (i < hi && i + 3 >= hi)
+        for (int q = 0; q < 4; ++q) v[u][q] = i + q < hi ? r[i + q] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < VER_UNROLL; ++u) {
+      const int i = i0 + u * 4 * 256;
+      for (int q = 0; q < 4; ++q)
+        if (i + q < hi) take(v[u][q], i + q);
+    }
+  }
+  const float M = block_max(mz, shv);
+  const float S = block_sum(mz == -INFINITY ? 0.f : s * expf(mz - M), shv);
+  block_argmax(bv, bi, shv, shi);
+  if (tid == 0) out[(size_t)row * VSPLIT + part] = RowStat{M, S, bv, bi};
+}
+
+// merge the slices of one row: max z, sum exp(z - max), arg-max
+struct RowSum {
+  float M, S;
+  int arg;
+};
+__device__ __forceinline__ RowSum merge_row(const RowStat *st) {
+  float M = -INFINITY, bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int p = 0; p < VSPLIT; ++p) {
+    M = fmaxf(M, st[p].mx);
+    if (better(st[p].best, st[p].arg, bv, bi)) { bv = st[p].best; bi = st[p].arg; }
+  }
+  float S = 0.f;
+  for (int p = 0; p < VSPLIT; ++p)
+    if (st[p].mx != -INFINITY) S += st[p].sum * expf(st[p].mx - M);
+  return RowSum{M, S, bi};
+}
+
+// Block-wide inverse-CDF draw over ids 0..V-1 with weights w(i) >= 0 (id
+// order).  Ids go in blocks of 256 (lane l of a wave holds ids 4l..4l+3 of a
+// block, one 16-byte load per row); wave w owns a contiguous run of blocks.
+// Pass 1 sums each wave's run; an in-order prefix over the waves finds the
+// run holding u * total; pass 2 walks that run block by block with a lane
+// prefix sum (lane order = id order) to the id.  Rounding that leaves no
+// crossing takes the highest id of positive weight.  W(base, v[4]) gives the
+// 4 weights of ids base..base+3 (ids >= V weigh 0).
+constexpr int DRAW_THREADS = 1024;
+constexpr int DRAW_WAVES = DRAW_THREADS / 64;
+
+template <typename W>
+__device__ int draw_ids(int V, float u, W w4, float *s_wave, int *s_pick) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int nblk = (V + 255) / 256;
+  const int b0 = (int)((long)wave * nblk / DRAW_WAVES), b1 = (int)((long)(wave + 1) * nblk / DRAW_WAVES);
+  float acc = 0.f;
+  for (int blk = b0; blk < b1; ++blk) {
+    float v[4];
+    w4(blk * 256 + 4 * lane, v);
+    acc += (v[0] + v[1]) + (v[2] + v[3]);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) s_wave[wave] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    float run = 0.f;
+    for (int i = 0; i < DRAW_WAVES; ++i) run += s_wave[i];
+    const float goal = fminf(fmaxf(u, 0.f), 1.f) * run;
+    int pick = -1;
+    float base = 0.f;
+    run = 0.f;
+    for (int i = 0; i < DRAW_WAVES; ++i) {
+      if (s_wave[i] > 0.f && run + s_wave[i] > goal) { pick = i; base = run; break; }
+      run += s_wave[i];
+    }
+    float g2 = goal;
+    if (pick < 0) {   // past the end by rounding: the last id of positive weight,
+                      // which pass 2 returns when nothing crosses (goal = +inf)
+      for (int i = DRAW_WAVES - 1; i >= 0; --i)
+        if (s_wave[i] > 0.f) { pick = i; break; }
+      g2 = INFINITY;
+    }
+    s_pick[0] = pick;
+    s_wave[DRAW_WAVES] = base;
+    s_wave[DRAW_WAVES + 1] = g2;
+    s_pick[1] = -1;
+  }
+  __syncthreads();
+  if (wave == s_pick[0]) {
+    float run = s_wave[DRAW_WAVES];
+    const float goal = s_wave[DRAW_WAVES + 1];
+    int found = -1, last = -1;
+    for (int blk = b0; blk < b1 && found < 0; ++blk) {
+      float v[4];
+      w4(blk * 256 + 4 * lane, v);
+      const float ls = (v[0] + v[1]) + (v[2] + v[3]);
+      float x = ls;   // inclusive prefix over the lanes, fixed order
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const float t = __shfl_up(x, o, 64);
+        if (lane >= o) x += t;
+      }
+      const unsigned long long hit = __ballot(ls > 0.f && run + x > goal);
+      const unsigned long long nz = __ballot(ls > 0.f);
+      if (nz) {
+        const int l = 63 - __clzll((long long)nz);
+        const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
+                             __shfl(v[3], l, 64)};
+        for (int q = 3; q >= 0; --q)
+          if (vl[q] > 0.f) { last = blk * 256 + 4 * l + q; break; }
+      }
+      if (hit) {
+        const int l = __ffsll((long long)hit) - 1;
+        float r = run + __shfl(x, l, 64) - __shfl(ls, l, 64);   // prefix before lane l
+        const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
+                             __shfl(v[3], l, 64)};
+        int id = -1, lastl = -1;
+        for (int q = 0; q < 4; ++q) {
+          if (vl[q] > 0.f) lastl = blk * 256 + 4 * l + q;
+          if (vl[q] > 0.f && r + vl[q] > goal) { id = blk * 256 + 4 * l + q; break; }
+          r += vl[q];
+        }
+        found = id >= 0 ? id : lastl;
+      }
+      run += __shfl(x, 63, 64);
+    }
+    if (lane == 0) s_pick[1] = found >= 0 ? found : last;
+  }
+  __syncthreads();
+  return s_pick[1];
+}
+
+struct VerifyChainArgs {
+  int K, V;
+  float inv_t;                   // 0: greedy
+  const float *tl, *dl;          // [B, K+1, V], [B, K, V]
+  const RowStat *ts, *ds;        // [B*(K+1)][VSPLIT], [B*K][VSPLIT]
+  const int32_t *drafts;         // [B, K]
+  const float *u;                // [B, K+1]
+  int32_t *n_acc, *next;         // [B]
+  uint32_t *err;
+};
+
+constexpr int VER_MAXK = 64;     // drafts per sequence (max_steps <= 63)
+
+__global__ __launch_bounds__(DRAW_THREADS) void k_verify_chain(VerifyChainArgs a) {
+  __shared__ float s_wave[DRAW_WAVES + 2];
+  __shared__ int s_pick[2];
+  __shared__ RowSum s_t[VER_MAXK + 1], s_d[VER_MAXK];
+  __shared__ int s_x[VER_MAXK];
+  __shared__ float s_lt[VER_MAXK], s_ld[VER_MAXK];
+  __shared__ int s_n, s_mode;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int K = a.K, V = a.V;
+  const bool sampled = a.inv_t > 0.f;
+  // row statistics and the drafts' own logits, in parallel
+  if (tid <= K) s_t[tid] = merge_row(a.ts + ((size_t)b * (K + 1) + tid) * VSPLIT);
+  if (sampled && tid < K) s_d[tid] = merge_row(a.ds + ((size_t)b * K + tid) * VSPLIT);
+  if (tid < K) {
+    const int x = a.drafts[(size_t)b * K + tid];
+    const bool ok = x >= 0 && x < V;
+    s_x[tid] = ok ? x : -1;
+    if (!ok) atomicOr(a.err, ERRF_TOKEN);
+    if (sampled) {
+      s_lt[tid] = ok ? a.tl[((size_t)b * (K + 1) + tid) * V + x] : 0.f;
+      s_ld[tid] = ok ? a.dl[((size_t)b * K + tid) * V + x] : 0.f;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int n = 0, mode = 0;         // mode 0: draw from p_target row n; 1: the residual at n
+    for (; n < K; ++n) {
+      const int x = s_x[n];
+      if (x < 0) break;          // an invalid draft is never kept
+      if (!sampled) {
+        if (s_t[n].arg != x) break;
+      } else {
+        const float pt = expf(s_lt[n] * a.inv_t - s_t[n].M) / s_t[n].S;
+        const float pd = expf(s_ld[n] * a.inv_t - s_d[n].M) / s_d[n].S;
+        const float r = a.u[(size_t)b * (K + 1) + n];
+        if (!(r < fminf(1.f, pt / pd))) { mode = 1; break; }
+      }
+    }
+    s_n = n;
+    s_mode = mode;
+  }
+  __syncthreads();
+  const int n = s_n;
+  int next;
+  if (!sampled) {
+    next = s_t[n].arg;
+  } else {
+    const float it = a.inv_t, u = a.u[(size_t)b * (K + 1) + K];
+    const RowSum t = s_t[n];
+    const float *trow = a.tl + ((size_t)b * (K + 1) + n) * V;
+    auto wt = [&](int i0, float (&v)[4]) {   // p_target up to its normaliser
+      if (i0 + 3 < V) {
+        const f32x4 x = *(const f32x4 *)(trow + i0);
+        v[0] = expf(x.x * it - t.M); v[1] = expf(x.y * it - t.M);
+        v[2] = expf(x.z * it - t.M); v[3] = expf(x.w * it - t.M);
+      } else {
+        for (int q = 0; q < 4; ++q) v[q] = i0 + q < V ? expf(trow[i0 + q] * it - t.M) : 0.f;
+      }
+    };
+    if (s_mode == 1) {   // max(0, p_target - p_draft) at the rejected position
+      const RowSum d = s_d[n];
+      const float *drow = a.dl + ((size_t)b * K + n) * V;
+      const float ist = 1.f / t.S, isd = 1.f / d.S;
+      auto wr = [&](int i0, float (&v)[4]) {
+        float p[4], q4[4];
+        if (i0 + 3 < V) {
+          const f32x4 x = *(const f32x4 *)(trow + i0), y = *(const f32x4 *)(drow + i0);
+          p[0] = x.x; p[1] = x.y; p[2] = x.z; p[3] = x.w;
+          q4[0] = y.x; q4[1] = y.y; q4[2] = y.z; q4[3] = y.w;
+        } else {
+          for (int q = 0; q < 4; ++q) {
+            p[q] = i0 + q < V ? trow[i0 + q] : -INFINITY;
+            q4[q] = i0 + q < V ? drow[i0 + q] : -INFINITY;
+          }
+        }
+        for (int q = 0; q < 4; ++q)
+          v[q] = fmaxf(0.f, expf(p[q] * it - t.M) * ist - expf(q4[q] * it - d.M) * isd);
+      };
+      next = draw_ids(V, u, wr, s_wave, s_pick);
+      if (next < 0) next = draw_ids(V, u, wt, s_wave, s_pick);   // identical distributions
+    } else {
+      next = draw_ids(V, u, wt, s_wave, s_pick);
+    }
+  }
+  if (tid == 0) {
+    a.n_acc[b] = n;
+    a.next[b] = next;
+  }
+}
+
+struct VerifyTreeArgs {
+  int nodes, V;
+  const RowStat *ts;             // [B*(nodes+1)][VSPLIT]
+  const int32_t *tokens, *parent;   // [B, nodes]
+  int32_t *n_acc, *path, *next;  // [B], [B, nodes], [B]
+};
+
+// one wave per tree; lane j holds node j (v <= 64), so each step of the walk
+// is one ballot over the nodes: the first child of the current position
+// whose token is the target's choice there
+__global__ __launch_bounds__(64) void k_verify_tree(VerifyTreeArgs a) {
+  __shared__ int s_arg[MAX_VERIFY_NODES + 1];
+  const int b = blockIdx.x, lane = threadIdx.x, v = a.nodes;
+  for (int j = lane; j <= v; j += 64) s_arg[j] = merge_row(a.ts + ((size_t)b * (v + 1) + j) * VSPLIT).arg;
+  const int tok = lane < v ? a.tokens[(size_t)b * v + lane] : -1;
+  const int par = lane < v ? a.parent[(size_t)b * v + lane] : -2;
+  __syncthreads();
+  int at = -1, n = 0;
+  int32_t *path = a.path + (size_t)b * v;
+  while (n < v) {   // a path has at most v nodes (also bounds a malformed parent table)
+    const int want = s_arg[at + 1];
+    const unsigned long long m = __ballot(lane < v && par == at && tok == want);
+    if (!m) break;
+    at = __ffsll((long long)m) - 1;
+    if (lane == 0) path[n] = at;
+    ++n;
+  }
+  for (int j = n + lane; j < v; j += 64) path[j] = -1;
+  if (lane == 0) {
+    a.n_acc[b] = n;
+    a.next[b] = s_arg[at + 1];
+  }
+}
+
+size_t verify_stats_bytes(int rows) { return (size_t)rows * VSPLIT * sizeof(RowStat); }
+
+void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, const float *dl,
+                         const int32_t *drafts, const float *u, int32_t *n_acc, int32_t *next,
+                         void *stats, uint32_t *err, hipStream_t s) {
+  RowStat *ts = (RowStat *)stats;
+  RowStat *ds = ts + (size_t)B * (K + 1) * VSPLIT;
+  const float it = inv_t > 0.f ? inv_t : 1.f;
+  hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * (K + 1)), dim3(256), 0, s, tl, V, it, ts);
+  if (inv_t > 0.f)
+    hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * K), dim3(256), 0, s, dl, V, it, ds);
+  VerifyChainArgs a{K, V, inv_t, tl, dl, ts, ds, drafts, u, n_acc, next, err};
+  hipLaunchKernelGGL(k_verify_chain, dim3(B), dim3(DRAW_THREADS), 0, s, a);
+}
+
+void launch_verify_tree(int B, int nodes, int V, const float *tl, const int32_t *tokens,
+                        const int32_t *parent, int32_t *n_acc, int32_t *path, int32_t *next,
+                        void *stats, hipStream_t s) {
+  RowStat *ts = (RowStat *)stats;
+  hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * (nodes + 1)), dim3(256), 0, s, tl, V, 1.f, ts);
+  VerifyTreeArgs a{nodes, V, ts, tokens, parent, n_acc, path, next};
+  hipLaunchKernelGGL(k_verify_tree, dim3(B), dim3(64), 0, s, a);
+}
+
+}  // namespace prism

@@ -177,6 +177,27 @@ class Drafter:
         B.prism_draft_tree(self.ctx, b, depth, t)
         return out
 
+    def verify_chain(self, target_logits, draft_tokens, temperature: float = 0.0,
+                     draft_logits=None, uniforms=None):
+        """Sec. 2 verification of B chains of K drafts; returns kept counts
+        and next tokens [B]."""
+        Bn, K = int(draft_tokens.shape[0]), int(draft_tokens.shape[1])
+        n = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        nxt = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        B.prism_verify_chain(self.ctx, Bn, K, temperature, target_logits, draft_logits,
+                             draft_tokens, uniforms, n, nxt)
+        return {"n": n, "next": nxt}
+
+    def verify_tree(self, target_logits, tokens, parent):
+        """Greedy verification of B draft trees; returns kept counts, kept
+        node paths [B, nodes] (-1 padded) and next tokens."""
+        Bn, v = int(tokens.shape[0]), int(tokens.shape[1])
+        n = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        path = torch.empty((Bn, v), dtype=torch.int32, device=self.device)
+        nxt = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        B.prism_verify_tree(self.ctx, Bn, v, target_logits, tokens, parent, n, path, nxt)
+        return {"n": n, "path": path, "next": nxt}
+
     def step(self, k: int, inp, rows: dict, topk: int = 1, logits=False, batch=None):
         """One pass of step k on explicit rows.  `rows` holds device tensors:
         tokens, feat, seq, pos, slot and optionally feat_rows, tree_bits;

@@ -7,4 +7,5 @@ from .configs import (DraftConfig, CONFIGS, TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_
                       L2_7B_BS1_M2, SMALL_BF16_CHAIN,
                       SMALL_BF16_TREE, SMALL_F32_CHAIN)
 from .gen import (ParamSet, Weights, Inputs, make_weights, make_param_set, make_inputs,
-                  ctx_lengths, new_counts, host_weights, host_inputs, to_host, derive_seed, torch_dtype)
+                  ctx_lengths, new_counts, make_verify_chain,
+                  make_verify_tree_targets, host_weights, host_inputs, to_host, derive_seed, torch_dtype)

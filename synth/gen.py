@@ -216,6 +216,61 @@ def make_inputs(cfg: DraftConfig, device="cpu", extra_blocks: int = 0) -> Inputs
     return inp
 
 
+T_VLOG, T_VTGT, T_VTOK, T_VAGR, T_VUNI, T_VPATH = range(200, 206)
+
+
+def make_verify_chain(V: int, B: int, K: int, seed: int = 0, device="cpu", noise: float = 0.5):
+    """Synthetic inputs of chain verification: draft logits N(0, 2) [B, K, V];
+    draft tokens uniform on [0, V), placed as each draft row's maximum; target
+    logits = the draft rows plus N(0, noise) (row K: N(0, 2)), with the
+    target's maximum placed on the draft for the first a_b positions and
+    away from it at position a_b (a_b uniform on 0..K per sequence); the
+    uniforms [B, K+1] of the rejection rule."""
+    g = lambda tid: _gen(device, seed, tid)
+    dl = torch.randn((B, K, V), generator=g(T_VLOG), device=device) * 2.0
+    tok = torch.randint(0, V, (B, K), generator=g(T_VTOK), device=device, dtype=torch.int64)
+    dl.scatter_(2, tok[..., None], dl.amax(dim=2, keepdim=True) + 1.0)
+    tl = torch.randn((B, K + 1, V), generator=g(T_VTGT), device=device) * noise
+    tl[:, :K] += dl
+    tl[:, K] *= 2.0 / noise
+    agree = torch.randint(0, K + 1, (B,), generator=g(T_VAGR), device=device)
+    for b in range(B):
+        a = int(agree[b])
+        for i in range(K):
+            row = tl[b, i]
+            if i < a:
+                row[tok[b, i]] = row.max() + 1.0
+            elif i == a:
+                row[tok[b, i]] = row.min() - 1.0
+    u = torch.rand((B, K + 1), generator=g(T_VUNI), device=device)
+    return {"target_logits": tl.contiguous(), "draft_logits": dl.contiguous(),
+            "draft_tokens": tok.to(torch.int32).contiguous(), "uniforms": u}
+
+
+def make_verify_tree_targets(tokens: torch.Tensor, parent: torch.Tensor, V: int, seed: int = 0):
+    """Synthetic target logits [B, v+1, V] N(0, 2) for draft trees
+    (tokens / parent [B, v]): along a random root path of each tree (a
+    random child at each level, random length) the target's maximum is
+    placed on the path's next token."""
+    device = tokens.device
+    B, v = tokens.shape
+    g = _gen(device, seed, T_VTGT)
+    tl = torch.randn((B, v + 1, V), generator=g, device=device) * 2.0
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, T_VPATH])))
+    tk, pa = tokens.cpu().numpy(), parent.cpu().numpy()
+    for b in range(B):
+        at = -1
+        for _ in range(int(rng.integers(0, v + 1))):
+            kids = [j for j in range(v) if pa[b, j] == at]
+            if not kids:
+                break
+            j = int(kids[rng.integers(0, len(kids))])
+            row = tl[b, at + 1]
+            row[int(tk[b, j])] = row.max() + 1.0
+            at = j
+    return tl.contiguous()
+
+
 def logical_prior_kv(kp: torch.Tensor, vp: torch.Tensor, btab: torch.Tensor, L: int,
                      cfg: DraftConfig):
     """Prior-context K and V of one sequence as [L, n_kv, d] host arrays.
