@@ -485,9 +485,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   }
 }
 
+constexpr int CMB_PRE = 24;   // partial-output loads per thread issued before the softmax stats
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  __shared__ float wch[ATT_MAXCH];
+  __shared__ float wch[ATT_MAXCH], lch[ATT_MAXCH];
   __shared__ float red[256];
   __shared__ float sh[8];
   const int h = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
@@ -498,31 +499,42 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   if (total > a.nch * span && h == 0 && tid == 0) atomicOr(a.err, ERRF_CAPACITY);
   const int nch = min((total + span - 1) / span, a.nch);
   const size_t base = ((size_t)r * a.nq + h) * a.nch;
+  // output dims: thread = (dim, chunk group); its chunks are grp, grp + G, ...
+  const int d = a.d, G = 256 / d;
+  const int dim = tid % d, grp = tid / d;
+  const bool has_grp = grp < G;
+  // the first CMB_PRE partial outputs of this thread go out with the stats
+  float pre[CMB_PRE];
+#pragma unroll
+  for (int j = 0; j < CMB_PRE; ++j) {
+    const int c = grp + j * G;
+    pre[j] = has_grp && c < nch ? a.po[(base + c) * d + dim] : 0.f;
+  }
   // chunk weights exp(m_c - M) and the total sum, in fixed order
   float m = -INFINITY;
-  for (int c = tid; c < nch; c += 256)
-    if (a.pl[base + c] > 0.f) m = fmaxf(m, a.pm[base + c]);
-  const float M = block_max(m, sh);
+  for (int c = tid; c < nch; c += 256) {
+    const float l = a.pl[base + c], mc = a.pm[base + c];
+    lch[c] = l;
+    wch[c] = mc;
+    if (l > 0.f) m = fmaxf(m, mc);
+  }
+  const float M = block_max(m, sh);        // its barriers make lch / wch visible
   float lp = 0.f;
   for (int c = tid; c < nch; c += 256) {
-    const float l = a.pl[base + c];
-    const float w = l > 0.f ? expf(a.pm[base + c] - M) : 0.f;
+    const float l = lch[c];
+    const float w = l > 0.f ? expf(wch[c] - M) : 0.f;
     wch[c] = w;
     lp += l * w;
   }
   const float lsum = block_sum(lp, sh);   // ends with a barrier: wch is visible
-  // output dims: thread = (dim, chunk group)
-  const int d = a.d, G = 256 / d;
-  const int dim = tid % d, grp = tid / d;
   float o = 0.f;
-  if (grp < G) {
-    int c = grp;
-    for (; c + 3 * G < nch; c += 4 * G) {
-      const float p0 = a.po[(base + c) * d + dim], p1 = a.po[(base + c + G) * d + dim];
-      const float p2 = a.po[(base + c + 2 * G) * d + dim], p3 = a.po[(base + c + 3 * G) * d + dim];
-      o += p0 * wch[c] + p1 * wch[c + G] + p2 * wch[c + 2 * G] + p3 * wch[c + 3 * G];
+  if (has_grp) {
+#pragma unroll
+    for (int j = 0; j < CMB_PRE; ++j) {
+      const int c = grp + j * G;
+      if (c < nch) o += pre[j] * wch[c];
     }
-    for (; c < nch; c += G) o += a.po[(base + c) * d + dim] * wch[c];
+    for (int c = grp + CMB_PRE * G; c < nch; c += G) o += a.po[(base + c) * d + dim] * wch[c];
   }
   red[tid] = o;
   __syncthreads();

@@ -261,56 +261,58 @@ __device__ __forceinline__ void put_act(const ActOut &o, size_t i, float v) {
   }
 }
 
-// Row scales 1/sqrt(mean(x^2) + eps) from per-tile sums of squares.  Loads
-// are issued here (before the main loop) and reduced in finish_scales.
-constexpr int SS_PER_THREAD = 4;
+// Row scales 1/sqrt(mean(x^2) + eps) of rows r0 .. r0 + nr - 1 from the
+// producer's partial sums of squares (layout [part][R]).  Thread t serves row
+// r0 + t / tpr and adds parts t % tpr, t % tpr + tpr, ... in that order; the
+// tpr threads of a row (adjacent lanes of one wave) then meet in a fixed
+// butterfly, so the result does not depend on scheduling.  The loads are
+// issued before the main loop (issue_scales) and reduced after it
+// (finish_scales).
+constexpr int SS_PER_THREAD = 16;
 struct ScaleLoads {
   float v[SS_PER_THREAD];
 };
-__device__ __forceinline__ ScaleLoads issue_scales(const RowNorm &nm, int R) {
+__host__ __device__ inline int scale_tpr(int threads, int nr) {
+  int t = 64;
+  while (t > 1 && t * nr > threads) t >>= 1;
+  return t;
+}
+__host__ __device__ inline bool scales_fit(int threads, int nr, int n_parts) {
+  return nr <= threads && n_parts <= SS_PER_THREAD * scale_tpr(threads, nr);
+}
+__device__ __forceinline__ ScaleLoads issue_scales(const RowNorm &nm, int R, int r0, int nr) {
   ScaleLoads s;
-  const int tot = nm.n_tiles * R;
+  const int tpr = scale_tpr(blockDim.x, nr);
+  const int r = threadIdx.x / tpr, sub = threadIdx.x % tpr;
 #pragma unroll
   for (int j = 0; j < SS_PER_THREAD; ++j) {
-    const int i = threadIdx.x + j * blockDim.x;
-    s.v[j] = i < tot ? nm.ss[i] : 0.f;
+    const int p = sub + j * tpr;
+    s.v[j] = r < nr && p < nm.n_parts ? nm.ss[(size_t)p * R + r0 + r] : 0.f;
   }
   return s;
 }
-int own_scale_capacity(int threads) { return SS_PER_THREAD * threads; }
-
-// sums per row (ss layout [tile][R], so row = index % R): thread, then wave
-// butterfly, then waves in order through LDS.  tmp: one float per wave.
-__device__ __forceinline__ void finish_scales(const RowNorm &nm, int R, const ScaleLoads &s,
-                                              float *rowscale, float *tmp) {
-  const int nw = blockDim.x >> 6, wave = threadIdx.x >> 6;
-  for (int r = 0; r < R; ++r) {
-    float acc = 0.f;
+// every thread of the block calls it (barrier); rowscale[0 .. nr - 1]
+__device__ __forceinline__ void finish_scales(const RowNorm &nm, int nr, const ScaleLoads &s,
+                                              float *rowscale) {
+  const int tpr = scale_tpr(blockDim.x, nr);
+  float acc = 0.f;
 #pragma unroll
-    for (int j = 0; j < SS_PER_THREAD; ++j) {
-      const int i = threadIdx.x + j * blockDim.x;
-      if (i < nm.n_tiles * R && i % R == r) acc += s.v[j];
-    }
-    acc = wave_sum(acc);
-    if ((threadIdx.x & 63) == 0) tmp[wave] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      float t = 0.f;
-      for (int i = 0; i < nw; ++i) t += tmp[i];
-      rowscale[r] = 1.0f / sqrtf(t / (float)nm.n + nm.eps);
-    }
-    __syncthreads();
-  }
+  for (int j = 0; j < SS_PER_THREAD; ++j) acc += s.v[j];
+  for (int o = 1; o < tpr; o <<= 1) acc += __shfl_xor(acc, o, 64);
+  const int r = threadIdx.x / tpr;
+  if (r < nr && threadIdx.x % tpr == 0) rowscale[r] = 1.0f / sqrtf(acc / (float)nm.n + nm.eps);
+  __syncthreads();
 }
 
 // Epilogue of one 16x16 accumulator tile in the MFMA layout: the lane holds
 // output rows n0..n0+3 (tiled order) of batch row r = (lane & 15) + 16 rt.
 // Every lane of the wave must call it (it shuffles).  scale: the row's
 // RMSNorm scale (1 if none); cbase / rpos: the row's cache slot and position
-// (QKV only).
+// (QKV only).  EPI_NORM returns the tile's sum of squares of row r (valid in
+// lanes 0..15); the caller stores it.
 template <typename T, int EPI>
-__device__ __forceinline__ void epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
-                                              float scale, long cbase, int rpos) {
+__device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
+                                               float scale, long cbase, int rpos) {
   const int lane = threadIdx.x & 63, q4 = lane >> 4;
   const int n0 = tile * 16 + 4 * q4;
   const bool live = r < g.R;
@@ -332,7 +334,7 @@ __device__ __forceinline__ void epilogue_tile(const GemmLaunch &g, int tile, int
     // tile sum over the 4 lanes holding row r: fixed butterfly order
     ss += __shfl_xor(ss, 16, 64);
     ss += __shfl_xor(ss, 32, 64);
-    if (live && q4 == 0) g.ss[(size_t)tile * g.R + r] = ss;
+    return ss;
   } else if (EPI == EPI_SWIGLU) {
     if (live) {
       // rows interleave (gate c, up c, gate c + 1, up c + 1)
@@ -348,7 +350,7 @@ __device__ __forceinline__ void epilogue_tile(const GemmLaunch &g, int tile, int
     float pv[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) pv[i] = __shfl_xor(v[i], 32, 64);
-    if (!live) return;
+    if (!live) return 0.f;
     if (f0 < qd + kd) {
       const bool isq = f0 < qd;
       const int fr = isq ? f0 : f0 - qd;
@@ -393,6 +395,7 @@ __device__ __forceinline__ void epilogue_tile(const GemmLaunch &g, int tile, int
       }
     }
   }
+  return 0.f;
 }
 
 // cache slot (block, head 0, offset) and position of row r, or -1
@@ -423,10 +426,10 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   const int kw = g.kw;
   const int t0 = blockIdx.x * NT;
   const TiledMat &m = g.m;
-  const bool has_norm = g.norm.scale != nullptr || g.norm.n_tiles > 0;
-  const bool own_scales = g.norm.scale == nullptr && g.norm.n_tiles > 0;
+  const bool has_norm = g.norm.scale != nullptr || g.norm.n_parts > 0;
+  const bool own_scales = g.norm.scale == nullptr && g.norm.n_parts > 0;
   ScaleLoads sl;
-  if (own_scales) sl = issue_scales(g.norm, g.R);
+  if (own_scales) sl = issue_scales(g.norm, g.R, 0, g.R);
 
   // QKV: wave 0 looks up its rows' cache slots and positions before the
   // main loop, so these dependent loads overlap the weight stream
@@ -469,7 +472,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   }
   if (own_scales) {
     __syncthreads();
-    finish_scales(g.norm, g.R, sl, rowscale, (float *)&red[(kw - 1) * NT * RT * 64]);
+    finish_scales(g.norm, g.R, sl, rowscale);
   } else if (kw > 1) {
     __syncthreads();
   }
@@ -486,7 +489,8 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     for (int rt = 0; rt < RT; ++rt) {
       const int r = (lane & 15) + 16 * rt;
       const float sc = has_norm && r < g.R ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
-      epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt]);
+      const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt]);
+      if (EPI == EPI_NORM && r < g.R && lane < 16) g.ss[(size_t)(t0 + n) * g.R + r] = ss;
     }
 }
 
@@ -522,23 +526,68 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
     }
 }
 
-// One wave per (tile, 16-row group): the slices' partial sums in slice
-// order, then the shared epilogue.  Row scales come precomputed.
+// Tiles per workgroup of the finish pass (a divisor of n_tiles, at most 8).
+static int finish_tiles(int n_tiles) {
+  for (int f = 8; f > 1; f >>= 1)
+    if (n_tiles % f == 0) return f;
+  return 1;
+}
+
+// One wave per (tile, 16-row group), FT = blockDim.x / 64 consecutive tiles
+// per workgroup: the slices' partial sums in slice order, then the shared
+// epilogue.  The row scales of a normed operand (QKV, SWIGLU) are reduced
+// here from the producer's partials (or come precomputed).  EPI_NORM sums of
+// squares are added over the workgroup's tiles in wave order, which leaves
+// one partial per workgroup and row (n_tiles / FT per row in all).
+constexpr int FIN_UNROLL = 8;
 template <typename T, int EPI>
-__global__ __launch_bounds__(64) void k_gemm_finish(GemmLaunch g) {
-  const int tile = blockIdx.x, lane = threadIdx.x;
-  const int r = (lane & 15) + 16 * blockIdx.y;
+__global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
+  __shared__ float rowscale[16];
+  __shared__ float ssw[8][16];    // [wave][row of the group]
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int ft = blockDim.x >> 6;
+  const int tile = blockIdx.x * ft + wave;
+  const int r0 = 16 * blockIdx.y, nr = min(16, g.R - r0);
+  const int r = (lane & 15) + r0;
+  const bool own = g.norm.scale == nullptr && g.norm.n_parts > 0;
+  ScaleLoads sl;
+  if (own) sl = issue_scales(g.norm, g.R, r0, nr);
   const int n0 = tile * 16 + 4 * (lane >> 4);
   f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
   long cbase = -1;
   int rpos = 0;
-  float sc = 1.f;
   if (r < g.R) {
-    for (int sl = 0; sl < g.split; ++sl) a += *(const f32x4 *)(g.part + ((size_t)sl * g.R + r) * g.m.N + n0);
-    if (g.norm.scale) sc = g.norm.scale[r];
     if (EPI == EPI_QKV) cbase = cache_base(g, r, rpos);
+    // slices in order, their loads issued FIN_UNROLL at a time
+    const f32x4 *pp = (const f32x4 *)(g.part + (size_t)r * g.m.N + n0);
+    const size_t stride = (size_t)g.R * g.m.N / 4;
+    for (int s0 = 0; s0 < g.split; s0 += FIN_UNROLL) {
+      f32x4 v[FIN_UNROLL];
+#pragma unroll
+      for (int j = 0; j < FIN_UNROLL; ++j)
+        v[j] = s0 + j < g.split ? pp[(size_t)(s0 + j) * stride] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < FIN_UNROLL; ++j)
+        if (s0 + j < g.split) a += v[j];
+    }
   }
-  epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos);
+  float sc = 1.f;
+  if (own) {
+    finish_scales(g.norm, nr, sl, rowscale);
+    if (r < g.R) sc = rowscale[r - r0];
+  } else if (g.norm.scale && r < g.R) {
+    sc = g.norm.scale[r];
+  }
+  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos);
+  if constexpr (EPI == EPI_NORM) {
+    if (lane < 16) ssw[wave][lane] = ss;
+    __syncthreads();
+    if (threadIdx.x < nr) {
+      float t = 0.f;
+      for (int w = 0; w < ft; ++w) t += ssw[w][threadIdx.x];
+      g.ss[(size_t)blockIdx.x * g.R + r0 + threadIdx.x] = t;
+    }
+  }
 }
 
 // LM head: each wave covers NT 16-row vocab tiles over the full K; a
@@ -551,14 +600,13 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   extern __shared__ float xs_lm[];   // GEMV path: VR * K staged activations
   __shared__ float sl[RT * 16][64 * NT + 1];
   __shared__ float rowscale[MAX_ROWS];
-  __shared__ float tmp[256];
   const TiledMat &m = g.m;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int t0 = (blockIdx.x * 4 + wave) * NT;
-  const bool has_norm = g.norm.scale != nullptr || g.norm.n_tiles > 0;
-  const bool own_scales = g.norm.scale == nullptr && g.norm.n_tiles > 0;
+  const bool has_norm = g.norm.scale != nullptr || g.norm.n_parts > 0;
+  const bool own_scales = g.norm.scale == nullptr && g.norm.n_parts > 0;
   ScaleLoads sc;
-  if (own_scales) sc = issue_scales(g.norm, g.R);
+  if (own_scales) sc = issue_scales(g.norm, g.R, 0, g.R);
   f32x4 acc[NT][RT];
 #pragma unroll
   for (int n = 0; n < NT; ++n)
@@ -575,7 +623,7 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   }
   if (own_scales) {
     __syncthreads();
-    finish_scales(g.norm, g.R, sc, rowscale, tmp);
+    finish_scales(g.norm, g.R, sc, rowscale);
   }
   const int q4 = lane >> 4;
 #pragma unroll
@@ -661,10 +709,11 @@ static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
   const int groups = g.m.n_tiles / NT;
   hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), dim3((groups + 3) / 4, g.split), dim3(256), 0,
                      s, g);
-  const dim3 fg(g.m.n_tiles, (g.R + 15) / 16);
-  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, dim3(64), 0, s, g);
-  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, dim3(64), 0, s, g);
-  else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, dim3(64), 0, s, g);
+  const int ft = finish_tiles(g.m.n_tiles);
+  const dim3 fg(g.m.n_tiles / ft, (g.R + 15) / 16), fb(64 * ft);
+  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, fb, 0, s, g);
+  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, fb, 0, s, g);
+  else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, fb, 0, s, g);
 }
 
 template <typename T, bool PAIR>
@@ -718,6 +767,17 @@ void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s) {
 }
 
 int lm_workgroups(int n_tiles, int nt) { return (n_tiles / nt + 3) / 4; }
+
+int gemm_ss_parts(const GemmLaunch &g) {
+  return g.split > 0 ? g.m.n_tiles / finish_tiles(g.m.n_tiles) : g.m.n_tiles;
+}
+
+bool gemm_own_scales(const GemmLaunch &g, int n_parts) {
+  if (g.split > 0) return scales_fit(64 * finish_tiles(g.m.n_tiles), g.R < 16 ? g.R : 16, n_parts);
+  return g.R <= MAX_ROWS && scales_fit(64 * g.kw, g.R, n_parts);
+}
+
+bool lm_own_scales(int R, int n_parts) { return R <= MAX_ROWS && scales_fit(256, R, n_parts); }
 
 template <typename T, bool PAIR>
 static void lm_rt(const LmLaunch &g, hipStream_t s) {

@@ -55,9 +55,10 @@ struct ActOut {
 // by RMSNorm(x) * g takes x*g as its operand and scales row r of its result
 // by 1/sqrt(sum_t ss[t*R + r] / n + eps).
 struct RowNorm {
-  const float *ss = nullptr;     // partials, reduced by the consumer itself, or
+  const float *ss = nullptr;     // partial sums of squares [n_parts][R], reduced by
+                                 // the consumer itself, or
   const float *scale = nullptr;  // row scales already reduced (launch_rowscale)
-  int n_tiles = 0;
+  int n_parts = 0;               // partial sums per row
   int n = 0;
   float eps = 0.f;
 };
@@ -111,13 +112,13 @@ struct GemmLaunch {
   int split;       // > 0: batched path, K split over `split` workgroup slices
   float *part;     // batched path: slice partial sums [split][R][N]
   int epi;
-  RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_tiles = 0: none
+  RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_parts = 0: none
   // EPI_NORM: y = acc (+ res) -> y [R, ldy] fp32; (y * gain) -> g planes; ss
   const float *res; int ldres;
   float *y; int ldy;
   const void *gain;
   ActOut g;
-  float *ss;
+  float *ss;       // [gemm_ss_parts][R]
   // EPI_SWIGLU: interleaved gate/up rows -> z planes [R, N/2]
   ActOut z;
   // EPI_QKV: q (fp32 [R, nq*d]) and the cache slots of k, v
@@ -150,9 +151,13 @@ void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
 int lm_workgroups(int n_tiles, int nt);
 // LDS of the staged activations of the GEMV main loop
 size_t gemv_lds_bytes(int R, int K);
-// largest number of partial entries (tiles x rows) a consumer reduces itself
-int own_scale_capacity(int threads);
-void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, float *scale,
+// partial sums of squares per row that an EPI_NORM launch writes
+int gemm_ss_parts(const GemmLaunch &g);
+// whether the launch (its finish pass, if split) reduces the row scales of
+// its operand from n_parts partials per row itself
+bool gemm_own_scales(const GemmLaunch &g, int n_parts);
+bool lm_own_scales(int R, int n_parts);
+void launch_rowscale(int R, const float *ss, int n_parts, int n, float eps, float *scale,
                      hipStream_t s);
 // rotated rows: the first rot_rows destination rows hold rotated heads of size d
 void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_stride,

@@ -86,19 +86,19 @@ void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, con
 
 // ---------------------------------------------------------------------------
 // Row scales for batched consumers: scale[r] = 1/sqrt(sum_t ss[t*R + r]/n + eps)
-__global__ __launch_bounds__(256) void k_rowscale(int R, const float *ss, int n_tiles, int n,
+__global__ __launch_bounds__(256) void k_rowscale(int R, const float *ss, int n_parts, int n,
                                                   float eps, float *scale) {
   __shared__ float sh[8];
   const int r = blockIdx.x;
   float acc = 0.f;
-  for (int t = threadIdx.x; t < n_tiles; t += blockDim.x) acc += ss[(size_t)t * R + r];
+  for (int t = threadIdx.x; t < n_parts; t += blockDim.x) acc += ss[(size_t)t * R + r];
   const float tot = block_sum(acc, sh);
   if (threadIdx.x == 0) scale[r] = 1.0f / sqrtf(tot / (float)n + eps);
 }
 
-void launch_rowscale(int R, const float *ss, int n_tiles, int n, float eps, float *scale,
+void launch_rowscale(int R, const float *ss, int n_parts, int n, float eps, float *scale,
                      hipStream_t s) {
-  hipLaunchKernelGGL(k_rowscale, dim3(R), dim3(256), 0, s, R, ss, n_tiles, n, eps, scale);
+  hipLaunchKernelGGL(k_rowscale, dim3(R), dim3(256), 0, s, R, ss, n_parts, n, eps, scale);
 }
 
 // ---------------------------------------------------------------------------

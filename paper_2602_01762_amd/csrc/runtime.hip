@@ -69,7 +69,7 @@ struct prism_ctx {
   ActOut xfc;                       // FC operand planes [R, H + feat_max]
   float *u = nullptr, *r1 = nullptr;  // residual stream rows [R, H]
   ActOut ug, r1g, hg;               // (x * gain) operand planes [R, H]
-  float *ss_u = nullptr, *ss_r1 = nullptr, *ss_h = nullptr;  // [H/16][R]
+  float *ss_u = nullptr, *ss_r1 = nullptr, *ss_h = nullptr;  // [parts <= H/16][R]
   float *sc_u = nullptr, *sc_r1 = nullptr, *sc_h = nullptr;  // row scales [R]
   float *q = nullptr;               // [R, nq*d] fp32
   float *pm = nullptr, *pl = nullptr, *po = nullptr;         // attention partials
@@ -159,8 +159,9 @@ static Plan plan_for(const TiledMat &t, int R) {
 }
 
 // Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
-// fragment reuse) and K slices across workgroups: about one workgroup of 4
-// waves per CU (longer slices stream better than more of them), at least 4
+// fragment reuse) and K slices across workgroups: at most one workgroup of
+// 4 waves per CU (longer slices stream better than more of them, and a grid
+// just above the CU count leaves a few CUs with twice the work), at least 4
 // k-blocks per slice, and fp32 slice partials of at most 1/8 of the weight
 // bytes (split * R * N * 4 <= N * K * 2 / 8).
 static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
@@ -168,7 +169,7 @@ static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
   if (R > 32 && nt == 4) nt = 2;
   const int wgs = (t.n_tiles / nt + 3) / 4;
-  int sp = (256 + wgs - 1) / wgs;
+  int sp = 256 / wgs;
   if (sp > t.nkb / 4) sp = t.nkb / 4;
   if (sp > t.K / (16 * R)) sp = t.K / (16 * R);
   split = sp < 1 ? 1 : sp;
@@ -519,18 +520,19 @@ static Act act_of(const ActOut &o, int ld) {
   return a;
 }
 
-// RMSNorm row scales for a consumer: reduced by the consumer itself when
-// its threads can hold all partials, else by a small kernel first.
-static RowNorm norm_for(prism_ctx *c, const float *ss, float *scale, int R, int threads,
+// RMSNorm row scales for a consumer: reduced by the consumer itself from the
+// producer's n_parts partials per row when it can hold them all (own), else
+// by a small kernel first.
+static RowNorm norm_for(prism_ctx *c, const float *ss, int n_parts, bool own, float *scale, int R,
                         hipStream_t s) {
   RowNorm n;
-  n.n_tiles = c->H / 16;
+  n.n_parts = n_parts;
   n.n = c->H;
   n.eps = c->cfg.rms_eps;
-  if (n.n_tiles * R <= own_scale_capacity(threads)) {
+  if (own) {
     n.ss = ss;
   } else {
-    launch_rowscale(R, ss, n.n_tiles, c->H, n.eps, scale, s);
+    launch_rowscale(R, ss, n_parts, c->H, n.eps, scale, s);
     n.scale = scale;
   }
   return n;
@@ -575,10 +577,6 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   return g;
 }
 
-// threads of a consumer that reduces its own row scales (0: batched path,
-// which takes precomputed scales)
-static int scale_threads(const GemmLaunch &g) { return g.split > 0 ? 0 : 64 * g.kw; }
-
 // Front of a pass: fusion FC and QKV (RoPE, KV append) for p.R rows -> u
 // and q in the workspace.
 static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
@@ -597,9 +595,10 @@ static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStre
   }
   g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
   launch_gemm(bf, g, s);
+  const int parts_u = gemm_ss_parts(g);
   // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
   g = gemm_of(c, S.qkv, act_of(c->ug, H), R, EPI_QKV);
-  g.norm = norm_for(c, c->ss_u, c->sc_u, R, scale_threads(g), s);
+  g.norm = norm_for(c, c->ss_u, parts_u, gemm_own_scales(g, parts_u), c->sc_u, R, s);
   g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
   g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
   launch_gemm(bf, g, s);
@@ -622,9 +621,10 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   g.res = u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
   g.ss = c->ss_r1;
   launch_gemm(bf, g, s);
+  const int parts_r1 = gemm_ss_parts(g);
   // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
   g = gemm_of(c, S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
-  g.norm = norm_for(c, c->ss_r1, c->sc_r1, R, scale_threads(g), s);
+  g.norm = norm_for(c, c->ss_r1, parts_r1, gemm_own_scales(g, parts_r1), c->sc_r1, R, s);
   g.z = c->z; g.z.ld = c->I;
   launch_gemm(bf, g, s);
   // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
@@ -632,6 +632,7 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
   g.g.ld = H; g.ss = c->ss_h;
   launch_gemm(bf, g, s);
+  const int parts_h = gemm_ss_parts(g);
   // logits = LM_head RMSNorm(h; g_final)  ->  top-k partials
   LmLaunch lmg{};
   lmg.m = c->lm;
@@ -648,7 +649,7 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
     else if (c->lm.n_tiles % 2 == 0) lmg.nt = 2;
   }
   lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);
-  lmg.norm = norm_for(c, c->ss_h, c->sc_h, R, 256, s);
+  lmg.norm = norm_for(c, c->ss_h, parts_h, lm_own_scales(R, parts_h), c->sc_h, R, s);
   lmg.logits = p.logits;
   lmg.ld_logits = p.ld_logits;
   if (p.u && !lmg.logits) {   // the sampler reads the draw's group back from the logits
