@@ -283,7 +283,7 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-constexpr int ATT_MAXSUB = 8;    // 64-slot steps per workgroup
+constexpr int ATT_MAXSUB = 16;    // 64-slot steps per workgroup
 
 template <int DK>   // head_dim / 32
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {

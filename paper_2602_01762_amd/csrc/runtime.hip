@@ -249,7 +249,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   // units (two resident workgroups per CU), so that each workgroup streams
   // several steps after its dependent lookups
   c->nsub = 1;
-  while (c->nsub < 8 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 512)
+  while (c->nsub < 16 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 512)
     c->nsub *= 2;
   c->nch = attention_chunks(c->max_slots, c->nsub);
   if (c->nch > 1024) {
