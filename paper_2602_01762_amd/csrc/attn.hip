@@ -300,7 +300,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   const int span = ATT_S * a.nsub;
   const int tbeg = c * span;
   if (tbeg >= total) return;                 // uniform across the workgroup
-  const int d = a.d, g = a.nq / a.nkv, ndk = d >> 5, ndt = d >> 4;
+  // the launcher instantiates DK = d / 32, so every head-dim loop below is full
+  constexpr int d = 32 * DK;
+  const int g = a.nq / a.nkv;
   const int bs = a.kv.bs;
 
   __shared__ bf16_t vt[4][32 * DK][16];     // per wave: V tile as [dim][slot]
@@ -322,7 +324,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
   for (int kk = 0; kk < ATT_MAXDK; ++kk) {
     qh[kk] = ql[kk] = u32x4{0, 0, 0, 0};
-    if (kk < ndk && col < g) {
+    if (col < g) {
       const float *qp = a.q + (size_t)r * a.nq * d + (size_t)(j * g + col) * d + 32 * kk + 8 * q4;
       const f32x4 x0 = *(const f32x4 *)qp, x1 = *(const f32x4 *)(qp + 4);
       const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
@@ -349,14 +351,16 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     }
     return ((long)blk * a.nkv + j) * bs * d + (long)(t % bs) * d;
   };
+  // K/V rows of one slot.  The loads are unconditional (an invisible slot
+  // reads slot 0 of block 0 instead, and its values are masked at use), so
+  // that the compiler can count them exactly and the next step's loads stay
+  // in flight while the current step computes.
   auto load_kv = [&](long off, u32x4 (&ka)[ATT_MAXDK], u32x4 (&va)[ATT_MAXDK]) {
+    const long o = off >= 0 ? off : 0;
 #pragma unroll
     for (int kk = 0; kk < ATT_MAXDK; ++kk) {
-      ka[kk] = va[kk] = u32x4{0, 0, 0, 0};
-      if (kk < ndk && off >= 0) {
-        ka[kk] = *(const u32x4 *)((const bf16_t *)a.kv.k_pool + off + 32 * kk + 8 * q4);
-        va[kk] = *(const u32x4 *)((const bf16_t *)a.kv.v_pool + off + 32 * kk + 8 * q4);
-      }
+      ka[kk] = *(const u32x4 *)((const bf16_t *)a.kv.k_pool + o + 32 * kk + 8 * q4);
+      va[kk] = *(const u32x4 *)((const bf16_t *)a.kv.v_pool + o + 32 * kk + 8 * q4);
     }
   };
 
@@ -380,12 +384,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < ATT_MAXDK; ++kk) {
-      if (kk < ndk) {
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
-                                                      __builtin_bit_cast(bf16x8, qh[kk]), sc, 0, 0, 0);
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
-                                                      __builtin_bit_cast(bf16x8, ql[kk]), sc, 0, 0, 0);
-      }
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
+                                                    __builtin_bit_cast(bf16x8, qh[kk]), sc, 0, 0, 0);
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
+                                                    __builtin_bit_cast(bf16x8, ql[kk]), sc, 0, 0, 0);
     }
     const int vis = off >= 0 ? 1 : 0;
     float sv[4] = {sc.x, sc.y, sc.z, sc.w};
@@ -408,16 +410,15 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     ps += __shfl_xor(ps, 32, 64);
     l_run = l_run * al + ps;
     m_run = mn;
-    // V tile -> LDS as [dim][slot]
+    // V tile -> LDS as [dim][slot] (zero rows for invisible slots)
 #pragma unroll
     for (int kk = 0; kk < ATT_MAXDK; ++kk) {
-      if (kk < ndk) {
-        const uint32_t w4[4] = {va[kk].x, va[kk].y, va[kk].z, va[kk].w};
+      const uint32_t w4[4] = {vis ? va[kk].x : 0u, vis ? va[kk].y : 0u, vis ? va[kk].z : 0u,
+                              vis ? va[kk].w : 0u};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          vt[wave][32 * kk + 8 * q4 + 2 * e][col] = (bf16_t)(w4[e] & 0xffffu);
-          vt[wave][32 * kk + 8 * q4 + 2 * e + 1][col] = (bf16_t)(w4[e] >> 16);
-        }
+      for (int e = 0; e < 4; ++e) {
+        vt[wave][32 * kk + 8 * q4 + 2 * e][col] = (bf16_t)(w4[e] & 0xffffu);
+        vt[wave][32 * kk + 8 * q4 + 2 * e + 1][col] = (bf16_t)(w4[e] >> 16);
       }
     }
     wave_lds_sync();
@@ -435,12 +436,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     const s16x4 pal = __builtin_bit_cast(s16x4, uint2{pack2(pl[0], pl[1]), pack2(pl[2], pl[3])});
 #pragma unroll
     for (int dt = 0; dt < ATT_MAXDT; ++dt) {
-      if (dt < ndt) {
-        o[dt].x *= ah[0]; o[dt].y *= ah[1]; o[dt].z *= ah[2]; o[dt].w *= ah[3];
-        const s16x4 vb = *(const s16x4 *)&vt[wave][16 * dt + col][4 * q4];
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pah, vb, o[dt], 0, 0, 0);
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pal, vb, o[dt], 0, 0, 0);
-      }
+      o[dt].x *= ah[0]; o[dt].y *= ah[1]; o[dt].z *= ah[2]; o[dt].w *= ah[3];
+      const s16x4 vb = *(const s16x4 *)&vt[wave][16 * dt + col][4 * q4];
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pah, vb, o[dt], 0, 0, 0);
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pal, vb, o[dt], 0, 0, 0);
     }
     wave_lds_sync();                          // reads done before the next step's writes
     off = off_n;
@@ -456,15 +455,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     mg_l[wave][col] = l_run;
   }
 #pragma unroll
-  for (int dt = 0; dt < ATT_MAXDT; ++dt)
-    if (dt < ndt) {
-      const float ov[4] = {o[dt].x, o[dt].y, o[dt].z, o[dt].w};
+  for (int dt = 0; dt < ATT_MAXDT; ++dt) {
+    const float ov[4] = {o[dt].x, o[dt].y, o[dt].z, o[dt].w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int h = 4 * q4 + i;
-        if (h < g) mg_o[wave][h * d + 16 * dt + col] = ov[i];
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int h = 4 * q4 + i;
+      if (h < g) mg_o[wave][h * d + 16 * dt + col] = ov[i];
     }
+  }
   __syncthreads();
   for (int e = tid; e < g * d; e += 256) {
     const int h = e / d, dim = e % d;
