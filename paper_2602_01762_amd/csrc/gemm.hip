@@ -162,22 +162,16 @@ __device__ __forceinline__ void stage_gather(const Gather &gx, int R, int K, flo
   }
 }
 
+// x rows staged in LDS as fp32: gathered fusion-FC rows, or R rows of the
+// hi/lo operand (rows R .. RR-1 zero), 8 columns per thread step
 template <int RR>
-__device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
-                                              int K, float *xs, int kb0, int kb1, f32x4 &out,
-                                              const Gather *gx = nullptr, uint32_t *err = nullptr) {
-  const int lane = threadIdx.x & 63, kq = lane >> 4;
-  const u32x4 z4 = {0, 0, 0, 0};
-  const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
-  u32x4 a[UV];
-  {
-    const int nb = kb1 - kb0;
-#pragma unroll
-    for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
+__device__ __forceinline__ void stage_x(const Act &x, int R, int K, float *xs, const Gather *gx,
+                                        uint32_t *err) {
+  if (gx && gx->embed) {
+    stage_gather<RR>(*gx, R, K, xs, err);
+    return;
   }
-  // stage x rows (8 columns per thread step) as fp32
-  if (gx && gx->embed) stage_gather<RR>(*gx, R, K, xs, err);
-  else for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
+  for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
     const int r = i / K, k = i % K;
     float v[8];
     if (r < R) {
@@ -196,19 +190,16 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
     *(f32x4 *)(xs + i) = f32x4{v[0], v[1], v[2], v[3]};
     *(f32x4 *)(xs + i + 4) = f32x4{v[4], v[5], v[6], v[7]};
   }
-  __syncthreads();
-  float acc[RR];
+}
+
+// one batch of a GEMV wave: up to UV loaded k-blocks (nb of them live)
+// starting at k-block kb, times the staged rows
+template <int RR>
+__device__ __forceinline__ void valu_batch(const u32x4 (&a)[UV], int nb, int kb, int kq,
+                                           const float *xs, int K, float (&acc)[RR]) {
 #pragma unroll
-  for (int r = 0; r < RR; ++r) acc[r] = 0.f;
-  for (int kb = kb0; kb < kb1; kb += UV) {
-    const int nb = kb1 - kb;
-    if (kb > kb0) {
-#pragma unroll
-      for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
-    }
-#pragma unroll
-    for (int u = 0; u < UV; ++u) {
-      if (u < nb) {
+  for (int u = 0; u < UV; ++u) {
+    if (u < nb) {
       const int k0 = (kb + u) * 32 + kq * 8;
       const uint32_t w[4] = {a[u].x, a[u].y, a[u].z, a[u].w};
 #pragma unroll
@@ -222,10 +213,14 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
         t += lo_bf(w[3]) * x1.z; t += hi_bf(w[3]) * x1.w;
         acc[r] = t;
       }
-      }
     }
-    wp += UV * 64;
   }
+}
+
+// A GEMV wave's per-lane sums -> the MFMA accumulator layout of its tile
+template <int RR>
+__device__ __forceinline__ f32x4 valu_result(float (&acc)[RR]) {
+  const int lane = threadIdx.x & 63;
   // sum the 4 k-quarters of each tile row (lanes l, l^16, l^32, l^48)
 #pragma unroll
   for (int r = 0; r < RR; ++r) {
@@ -246,7 +241,71 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
     }
     v[i] = t;
   }
-  out = f32x4{v[0], v[1], v[2], v[3]};
+  return f32x4{v[0], v[1], v[2], v[3]};
+}
+
+template <int RR>
+__device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
+                                              int K, float *xs, int kb0, int kb1, f32x4 &out,
+                                              const Gather *gx = nullptr, uint32_t *err = nullptr) {
+  const int lane = threadIdx.x & 63, kq = lane >> 4;
+  const u32x4 z4 = {0, 0, 0, 0};
+  const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
+  u32x4 a[UV];
+  {
+    const int nb = kb1 - kb0;
+#pragma unroll
+    for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
+  }
+  stage_x<RR>(x, R, K, xs, gx, err);
+  __syncthreads();
+  float acc[RR];
+#pragma unroll
+  for (int r = 0; r < RR; ++r) acc[r] = 0.f;
+  for (int kb = kb0; kb < kb1; kb += UV) {
+    const int nb = kb1 - kb;
+    if (kb > kb0) {
+#pragma unroll
+      for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
+    }
+    valu_batch<RR>(a, nb, kb, kq, xs, K, acc);
+    wp += UV * 64;
+  }
+  out = valu_result<RR>(acc);
+}
+
+// The same over NT consecutive tiles per wave, each over the full K (nkb a
+// multiple of UV, so the wave's weights are one contiguous stream of NT *
+// nkb k-blocks).  Longer streams per wave and a grid that fits the chip in
+// one round read HBM faster than one tile per wave.
+template <int RR, int NT>
+__device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0, int nkb,
+                                                    const Act &x, int R, int K, float *xs,
+                                                    bool live, f32x4 (&out)[NT]) {
+  const int lane = threadIdx.x & 63, kq = lane >> 4;
+  const u32x4 z4 = {0, 0, 0, 0};
+  const u32x4 *wp = w0 + lane;
+  const int nkb_live = live ? nkb : 0;
+  u32x4 a[UV];
+#pragma unroll
+  for (int u = 0; u < UV; ++u) a[u] = u < nkb_live ? __builtin_nontemporal_load(wp + u * 64) : z4;
+  stage_x<RR>(x, R, K, xs, nullptr, nullptr);
+  __syncthreads();
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    float acc[RR];
+#pragma unroll
+    for (int r = 0; r < RR; ++r) acc[r] = 0.f;
+    for (int kb = 0; kb < nkb_live; kb += UV) {
+      if (n > 0 || kb > 0) {
+#pragma unroll
+        for (int u = 0; u < UV; ++u) a[u] = __builtin_nontemporal_load(wp + u * 64);
+      }
+      valu_batch<RR>(a, UV, kb, kq, xs, K, acc);
+      wp += UV * 64;
+    }
+    out[n] = valu_result<RR>(acc);
+  }
 }
 
 // store an fp32 value as the storage-type operand (hi/lo pair for bf16)
@@ -615,8 +674,11 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   const bool live = t0 < m.n_tiles;    // n_tiles is a multiple of NT
   if constexpr (VR > 0) {
     // every wave takes part (staging barrier); idle waves stream nothing
-    mainloop_valu<VR>((const u32x4 *)m.w + (size_t)(live ? t0 : 0) * m.nkb * 64, g.x, g.R, m.K,
-                      xs_lm, 0, live ? m.nkb : 0, acc[0][0]);
+    f32x4 res[NT];
+    mainloop_valu_tiles<VR, NT>((const u32x4 *)m.w + (size_t)(live ? t0 : 0) * m.nkb * 64, m.nkb,
+                                g.x, g.R, m.K, xs_lm, live, res);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) acc[n][0] = res[n];
   } else if (live) {
     mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, 0,
                               m.nkb, acc);
@@ -786,7 +848,8 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
     if (g.gemv) {
       const size_t lds = gemv_lds_bytes(g.R, g.m.K);
       // one row (LM_GEMV_MAX_ROWS): more rows take the MFMA tiles
-      hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 1>), grid, blk, lds, s, g);
+      if (g.nt == 4) hipLaunchKernelGGL((k_lmhead<T, 1, 4, PAIR, 1>), grid, blk, lds, s, g);
+      else hipLaunchKernelGGL((k_lmhead<T, 1, 1, PAIR, 1>), grid, blk, lds, s, g);
       return;
     }
   }

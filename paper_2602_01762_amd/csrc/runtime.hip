@@ -643,6 +643,10 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   lmg.inv_temp = p.u ? p.inv_temp : 1.f;
   lmg.gemv = (c->bf16 && R <= LM_GEMV_MAX_ROWS && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
   lmg.nt = 1;
+  // one row: four consecutive vocab tiles per wave when that still gives
+  // about four waves per CU (longer weight streams, one round of workgroups)
+  if (lmg.gemv && c->lm.n_tiles % 16 == 0 && c->lm.nkb % 16 == 0 && c->lm.n_tiles / 4 >= 1024)
+    lmg.nt = 4;
   if (!lmg.gemv && R > LM_GEMV_MAX_ROWS) {   // batched rows: several vocab tiles per wave share B fragments
     if (R > 16 && R <= 32 && c->lm.n_tiles % 8 == 0) lmg.nt = 8;
     else if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
