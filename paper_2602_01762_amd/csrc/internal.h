@@ -185,6 +185,9 @@ struct LmSampleArgs {
   int *tok_a;                      // optional [R] copy
   int *tok_b; int ld_b;            // optional [R * ld_b] copy
 };
+// whether the sampler takes n_wg LM-head partials per row and groups of
+// `group` ids
+bool lm_sample_fits(int n_wg, int group);
 void launch_lm_sample(const LmSampleArgs &a, hipStream_t s);
 // ---- launchers (verify.hip) -----------------------------------------------
 // workspace for the per-slice statistics of `rows` logits rows

@@ -206,86 +206,120 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
 // ---------------------------------------------------------------------------
 // Stochastic drafting: inverse-CDF draw of row r (one workgroup).  Groups
 // are contiguous vocab ranges in id order; thread t owns a contiguous run of
-// groups, so the exclusive prefix of the per-thread sums (taken in thread
-// order) orders the whole vocabulary.  The first group whose running sum
-// passes u * S holds the token; wave 0 then scans that group's ids with a
-// fixed-order wave prefix sum.  A draw that rounding pushes past the last
-// group takes the highest id of nonzero probability.
+// at most SAMP_PER groups, so an exclusive prefix of the per-thread sums in
+// thread order orders the whole vocabulary.  The prefix is a fixed-order
+// scan (a wave scan, then the four wave totals in order), so the draw does
+// not depend on scheduling.  The first group whose running sum passes u * S
+// holds the token; wave 0 then scans that group's ids with a fixed-order wave
+// prefix sum.  A draw that rounding pushes past the last group takes the
+// highest id of nonzero probability.  Every load goes out unconditionally
+// (clamped index, masked value), so that each phase costs one memory
+// latency.
+constexpr int SAMP_PER = 8;         // groups per thread: n_wg <= 2048
+constexpr int SAMP_GROUP_MAX = 512; // ids per group scanned by wave 0
+__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(x, o, 64);
+    if (lane >= o) x += t;
+  }
+  return x;
+}
+
 __global__ __launch_bounds__(256) void k_lm_sample(LmSampleArgs a) {
   __shared__ float shv[8];
-  __shared__ float s_pre[256];
-  __shared__ int s_cg[256];
-  __shared__ float s_cb[256];
-  __shared__ float s_S;
+  __shared__ float s_wtot[4];
+  __shared__ int s_hit[4], s_last[4];
   __shared__ int s_g;
   __shared__ float s_base;
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *pm = a.pmax + (size_t)r * a.n_wg;
   const float *ps = a.psum + (size_t)r * a.n_wg;
-  float m = -INFINITY;
-  for (int g = tid; g < a.n_wg; g += 256) m = fmaxf(m, pm[g]);
-  const float M = block_max(m, shv);
-  const int per = (a.n_wg + 255) / 256;
-  const int g0 = tid * per < a.n_wg ? tid * per : a.n_wg;
-  const int g1 = g0 + per < a.n_wg ? g0 + per : a.n_wg;
-  auto weight = [&](int g) { return pm[g] == -INFINITY ? 0.f : ps[g] * expf(pm[g] - M); };
-  float loc = 0.f;
-  for (int g = g0; g < g1; ++g) loc += weight(g);
-  s_pre[tid] = loc;
-  __syncthreads();
-  if (tid == 0) {   // exclusive prefix in thread (= id) order
-    float run = 0.f;
-    for (int i = 0; i < 256; ++i) {
-      const float t = s_pre[i];
-      s_pre[i] = run;
-      run += t;
-    }
-    s_S = run;
+  const int per = (a.n_wg + 255) / 256;   // <= SAMP_PER (checked by the launcher)
+  const int g0 = tid * per;
+  float vm[SAMP_PER], vs[SAMP_PER];
+#pragma unroll
+  for (int i = 0; i < SAMP_PER; ++i) {
+    const int g = g0 + i < a.n_wg ? g0 + i : 0;
+    vm[i] = pm[g];
+    vs[i] = ps[g];
   }
-  __syncthreads();
-  const float S = s_S;
   const float u = fminf(fmaxf(a.u[(size_t)r * a.ld_u], 0.f), 1.f);
-  const float goal = u * S;
-  {
-    float run = s_pre[tid];
-    int cg = 0x7fffffff;
-    float cb = 0.f;
-    for (int g = g0; g < g1; ++g) {
-      const float w = weight(g);
-      if (w > 0.f && run + w > goal) {
-        cg = g;
-        cb = run;
-        break;
-      }
-      run += w;
-    }
-    s_cg[tid] = cg;
-    s_cb[tid] = cb;
+  auto mine = [&](int i) { return i < per && g0 + i < a.n_wg; };
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < SAMP_PER; ++i)
+    if (mine(i)) m = fmaxf(m, vm[i]);
+  const float M = block_max(m, shv);
+  float w[SAMP_PER], loc = 0.f;
+#pragma unroll
+  for (int i = 0; i < SAMP_PER; ++i) {
+    w[i] = mine(i) && vm[i] != -INFINITY ? vs[i] * expf(vm[i] - M) : 0.f;
+    loc += w[i];
   }
+  // exclusive prefix of the thread sums, in thread order
+  const float incl = wave_incl_scan(loc, lane);
+  if (lane == 63) s_wtot[wave] = incl;
   __syncthreads();
-  if (tid == 0) {
-    int g = -1;
-    float base = 0.f;
-    for (int i = 0; i < 256; ++i)
-      if (s_cg[i] != 0x7fffffff) {
-        g = s_cg[i];
-        base = s_cb[i];
-        break;
+  float wbase = 0.f, S = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (q < wave) wbase += s_wtot[q];
+    S += s_wtot[q];
+  }
+  const float goal = u * S;
+  // this thread's first group that passes the goal
+  int cg = 0x7fffffff;
+  float cb = 0.f;
+  {
+    float run = wbase + incl - loc;
+#pragma unroll
+    for (int i = 0; i < SAMP_PER; ++i) {
+      if (cg == 0x7fffffff && w[i] > 0.f && run + w[i] > goal) {
+        cg = g0 + i;
+        cb = run;
       }
-    if (g < 0) {    // past the end by rounding: the last group of nonzero weight
-      float run = S;
-      for (int q = a.n_wg - 1; q >= 0; --q) {
-        const float w = weight(q);
-        run -= w;
-        if (w > 0.f) {
-          g = q;
-          base = run;
-          break;
-        }
-      }
+      run += w[i];
     }
-    s_g = g;
-    s_base = base;
+  }
+  // the lowest thread with a hit wins (groups are in thread order)
+  const unsigned long long hb = __ballot(cg != 0x7fffffff);
+  if (lane == 0) s_hit[wave] = hb ? 64 * wave + __ffsll((long long)hb) - 1 : 0x7fffffff;
+  // fallback: the last group of nonzero weight
+  int lastg = -1;
+  float lastw = 0.f;
+#pragma unroll
+  for (int i = 0; i < SAMP_PER; ++i)
+    if (w[i] > 0.f) {
+      lastg = g0 + i;
+      lastw = w[i];
+    }
+  __syncthreads();
+  int win = 0x7fffffff;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) win = min(win, s_hit[q]);
+  if (win != 0x7fffffff) {
+    if (tid == win) {
+      s_g = cg;
+      s_base = cb;
+    }
+  } else {
+    int hl = lastg;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) hl = max(hl, __shfl_xor(hl, o, 64));
+    if (lane == 0) s_last[wave] = hl;
+    __syncthreads();
+    int gl = -1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) gl = max(gl, s_last[q]);
+    if (gl >= 0 && lastg == gl) {   // its owner: base = S - its weight (all later weights are zero)
+      s_g = gl;
+      s_base = S - lastw;
+    }
+    if (gl < 0 && tid == 0) {
+      s_g = -1;
+      s_base = 0.f;
+    }
   }
   __syncthreads();
   if (tid >= 64) return;
@@ -294,24 +328,25 @@ __global__ __launch_bounds__(256) void k_lm_sample(LmSampleArgs a) {
   if (g >= 0) {
     const float *lg = a.logits + (size_t)r * a.ld_logits;
     const int id0 = g * a.group;
+    constexpr int NC = SAMP_GROUP_MAX / 64;
+    float e[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int id = id0 + 64 * c + lane;
+      e[c] = lg[id < a.V && 64 * c < a.group ? id : id0];
+    }
     float run = s_base;
     int last_nz = -1;
-    for (int i0 = 0; i0 < a.group; i0 += 64) {
-      const int id = id0 + i0 + lane;
-      const float e = id < a.V ? expf(lg[id] * a.inv_temp - M) : 0.f;
-      float x = e;   // inclusive prefix over the wave, fixed order
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const float t = __shfl_up(x, o, 64);
-        if (lane >= o) x += t;
-      }
-      const unsigned long long hit = __ballot(e > 0.f && run + x > goal);
-      const unsigned long long nz = __ballot(e > 0.f);
-      if (nz) last_nz = id0 + i0 + 63 - __clzll((long long)nz);
-      if (hit) {
-        tok = id0 + i0 + __ffsll((long long)hit) - 1;
-        break;
-      }
+    for (int c = 0; c < NC; ++c) {
+      if (64 * c >= a.group || tok >= 0) break;
+      const int id = id0 + 64 * c + lane;
+      const float ev = id < a.V ? expf(e[c] * a.inv_temp - M) : 0.f;
+      const float x = wave_incl_scan(ev, lane);   // inclusive prefix over the wave, fixed order
+      const unsigned long long hit = __ballot(ev > 0.f && run + x > goal);
+      const unsigned long long nz = __ballot(ev > 0.f);
+      if (nz) last_nz = id0 + 64 * c + 63 - __clzll((long long)nz);
+      if (hit) tok = id0 + 64 * c + __ffsll((long long)hit) - 1;
       run += __shfl(x, 63, 64);
     }
     if (tok < 0) tok = last_nz;
@@ -325,6 +360,10 @@ __global__ __launch_bounds__(256) void k_lm_sample(LmSampleArgs a) {
     if (a.tok_a) a.tok_a[r] = tok;
     if (a.tok_b) a.tok_b[(size_t)r * a.ld_b] = tok;
   }
+}
+
+bool lm_sample_fits(int n_wg, int group) {
+  return n_wg <= 256 * SAMP_PER && group <= SAMP_GROUP_MAX && group % 64 == 0;
 }
 
 void launch_lm_sample(const LmSampleArgs &a, hipStream_t s) {

@@ -917,6 +917,10 @@ prism_status prism_draft_chain_sample(prism_ctx *c, const prism_batch *batch, in
   if (!(temperature > 0.f) || !std::isfinite(1.f / temperature))
     return fail(c, PRISM_ERR_INVALID_ARG, "temperature %g must be positive", (double)temperature);
   if (!d_uniforms) return fail(c, PRISM_ERR_INVALID_ARG, "d_uniforms is NULL");
+  // the widest LM-head plan: one tile per wave (most partials), 8 tiles per
+  // wave (largest groups)
+  if (!lm_sample_fits(c->n_wg_lm, 64 * 8))
+    return fail(c, PRISM_ERR_UNSUPPORTED, "vocabulary of %d ids is too large for the sampler", c->V);
   const prism_batch b = *batch;
   const KvArgs kv = kv_of(c, &b);
   const float inv_temp = 1.f / temperature;

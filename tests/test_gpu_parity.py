@@ -119,6 +119,34 @@ def test_chain_sample_parity(cfg):
     dr.close()
 
 
+# The ends of the unit interval: u = 0 draws the first id of nonzero
+# probability; u = 1 (and u just below 1, where rounding can leave the running
+# sum short of u * S) takes the last one, the id the inverse CDF reaches at
+# the top of the distribution.
+def test_chain_sample_extreme_uniforms():
+    cfg = SMALL_BF16_CHAIN.with_(name="small_bf16_sample_edges", temperature=1.0)
+    log("sampled chain, extreme uniforms", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    B, K = inp.uniforms.shape
+    edges = torch.tensor([0.0, 1.0, 0.99999994, 1e-7, 0.5], dtype=torch.float32)
+    u = torch.stack([edges[(torch.arange(K) + b) % len(edges)] for b in range(B)])
+    inp.uniforms = u.to(inp.uniforms.device).contiguous()
+    out = dr.chain_sample(inp, cfg.temperature, logits=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    toks = out["tokens"].cpu().numpy()
+    for b in range(B):
+        for k in range(K):
+            if float(u[b, k]) == 0.0:
+                assert toks[b, k] == 0, (b, k, toks[b, k])
+    # every draw (u = 1 included) lies in its token's CDF interval
+    seqs = list(range(B))
+    orc, hi = oracle_for(cfg, w, inp, seqs)
+    res = check_sampled_chain(cfg, out, orc, hi, seqs, cfg.temperature)
+    log(cfg.name, res)
+    dr.close()
+
+
 def test_catchup_of_one_token_equals_chain():
     cfg = SMALL_BF16_CHAIN.with_(n_new=(1, 1))
     dr, w, inp = gpu_setup(cfg)
