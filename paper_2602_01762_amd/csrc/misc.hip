@@ -105,7 +105,6 @@ void launch_rowscale(int R, const float *ss, int n_parts, int n, float eps, floa
 // Merge the LM-head partials of row r:
 //   lse = M + log(sum_i s_i exp(m_i - M)),  top-k by (logit desc, id asc),
 //   log-prob = logit - lse.
-constexpr int CMB_UNROLL = 8;
 struct LmCombArgs {
   int R, n_wg, topk, V;
   const float *pmax, *psum, *pval;
@@ -116,72 +115,91 @@ struct LmCombArgs {
   int *tok_b; int ld_b; // optional [R * ld_b]: ids[r][0]
 };
 
-// KB: a power of two >= topk; each thread keeps a sorted list of KB
-// candidates in registers (fixed indices, so no dynamic register indexing),
-// and the block then takes k rounds of arg-max over the list heads.
+// KB: a power of two >= topk.  Each LM-head workgroup's k candidates come
+// sorted (best first), so thread t takes the lists of workgroups t, t + 256,
+// ... and merges them into one sorted register list of compile-time length
+// (fixed indices: no dynamic register indexing); the block then takes k
+// rounds of arg-max over the list heads.  The loads of a batch of CL lists
+// (their max and sum partials and their candidates) go out together before
+// any is used, from clamped indices, so a merge over up to 256 * CL
+// workgroups costs one memory latency.
 template <int KB>
 __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
+  constexpr int CL = 16 / KB > 1 ? 16 / KB : 1;   // lists per thread and batch
   __shared__ float shv[8];
   __shared__ int shi[8];
   const int r = blockIdx.x, tid = threadIdx.x;
+  const int k = a.topk;
   const float *pm = a.pmax + (size_t)r * a.n_wg;
   const float *ps = a.psum + (size_t)r * a.n_wg;
-  float m = -INFINITY, s = 0.f;
-  for (int i0 = 0; i0 < a.n_wg; i0 += 256 * CMB_UNROLL) {
-    float vm[CMB_UNROLL], vs[CMB_UNROLL];
+  const float *pv = a.pval + (size_t)r * a.n_wg * k;
+  const int *pi = a.pid + (size_t)r * a.n_wg * k;
+  float m = -INFINITY, s = 0.f;   // log-sum-exp: online merge in list order
+  float lv[KB];                   // this thread's sorted candidates
+  int li[KB];
 #pragma unroll
-    for (int u = 0; u < CMB_UNROLL; ++u) {
-      const int i = i0 + u * 256 + tid;
-      vm[u] = i < a.n_wg ? pm[i] : -INFINITY;
-      vs[u] = i < a.n_wg ? ps[i] : 0.f;
-    }
-    // online merge of this thread's partials, in index order
+  for (int j = 0; j < KB; ++j) { lv[j] = -INFINITY; li[j] = 0x7fffffff; }
+  for (int l0 = 0; l0 * 256 < a.n_wg; l0 += CL) {
+    float vm[CL], vs[CL], cv[CL][KB];
+    int ci[CL][KB];
 #pragma unroll
-    for (int u = 0; u < CMB_UNROLL; ++u) {
-      if (vm[u] == -INFINITY) continue;
-      if (vm[u] > m) {
-        s = s * expf(m - vm[u]) + vs[u];
-        m = vm[u];
-      } else {
-        s += vs[u] * expf(vm[u] - m);
+    for (int l = 0; l < CL; ++l) {
+      const int w = tid + 256 * (l0 + l);
+      const int wc = w < a.n_wg ? w : 0;
+      vm[l] = pm[wc];
+      vs[l] = ps[wc];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const int jc = j < k ? j : 0;
+        cv[l][j] = pv[(size_t)wc * k + jc];
+        ci[l][j] = pi[(size_t)wc * k + jc];
       }
+    }
+#pragma unroll
+    for (int l = 0; l < CL; ++l) {
+      if (tid + 256 * (l0 + l) >= a.n_wg) continue;
+      if (vm[l] != -INFINITY) {
+        if (vm[l] > m) {
+          s = s * expf(m - vm[l]) + vs[l];
+          m = vm[l];
+        } else {
+          s += vs[l] * expf(vm[l] - m);
+        }
+      }
+      // merge this list into the running one, keeping the best KB (each
+      // step takes the better head and shifts that list)
+      float bv[KB], ov[KB];
+      int bi[KB], oi[KB];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const bool ok = j < k;
+        bv[j] = ok ? cv[l][j] : -INFINITY;
+        bi[j] = ok ? ci[l][j] : 0x7fffffff;
+      }
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        const bool take_b = better(bv[0], bi[0], lv[0], li[0]);
+        ov[j] = take_b ? bv[0] : lv[0];
+        oi[j] = take_b ? bi[0] : li[0];
+#pragma unroll
+        for (int q = 0; q < KB - 1; ++q) {
+          bv[q] = take_b ? bv[q + 1] : bv[q];
+          bi[q] = take_b ? bi[q + 1] : bi[q];
+          lv[q] = take_b ? lv[q] : lv[q + 1];
+          li[q] = take_b ? li[q] : li[q + 1];
+        }
+        bv[KB - 1] = take_b ? -INFINITY : bv[KB - 1];
+        bi[KB - 1] = take_b ? 0x7fffffff : bi[KB - 1];
+        lv[KB - 1] = take_b ? lv[KB - 1] : -INFINITY;
+        li[KB - 1] = take_b ? li[KB - 1] : 0x7fffffff;
+      }
+#pragma unroll
+      for (int j = 0; j < KB; ++j) { lv[j] = ov[j]; li[j] = oi[j]; }
     }
   }
   const float M = block_max(m, shv);
   const float S = block_sum(m == -INFINITY ? 0.f : s * expf(m - M), shv);
   const float lse = M + logf(S);
-
-  const int k = a.topk;
-  const int nc = a.n_wg * k;
-  const float *pv = a.pval + (size_t)r * nc;
-  const int *pi = a.pid + (size_t)r * nc;
-  // thread-local sorted list (best first) of a strided subset
-  float lv[KB];
-  int li[KB];
-#pragma unroll
-  for (int j = 0; j < KB; ++j) { lv[j] = -INFINITY; li[j] = 0x7fffffff; }
-  for (int i0 = 0; i0 < nc; i0 += 256 * CMB_UNROLL) {
-    float cv[CMB_UNROLL];
-    int ci[CMB_UNROLL];
-#pragma unroll
-    for (int u = 0; u < CMB_UNROLL; ++u) {
-      const int i = i0 + u * 256 + tid;
-      cv[u] = i < nc ? pv[i] : -INFINITY;
-      ci[u] = i < nc ? pi[i] : 0x7fffffff;
-    }
-#pragma unroll
-    for (int u = 0; u < CMB_UNROLL; ++u) {
-      if (!better(cv[u], ci[u], lv[KB - 1], li[KB - 1])) continue;
-      lv[KB - 1] = cv[u];
-      li[KB - 1] = ci[u];
-#pragma unroll
-      for (int j = KB - 1; j > 0; --j)   // bubble the new entry to its place
-        if (better(lv[j], li[j], lv[j - 1], li[j - 1])) {
-          const float tv = lv[j]; lv[j] = lv[j - 1]; lv[j - 1] = tv;
-          const int ti = li[j]; li[j] = li[j - 1]; li[j - 1] = ti;
-        }
-    }
-  }
   for (int j = 0; j < k; ++j) {
     float v = lv[0];
     int id = li[0];
