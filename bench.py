@@ -63,13 +63,29 @@ WORKLOADS = {
 }
 
 
+def lm_workgroups(cfg, rows):
+    """Workgroups of one LM-head launch (the library's plan: 16-id vocab tiles,
+    4 waves per workgroup, tiles per wave by rows)."""
+    tiles, nkb = cfg.vocab // 16, cfg.hidden // 32
+    if rows == 1 and cfg.dtype == "bf16":
+        nt = 4 if tiles % 16 == 0 and nkb % 16 == 0 and tiles // 4 >= 1024 else 1
+    elif 16 < rows <= 32 and tiles % 8 == 0:
+        nt = 8
+    elif rows <= 32 and tiles % 4 == 0:
+        nt = 4
+    else:
+        nt = 2 if tiles % 2 == 0 else 1
+    return (tiles // nt + 3) // 4
+
+
 def lm_head_bytes(cfg, rows):
     """Algorithmic HBM bytes of one LM-head launch: the [V, H] weight stream,
-    the normalised input rows, and the per-workgroup top-k partials."""
+    the normalised input rows (a hi/lo pair of bf16 planes, or fp32), and the
+    per-workgroup partials (max, sum and k values and ids per row)."""
     es = 2 if cfg.dtype == "bf16" else 4
-    n_wg = (cfg.vocab // 16 + 3) // 4
     k = max(1, cfg.tree_width)
-    return cfg.vocab * cfg.hidden * es + rows * cfg.hidden * es + rows * n_wg * (2 + 2 * k) * 4
+    return (cfg.vocab * cfg.hidden * es + rows * cfg.hidden * 4
+            + rows * lm_workgroups(cfg, rows) * (2 + 2 * k) * 4)
 
 
 def step_weight_bytes(cfg, s):
