@@ -27,12 +27,22 @@ COPY_BYTES = 256 << 20      # counter-calibration copy
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lmhead_traffic.json")
 
 
-def kernel_source_digest():
+def kernel_source_digest(read=None):
+    """Digest of the LM-head kernel's code (its sources without // comments
+    and blank lines), so that the counter figures go stale with the code but
+    not with its documentation."""
     import hashlib
     h = hashlib.sha256()
     for f in ("gemm.hip", "device.h", "internal.h"):
-        with open(os.path.join(ROOT, "paper_2602_01762_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        if read is None:
+            with open(os.path.join(ROOT, "paper_2602_01762_amd", "csrc", f)) as fh:
+                text = fh.read()
+        else:
+            text = read(f)
+        for line in text.splitlines():
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

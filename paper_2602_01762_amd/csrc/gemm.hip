@@ -1,20 +1,27 @@
-// Skinny GEMMs of the drafting step on MFMA: Y[R, N] = X[R, K] . W[N, K]^T
-// with R <= 64 rows (batch rows or tree nodes) and N, K in the thousands.
+// Skinny products of the drafting step: Y[R, N] = X[R, K] . W[N, K]^T with
+// R <= 64 rows (batch rows or tree nodes) and N, K in the thousands, and the
+// LM head with its fused top-k partials.
 //
 // These products are HBM-bound (a weight byte feeds 2R flops), so the design
 // is about streaming W: W is pre-tiled so that every wave-wide load is one
-// contiguous KiB (see TiledMat), each wave keeps 8 KiB of loads in flight,
-// and up to 16 waves of one workgroup split K so that small matrices still
-// put enough bytes in flight; their partial sums meet in LDS in wave order
-// (deterministic, no second pass).  The MFMA takes 16 rows of W as its M
-// side and 16 rows of X as its N side; for R = 1 most of the B fragment is
-// zero, which costs MFMA cycles that are idle anyway.  bf16 activations come
-// as hi/lo pairs (two MFMAs per W fragment), so the products see fp32-exact
-// activations at no extra HBM traffic.
+// contiguous KiB (see TiledMat), and each wave issues a batch of k-block
+// loads (16 KiB in the GEMV, about 96 VGPRs of A and B in the MFMA loop)
+// before it consumes them.
+//  * 1-2 rows: VALU GEMV.  The workgroup stages its rows in LDS as fp32 and
+//    each lane multiplies its weights by LDS-broadcast activations; up to 16
+//    waves of one workgroup split K and meet in LDS in wave order.  The
+//    one-row LM head streams four consecutive vocab tiles per wave instead.
+//  * More rows: MFMA with 16 rows of W as the M side and 16 rows of X as the
+//    N side; bf16 activations come as hi/lo pairs (two MFMAs per W fragment),
+//    so the products see fp32-exact activations at no extra HBM traffic.
+//    Wide products split K across the waves of a workgroup (LDS reduction);
+//    narrow ones split it across workgroups, and a finish pass adds the
+//    slices in order.  Every reduction has a fixed order (deterministic).
 //
 // Epilogues write whatever the next kernel needs: the fp32 residual row,
-// (y * gain) as the next operand, per-tile sums of squares for the next
-// RMSNorm, the SwiGLU product, or q and the rotated k, v cache slots.
+// (y * gain) as the next operand, partial sums of squares for the next
+// RMSNorm (reduced by the consumer itself), the SwiGLU product, or q and the
+// rotated k, v cache slots.
 #include "device.h"
 
 namespace prism {

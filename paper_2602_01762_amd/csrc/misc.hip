@@ -85,7 +85,8 @@ void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, con
 }
 
 // ---------------------------------------------------------------------------
-// Row scales for batched consumers: scale[r] = 1/sqrt(sum_t ss[t*R + r]/n + eps)
+// Row scales for consumers that cannot reduce the producer's partials
+// themselves: scale[r] = 1/sqrt(sum_t ss[t*R + r]/n + eps)
 __global__ __launch_bounds__(256) void k_rowscale(int R, const float *ss, int n_parts, int n,
                                                   float eps, float *scale) {
   __shared__ float sh[8];
