@@ -1,0 +1,53 @@
+"""Host-side logic of bench.py: the LM head's launch plan and algorithmic
+bytes, the counter-figure digest, and the refusal of several GPUs."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from synth import L2_7B_BS1, L3_70B_BS32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE  # noqa: E402
+
+
+def test_lm_workgroups_follow_the_launch_plan():
+    # one row: 4 tiles per wave when 1024 such waves remain, else 1; more rows:
+    # 4 tiles per wave up to 16 rows, 8 at 17-32 rows
+    assert bench.lm_workgroups(L3_8B_BS1, 1) == 8016 // 16
+    assert bench.lm_workgroups(L2_7B_BS1, 1) == 2000 // 4
+    assert bench.lm_workgroups(L3_8B_BS16, 16) == 8016 // 16
+    assert bench.lm_workgroups(L3_8B_TREE, 32) == (8016 // 8 + 3) // 4
+    assert bench.lm_workgroups(L3_70B_BS32, 32) == (8016 // 8 + 3) // 4
+
+
+def test_lm_head_bytes():
+    # weights + the row's hi/lo planes + (max, sum, value, id) per workgroup
+    assert bench.lm_head_bytes(L3_8B_BS1, 1) == 128256 * 4096 * 2 + 4096 * 4 + 501 * 16
+
+
+def _digest_with(edit):
+    base = os.path.join(ROOT, "paper_2602_01762_amd", "csrc")
+
+    def read(f):
+        with open(os.path.join(base, f)) as fh:
+            text = fh.read()
+        return edit(f, text)
+    return bench.kernel_source_digest(read)
+
+
+def test_digest_ignores_comments_but_not_code():
+    ref = bench.kernel_source_digest()
+    assert _digest_with(lambda f, t: t) == ref
+    assert _digest_with(lambda f, t: t + "\n// a new comment\n\n") == ref
+    assert _digest_with(lambda f, t: t.replace("constexpr int UV = 16;", "constexpr int UV = 16;  // batch")
+                        if f == "gemm.hip" else t) == ref
+    assert _digest_with(lambda f, t: t.replace("constexpr int UV = 16;", "constexpr int UV = 8;")
+                        if f == "gemm.hip" else t) != ref
+
+
+def test_several_gpus_are_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0
+    assert "single-GPU" in r.stdout + r.stderr
