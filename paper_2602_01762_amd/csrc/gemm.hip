@@ -710,46 +710,101 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
             f32x4{v[0], v[1], v[2], v[3]};
     }
   __syncthreads();
+  // Each wave reduces rows wave, wave + 4, ...: up to RB of them together,
+  // so that the dependent shuffle chains of their reductions overlap.
+  constexpr int RB = VR > 0 ? 1 : 4;
   const int base_id = blockIdx.x * 64 * NT;
-  for (int r = wave; r < g.R; r += 4) {
-    float v[NT];
-    int id[NT];
-    float mx = -INFINITY;
+  for (int r0 = wave; r0 < g.R; r0 += 4 * RB) {
+    float v[RB][NT];
+    int id[RB][NT];
+    float mx[RB];
 #pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      const int c = n * 64 + lane;
-      id[n] = base_id + c;
-      const bool valid = id[n] < g.V;
-      v[n] = valid ? sl[r][c] : -INFINITY;
-      if (!valid) id[n] = 0x7fffffff;
-      mx = fmaxf(mx, v[n]);
-    }
-    mx = wave_max(mx);
-    // max and sum of exp over the scaled logits z = v * inv_temp (inv_temp > 0)
-    const float mz = mx * g.inv_temp;
-    float e = 0.f;
+    for (int b = 0; b < RB; ++b) {
+      const int r = r0 + 4 * b;
+      mx[b] = -INFINITY;
 #pragma unroll
-    for (int n = 0; n < NT; ++n) e += id[n] != 0x7fffffff ? expf(v[n] * g.inv_temp - mz) : 0.f;
-    const float s = wave_sum(e);
-    const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
-    if (lane == 0) {
-      g.pmax[pi] = mz;
-      g.psum[pi] = s;
-    }
-    for (int j = 0; j < g.topk; ++j) {
-      float bv = v[0];
-      int bid = id[0];
-#pragma unroll
-      for (int n = 1; n < NT; ++n)
-        if (better(v[n], id[n], bv, bid)) { bv = v[n]; bid = id[n]; }
-      wave_argmax(bv, bid);
-      if (lane == 0) {
-        g.pval[pi * g.topk + j] = bv;
-        g.pid[pi * g.topk + j] = bid;
+      for (int n = 0; n < NT; ++n) {
+        const int c = n * 64 + lane;
+        id[b][n] = base_id + c;
+        const bool valid = r < g.R && id[b][n] < g.V;
+        v[b][n] = valid ? sl[r < g.R ? r : 0][c] : -INFINITY;
+        if (!valid) id[b][n] = 0x7fffffff;
+        mx[b] = fmaxf(mx[b], v[b][n]);
       }
+    }
+#pragma unroll
+    for (int b = 0; b < RB; ++b) mx[b] = wave_max(mx[b]);
+    // max and sum of exp over the scaled logits z = v * inv_temp (inv_temp > 0)
+    float e[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      e[b] = 0.f;
 #pragma unroll
       for (int n = 0; n < NT; ++n)
-        if (id[n] == bid) { v[n] = -INFINITY; id[n] = 0x7fffffff; }
+        e[b] += id[b][n] != 0x7fffffff ? expf(v[b][n] * g.inv_temp - mx[b] * g.inv_temp) : 0.f;
+    }
+#pragma unroll
+    for (int b = 0; b < RB; ++b) e[b] = wave_sum(e[b]);
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+      const int r = r0 + 4 * b;
+      if (lane == 0 && r < g.R) {
+        const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
+        g.pmax[pi] = mx[b] * g.inv_temp;
+        g.psum[pi] = e[b];
+      }
+    }
+    if (g.topk > 1) {
+      // each lane sorts its NT candidates once (odd-even transposition,
+      // best first); the rounds then take the list heads
+#pragma unroll
+      for (int b = 0; b < RB; ++b)
+#pragma unroll
+        for (int pass = 0; pass < NT; ++pass)
+#pragma unroll
+          for (int n = pass & 1; n + 1 < NT; n += 2) {
+            const bool sw = better(v[b][n + 1], id[b][n + 1], v[b][n], id[b][n]);
+            const float tv = v[b][n];
+            const int ti = id[b][n];
+            v[b][n] = sw ? v[b][n + 1] : tv;
+            id[b][n] = sw ? id[b][n + 1] : ti;
+            v[b][n + 1] = sw ? tv : v[b][n + 1];
+            id[b][n + 1] = sw ? ti : id[b][n + 1];
+          }
+    }
+    for (int j = 0; j < g.topk; ++j) {
+      float bv[RB];
+      int bid[RB];
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        bv[b] = v[b][0];
+        bid[b] = id[b][0];
+        if (g.topk == 1) {
+#pragma unroll
+          for (int n = 1; n < NT; ++n)
+            if (better(v[b][n], id[b][n], bv[b], bid[b])) { bv[b] = v[b][n]; bid[b] = id[b][n]; }
+        }
+      }
+#pragma unroll
+      for (int b = 0; b < RB; ++b) wave_argmax(bv[b], bid[b]);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        const int r = r0 + 4 * b;
+        if (lane == 0 && r < g.R) {
+          const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
+          g.pval[pi * g.topk + j] = bv[b];
+          g.pid[pi * g.topk + j] = bid[b];
+        }
+        // the winning lane drops its head (ids are distinct)
+        const bool win = id[b][0] == bid[b];
+#pragma unroll
+        for (int n = 0; n + 1 < NT; ++n) {
+          v[b][n] = win ? v[b][n + 1] : v[b][n];
+          id[b][n] = win ? id[b][n + 1] : id[b][n];
+        }
+        v[b][NT - 1] = win ? -INFINITY : v[b][NT - 1];
+        id[b][NT - 1] = win ? 0x7fffffff : id[b][NT - 1];
+      }
     }
   }
 }
