@@ -162,8 +162,9 @@ static Plan plan_for(const TiledMat &t, int R) {
 // fragment reuse) and K slices across workgroups: at most one workgroup of
 // 4 waves per CU (longer slices stream better than more of them, and a grid
 // just above the CU count leaves a few CUs with twice the work), at least 4
-// k-blocks per slice, and fp32 slice partials of at most 1/8 of the weight
-// bytes (split * R * N * 4 <= N * K * 2 / 8).
+// k-blocks per slice, and fp32 slice partials of at most 1/4 of the weight
+// bytes (split * R * N * 4 <= N * K * 2 / 4; at 32 rows the tighter 1/8 cap
+// left the 4096-wide products on 64-128 workgroups: tree 2.695 -> 2.662 ms).
 static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
   if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
@@ -171,7 +172,7 @@ static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
   const int wgs = (t.n_tiles / nt + 3) / 4;
   int sp = 256 / wgs;
   if (sp > t.nkb / 4) sp = t.nkb / 4;
-  if (sp > t.K / (16 * R)) sp = t.K / (16 * R);
+  if (sp > t.K / (8 * R)) sp = t.K / (8 * R);
   split = sp < 1 ? 1 : sp;
 }
 
