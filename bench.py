@@ -79,7 +79,7 @@ def lm_workgroups(cfg, rows):
     tiles, nkb = cfg.vocab // 16, cfg.hidden // 32
     if rows == 1 and cfg.dtype == "bf16":
         nt = 4 if tiles % 16 == 0 and nkb % 16 == 0 and tiles // 4 >= 1024 else 1
-    elif 16 < rows <= 32 and tiles % 8 == 0:
+    elif rows <= 32 and tiles % 8 == 0:
         nt = 8
     elif rows <= 32 and tiles % 4 == 0:
         nt = 4

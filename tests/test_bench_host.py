@@ -12,11 +12,11 @@ from synth import L2_7B_BS1, L3_70B_BS32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE  # n
 
 
 def test_lm_workgroups_follow_the_launch_plan():
-    # one row: 4 tiles per wave when 1024 such waves remain, else 1; more rows:
-    # 4 tiles per wave up to 16 rows, 8 at 17-32 rows
+    # one row: 4 tiles per wave when 1024 such waves remain, else 1; 2-32
+    # rows: 8 tiles per wave
     assert bench.lm_workgroups(L3_8B_BS1, 1) == 8016 // 16
     assert bench.lm_workgroups(L2_7B_BS1, 1) == 2000 // 4
-    assert bench.lm_workgroups(L3_8B_BS16, 16) == 8016 // 16
+    assert bench.lm_workgroups(L3_8B_BS16, 16) == (8016 // 8 + 3) // 4
     assert bench.lm_workgroups(L3_8B_TREE, 32) == (8016 // 8 + 3) // 4
     assert bench.lm_workgroups(L3_70B_BS32, 32) == (8016 // 8 + 3) // 4
 
