@@ -75,7 +75,7 @@ __device__ __forceinline__ void load8(const T *p, float (&v)[8]) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
-  const int c = blockIdx.x, j = blockIdx.y, r = blockIdx.z;
+  const int c = blockIdx.z, j = blockIdx.x, r = blockIdx.y;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   int b, L, prefix, total;
   uint64_t bits;
@@ -288,7 +288,7 @@ constexpr int ATT_MAXSUB = 16;    // 64-slot steps per workgroup
 template <int DK>   // head_dim / 32
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   constexpr int ATT_MAXDK = DK, ATT_MAXDT = 2 * DK;
-  const int c = blockIdx.x, j = blockIdx.y, r = blockIdx.z;
+  const int c = blockIdx.z, j = blockIdx.x, r = blockIdx.y;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, q4 = lane >> 4;
   int b, L, prefix, total;
@@ -575,7 +575,9 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   a.po = po;
   a.o = o;
   a.err = err;
-  dim3 g1(a.nch, nkv, R), g2(nq, R);
+  // chunk index slowest: every row's first chunks are dispatched before any
+  // row's later ones, so the last workgroups to start are the short tails
+  dim3 g1(nkv, R, a.nch), g2(nq, R);
   if (bf16) {
     if (d == 64) hipLaunchKernelGGL(k_attn_mfma<2>, g1, dim3(256), 0, s, a);
     else if (d == 128) hipLaunchKernelGGL(k_attn_mfma<4>, g1, dim3(256), 0, s, a);
