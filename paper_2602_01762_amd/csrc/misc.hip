@@ -580,17 +580,40 @@ struct TreeFinArgs {
   int32_t *front_out;
 };
 
+// Final top-v of the C candidates of sequence b.  Every candidate's score,
+// token and parent goes out in one batch of loads (unconditional, clamped
+// index) into LDS; the ranks, outputs and copies then read LDS only.
 __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
+  constexpr int PER = (TREE_MAXC + 255) / 256;
   __shared__ float sc[TREE_MAXC];
+  __shared__ int tk[TREE_MAXC], pa[TREE_MAXC];
   __shared__ short outpos[TREE_MAXC];
   __shared__ int sel[64];
   __shared__ int par[64];
   const TreeWs &t = a.t;
   const int b = blockIdx.x, tid = threadIdx.x;
   const int C = t.C, w = t.w;
-  for (int i = tid; i < C; i += blockDim.x) {
-    sc[i] = t.cand_score[(size_t)b * C + i];
-    outpos[i] = -1;
+  {
+    float vs[PER];
+    int vt[PER], vp[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int i = tid + 256 * q;
+      const size_t ci = (size_t)b * C + (i < C ? i : 0);
+      vs[q] = t.cand_score[ci];
+      vt[q] = t.cand_tok[ci];
+      vp[q] = t.cand_par[ci];
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int i = tid + 256 * q;
+      if (i < C) {
+        sc[i] = vs[q];
+        tk[i] = vt[q];
+        pa[i] = vp[q];
+        outpos[i] = -1;
+      }
+    }
   }
   __syncthreads();
   for (int i = tid; i < C; i += blockDim.x) {
@@ -604,11 +627,11 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
   __syncthreads();
   if (tid < a.v) {
     const int n = sel[tid];
-    const int p = t.cand_par[(size_t)b * C + n];
+    const int p = pa[n];
     const int po = p >= 0 ? outpos[p] : -1;
     par[tid] = po;
     const size_t o = (size_t)b * a.v + tid;
-    a.tokens[o] = t.cand_tok[(size_t)b * C + n];
+    a.tokens[o] = tk[n];
     a.parent[o] = po;
     a.depth[o] = n < w ? 1 : 2 + (n - w) / (w * w);
     a.score[o] = sc[n];
@@ -623,12 +646,11 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
     }
     a.mask[(size_t)b * a.v + tid] = m;
   }
-  if (a.c_tok)
-    for (int i = tid; i < C; i += blockDim.x) a.c_tok[(size_t)b * C + i] = t.cand_tok[(size_t)b * C + i];
-  if (a.c_par)
-    for (int i = tid; i < C; i += blockDim.x) a.c_par[(size_t)b * C + i] = t.cand_par[(size_t)b * C + i];
-  if (a.c_score)
-    for (int i = tid; i < C; i += blockDim.x) a.c_score[(size_t)b * C + i] = sc[i];
+  for (int i = tid; i < C; i += blockDim.x) {
+    if (a.c_tok) a.c_tok[(size_t)b * C + i] = tk[i];
+    if (a.c_par) a.c_par[(size_t)b * C + i] = pa[i];
+    if (a.c_score) a.c_score[(size_t)b * C + i] = sc[i];
+  }
   if (a.front_out) {
     const int nf = (t.D - 1) * w;
     for (int i = tid; i < nf; i += blockDim.x)
