@@ -275,14 +275,6 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return f2bf(lo) | (f2bf(hi) << 16);
 }
 
-// order the wave's LDS writes before its later reads (and the reverse): the
-// tile is private to the wave, so no workgroup barrier is needed
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-
 constexpr int ATT_MAXSUB = 16;    // 64-slot steps per workgroup
 
 template <int DK>   // head_dim / 32

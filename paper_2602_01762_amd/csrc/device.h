@@ -111,6 +111,14 @@ __device__ __forceinline__ void block_argmax(float &v, int &id, float *shv, int 
     if (better(shv[i], shi[i], v, id)) { v = shv[i]; id = shi[i]; }
 }
 
+// order a wave's LDS writes before its later reads (and the reverse) when
+// the data is private to the wave, so no workgroup barrier is needed
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 __device__ __forceinline__ float silu(float y) { return y / (1.0f + expf(-y)); }
 
 // Token of row r from the LM head's top-1 partials (larger logit wins, ties
@@ -136,6 +144,45 @@ __device__ __forceinline__ int token_from_lm(const TokFromLm &t, int r, float *s
       if (better(v[u], id[u], bv, bid)) { bv = v[u]; bid = id[u]; }
   }
   block_argmax(bv, bid, shv, shi);
+  return bid;
+}
+
+// The same resolved by one wave on its own (no workgroup barrier), in two
+// halves so that the partials' loads can be issued ahead of other loads:
+// the first PRE * 64 entries go out in issue_tok, the rest (larger grids)
+// are read in finish_tok, which returns the token in every lane.
+template <int PRE>
+struct TokLoads {
+  float v[PRE];
+  int id[PRE];
+};
+template <int PRE>
+__device__ __forceinline__ TokLoads<PRE> issue_tok(const TokFromLm &t, int r) {
+  const int lane = threadIdx.x & 63;
+  const float *pv = t.pval + (size_t)r * t.n_wg;
+  const int *pi = t.pid + (size_t)r * t.n_wg;
+  TokLoads<PRE> l;
+#pragma unroll
+  for (int u = 0; u < PRE; ++u) {
+    const int i = u * 64 + lane;
+    l.v[u] = i < t.n_wg ? pv[i] : -INFINITY;
+    l.id[u] = i < t.n_wg ? pi[i] : 0x7fffffff;
+  }
+  return l;
+}
+template <int PRE>
+__device__ __forceinline__ int finish_tok(const TokFromLm &t, int r, const TokLoads<PRE> &l) {
+  const int lane = threadIdx.x & 63;
+  float bv = -INFINITY;
+  int bid = 0x7fffffff;
+#pragma unroll
+  for (int u = 0; u < PRE; ++u)
+    if (better(l.v[u], l.id[u], bv, bid)) { bv = l.v[u]; bid = l.id[u]; }
+  const float *pv = t.pval + (size_t)r * t.n_wg;
+  const int *pi = t.pid + (size_t)r * t.n_wg;
+  for (int i = PRE * 64 + lane; i < t.n_wg; i += 64)
+    if (better(pv[i], pi[i], bv, bid)) { bv = pv[i]; bid = pi[i]; }
+  wave_argmax(bv, bid);
   return bid;
 }
 

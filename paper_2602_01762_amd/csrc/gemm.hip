@@ -86,110 +86,90 @@ __device__ __forceinline__ void mainloop(const u32x4 *__restrict__ w0, int nkb, 
   }
 }
 
-// GEMV main loop for a few rows (R <= RR <= 4) of a bf16 matrix: the
-// workgroup first stages the activation rows in LDS as fp32 (hi + lo), then
-// each lane multiplies its 8 weights of a k-block by the matching fp32
+// GEMV main loop for a few rows (R <= RR <= 4) of a bf16 matrix: each wave
+// stages the activation columns of its own K range in LDS as fp32 (hi + lo),
+// then each lane multiplies its 8 weights of a k-block by the matching fp32
 // activations (an LDS broadcast: the 16 lanes of a k-quarter read the same
 // address).  Only weight fragments occupy registers, so 16 k-blocks
 // (16 KiB) stay in flight per wave, and the products are fp32-exact.  The
 // first batch of weight loads is issued before the staging so the two
-// overlap.  Every wave of the workgroup must call this (it contains a
-// barrier); waves without work pass kb0 == kb1.  Leaves the result in the
-// MFMA accumulator layout so that all epilogues are shared.
+// overlap; as the staged columns are private to the wave, no workgroup
+// barrier separates a wave's staging from its products.  Leaves the result
+// in the MFMA accumulator layout so that all epilogues are shared.
 constexpr int UV = 16;
 
 __device__ __forceinline__ float lo_bf(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_bf(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Staging of gathered fusion-FC rows x_r = [E(token_r) ; feature row] (K =
-// H + F columns) as fp32: the tokens come from the rows or from the previous
-// LM head's partials; an out-of-range token flags ERRF_TOKEN and reads as a
-// zero embedding.
-template <int RR>
-__device__ __forceinline__ void stage_gather(const Gather &gx, int R, int K, float *xs,
-                                             uint32_t *err) {
-  __shared__ int s_tok[RR];
-  __shared__ float s_v[16];
-  __shared__ int s_i[16];
-  const bool lead = blockIdx.x == 0 && threadIdx.x == 0;
-  for (int r = 0; r < R; ++r) {
-    int tok;
-    if (gx.lm.pval) {
-      tok = token_from_lm(gx.lm, r, s_v, s_i);
-      if (lead && gx.lm.rec) gx.lm.rec[(size_t)r * gx.lm.ld_rec] = tok;
-    } else {
-      tok = gx.in.tokens[r];
-    }
-    if (tok < 0 || tok >= gx.V) {
-      if (lead) atomicOr(err, ERRF_TOKEN);
-      tok = -1;
-    }
-    if (threadIdx.x == 0) s_tok[r] = tok;
-  }
-  __syncthreads();
-  const int H = gx.H;
-  for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
-    const int r = i / K, k = i % K;
-    float v[8];
+// 8 columns of a staged row from a packed bf16 plane (8 values) or from the
+// hi + lo pair of planes
+__device__ __forceinline__ void unpack8(const u32x4 q, float (&v)[8]) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-    for (int m = 0; m < 8; ++m) v[m] = 0.f;
-    if (r < R) {
-      if (k < H) {
-        const int tok = s_tok[r];
-        if (tok >= 0) {
-          const u32x4 e = *(const u32x4 *)((const bf16_t *)gx.embed + (size_t)tok * H + k);
-          const uint32_t ew[4] = {e.x, e.y, e.z, e.w};
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            v[2 * m] = lo_bf(ew[m]);
-            v[2 * m + 1] = hi_bf(ew[m]);
-          }
-        }
-      } else {
-        const int fr = gx.in.feat_rows ? gx.in.feat_rows[r] : r;
-        const size_t o = (size_t)fr * gx.in.feat_ld + (k - H);
-        if (gx.in.feat_bf16) {
-          const u32x4 f = *(const u32x4 *)((const bf16_t *)gx.in.feat + o);
-          const uint32_t fw[4] = {f.x, f.y, f.z, f.w};
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            v[2 * m] = lo_bf(fw[m]);
-            v[2 * m + 1] = hi_bf(fw[m]);
-          }
-        } else {
-          const f32x4 f0 = *(const f32x4 *)((const float *)gx.in.feat + o);
-          const f32x4 f1 = *(const f32x4 *)((const float *)gx.in.feat + o + 4);
-          v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
-          v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
-        }
-      }
-    }
-    *(f32x4 *)(xs + i) = f32x4{v[0], v[1], v[2], v[3]};
-    *(f32x4 *)(xs + i + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  for (int m = 0; m < 4; ++m) {
+    v[2 * m] = lo_bf(w[m]);
+    v[2 * m + 1] = hi_bf(w[m]);
   }
 }
 
-// x rows staged in LDS as fp32: gathered fusion-FC rows, or R rows of the
-// hi/lo operand (rows R .. RR-1 zero), 8 columns per thread step
-template <int RR>
-__device__ __forceinline__ void stage_x(const Act &x, int R, int K, float *xs, const Gather *gx,
-                                        uint32_t *err) {
-  if (gx && gx->embed) {
-    stage_gather<RR>(*gx, R, K, xs, err);
-    return;
+// One wave stages the columns [c0, c1) (multiples of 32) of the operand rows
+// as fp32 into xs (row stride K); rows R .. RR-1 read as zero.  Plain
+// operands come as hi/lo planes; gathered fusion-FC rows are x_r =
+// [E(tok_r) ; feature row] (K = H + F columns), and tok_r < 0 reads a zero
+// embedding.
+template <int RR, bool GX>
+__device__ __forceinline__ void stage_wave(const Act &x, const Gather &gx, const int (&tok)[RR],
+                                           int R, int K, float *xs, int c0, int c1) {
+  const int lane = threadIdx.x & 63;
+  for (int k = c0 + lane * 8; k < c1; k += 512) {
+#pragma unroll
+    for (int r = 0; r < RR; ++r) {
+      float v[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) v[m] = 0.f;
+      if (r < R) {
+        if constexpr (!GX) {
+          float h[8], l[8];
+          unpack8(*(const u32x4 *)((const bf16_t *)x.hi + (size_t)r * x.ld + k), h);
+          unpack8(*(const u32x4 *)((const bf16_t *)x.lo + (size_t)r * x.ld + k), l);
+#pragma unroll
+          for (int m = 0; m < 8; ++m) v[m] = h[m] + l[m];
+        } else if (k < gx.H) {
+          if (tok[r] >= 0)
+            unpack8(*(const u32x4 *)((const bf16_t *)gx.embed + (size_t)tok[r] * gx.H + k), v);
+        } else {
+          const int fr = gx.in.feat_rows ? gx.in.feat_rows[r] : r;
+          const size_t o = (size_t)fr * gx.in.feat_ld + (k - gx.H);
+          if (gx.in.feat_bf16) {
+            unpack8(*(const u32x4 *)((const bf16_t *)gx.in.feat + o), v);
+          } else {
+            const f32x4 f0 = *(const f32x4 *)((const float *)gx.in.feat + o);
+            const f32x4 f1 = *(const f32x4 *)((const float *)gx.in.feat + o + 4);
+            v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+            v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
+          }
+        }
+      }
+      *(f32x4 *)(xs + r * K + k) = f32x4{v[0], v[1], v[2], v[3]};
+      *(f32x4 *)(xs + r * K + k + 4) = f32x4{v[4], v[5], v[6], v[7]};
+    }
   }
+}
+
+// x rows staged in LDS as fp32 by the whole workgroup (every wave multiplies
+// all K columns): R rows of the hi/lo operand (rows R .. RR-1 zero), 8
+// columns per thread step
+template <int RR>
+__device__ __forceinline__ void stage_x(const Act &x, int R, int K, float *xs) {
   for (int i = threadIdx.x * 8; i < RR * K; i += blockDim.x * 8) {
     const int r = i / K, k = i % K;
     float v[8];
     if (r < R) {
-      const u32x4 h = *(const u32x4 *)((const bf16_t *)x.hi + (size_t)r * x.ld + k);
-      const u32x4 l = *(const u32x4 *)((const bf16_t *)x.lo + (size_t)r * x.ld + k);
-      const uint32_t hw[4] = {h.x, h.y, h.z, h.w}, lw[4] = {l.x, l.y, l.z, l.w};
+      float h[8], l[8];
+      unpack8(*(const u32x4 *)((const bf16_t *)x.hi + (size_t)r * x.ld + k), h);
+      unpack8(*(const u32x4 *)((const bf16_t *)x.lo + (size_t)r * x.ld + k), l);
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        v[2 * m] = lo_bf(hw[m]) + lo_bf(lw[m]);
-        v[2 * m + 1] = hi_bf(hw[m]) + hi_bf(lw[m]);
-      }
+      for (int m = 0; m < 8; ++m) v[m] = h[m] + l[m];
     } else {
 #pragma unroll
       for (int m = 0; m < 8; ++m) v[m] = 0.f;
@@ -251,21 +231,50 @@ __device__ __forceinline__ f32x4 valu_result(float (&acc)[RR]) {
   return f32x4{v[0], v[1], v[2], v[3]};
 }
 
-template <int RR>
+template <int RR, bool GX>
 __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
                                               int K, float *xs, int kb0, int kb1, f32x4 &out,
-                                              const Gather *gx = nullptr, uint32_t *err = nullptr) {
+                                              const Gather &gx, uint32_t *err) {
   const int lane = threadIdx.x & 63, kq = lane >> 4;
   const u32x4 z4 = {0, 0, 0, 0};
   const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
+  // gathered FC rows: a wave whose K range covers embedding columns resolves
+  // the rows' tokens itself; the previous LM head's partials are requested
+  // ahead of the weights, so that the argmax does not wait for them
+  const bool need_tok = GX && kb1 > kb0 && kb0 * 32 < gx.H;
+  const bool from_lm = need_tok && gx.lm.pval;
+  constexpr int PRE = RR == 1 ? 8 : 2;   // entries per lane issued early (registers)
+  TokLoads<PRE> tl[RR];
+  if (from_lm) {
+#pragma unroll
+    for (int r = 0; r < RR; ++r)
+      if (r < R) tl[r] = issue_tok<PRE>(gx.lm, r);
+  }
   u32x4 a[UV];
   {
     const int nb = kb1 - kb0;
 #pragma unroll
     for (int u = 0; u < UV; ++u) a[u] = u < nb ? __builtin_nontemporal_load(wp + u * 64) : z4;
   }
-  stage_x<RR>(x, R, K, xs, gx, err);
-  __syncthreads();
+  int tok[RR];
+#pragma unroll
+  for (int r = 0; r < RR; ++r) tok[r] = -1;
+  if (need_tok) {
+    const bool lead = blockIdx.x == 0 && threadIdx.x == 0;   // wave 0 covers column 0
+#pragma unroll
+    for (int r = 0; r < RR; ++r) {
+      if (r >= R) continue;
+      int t = from_lm ? finish_tok(gx.lm, r, tl[r]) : gx.in.tokens[r];
+      if (lead && from_lm && gx.lm.rec) gx.lm.rec[(size_t)r * gx.lm.ld_rec] = t;
+      if (t < 0 || t >= gx.V) {
+        if (lead) atomicOr(err, ERRF_TOKEN);
+        t = -1;
+      }
+      tok[r] = t;
+    }
+  }
+  stage_wave<RR, GX>(x, gx, tok, R, K, xs, kb0 * 32, kb1 * 32);
+  wave_lds_sync();
   float acc[RR];
 #pragma unroll
   for (int r = 0; r < RR; ++r) acc[r] = 0.f;
@@ -296,7 +305,7 @@ __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0
   u32x4 a[UV];
 #pragma unroll
   for (int u = 0; u < UV; ++u) a[u] = u < nkb_live ? __builtin_nontemporal_load(wp + u * 64) : z4;
-  stage_x<RR>(x, R, K, xs, nullptr, nullptr);
+  stage_x<RR>(x, R, K, xs);
   __syncthreads();
 #pragma unroll
   for (int n = 0; n < NT; ++n) {
@@ -482,8 +491,15 @@ __device__ __forceinline__ long cache_base(const GemmLaunch &g, int r, int &pos)
 template <int RT, int NT>
 constexpr int gemm_max_threads() { return RT * NT >= 2 ? 512 : 1024; }
 
-template <typename T, int RT, int NT, bool PAIR, int EPI, int VR>
+// kernel-only epilogue tag: EPI_NORM on fusion-FC rows that the GEMV main
+// loop gathers itself (no input norm), a separate instantiation so that the
+// other EPI_NORM products carry none of the gather's registers
+constexpr int EPI_NORM_GATHER = 3;
+
+template <typename T, int RT, int NT, bool PAIR, int EPI_K, int VR>
 __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunch g) {
+  constexpr bool GX = EPI_K == EPI_NORM_GATHER;
+  constexpr int EPI = GX ? EPI_NORM : EPI_K;
   // dynamic LDS: [(kw - 1) * NT * RT * 64] f32x4 partial sums, kw floats,
   // then (GEMV path, VR > 0) VR * K floats of staged activations
   extern __shared__ f32x4 red[];
@@ -492,8 +508,8 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   const int kw = g.kw;
   const int t0 = blockIdx.x * NT;
   const TiledMat &m = g.m;
-  const bool has_norm = g.norm.scale != nullptr || g.norm.n_parts > 0;
-  const bool own_scales = g.norm.scale == nullptr && g.norm.n_parts > 0;
+  const bool has_norm = !GX && (g.norm.scale != nullptr || g.norm.n_parts > 0);
+  const bool own_scales = !GX && g.norm.scale == nullptr && g.norm.n_parts > 0;
   ScaleLoads sl;
   if (own_scales) sl = issue_scales(g.norm, g.R, 0, g.R);
 
@@ -522,8 +538,8 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   const int kb1 = (int)((long)(wave + 1) * m.nkb / kw);
   if constexpr (VR > 0) {
     float *xs = (float *)&red[(kw - 1) * NT * RT * 64] + 64 * kw;
-    mainloop_valu<VR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0, kb1,
-                      acc[0][0], &g.gx, g.err);
+    mainloop_valu<VR, GX>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0,
+                          kb1, acc[0][0], g.gx, g.err);
   } else {
     mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
                               kb1, acc);
@@ -822,6 +838,12 @@ static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
   size_t lds = (size_t)((g.kw - 1) * NT * RT * 64) * sizeof(f32x4) +
                (size_t)64 * g.kw * sizeof(float);
   if (VR > 0) lds += (size_t)VR * g.m.K * sizeof(float);
+  if constexpr (VR > 0) {
+    if (g.epi == EPI_NORM && g.gx.embed) {
+      hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM_GATHER, VR>), grid, dim3(64 * g.kw), lds, s, g);
+      return;
+    }
+  }
   if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM, VR>), grid, dim3(64 * g.kw), lds, s, g);
   else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU, VR>), grid, dim3(64 * g.kw), lds, s, g);
   else if constexpr (NT <= 2) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
