@@ -64,7 +64,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 // larger value wins; equal values: lower id wins
 __device__ __forceinline__ bool better(float v, int id, float ov, int oid) {
-  return v > ov || (v == ov && id < oid);
+  // bitwise, not short-circuit: lane masks combine without exec-mask branches
+  return (v > ov) | ((v == ov) & (id < oid));
 }
 __device__ __forceinline__ void wave_argmax(float &v, int &id) {
 #pragma unroll
@@ -72,6 +73,82 @@ __device__ __forceinline__ void wave_argmax(float &v, int &id) {
     float ov = __shfl_xor(v, o, 64);
     int oid = __shfl_xor(id, o, 64);
     if (better(ov, oid, v, id)) { v = ov; id = oid; }
+  }
+}
+
+// The same over N independent values at once: each butterfly step issues
+// the N cross-lane reads together, so their latencies overlap instead of
+// adding up (the results equal N separate calls)
+template <int N>
+__device__ __forceinline__ void wave_max_n(float (&v)[N]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float t[N];
+#pragma unroll
+    for (int b = 0; b < N; ++b) t[b] = __shfl_xor(v[b], o, 64);
+#pragma unroll
+    for (int b = 0; b < N; ++b) v[b] = fmaxf(v[b], t[b]);
+  }
+}
+template <int N>
+__device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float t[N];
+#pragma unroll
+    for (int b = 0; b < N; ++b) t[b] = __shfl_xor(v[b], o, 64);
+#pragma unroll
+    for (int b = 0; b < N; ++b) v[b] += t[b];
+  }
+#pragma unroll
+  for (int b = 0; b < N; ++b) v[b] = __shfl(v[b], 0, 64);
+}
+template <int N>
+__device__ __forceinline__ void wave_argmax_n(float (&v)[N], int (&id)[N]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov[N];
+    int oid[N];
+#pragma unroll
+    for (int b = 0; b < N; ++b) {
+      ov[b] = __shfl_xor(v[b], o, 64);
+      oid[b] = __shfl_xor(id[b], o, 64);
+    }
+#pragma unroll
+    for (int b = 0; b < N; ++b)
+      if (better(ov[b], oid[b], v[b], id[b])) { v[b] = ov[b]; id[b] = oid[b]; }
+  }
+}
+
+// (value, id) candidates as one 64-bit key whose unsigned order is the
+// candidate order above: larger value wins, equal values -> lower id.  The
+// high word is the value mapped to an order-preserving unsigned integer (-0
+// taken as +0, NaN lowest), the low word the complemented id.
+__device__ __forceinline__ uint64_t cand_key(float v, int id) {
+  uint32_t u = __float_as_uint(v + 0.0f);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  u = v != v ? 0u : u;
+  return ((uint64_t)u << 32) | (uint64_t)(~(uint32_t)id);
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t u = (uint32_t)(k >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+__device__ __forceinline__ int key_id(uint64_t k) { return (int)~(uint32_t)k; }
+// butterfly maxima of N keys at once (every lane ends with each maximum)
+template <int N>
+__device__ __forceinline__ void wave_max_key_n(uint64_t (&k)[N]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint64_t t[N];
+#pragma unroll
+    for (int b = 0; b < N; ++b) {
+      const uint32_t hi = __shfl_xor((uint32_t)(k[b] >> 32), o, 64);
+      const uint32_t lo = __shfl_xor((uint32_t)k[b], o, 64);
+      t[b] = ((uint64_t)hi << 32) | lo;
+    }
+#pragma unroll
+    for (int b = 0; b < N; ++b) k[b] = t[b] > k[b] ? t[b] : k[b];
   }
 }
 

@@ -748,8 +748,7 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
         mx[b] = fmaxf(mx[b], v[b][n]);
       }
     }
-#pragma unroll
-    for (int b = 0; b < RB; ++b) mx[b] = wave_max(mx[b]);
+    wave_max_n<RB>(mx);
     // max and sum of exp over the scaled logits z = v * inv_temp (inv_temp > 0)
     float e[RB];
 #pragma unroll
@@ -759,8 +758,7 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
       for (int n = 0; n < NT; ++n)
         e[b] += id[b][n] != 0x7fffffff ? expf(v[b][n] * g.inv_temp - mx[b] * g.inv_temp) : 0.f;
     }
-#pragma unroll
-    for (int b = 0; b < RB; ++b) e[b] = wave_sum(e[b]);
+    wave_sum_n<RB>(e);
 #pragma unroll
     for (int b = 0; b < RB; ++b) {
       const int r = r0 + 4 * b;
@@ -770,6 +768,12 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
         g.psum[pi] = e[b];
       }
     }
+    // top-k on 64-bit candidate keys (one unsigned compare per pair)
+    uint64_t key[RB][NT];
+#pragma unroll
+    for (int b = 0; b < RB; ++b)
+#pragma unroll
+      for (int n = 0; n < NT; ++n) key[b][n] = cand_key(v[b][n], id[b][n]);
     if (g.topk > 1) {
       // each lane sorts its NT candidates once (odd-even transposition,
       // best first); the rounds then take the list heads
@@ -779,47 +783,36 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
         for (int pass = 0; pass < NT; ++pass)
 #pragma unroll
           for (int n = pass & 1; n + 1 < NT; n += 2) {
-            const bool sw = better(v[b][n + 1], id[b][n + 1], v[b][n], id[b][n]);
-            const float tv = v[b][n];
-            const int ti = id[b][n];
-            v[b][n] = sw ? v[b][n + 1] : tv;
-            id[b][n] = sw ? id[b][n + 1] : ti;
-            v[b][n + 1] = sw ? tv : v[b][n + 1];
-            id[b][n + 1] = sw ? ti : id[b][n + 1];
+            const uint64_t lo = key[b][n], hi = key[b][n + 1];
+            key[b][n] = hi > lo ? hi : lo;
+            key[b][n + 1] = hi > lo ? lo : hi;
           }
     }
+    const uint64_t none = cand_key(-INFINITY, 0x7fffffff);
     for (int j = 0; j < g.topk; ++j) {
-      float bv[RB];
-      int bid[RB];
+      uint64_t bk[RB];
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
-        bv[b] = v[b][0];
-        bid[b] = id[b][0];
+        bk[b] = key[b][0];
         if (g.topk == 1) {
 #pragma unroll
-          for (int n = 1; n < NT; ++n)
-            if (better(v[b][n], id[b][n], bv[b], bid[b])) { bv[b] = v[b][n]; bid[b] = id[b][n]; }
+          for (int n = 1; n < NT; ++n) bk[b] = key[b][n] > bk[b] ? key[b][n] : bk[b];
         }
       }
-#pragma unroll
-      for (int b = 0; b < RB; ++b) wave_argmax(bv[b], bid[b]);
+      wave_max_key_n<RB>(bk);
 #pragma unroll
       for (int b = 0; b < RB; ++b) {
         const int r = r0 + 4 * b;
         if (lane == 0 && r < g.R) {
           const size_t pi = (size_t)r * g.n_wg + blockIdx.x;
-          g.pval[pi * g.topk + j] = bv[b];
-          g.pid[pi * g.topk + j] = bid[b];
+          g.pval[pi * g.topk + j] = key_value(bk[b]);
+          g.pid[pi * g.topk + j] = key_id(bk[b]);
         }
         // the winning lane drops its head (ids are distinct)
-        const bool win = id[b][0] == bid[b];
+        const bool win = key[b][0] == bk[b];
 #pragma unroll
-        for (int n = 0; n + 1 < NT; ++n) {
-          v[b][n] = win ? v[b][n + 1] : v[b][n];
-          id[b][n] = win ? id[b][n + 1] : id[b][n];
-        }
-        v[b][NT - 1] = win ? -INFINITY : v[b][NT - 1];
-        id[b][NT - 1] = win ? 0x7fffffff : id[b][NT - 1];
+        for (int n = 0; n + 1 < NT; ++n) key[b][n] = win ? key[b][n + 1] : key[b][n];
+        key[b][NT - 1] = win ? none : key[b][NT - 1];
       }
     }
   }
