@@ -201,23 +201,44 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   const float M = block_max(m, shv);
   const float S = block_sum(m == -INFINITY ? 0.f : s * expf(m - M), shv);
   const float lse = M + logf(S);
-  for (int j = 0; j < k; ++j) {
-    float v = lv[0];
-    int id = li[0];
-    block_argmax(v, id, shv, shi);
-    if (li[0] == id) {   // ids are distinct: exactly one thread owns the winner
+  // each wave takes the best k of its lanes' lists (k rounds of a wave
+  // arg-max over the list heads, on 64-bit candidate keys, no barriers),
+  // then thread 0 merges the four waves' sorted lists
+  __shared__ uint64_t s_wk[4][KB];
+  const int wave = tid >> 6, lane = tid & 63;
+  uint64_t lk[KB];
 #pragma unroll
-      for (int q = 0; q < KB - 1; ++q) { lv[q] = lv[q + 1]; li[q] = li[q + 1]; }
-      lv[KB - 1] = -INFINITY;
-      li[KB - 1] = 0x7fffffff;
+  for (int j = 0; j < KB; ++j) lk[j] = cand_key(lv[j], li[j]);
+  const uint64_t none = cand_key(-INFINITY, 0x7fffffff);
+#pragma unroll
+  for (int j = 0; j < KB; ++j) {
+    if (j >= k) break;
+    uint64_t b[1] = {lk[0]};
+    wave_max_key_n<1>(b);
+    if (lane == 0) s_wk[wave][j] = b[0];
+    const bool win = lk[0] == b[0];   // keys are distinct: one owner (or all spent)
+#pragma unroll
+    for (int q = 0; q + 1 < KB; ++q) lk[q] = win ? lk[q + 1] : lk[q];
+    lk[KB - 1] = win ? none : lk[KB - 1];
+  }
+  __syncthreads();
+  if (tid != 0) return;
+  int hd[4] = {0, 0, 0, 0};
+  for (int j = 0; j < k; ++j) {
+    int bw = 0;
+    uint64_t best = hd[0] < k ? s_wk[0][hd[0]] : 0ull;
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const uint64_t c = hd[w] < k ? s_wk[w][hd[w]] : 0ull;
+      if (c > best) { best = c; bw = w; }
     }
-    if (tid == 0) {
-      a.ids[(size_t)r * k + j] = id;
-      if (a.logp) a.logp[(size_t)r * k + j] = v - lse;
-      if (j == 0) {
-        if (a.tok_a) a.tok_a[r] = id;
-        if (a.tok_b) a.tok_b[(size_t)r * a.ld_b] = id;
-      }
+    ++hd[bw];
+    const int id = key_id(best);
+    a.ids[(size_t)r * k + j] = id;
+    if (a.logp) a.logp[(size_t)r * k + j] = key_value(best) - lse;
+    if (j == 0) {
+      if (a.tok_a) a.tok_a[r] = id;
+      if (a.tok_b) a.tok_b[(size_t)r * a.ld_b] = id;
     }
   }
 }
