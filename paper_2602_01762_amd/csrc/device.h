@@ -50,17 +50,40 @@ template <> struct Ty<bf16_t> {
   }
 };
 
-// ---- wave64 reductions (butterfly; every lane ends with the same value,
-// the same operation order on every run) --------------------------------
+// ---- wave64 reductions (every lane ends with the same value, the same
+// operation order on every run).  Partners within a row of 16 lanes come by
+// DPP (quad permutes, then the half-row and row mirrors), which the VALU
+// executes without the LDS permute unit; the four row results are then read
+// as scalars and combined in row order. ----------------------------------
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+constexpr int DPP_QUAD_XOR1 = 0xB1;      // quad_perm [1, 0, 3, 2]
+constexpr int DPP_QUAD_XOR2 = 0x4E;      // quad_perm [2, 3, 0, 1]
+constexpr int DPP_ROW_MIRROR = 0x140;    // lane i of a row <- lane 15 - i
+constexpr int DPP_HALF_MIRROR = 0x141;   // lane i of a half-row <- lane 7 - i
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(v)));
+}
+__device__ __forceinline__ float readlane_f32(float v, int l) {
+  return __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v), l));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_f32<DPP_QUAD_XOR1>(v));
+  v = fmaxf(v, dpp_f32<DPP_QUAD_XOR2>(v));
+  v = fmaxf(v, dpp_f32<DPP_HALF_MIRROR>(v));
+  v = fmaxf(v, dpp_f32<DPP_ROW_MIRROR>(v));
+  return fmaxf(fmaxf(readlane_f32(v, 0), readlane_f32(v, 16)),
+               fmaxf(readlane_f32(v, 32), readlane_f32(v, 48)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return __shfl(v, 0, 64);
+  v += dpp_f32<DPP_QUAD_XOR1>(v);
+  v += dpp_f32<DPP_QUAD_XOR2>(v);
+  v += dpp_f32<DPP_HALF_MIRROR>(v);
+  v += dpp_f32<DPP_ROW_MIRROR>(v);
+  return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
 }
 // larger value wins; equal values: lower id wins
 __device__ __forceinline__ bool better(float v, int id, float ov, int oid) {
@@ -82,26 +105,12 @@ __device__ __forceinline__ void wave_argmax(float &v, int &id) {
 template <int N>
 __device__ __forceinline__ void wave_max_n(float (&v)[N]) {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float t[N];
-#pragma unroll
-    for (int b = 0; b < N; ++b) t[b] = __shfl_xor(v[b], o, 64);
-#pragma unroll
-    for (int b = 0; b < N; ++b) v[b] = fmaxf(v[b], t[b]);
-  }
+  for (int b = 0; b < N; ++b) v[b] = wave_max(v[b]);
 }
 template <int N>
 __device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float t[N];
-#pragma unroll
-    for (int b = 0; b < N; ++b) t[b] = __shfl_xor(v[b], o, 64);
-#pragma unroll
-    for (int b = 0; b < N; ++b) v[b] += t[b];
-  }
-#pragma unroll
-  for (int b = 0; b < N; ++b) v[b] = __shfl(v[b], 0, 64);
+  for (int b = 0; b < N; ++b) v[b] = wave_sum(v[b]);
 }
 template <int N>
 __device__ __forceinline__ void wave_argmax_n(float (&v)[N], int (&id)[N]) {
@@ -135,20 +144,35 @@ __device__ __forceinline__ float key_value(uint64_t k) {
   return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
 }
 __device__ __forceinline__ int key_id(uint64_t k) { return (int)~(uint32_t)k; }
-// butterfly maxima of N keys at once (every lane ends with each maximum)
+// Maxima of N keys at once; every lane ends with each maximum.  Within each
+// row of 16 lanes the partners come by DPP (quad permutes, then the half-row
+// and row mirrors), which the VALU executes; the four row maxima are then
+// read as scalars.  No LDS permute is involved: a wave's 64-bit arg-max
+// costs about 30 VALU operations instead of 12 dependent LDS permutes.
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_key(uint64_t k) {
+  return ((uint64_t)dpp_u32<CTRL>((uint32_t)(k >> 32)) << 32) | dpp_u32<CTRL>((uint32_t)k);
+}
+__device__ __forceinline__ uint64_t readlane_key(uint64_t k, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(k >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, l);
+}
 template <int N>
 __device__ __forceinline__ void wave_max_key_n(uint64_t (&k)[N]) {
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t t[N];
+  for (int b = 0; b < N; ++b) { const uint64_t t = dpp_key<DPP_QUAD_XOR1>(k[b]); k[b] = t > k[b] ? t : k[b]; }
 #pragma unroll
-    for (int b = 0; b < N; ++b) {
-      const uint32_t hi = __shfl_xor((uint32_t)(k[b] >> 32), o, 64);
-      const uint32_t lo = __shfl_xor((uint32_t)k[b], o, 64);
-      t[b] = ((uint64_t)hi << 32) | lo;
-    }
+  for (int b = 0; b < N; ++b) { const uint64_t t = dpp_key<DPP_QUAD_XOR2>(k[b]); k[b] = t > k[b] ? t : k[b]; }
 #pragma unroll
-    for (int b = 0; b < N; ++b) k[b] = t[b] > k[b] ? t[b] : k[b];
+  for (int b = 0; b < N; ++b) { const uint64_t t = dpp_key<DPP_HALF_MIRROR>(k[b]); k[b] = t > k[b] ? t : k[b]; }
+#pragma unroll
+  for (int b = 0; b < N; ++b) { const uint64_t t = dpp_key<DPP_ROW_MIRROR>(k[b]); k[b] = t > k[b] ? t : k[b]; }
+#pragma unroll
+  for (int b = 0; b < N; ++b) {
+    const uint64_t r0 = readlane_key(k[b], 0), r1 = readlane_key(k[b], 16);
+    const uint64_t r2 = readlane_key(k[b], 32), r3 = readlane_key(k[b], 48);
+    const uint64_t m01 = r1 > r0 ? r1 : r0, m23 = r3 > r2 ? r3 : r2;
+    k[b] = m23 > m01 ? m23 : m01;
   }
 }
 

@@ -676,7 +676,10 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
 // workgroup (4 waves) covers 64*NT vocab ids.  The epilogue applies the
 // final-norm row scale and reduces the workgroup's logits of each row to
 // partials: max, sum of exp(logit - max), and the top-k (logit desc, id asc);
-// optional fp32 logits store.
+// optional fp32 logits store.  With no_part set it only stores the logits
+// (top-k > 1 on MFMA tiles: there the in-kernel top-k rounds, run by one wave
+// per SIMD after the weight stream, cost more than storing the logits and
+// reducing them in a separate, fully occupied pass).
 template <typename T, int RT, int NT, bool PAIR, int VR>
 __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   extern __shared__ float xs_lm[];   // GEMV path: VR * K staged activations
@@ -719,12 +722,15 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
       if (r >= g.R) continue;
       const float s = has_norm ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
       const float v[4] = {acc[n][rt].x * s, acc[n][rt].y * s, acc[n][rt].z * s, acc[n][rt].w * s};
+      if (!g.no_part) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sl[r][(wave * NT + n) * 16 + 4 * q4 + i] = v[i];
+        for (int i = 0; i < 4; ++i) sl[r][(wave * NT + n) * 16 + 4 * q4 + i] = v[i];
+      }
       if (live && g.logits)
         *(f32x4 *)(g.logits + (size_t)r * g.ld_logits + (t0 + n) * 16 + 4 * q4) =
             f32x4{v[0], v[1], v[2], v[3]};
     }
+  if (g.no_part) return;   // uniform: the partials come from k_lm_topk
   __syncthreads();
   // Each wave reduces rows wave, wave + 4, ...: up to RB of them together,
   // so that the dependent shuffle chains of their reductions overlap.

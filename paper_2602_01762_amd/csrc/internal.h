@@ -143,6 +143,7 @@ struct LmLaunch {
   int nt;                          // vocab tiles per wave (1, 2, 4 or 8)
   int gemv;                        // 1: VALU GEMV main loop (bf16, one row)
   float inv_temp;                  // pmax / psum describe logits * inv_temp (1: greedy)
+  int no_part;                     // 1: store the logits only (k_lm_topk writes the partials)
 };
 
 // ---- launchers (gemm.hip) -------------------------------------------------
@@ -198,6 +199,19 @@ void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, cons
 void launch_verify_tree(int B, int nodes, int V, const float *tl, const int32_t *tokens,
                         const int32_t *parent, int32_t *n_acc, int32_t *path, int32_t *next,
                         void *stats, hipStream_t s);
+// top-k partials from stored logits [R, ld] (rows whose LM head skips its
+// epilogue): n_wg = lm_topk_chunks(V) chunks per row, topk <= TK_MAXK, in the
+// layout of the LM-head partials
+constexpr int TK_MAXK = 16;
+struct LmTopkArgs {
+  const float *logits; long ld;
+  int R, V, topk, n_wg;
+  float inv_temp;
+  float *pmax, *psum, *pval;
+  int *pid;
+};
+int lm_topk_chunks(int V);
+void launch_lm_topk(const LmTopkArgs &a, hipStream_t s);
 // merge LM-head partials: top-k ids, optional log-probs, and the chain's token copies
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,

@@ -410,6 +410,141 @@ void launch_lm_sample(const LmSampleArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_sample, dim3(a.R), dim3(256), 0, s, a);
 }
 
+// Top-k partials from stored fp32 logits, for rows whose LM head skips its
+// own epilogue: workgroup (chunk c, row r) reduces the ids [c * TK_CHUNK,
+// (c + 1) * TK_CHUNK) of row r to the partials the LM-head epilogue writes
+// (max, sum of exp(logit - max), and the top-k sorted best first), so the
+// merge kernel takes them unchanged.  Thread t holds ids t, t + 256, ...
+// (coalesced loads).
+//
+// The top-k is exact but filters first, because the arithmetic of k full
+// arg-max rounds over every candidate bounds this kernel: each wave finds a
+// threshold T_w, the k-th largest of its 64 lane maxima (k rounds over one
+// float per lane; lanes that tie are removed together, so at least k lane
+// maxima are >= T_w, and so are the wave's k best).  The workgroup keeps
+// only the candidates >= max_w T_w (typically about k of them) in LDS, and
+// each candidate's place is the number of better ones.  A chunk with fewer
+// than k or more than TK_CAP such candidates (ties, NaN) takes the plain
+// path instead: per-thread sorted keys, k rounds of wave arg-max, and wave 0
+// merging the four wave lists the same way.
+constexpr int TK_PER = 16;
+constexpr int TK_CHUNK = 256 * TK_PER;
+constexpr int TK_CAP = 256;
+__global__ __launch_bounds__(256) void k_lm_topk(LmTopkArgs a) {
+  __shared__ float sh[8];
+  __shared__ float s_thr[4];
+  __shared__ int s_n;
+  __shared__ uint64_t s_cand[TK_CAP];
+  __shared__ uint64_t wl[4][TK_MAXK];
+  const int c = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int base = c * TK_CHUNK;
+  const float *row = a.logits + (size_t)r * a.ld;
+  const int k = a.topk;
+  float v[TK_PER];
+#pragma unroll
+  for (int j = 0; j < TK_PER; ++j) {
+    const int id = base + tid + 256 * j;
+    v[j] = id < a.V ? row[id] : -INFINITY;
+  }
+  if (tid == 0) s_n = 0;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < TK_PER; ++j) mx = fmaxf(mx, v[j]);
+  const float M = block_max(mx, sh);
+  float e = 0.f;
+#pragma unroll
+  for (int j = 0; j < TK_PER; ++j)
+    e += base + tid + 256 * j < a.V ? expf(v[j] * a.inv_temp - M * a.inv_temp) : 0.f;
+  const float S = block_sum(e, sh);
+  const size_t pi = (size_t)r * a.n_wg + c;
+  if (tid == 0) {
+    a.pmax[pi] = M * a.inv_temp;
+    a.psum[pi] = S;
+  }
+  // the wave's threshold: k-th largest lane maximum (ties removed together)
+  float cur = mx, thr = -INFINITY;
+  int removed = 0;
+  for (int j = 0; j < k && removed < k; ++j) {
+    thr = wave_max(cur);
+    const bool hit = cur == thr;
+    removed += __popcll(__ballot(hit));
+    cur = hit ? -INFINITY : cur;
+  }
+  if (lane == 0) s_thr[wave] = thr;
+  __syncthreads();
+  const float T = fmaxf(fmaxf(s_thr[0], s_thr[1]), fmaxf(s_thr[2], s_thr[3]));
+#pragma unroll
+  for (int j = 0; j < TK_PER; ++j) {
+    const int id = base + tid + 256 * j;
+    if (id < a.V && v[j] >= T) {
+      const int slot = atomicAdd(&s_n, 1);
+      if (slot < TK_CAP) s_cand[slot] = cand_key(v[j], id);
+    }
+  }
+  __syncthreads();
+  const int n = s_n;
+  if (n >= k && n <= TK_CAP) {   // uniform
+    if (tid < n) {
+      const uint64_t mine = s_cand[tid];
+      int rank = 0;
+      for (int i = 0; i < n; ++i) rank += s_cand[i] > mine ? 1 : 0;
+      if (rank < k) {
+        a.pval[pi * k + rank] = key_value(mine);
+        a.pid[pi * k + rank] = key_id(mine);
+      }
+    }
+    return;
+  }
+  // plain path
+  uint64_t key[TK_PER];
+#pragma unroll
+  for (int j = 0; j < TK_PER; ++j) {
+    const int id = base + tid + 256 * j;
+    key[j] = cand_key(v[j], id < a.V ? id : 0x7fffffff);
+  }
+  // odd-even transposition sort, best first
+#pragma unroll
+  for (int pass = 0; pass < TK_PER; ++pass)
+#pragma unroll
+    for (int j = pass & 1; j + 1 < TK_PER; j += 2) {
+      const uint64_t lo = key[j], hi = key[j + 1];
+      key[j] = hi > lo ? hi : lo;
+      key[j + 1] = hi > lo ? lo : hi;
+    }
+  const uint64_t none = cand_key(-INFINITY, 0x7fffffff);
+  for (int j = 0; j < k; ++j) {
+    uint64_t bk[1] = {key[0]};
+    wave_max_key_n<1>(bk);
+    if (lane == 0) wl[wave][j] = bk[0];
+    // the winning lane drops its head (ids are distinct; "none" keys are
+    // only ever dropped for one another)
+    const bool win = key[0] == bk[0];
+#pragma unroll
+    for (int q = 0; q + 1 < TK_PER; ++q) key[q] = win ? key[q + 1] : key[q];
+    key[TK_PER - 1] = win ? none : key[TK_PER - 1];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  // lane l holds candidate l % k of wave l / k (4 k <= 64)
+  uint64_t ck = lane < 4 * k ? wl[lane / k][lane % k] : none;
+  for (int j = 0; j < k; ++j) {
+    uint64_t bk[1] = {ck};
+    wave_max_key_n<1>(bk);
+    if (lane == 0) {
+      a.pval[pi * k + j] = key_value(bk[0]);
+      a.pid[pi * k + j] = key_id(bk[0]);
+    }
+    ck = ck == bk[0] ? none : ck;
+  }
+}
+
+int lm_topk_chunks(int V) { return (V + TK_CHUNK - 1) / TK_CHUNK; }
+
+void launch_lm_topk(const LmTopkArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(k_lm_topk, dim3(a.n_wg, a.R), dim3(256), 0, s, a);
+}
+
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
                        int *tok_b, int ld_b, hipStream_t s) {

@@ -665,10 +665,29 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
     lmg.ld_logits = c->V;
   }
   lmg.pmax = c->lm_max; lmg.psum = c->lm_sum; lmg.pval = c->lm_val; lmg.pid = c->lm_id;
+  // top-k > 1 on MFMA tiles (tree levels): the LM head stores the logits
+  // and a separate pass reduces them to the partials
+  const bool topk_pass = !p.u && !lmg.gemv && p.topk > 1 && p.topk <= TK_MAXK;
+  if (topk_pass) {
+    if (!lmg.logits) {
+      lmg.logits = c->samp_logits;
+      lmg.ld_logits = c->V;
+    }
+    lmg.no_part = 1;
+  }
   const bool prof = c->profile && c->prof_used * 2 + 1 < (int)c->prof_ev.size();
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
   launch_lmhead(bf, lmg, s);
   if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used++ + 1], s);
+  if (topk_pass) {
+    LmTopkArgs ta{};
+    ta.logits = lmg.logits; ta.ld = lmg.ld_logits;
+    ta.R = R; ta.V = c->V; ta.topk = p.topk; ta.n_wg = lm_topk_chunks(c->V);
+    ta.inv_temp = 1.f;
+    ta.pmax = c->lm_max; ta.psum = c->lm_sum; ta.pval = c->lm_val; ta.pid = c->lm_id;
+    launch_lm_topk(ta, s);
+    lmg.n_wg = ta.n_wg;
+  }
   c->lm_nwg_last = lmg.n_wg;
   if (p.u) {
     LmSampleArgs sa{};

@@ -195,6 +195,47 @@ def test_step_api_matches_chain_first_step():
     dr.close()
 
 
+@pytest.mark.parametrize("lm", ["random", "zero", "pairs"])
+def test_step_topk_matches_its_logits(lm):
+    """Top-k > 1 on batched rows: the LM head stores the logits and a separate
+    pass reduces them to the top-k partials.  Its filtered path (random
+    logits, and exact ties between id pairs) and its plain path (every logit
+    0) must give the exact top-k of the logits the same call returns, ordered
+    by (value desc, id asc), with log-probabilities logit - logsumexp."""
+    from synth import make_inputs, make_weights
+    from paper_2602_01762_amd import Drafter
+    cfg = SMALL_BF16_CHAIN.with_(tree_width=4, tree_nodes=12)
+    w = make_weights(cfg, "cuda")
+    if lm == "zero":
+        w.lm_head.zero_()
+    elif lm == "pairs":
+        w.lm_head[1::2] = w.lm_head[0::2]
+    inp = make_inputs(cfg, "cuda")
+    dr = Drafter(cfg)
+    dr.load(w)
+    B, k = cfg.batch, 4
+    dev = inp.tokens.device
+    rows = {"tokens": inp.tokens, "feat": inp.features,
+            "seq": torch.arange(B, dtype=torch.int32, device=dev),
+            "pos": inp.ctx_lens.clone(), "slot": inp.ctx_lens.clone()}
+    st = dr.step(1, inp, rows, topk=k, logits=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    lg = st["logits"].cpu().numpy().astype(np.float64)
+    ids = st["ids"].cpu().numpy()
+    logp = st["logp"].cpu().numpy()
+    V = lg.shape[1]
+    for r in range(B):
+        order = np.lexsort((np.arange(V), -lg[r]))[:k]
+        assert ids[r].tolist() == order.tolist(), (lm, r)
+        m = lg[r].max()
+        lse = m + np.log(np.exp(lg[r] - m).sum())
+        np.testing.assert_allclose(logp[r], lg[r, order] - lse, atol=1e-4, rtol=0)
+    if lm == "zero":
+        assert (ids == np.arange(k)).all()
+    dr.close()
+
+
 def run_tree_parity(cfg, seqs=None):
     log("tree parity", cfg.name)
     dr, w, inp = gpu_setup(cfg)
