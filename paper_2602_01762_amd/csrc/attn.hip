@@ -361,17 +361,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < ATT_MAXDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // this lane's slot of a step: row `col` of the wave's 16-slot tile
-  long off = slot_off(tbeg + 16 * wave + col);
-  u32x4 ka[ATT_MAXDK], va[ATT_MAXDK];
-  load_kv(off, ka, va);
-  for (int sub = 0; sub < a.nsub; ++sub) {
-    const int t0 = tbeg + sub * ATT_S;
-    if (t0 >= tend) break;                    // uniform
-    // next step's rows, in flight while this step computes
-    const long off_n = sub + 1 < a.nsub ? slot_off(t0 + ATT_S + 16 * wave + col) : -1;
-    u32x4 kn[ATT_MAXDK], vn[ATT_MAXDK];
-    load_kv(off_n, kn, vn);
+  // One 64-slot step of the wave's 16 slots t0 + 16 wave + [0, 16): lane
+  // (col, q4) holds the K/V rows of slot col (offset off, -1 = invisible).
+  auto step = [&](long off, const u32x4 (&ka)[ATT_MAXDK], const u32x4 (&va)[ATT_MAXDK]) {
     // scores S[slot 4 q4 + i][head col]
     f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -381,25 +373,24 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ka[kk]),
                                                     __builtin_bit_cast(bf16x8, ql[kk]), sc, 0, 0, 0);
     }
-    const int vis = off >= 0 ? 1 : 0;
+    const bool vis = off >= 0;
+    // visibility of every slot of the tile (bit s: lane s, i.e. slot s, q4 = 0)
+    const uint64_t vmask = __ballot(vis);
     float sv[4] = {sc.x, sc.y, sc.z, sc.w};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int vi = __shfl(vis, 4 * q4 + i, 64);
-      sv[i] = vi ? sv[i] * a.scale : -INFINITY;
-    }
+    for (int i = 0; i < 4; ++i) sv[i] = (vmask >> (4 * q4 + i)) & 1ull ? sv[i] * a.scale : -INFINITY;
     // online softmax of head col over these 16 slots (lanes col, col^16, ...)
     float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = fmaxf(mx, xor16_f(mx));
+    mx = fmaxf(mx, xor32_f(mx));
     const float mn = fmaxf(m_run, mx);
     const float al = m_run == -INFINITY ? 0.f : expf(m_run - mn);
     float p[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) p[i] = sv[i] == -INFINITY ? 0.f : expf(sv[i] - mn);
     float ps = (p[0] + p[1]) + (p[2] + p[3]);
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
+    ps += xor16_f(ps);
+    ps += xor32_f(ps);
     l_run = l_run * al + ps;
     m_run = mn;
     // V tile -> LDS as [dim][slot] (zero rows for invisible slots)
@@ -414,10 +405,19 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       }
     }
     wave_lds_sync();
-    // rescale O rows (heads 4 q4 + i) by their alpha, then O += P V
-    float ah[4];
+    // rescale O rows (heads 4 q4 + i) by their alpha, which is exactly 1
+    // for every head once its running max stops moving (most steps of a
+    // long context): the wave then skips the broadcasts and multiplies
+    if (__ballot(al != 1.f)) {
+      float ah[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ah[i] = __shfl(al, 4 * q4 + i, 64);
+      for (int i = 0; i < 4; ++i) ah[i] = __shfl(al, 4 * q4 + i, 64);
+#pragma unroll
+      for (int dt = 0; dt < ATT_MAXDT; ++dt) {
+        o[dt].x *= ah[0]; o[dt].y *= ah[1]; o[dt].z *= ah[2]; o[dt].w *= ah[3];
+      }
+    }
+    // O += P V
     float ph[4], pl[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -428,18 +428,28 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     const s16x4 pal = __builtin_bit_cast(s16x4, uint2{pack2(pl[0], pl[1]), pack2(pl[2], pl[3])});
 #pragma unroll
     for (int dt = 0; dt < ATT_MAXDT; ++dt) {
-      o[dt].x *= ah[0]; o[dt].y *= ah[1]; o[dt].z *= ah[2]; o[dt].w *= ah[3];
       const s16x4 vb = *(const s16x4 *)&vt[wave][16 * dt + col][4 * q4];
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pah, vb, o[dt], 0, 0, 0);
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pal, vb, o[dt], 0, 0, 0);
     }
     wave_lds_sync();                          // reads done before the next step's writes
-    off = off_n;
-#pragma unroll
-    for (int kk = 0; kk < ATT_MAXDK; ++kk) {
-      ka[kk] = kn[kk];
-      va[kk] = vn[kk];
-    }
+  };
+  // Steps in pairs over two register sets: each step's successor is already
+  // in flight while it computes, with no copies between the sets.
+  const int slot0 = tbeg + 16 * wave + col;  // this lane's slot in the first step
+  long off0 = slot_off(slot0), off1 = -1;
+  u32x4 k0[ATT_MAXDK], v0[ATT_MAXDK], k1[ATT_MAXDK], v1[ATT_MAXDK];
+  load_kv(off0, k0, v0);
+  for (int sub = 0; sub < a.nsub; sub += 2) {
+    const int t0 = tbeg + sub * ATT_S;
+    if (t0 >= tend) break;                    // uniform
+    off1 = sub + 1 < a.nsub ? slot_off(slot0 + (sub + 1) * ATT_S) : -1;
+    load_kv(off1, k1, v1);
+    step(off0, k0, v0);
+    if (sub + 1 >= a.nsub || t0 + ATT_S >= tend) break;   // uniform
+    off0 = sub + 2 < a.nsub ? slot_off(slot0 + (sub + 2) * ATT_S) : -1;
+    load_kv(off0, k0, v0);
+    step(off1, k1, v1);
   }
   // merge the 4 waves' states and write this chunk's partials
   if (q4 == 0) {

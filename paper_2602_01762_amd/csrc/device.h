@@ -85,6 +85,20 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_f32<DPP_ROW_MIRROR>(v);
   return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
 }
+// Value of lane l ^ 32 / l ^ 16 by the gfx950 permlane swaps (VALU, no LDS).
+// permlane32_swap(v, v) returns {v of lanes 0-31 in both halves, v of lanes
+// 32-63 in both halves}; permlane16_swap(v, v) does the same for the even
+// and odd rows of 16 within each half.
+__device__ __forceinline__ float xor32_f(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+__device__ __forceinline__ float xor16_f(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  return __uint_as_float((threadIdx.x & 16) ? r[0] : r[1]);
+}
 // larger value wins; equal values: lower id wins
 __device__ __forceinline__ bool better(float v, int id, float ov, int oid) {
   // bitwise, not short-circuit: lane masks combine without exec-mask branches
