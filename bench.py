@@ -88,14 +88,25 @@ def lm_workgroups(cfg, rows):
     return (tiles // nt + 3) // 4
 
 
+def lm_topk_pass(cfg, rows):
+    """Whether the LM head stores fp32 logits and a separate pass reduces them
+    to the top-k partials (the library's rule: greedy top-k > 1 on the MFMA
+    tiles, i.e. more than one row or fp32 weights)."""
+    gemv = rows == 1 and cfg.dtype == "bf16"
+    return max(1, cfg.tree_width) > 1 and not gemv and not cfg.temperature
+
+
 def lm_head_bytes(cfg, rows):
     """Algorithmic HBM bytes of one LM-head launch: the [V, H] weight stream,
-    the normalised input rows (a hi/lo pair of bf16 planes, or fp32), and the
-    per-workgroup partials (max, sum and k values and ids per row)."""
+    the normalised input rows (a hi/lo pair of bf16 planes, or fp32), and
+    either the per-workgroup partials (max, sum and k values and ids per row)
+    or, when a separate pass takes the top-k, the fp32 logits rows."""
     es = 2 if cfg.dtype == "bf16" else 4
     k = max(1, cfg.tree_width)
-    return (cfg.vocab * cfg.hidden * es + rows * cfg.hidden * 4
-            + rows * lm_workgroups(cfg, rows) * (2 + 2 * k) * 4)
+    base = cfg.vocab * cfg.hidden * es + rows * cfg.hidden * 4
+    if lm_topk_pass(cfg, rows):
+        return base + rows * cfg.vocab * 4
+    return base + rows * lm_workgroups(cfg, rows) * (2 + 2 * k) * 4
 
 
 def step_weight_bytes(cfg, s):
@@ -234,6 +245,20 @@ def main():
     value = drafted * args.steps / (total_ms / 1e3)
     assert dr.device_status() == 0
 
+    # per-call distribution: a second pass of the same number of calls, each
+    # between its own pair of events (kept out of the timed region above)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a0, a1 in ev:
+        a0.record()
+        call()
+        a1.record()
+    torch.cuda.synchronize()
+    per_call = np.array([a0.elapsed_time(a1) for a0, a1 in ev])
+    call_ms = {"median": round(float(np.median(per_call)), 4),
+               "p10": round(float(np.percentile(per_call, 10)), 4),
+               "p90": round(float(np.percentile(per_call, 90)), 4)}
+
     # dominant kernel: HIP events around every LM-head launch (same kernels,
     # launched directly on the stream so the events bracket each launch)
     binding.prism_profile_enable(dr.ctx, True)
@@ -250,7 +275,10 @@ def main():
     lm_us = lm_ms * 1e3 / max(lm_n, 1)
     lm_b = lm_head_bytes(cfg, rows)
     achieved = lm_b / (lm_us * 1e-6) / 1e9
-    roofline = {"kernel": "k_lmhead (LM head GEMV + fused top-k partials)", "bound": "hbm",
+    kname = ("k_lmhead (LM head, fp32 logits stored; top-k by k_lm_topk)" if lm_topk_pass(cfg, rows)
+             else "k_lmhead (LM head GEMV + fused top-k partials)" if rows == 1 and cfg.dtype == "bf16"
+             else "k_lmhead (LM head MFMA tiles + fused top-k partials)")
+    roofline = {"kernel": kname, "bound": "hbm",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                 "avg_launch_us": round(lm_us, 2), "launches_timed": lm_n,
@@ -268,6 +296,7 @@ def main():
                    "accepted_tokens_step1": list(cfg.n_new) if cfg.n_new else 1,
                    "temperature": cfg.temperature or 0.0},
         "per_draft_step_us": round(ms_per_step * 1e3 / K, 2),
+        "call_ms": call_ms,
         "weight_bytes_per_step_call": chain_bytes,
         "whole_call_hbm_frac_weights_only": round(chain_bytes / (ms_per_step * 1e-3) / 1e9
                                                   / HBM_PEAK_GBS, 4),

@@ -24,6 +24,11 @@ def test_lm_workgroups_follow_the_launch_plan():
 def test_lm_head_bytes():
     # weights + the row's hi/lo planes + (max, sum, value, id) per workgroup
     assert bench.lm_head_bytes(L3_8B_BS1, 1) == 128256 * 4096 * 2 + 4096 * 4 + 501 * 16
+    # top-1 on 16 rows: partials of 251 workgroups
+    assert bench.lm_head_bytes(L3_8B_BS16, 16) == 128256 * 4096 * 2 + 16 * 4096 * 4 + 16 * 251 * 16
+    # tree levels (top-8 on 32 rows): the launch stores the fp32 logits rows
+    assert bench.lm_topk_pass(L3_8B_TREE, 32) and not bench.lm_topk_pass(L3_8B_BS16, 16)
+    assert bench.lm_head_bytes(L3_8B_TREE, 32) == 128256 * 4096 * 2 + 32 * 4096 * 4 + 32 * 128256 * 4
 
 
 def _digest_with(edit):
