@@ -442,7 +442,8 @@ __device__ __forceinline__ void finish_scales(const RowNorm &nm, int nr, const S
 // lanes 0..15); the caller stores it.
 template <typename T, int EPI>
 __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
-                                               float scale, long cbase, int rpos) {
+                                               float scale, long cbase, int rpos,
+                                               const float *trow = nullptr) {
   const int lane = threadIdx.x & 63, q4 = lane >> 4;
   const int n0 = tile * 16 + 4 * q4;
   const bool live = r < g.R;
@@ -453,6 +454,10 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
       if (g.res) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
+      }
+      if (trow) {
+        const f32x4 t4 = *(const f32x4 *)(trow + n0);
+        v[0] += t4.x; v[1] += t4.y; v[2] += t4.z; v[3] += t4.w;
       }
       *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
 #pragma unroll
@@ -584,13 +589,26 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
       if (wave == 0 && r < g.R) cbase[rt] = cache_base(g, r, rpos[rt]);
     }
   }
+  // fusion FC with the embedding table: wave 0 resolves the rows' tokens
+  // itself (no wave's K range covers the embedding), the previous LM head's
+  // partials requested ahead of its weights
+  constexpr int TPRE = VR == 1 ? 8 : 2;
+  constexpr int TR = VR > 0 ? VR : 1;
+  const bool tab = GX && g.tab != nullptr;
+  TokLoads<TPRE> tl[TR];
+  if (GX && tab && wave == 0 && g.gx.lm.pval) {
+#pragma unroll
+    for (int r = 0; r < TR; ++r)
+      if (r < g.R) tl[r] = issue_tok<TPRE>(g.gx.lm, r);
+  }
   f32x4 acc[NT][RT];
 #pragma unroll
   for (int n = 0; n < NT; ++n)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int kb0 = (int)((long)wave * m.nkb / kw);
-  const int kb1 = (int)((long)(wave + 1) * m.nkb / kw);
+  const int nk = m.nkb - g.kb_lo;
+  const int kb0 = g.kb_lo + (int)((long)wave * nk / kw);
+  const int kb1 = g.kb_lo + (int)((long)(wave + 1) * nk / kw);
   if constexpr (VR > 0) {
     float *xs = (float *)&red[(kw - 1) * NT * RT * 64] + 64 * kw;
     mainloop_valu<VR, GX>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0,
@@ -614,6 +632,23 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     __syncthreads();
   }
   if (wave != 0) return;
+  const float *trow[TR];
+#pragma unroll
+  for (int r = 0; r < TR; ++r) trow[r] = nullptr;
+  if (GX && tab) {
+    const bool lead = blockIdx.x == 0 && lane == 0;
+#pragma unroll
+    for (int r = 0; r < TR; ++r) {
+      if (r >= g.R) continue;
+      int t = g.gx.lm.pval ? finish_tok(g.gx.lm, r, tl[r]) : g.gx.in.tokens[r];
+      if (lead && g.gx.lm.pval && g.gx.lm.rec) g.gx.lm.rec[(size_t)r * g.gx.lm.ld_rec] = t;
+      if (t < 0 || t >= g.gx.V) {
+        if (lead) atomicOr(g.err, ERRF_TOKEN);
+      } else {
+        trow[r] = g.tab + (size_t)t * m.N;
+      }
+    }
+  }
   for (int j = 1; j < kw; ++j)
 #pragma unroll
     for (int n = 0; n < NT; ++n)
@@ -626,7 +661,10 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     for (int rt = 0; rt < RT; ++rt) {
       const int r = (lane & 15) + 16 * rt;
       const float sc = has_norm && r < g.R ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
-      const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt]);
+      const float *tr = nullptr;
+#pragma unroll
+      for (int q = 0; q < TR; ++q) tr = r == q ? trow[q] : tr;
+      const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt], tr);
       if (EPI == EPI_NORM && r < g.R && lane < 16) g.ss[(size_t)(t0 + n) * g.R + r] = ss;
     }
 }
@@ -1015,6 +1053,49 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
   if (bf16) lm_rt<bf16_t, true>(g, s);
   else lm_rt<float, false>(g, s);
+}
+
+// Embedding half of a fusion FC for every token: T[v][n] = sum_{k < H}
+// W[n][k] E[v][k].  Wave w of workgroup (x, y) takes feature tile 4 x + w
+// against vocab rows 64 y .. 64 y + 63: W's tiled blocks are the A operand
+// as stored, E's rows the B operand, fp32 accumulation.  Runs at load time.
+__global__ __launch_bounds__(256) void k_embed_table(const u32x4 *__restrict__ w, int nkb_w,
+                                                     int kb_n, const bf16_t *__restrict__ E, int V,
+                                                     int H, int N, float *__restrict__ T) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, q4 = lane >> 4;
+  const int tile = blockIdx.x * 4 + wave;
+  const int v0 = blockIdx.y * 64;
+  const u32x4 *wp = w + (size_t)tile * nkb_w * 64 + lane;
+  const bf16_t *er[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int v = min(v0 + 16 * j + col, V - 1);
+    er[j] = E + (size_t)v * H + 8 * q4;
+  }
+  f32x4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int kb = 0; kb < kb_n; ++kb) {
+    const u32x4 a = wp[(size_t)kb * 64];
+    u32x4 b[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = *(const u32x4 *)(er[j] + (size_t)kb * 32);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = Ty<bf16_t>::mma(a, b[j], acc[j]);
+  }
+  // lane (col, q4) holds features 16 tile + 4 q4 + i of vocab row col
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int v = v0 + 16 * j + col;
+    if (v < V) *(f32x4 *)(T + (size_t)v * N + 16 * tile + 4 * q4) = acc[j];
+  }
+}
+
+void launch_embed_table(const TiledMat &w, const void *embed, int V, int H, float *T, hipStream_t s) {
+  const dim3 grid(w.N / 64, (V + 63) / 64);
+  hipLaunchKernelGGL(k_embed_table, grid, dim3(256), 0, s, (const u32x4 *)w.w, w.nkb, H / 32,
+                     (const bf16_t *)embed, V, H, w.N, T);
 }
 
 // Repack a row-major [n_src_rows, K] matrix into the tiled layout: source row

@@ -129,6 +129,11 @@ struct GemmLaunch {
   const double *inv_freq;
   uint32_t *err;
   Gather gx;       // GEMV fusion FC: rows gathered from E and the features
+  // GEMV fusion FC with the embedding table: the product covers k-blocks
+  // [kb_lo, nkb) (the feature columns), and EPI_NORM adds tab[token][n], the
+  // embedding half W_fc[:, :H] E[token] precomputed for every token
+  const float *tab;
+  int kb_lo;
 };
 
 struct LmLaunch {
@@ -199,6 +204,10 @@ void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, cons
 void launch_verify_tree(int B, int nodes, int V, const float *tl, const int32_t *tokens,
                         const int32_t *parent, int32_t *n_acc, int32_t *path, int32_t *next,
                         void *stats, hipStream_t s);
+// T[v][n] = sum_{k < H} W[n][k] E[v][k] for every token v: the embedding
+// half of a fusion FC in the tiled layout (k-blocks [0, H / 32) of each tile)
+// times the embedding rows, fp32 [V, N]; N a multiple of 64
+void launch_embed_table(const TiledMat &w, const void *embed, int V, int H, float *T, hipStream_t s);
 // top-k partials from stored logits [R, ld] (rows whose LM head skips its
 // epilogue): n_wg = lm_topk_chunks(V) chunks per row, topk <= TK_MAXK, in the
 // layout of the LM-head partials

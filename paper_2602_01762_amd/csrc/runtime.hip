@@ -24,6 +24,10 @@ struct Set {
   TiledMat fc, qkv, o, gu, down;
   void *g1 = nullptr, *g2 = nullptr;
   void *arena = nullptr;
+  // embedding half of the fusion FC for every token, W_fc[:, :H] E[v]
+  // (fp32 [V, H]); valid once both this set and the shared tensors are loaded
+  float *tab = nullptr;
+  bool tab_ready = false;
 };
 
 struct Plan {
@@ -57,6 +61,9 @@ struct prism_ctx {
   int H = 0, nq = 0, nkv = 0, d = 0, I = 0, V = 0, QKV = 0;
   int rows_max = 0, max_slots = 0, nch = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
   int feat_max = 0;
+  // one- and two-row passes take the fusion FC's embedding half from a
+  // per-set table (contexts of at most GEMV_MAX_ROWS sequences, bf16)
+  bool use_tab = false;
 
   void *embed = nullptr, *gf = nullptr, *shared_arena = nullptr;
   TiledMat lm;
@@ -260,6 +267,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->kmax = w > 1 ? w : 1;
   c->Cmax = Cmax;
   c->feat_max = k.feat_width > k.hidden ? k.feat_width : k.hidden;
+  c->use_tab = bf16 && k.max_batch <= GEMV_MAX_ROWS && k.hidden % 64 == 0;
   c->sets.resize(k.n_sets);
   c->fmap.resize(k.max_steps);
   for (int i = 0; i < k.max_steps; ++i) c->fmap[i] = i < k.n_sets ? i : k.n_sets - 1;
@@ -415,6 +423,12 @@ prism_status prism_draft_load_shared(prism_ctx *c, const void *d_embed, const vo
   launch_repack(c->bf16, d_lm_head, c->V, c->H, 1, 0, 0, c->d, c->lm, s);
   HIPCHK(c, hipGetLastError());
   HIPCHK(c, hipMemcpyAsync(c->gf, d_final_norm, (size_t)c->H * c->esz, hipMemcpyDeviceToDevice, s));
+  for (auto &S : c->sets) {   // embedding tables of the sets already loaded
+    if (!S.tab || !S.loaded) continue;
+    launch_embed_table(S.fc, c->embed, c->V, c->H, S.tab, s);
+    HIPCHK(c, hipGetLastError());
+    S.tab_ready = true;
+  }
   HIPCHK(c, hipStreamSynchronize(s));
   c->shared_loaded = true;
   return PRISM_OK;
@@ -450,8 +464,10 @@ prism_status prism_draft_load_params(prism_ctx *c, int32_t set, const prism_para
     S.gu = make_tiled(2 * c->I, H, c->bf16);
     S.down = make_tiled(H, c->I, c->bf16);
     const size_t gb = (size_t)H * c->esz;
+    const size_t tb = c->use_tab ? (size_t)c->V * H * 4 : 0;
     const size_t bytes = tiled_bytes(S.fc) + tiled_bytes(S.qkv) + tiled_bytes(S.o) +
-                         tiled_bytes(S.gu) + tiled_bytes(S.down) + 2 * ((gb + 255) & ~(size_t)255) + 6 * 256;
+                         tiled_bytes(S.gu) + tiled_bytes(S.down) + 2 * ((gb + 255) & ~(size_t)255) +
+                         tb + 7 * 256;
     if (hipMalloc(&S.arena, bytes) != hipSuccess)
       return fail(c, PRISM_ERR_OUT_OF_MEMORY, "arena of set %d (%zu bytes)", set, bytes);
     char *p = (char *)S.arena;
@@ -462,9 +478,11 @@ prism_status prism_draft_load_params(prism_ctx *c, int32_t set, const prism_para
     carve(p, &S.down.w, tiled_bytes(S.down));
     carve(p, &S.g1, gb);
     carve(p, &S.g2, gb);
+    if (tb) carve(p, (void **)&S.tab, tb);
     S.F = F;
   }
   S.loaded = false;
+  S.tab_ready = false;
   launch_repack(c->bf16, P->d_w_fc, H, H + F, 1, 0, 0, c->d, S.fc, s);
   // q, k, v rows stacked into one product; q and k heads pair-permuted for RoPE
   TiledMat qv = S.qkv;
@@ -480,8 +498,13 @@ prism_status prism_draft_load_params(prism_ctx *c, int32_t set, const prism_para
   HIPCHK(c, hipGetLastError());
   HIPCHK(c, hipMemcpyAsync(S.g1, P->d_g1, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
   HIPCHK(c, hipMemcpyAsync(S.g2, P->d_g2, (size_t)H * c->esz, hipMemcpyDeviceToDevice, s));
+  if (S.tab && c->shared_loaded) {
+    launch_embed_table(S.fc, c->embed, c->V, H, S.tab, s);
+    HIPCHK(c, hipGetLastError());
+  }
   HIPCHK(c, hipStreamSynchronize(s));
   S.loaded = true;
+  S.tab_ready = S.tab && c->shared_loaded;
   return PRISM_OK;
 }
 
@@ -591,6 +614,10 @@ static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStre
   if (g.gemv) {   // the GEMV stages [E(x) ; f] itself
     g.gx.embed = c->embed; g.gx.V = c->V; g.gx.H = H; g.gx.in = p.in; g.gx.lm = p.lm_in;
     g.err = c->err;
+    if (S.tab_ready) {   // or only f, the embedding half coming from the table
+      g.tab = S.tab;
+      g.kb_lo = H / (bf ? 32 : 16);
+    }
   } else {
     launch_fc_prep(bf, R, p.in, p.lm_in, c->embed, c->V, H, p.F, X, c->err, s);
   }
