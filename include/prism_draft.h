@@ -194,7 +194,9 @@ const char *prism_last_error(const prism_ctx *ctx);
 /* Load the frozen shared tensors (paper Table 2: E and LM_head are frozen
  * and shared by every module) and the final RMSNorm gain:
  * d_embed [V, H], d_lm_head [V, H], d_final_norm [H], all in the context
- * dtype.  Copies and repacks them; synchronizes `stream` before returning. */
+ * dtype.  Copies and repacks them; synchronizes `stream` before returning.
+ * Rebuilds the embedding tables of the sets already loaded (see
+ * prism_draft_load_params). */
 prism_status prism_draft_load_shared(prism_ctx *ctx, const void *d_embed,
                                      const void *d_lm_head,
                                      const void *d_final_norm, void *stream);
@@ -202,7 +204,12 @@ prism_status prism_draft_load_shared(prism_ctx *ctx, const void *d_embed,
 /* Load parameter set `set` (0..M-1), the weights of processing module
  * set+1 (paper Sec. 3.2: M modules, each a fusion FC and a transformer
  * layer).  Copies and repacks into the step-indexed arena; synchronizes
- * `stream`.  Allocates that set's arena slot on first use. */
+ * `stream`.  Allocates that set's arena slot on first use.  In bf16
+ * contexts of at most two sequences (max_batch <= 2) the slot also holds
+ * the set's embedding table, W_fc[:, :H] E[v] for every token v in fp32
+ * (V * H * 4 bytes, 2.1 GB at V = 128256, H = 4096), which one- and two-row
+ * passes read instead of the FC's embedding columns; it is built here once
+ * the shared tensors are loaded. */
 prism_status prism_draft_load_params(prism_ctx *ctx, int32_t set,
                                      const prism_param_set *params,
                                      void *stream);

@@ -31,6 +31,17 @@ def test_lm_head_bytes():
     assert bench.lm_head_bytes(L3_8B_TREE, 32) == 128256 * 4096 * 2 + 32 * 4096 * 4 + 32 * 128256 * 4
 
 
+def test_streamed_bytes_with_the_embedding_table():
+    # batch 1: the FC streams its feature columns plus one fp32 table row
+    full = bench.step_weight_bytes(L3_8B_BS1, 1)
+    assert bench.uses_embed_table(L3_8B_BS1, 1)
+    assert bench.step_streamed_bytes(L3_8B_BS1, 1, 1) == full - 2 * 4096 * 4096 + 4096 * 4
+    # batch 16 and the catch-up prefill rows keep the whole FC
+    assert not bench.uses_embed_table(L3_8B_BS16, 16)
+    assert bench.step_streamed_bytes(L3_8B_BS16, 1, 16) == bench.step_weight_bytes(L3_8B_BS16, 1)
+    assert not bench.uses_embed_table(L3_8B_BS1, 4)
+
+
 def _digest_with(edit):
     base = os.path.join(ROOT, "paper_2602_01762_amd", "csrc")
 
