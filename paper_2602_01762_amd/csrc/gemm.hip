@@ -664,6 +664,10 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
       const float *tr = nullptr;
 #pragma unroll
       for (int q = 0; q < TR; ++q) tr = r == q ? trow[q] : tr;
+      if (EPI == EPI_NORM && !GX && g.tab && r < g.R) {
+        const int t = g.tab_tok[r];
+        tr = t >= 0 ? g.tab + (size_t)t * m.N : nullptr;
+      }
       const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt], tr);
       if (EPI == EPI_NORM && r < g.R && lane < 16) g.ss[(size_t)(t0 + n) * g.R + r] = ss;
     }
@@ -682,7 +686,8 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
   const int t0 = (blockIdx.x * 4 + wave) * NT;
   if (t0 >= m.n_tiles) return;   // n_tiles is a multiple of NT; no barriers below
   const int S = gridDim.y, sl = blockIdx.y;
-  const int kb0 = (int)((long)sl * m.nkb / S), kb1 = (int)((long)(sl + 1) * m.nkb / S);
+  const int nk = m.nkb - g.kb_lo;
+  const int kb0 = g.kb_lo + (int)((long)sl * nk / S), kb1 = g.kb_lo + (int)((long)(sl + 1) * nk / S);
   f32x4 acc[NT][RT];
 #pragma unroll
   for (int n = 0; n < NT; ++n)
@@ -753,7 +758,12 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   } else if (g.norm.scale && r < g.R) {
     sc = g.norm.scale[r];
   }
-  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos);
+  const float *trow = nullptr;
+  if (EPI == EPI_NORM && g.tab && r < g.R) {
+    const int t = g.tab_tok[r];
+    trow = t >= 0 ? g.tab + (size_t)t * g.m.N : nullptr;
+  }
+  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos, trow);
   if constexpr (EPI == EPI_NORM) {
     if (lane < 16) ssw[wave][lane] = ss;
     __syncthreads();

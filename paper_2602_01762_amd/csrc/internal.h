@@ -134,6 +134,7 @@ struct GemmLaunch {
   // embedding half W_fc[:, :H] E[token] precomputed for every token
   const float *tab;
   int kb_lo;
+  const int32_t *tab_tok;   // batched path: each row's token (-1: none), written by the FC prep
 };
 
 struct LmLaunch {
@@ -171,7 +172,7 @@ void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_st
 
 // ---- launchers (misc.hip) -------------------------------------------------
 void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
-                    int V, int H, int F, ActOut X, uint32_t *err, hipStream_t s);
+                    int V, int H, int F, ActOut X, uint32_t *err, int32_t *tok_out, bool feat_only, hipStream_t s);
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
                       const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
                       ActOut o, uint32_t *err, hipStream_t s);

@@ -18,6 +18,8 @@ struct FcPrepArgs {
   int V, H, F;
   ActOut X;
   uint32_t *err;
+  int32_t *tok_out;   // optional [R]: the row's token, -1 if out of range
+  int feat_only;      // the embedding half comes from a table: write the feature columns only
 };
 
 template <typename T>
@@ -33,11 +35,12 @@ __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
     tok = a.in.tokens[r];
   }
   const int e0 = (blockIdx.x * 256 + threadIdx.x) * 8;   // 8 consecutive columns
-  if (e0 >= a.H + a.F) return;
   if (tok < 0 || tok >= a.V) {
     if (e0 == 0) atomicOr(a.err, ERRF_TOKEN);
     tok = -1;
   }
+  if (a.tok_out && e0 == 0) a.tok_out[r] = tok;
+  if (e0 >= a.H + a.F || (a.feat_only && e0 < a.H)) return;
   const size_t o = (size_t)r * a.X.ld + e0;
   float v[8];
   bool exact;   // value already representable in the storage type
@@ -77,8 +80,9 @@ __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
 }
 
 void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
-                    int V, int H, int F, ActOut X, uint32_t *err, hipStream_t s) {
-  FcPrepArgs a{in, lm, embed, V, H, F, X, err};
+                    int V, int H, int F, ActOut X, uint32_t *err, int32_t *tok_out, bool feat_only,
+                    hipStream_t s) {
+  FcPrepArgs a{in, lm, embed, V, H, F, X, err, tok_out, feat_only ? 1 : 0};
   dim3 grid((H + F + 2047) / 2048, R);
   if (bf16) hipLaunchKernelGGL(k_fc_prep<bf16_t>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(k_fc_prep<float>, grid, dim3(256), 0, s, a);

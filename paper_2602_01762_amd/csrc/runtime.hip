@@ -61,9 +61,9 @@ struct prism_ctx {
   int H = 0, nq = 0, nkv = 0, d = 0, I = 0, V = 0, QKV = 0;
   int rows_max = 0, max_slots = 0, nch = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
   int feat_max = 0;
-  // one- and two-row passes take the fusion FC's embedding half from a
-  // per-set table (contexts of at most GEMV_MAX_ROWS sequences, bf16)
+  // passes take the fusion FC's embedding half from a per-set table (bf16)
   bool use_tab = false;
+  int32_t *tab_tok = nullptr;       // batched FC rows' tokens for the table term [R]
 
   void *embed = nullptr, *gf = nullptr, *shared_arena = nullptr;
   TiledMat lm;
@@ -267,7 +267,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->kmax = w > 1 ? w : 1;
   c->Cmax = Cmax;
   c->feat_max = k.feat_width > k.hidden ? k.feat_width : k.hidden;
-  c->use_tab = bf16 && k.max_batch <= GEMV_MAX_ROWS && k.hidden % 64 == 0;
+  c->use_tab = bf16 && k.hidden % 64 == 0;
   c->sets.resize(k.n_sets);
   c->fmap.resize(k.max_steps);
   for (int i = 0; i < k.max_steps; ++i) c->fmap[i] = i < k.n_sets ? i : k.n_sets - 1;
@@ -332,6 +332,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->ids, R * c->kmax * 4);
   add((void **)&c->logp, R * c->kmax * 4);
   add((void **)&c->tokbuf, R * 4);
+  add((void **)&c->tab_tok, R * 4);
   add((void **)&c->samp_logits, R * c->V * 4);
   {   // verification rows: target and draft rows of a chain, or every node of a tree
     const int chain_rows = k.max_batch * (2 * k.max_steps + 1);
@@ -570,14 +571,21 @@ static bool use_gemv(const prism_ctx *c, int R, int K, int kw) {
   return lds <= c->lds_limit;
 }
 
-static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, int R, int epi) {
+// kb_lo: the product covers k-blocks [kb_lo, nkb) of m (the fusion FC's
+// feature columns when its embedding half comes from the table)
+static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, int R, int epi,
+                          int kb_lo = 0) {
   GemmLaunch g{};
   g.m = m;
   g.x = x;
   g.R = R;
   g.epi = epi;
+  g.kb_lo = kb_lo;
+  TiledMat pm = m;   // the planned range
+  pm.nkb -= kb_lo;
+  pm.K -= kb_lo * (c->bf16 ? 32 : 16);
   if (R > GEMV_MAX_ROWS) {
-    plan_batched(m, R, g.nt, g.split);
+    plan_batched(pm, R, g.nt, g.split);
     g.kw = 1;
     g.part = c->part;
     const int rt = R <= 16 ? 1 : (R <= 32 ? 2 : 4);
@@ -588,12 +596,12 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
       // about 1024 waves in all
       g.split = 0;
       int kw = 1024 / groups;
-      while (kw > 1 && ((kw - 1) * g.nt * rt > 48 || kw > m.nkb / 4)) --kw;
+      while (kw > 1 && ((kw - 1) * g.nt * rt > 48 || kw > pm.nkb / 4)) --kw;
       g.kw = kw < 1 ? 1 : kw;
     }
     return g;
   }
-  Plan pl = plan_for(m, R);
+  Plan pl = plan_for(pm, R);
   g.kw = pl.kw;
   g.nt = pl.nt;
   g.gemv = use_gemv(c, R, m.K, g.kw) ? 1 : 0;
@@ -610,16 +618,18 @@ static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStre
   // fusion FC: u = W_fc [E(x) ; f]  ->  u, (u * g1), sums of squares
   ActOut X = c->xfc;
   X.ld = H + p.F;
-  GemmLaunch g = gemm_of(c, S.fc, act_of(X, H + p.F), R, EPI_NORM);
-  if (g.gemv) {   // the GEMV stages [E(x) ; f] itself
+  // with the set's embedding table the product covers the feature columns
+  // only, and its epilogue adds the table row of each row's token
+  const int kb_lo = S.tab_ready ? H / (bf ? 32 : 16) : 0;
+  GemmLaunch g = gemm_of(c, S.fc, act_of(X, H + p.F), R, EPI_NORM, kb_lo);
+  if (S.tab_ready) g.tab = S.tab;
+  if (g.gemv) {   // the GEMV stages [E(x) ; f] (or f) itself
     g.gx.embed = c->embed; g.gx.V = c->V; g.gx.H = H; g.gx.in = p.in; g.gx.lm = p.lm_in;
     g.err = c->err;
-    if (S.tab_ready) {   // or only f, the embedding half coming from the table
-      g.tab = S.tab;
-      g.kb_lo = H / (bf ? 32 : 16);
-    }
   } else {
-    launch_fc_prep(bf, R, p.in, p.lm_in, c->embed, c->V, H, p.F, X, c->err, s);
+    if (S.tab_ready) g.tab_tok = c->tab_tok;
+    launch_fc_prep(bf, R, p.in, p.lm_in, c->embed, c->V, H, p.F, X, c->err,
+                   S.tab_ready ? c->tab_tok : nullptr, S.tab_ready, s);
   }
   g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
   launch_gemm(bf, g, s);
