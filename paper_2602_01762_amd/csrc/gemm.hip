@@ -256,14 +256,19 @@ __device__ __forceinline__ f32x4 valu_result(float (&acc)[RR]) {
 template <int RR, bool GX>
 __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, const Act &x, int R,
                                               int K, float *xs, int kb0, int kb1, f32x4 &out,
-                                              const Gather &gx, uint32_t *err) {
+                                              const Gather &gx, uint32_t *err,
+                                              const float *tab = nullptr, int N = 0, int t0 = 0,
+                                              f32x4 *tv = nullptr) {
   const int lane = threadIdx.x & 63, kq = lane >> 4;
   const u32x4 z4 = {0, 0, 0, 0};
   const u32x4 *wp = w0 + (size_t)kb0 * 64 + lane;
   // gathered FC rows: a wave whose K range covers embedding columns resolves
   // the rows' tokens itself; the previous LM head's partials are requested
-  // ahead of the weights, so that the argmax does not wait for them
-  const bool need_tok = GX && kb1 > kb0 && kb0 * 32 < gx.H;
+  // ahead of the weights, so that the argmax does not wait for them.  With
+  // the embedding table (tab), wave 0 resolves them for the epilogue and
+  // requests its tile's table values right after its first weight batch.
+  const bool tab_wave = GX && tab != nullptr && (threadIdx.x >> 6) == 0;
+  const bool need_tok = GX && ((kb1 > kb0 && kb0 * 32 < gx.H) || tab_wave);
   const bool from_lm = need_tok && gx.lm.pval;
   constexpr int PRE = RR == 1 ? 8 : 2;   // entries per lane issued early (registers)
   TokLoads<PRE> tl[RR];
@@ -294,6 +299,15 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
       }
       tok[r] = t;
     }
+  }
+  if (tab_wave) {
+    // lane (row, q4) of the epilogue layout: features 16 t0 + 4 q4 .. + 3
+    const int r = lane & 15;
+    int t = -1;
+#pragma unroll
+    for (int q = 0; q < RR; ++q) t = r == q ? tok[q] : t;
+    *tv = r < R && t >= 0 ? *(const f32x4 *)(tab + (size_t)t * N + 16 * t0 + 4 * kq)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
   }
   stage_wave<RR, GX>(x, gx, tok, R, K, xs, kb0 * 32, kb1 * 32);
   wave_lds_sync();
@@ -443,7 +457,7 @@ __device__ __forceinline__ void finish_scales(const RowNorm &nm, int nr, const S
 template <typename T, int EPI>
 __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
                                                float scale, long cbase, int rpos,
-                                               const float *trow = nullptr) {
+                                               f32x4 tadd = f32x4{0.f, 0.f, 0.f, 0.f}) {
   const int lane = threadIdx.x & 63, q4 = lane >> 4;
   const int n0 = tile * 16 + 4 * q4;
   const bool live = r < g.R;
@@ -455,10 +469,8 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
       }
-      if (trow) {
-        const f32x4 t4 = *(const f32x4 *)(trow + n0);
-        v[0] += t4.x; v[1] += t4.y; v[2] += t4.z; v[3] += t4.w;
-      }
+      // embedding-table term of the fusion FC (zero otherwise)
+      v[0] += tadd.x; v[1] += tadd.y; v[2] += tadd.z; v[3] += tadd.w;
       *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -589,19 +601,8 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
       if (wave == 0 && r < g.R) cbase[rt] = cache_base(g, r, rpos[rt]);
     }
   }
-  // fusion FC with the embedding table: wave 0 resolves the rows' tokens
-  // itself (no wave's K range covers the embedding), the previous LM head's
-  // partials requested ahead of its weights
-  constexpr int TPRE = VR == 1 ? 8 : 2;
-  constexpr int TR = VR > 0 ? VR : 1;
-  const bool tab = GX && g.tab != nullptr;
-  TokLoads<TPRE> tl[TR];
-  if (GX && tab && wave == 0 && g.gx.lm.pval) {
-#pragma unroll
-    for (int r = 0; r < TR; ++r)
-      if (r < g.R) tl[r] = issue_tok<TPRE>(g.gx.lm, r);
-  }
   f32x4 acc[NT][RT];
+  f32x4 tv = f32x4{0.f, 0.f, 0.f, 0.f};   // GEMV fusion FC: wave 0's embedding-table values
 #pragma unroll
   for (int n = 0; n < NT; ++n)
 #pragma unroll
@@ -612,7 +613,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   if constexpr (VR > 0) {
     float *xs = (float *)&red[(kw - 1) * NT * RT * 64] + 64 * kw;
     mainloop_valu<VR, GX>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0,
-                          kb1, acc[0][0], g.gx, g.err);
+                          kb1, acc[0][0], g.gx, g.err, g.tab, m.N, t0, &tv);
   } else {
     mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
                               kb1, acc);
@@ -632,23 +633,6 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     __syncthreads();
   }
   if (wave != 0) return;
-  const float *trow[TR];
-#pragma unroll
-  for (int r = 0; r < TR; ++r) trow[r] = nullptr;
-  if (GX && tab) {
-    const bool lead = blockIdx.x == 0 && lane == 0;
-#pragma unroll
-    for (int r = 0; r < TR; ++r) {
-      if (r >= g.R) continue;
-      int t = g.gx.lm.pval ? finish_tok(g.gx.lm, r, tl[r]) : g.gx.in.tokens[r];
-      if (lead && g.gx.lm.pval && g.gx.lm.rec) g.gx.lm.rec[(size_t)r * g.gx.lm.ld_rec] = t;
-      if (t < 0 || t >= g.gx.V) {
-        if (lead) atomicOr(g.err, ERRF_TOKEN);
-      } else {
-        trow[r] = g.tab + (size_t)t * m.N;
-      }
-    }
-  }
   for (int j = 1; j < kw; ++j)
 #pragma unroll
     for (int n = 0; n < NT; ++n)
@@ -661,14 +645,12 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     for (int rt = 0; rt < RT; ++rt) {
       const int r = (lane & 15) + 16 * rt;
       const float sc = has_norm && r < g.R ? (own_scales ? rowscale[r] : g.norm.scale[r]) : 1.f;
-      const float *tr = nullptr;
-#pragma unroll
-      for (int q = 0; q < TR; ++q) tr = r == q ? trow[q] : tr;
-      if (EPI == EPI_NORM && !GX && g.tab && r < g.R) {
+      f32x4 tadd = GX ? tv : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (EPI == EPI_NORM && !GX && g.tab && r < g.R) {   // batched rows: tokens from the prep
         const int t = g.tab_tok[r];
-        tr = t >= 0 ? g.tab + (size_t)t * m.N : nullptr;
+        if (t >= 0) tadd = *(const f32x4 *)(g.tab + (size_t)t * m.N + (t0 + n) * 16 + 4 * (lane >> 4));
       }
-      const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt], tr);
+      const float ss = epilogue_tile<T, EPI>(g, t0 + n, r, acc[n][rt], sc, cbase[rt], rpos[rt], tadd);
       if (EPI == EPI_NORM && r < g.R && lane < 16) g.ss[(size_t)(t0 + n) * g.R + r] = ss;
     }
 }
@@ -734,10 +716,15 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   if (own) sl = issue_scales(g.norm, g.R, r0, nr);
   const int n0 = tile * 16 + 4 * (lane >> 4);
   f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 tadd = f32x4{0.f, 0.f, 0.f, 0.f};   // fusion FC: the row's embedding-table term
   long cbase = -1;
   int rpos = 0;
   if (r < g.R) {
     if (EPI == EPI_QKV) cbase = cache_base(g, r, rpos);
+    // the row's token goes out first, its table row right after the first
+    // batch of slice loads, so the two dependent loads overlap the slices
+    const bool tab = EPI == EPI_NORM && g.tab;
+    const int ttok = tab ? g.tab_tok[r] : -1;
     // slices in order, their loads issued FIN_UNROLL at a time
     const f32x4 *pp = (const f32x4 *)(g.part + (size_t)r * g.m.N + n0);
     const size_t stride = (size_t)g.R * g.m.N / 4;
@@ -746,6 +733,7 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
 #pragma unroll
       for (int j = 0; j < FIN_UNROLL; ++j)
         v[j] = s0 + j < g.split ? pp[(size_t)(s0 + j) * stride] : f32x4{0.f, 0.f, 0.f, 0.f};
+      if (s0 == 0 && ttok >= 0) tadd = *(const f32x4 *)(g.tab + (size_t)ttok * g.m.N + n0);
 #pragma unroll
       for (int j = 0; j < FIN_UNROLL; ++j)
         if (s0 + j < g.split) a += v[j];
@@ -758,12 +746,7 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   } else if (g.norm.scale && r < g.R) {
     sc = g.norm.scale[r];
   }
-  const float *trow = nullptr;
-  if (EPI == EPI_NORM && g.tab && r < g.R) {
-    const int t = g.tab_tok[r];
-    trow = t >= 0 ? g.tab + (size_t)t * g.m.N : nullptr;
-  }
-  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos, trow);
+  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos, tadd);
   if constexpr (EPI == EPI_NORM) {
     if (lane < 16) ssw[wave][lane] = ss;
     __syncthreads();
