@@ -119,10 +119,10 @@ def step_weight_bytes(cfg, s):
 
 
 def uses_embed_table(cfg, rows):
-    """Whether a pass of `rows` rows takes the fusion FC's embedding half from
-    the per-set table (the library's rule: bf16 contexts of at most two
-    sequences, on the one- and two-row GEMV path)."""
-    return cfg.dtype == "bf16" and cfg.batch <= 2 and rows <= 2 and cfg.hidden % 64 == 0
+    """Whether a pass takes the fusion FC's embedding half from the per-set
+    table (the library's rule: bf16 contexts whose hidden size is a multiple
+    of 64, at any row count)."""
+    return cfg.dtype == "bf16" and cfg.hidden % 64 == 0
 
 
 def step_streamed_bytes(cfg, s, rows):

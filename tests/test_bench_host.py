@@ -36,10 +36,13 @@ def test_streamed_bytes_with_the_embedding_table():
     full = bench.step_weight_bytes(L3_8B_BS1, 1)
     assert bench.uses_embed_table(L3_8B_BS1, 1)
     assert bench.step_streamed_bytes(L3_8B_BS1, 1, 1) == full - 2 * 4096 * 4096 + 4096 * 4
-    # batch 16 and the catch-up prefill rows keep the whole FC
-    assert not bench.uses_embed_table(L3_8B_BS16, 16)
-    assert bench.step_streamed_bytes(L3_8B_BS16, 1, 16) == bench.step_weight_bytes(L3_8B_BS16, 1)
-    assert not bench.uses_embed_table(L3_8B_BS1, 4)
+    # batched rows too: one table row per row
+    assert bench.uses_embed_table(L3_8B_BS16, 16)
+    assert (bench.step_streamed_bytes(L3_8B_BS16, 1, 16)
+            == bench.step_weight_bytes(L3_8B_BS16, 1) - 2 * 4096 * 4096 + 16 * 4096 * 4)
+    # fp32 contexts keep the whole FC
+    from synth import TINY_F32
+    assert not bench.uses_embed_table(TINY_F32, 1)
 
 
 def _digest_with(edit):
