@@ -77,7 +77,7 @@ def lm_workgroups(cfg, rows):
     """Workgroups of one LM-head launch (the library's plan: 16-id vocab tiles,
     4 waves per workgroup, tiles per wave by rows)."""
     tiles, nkb = cfg.vocab // 16, cfg.hidden // 32
-    if rows == 1 and cfg.dtype == "bf16":
+    if rows == 1 and cfg.dtype == "bf16" and nkb % 16 == 0:
         nt = 4 if tiles % 16 == 0 and nkb % 16 == 0 and tiles // 4 >= 1024 else 1
     elif rows <= 32 and tiles % 8 == 0:
         nt = 8
@@ -92,7 +92,7 @@ def lm_topk_pass(cfg, rows):
     """Whether the LM head stores fp32 logits and a separate pass reduces them
     to the top-k partials (the library's rule: greedy top-k > 1 on the MFMA
     tiles, i.e. more than one row or fp32 weights)."""
-    gemv = rows == 1 and cfg.dtype == "bf16"
+    gemv = rows == 1 and cfg.dtype == "bf16" and (cfg.hidden // 32) % 16 == 0
     return max(1, cfg.tree_width) > 1 and not gemv and not cfg.temperature
 
 

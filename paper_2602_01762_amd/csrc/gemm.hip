@@ -327,9 +327,13 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
 }
 
 // The same over NT consecutive tiles per wave, each over the full K (nkb a
-// multiple of UV, so the wave's weights are one contiguous stream of NT *
-// nkb k-blocks).  Longer streams per wave and a grid that fits the chip in
-// one round read HBM faster than one tile per wave.
+// multiple of UV, which the host checks, so the wave's weights are one
+// contiguous stream of NT * nkb k-blocks).  Longer streams per wave and a
+// grid that fits the chip in one round read HBM faster than one tile per
+// wave.  Two register sets of UV / 2 k-blocks: batch j + 1 is in flight
+// while batch j is consumed, so the stream has no gap between batches (8B
+// LM head 163.0 -> 161.3 us, Llama-2 shape 50.1 -> 48.5 us against one set
+// of UV k-blocks loaded and then consumed).
 template <int RR, int NT>
 __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0, int nkb,
                                                     const Act &x, int R, int K, float *xs,
@@ -337,43 +341,12 @@ __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0
   const int lane = threadIdx.x & 63, kq = lane >> 4;
   const u32x4 z4 = {0, 0, 0, 0};
   const u32x4 *wp = w0 + lane;
-  const int nkb_live = live ? nkb : 0;
   constexpr int UP = UV / 2;
-  if (nkb % (2 * UP) == 0) {
-    // two register sets of UP k-blocks: batch j + 1 is in flight while
-    // batch j is consumed, so the stream has no gap between batches (8B LM
-    // head 163.0 -> 161.3 us, Llama-2 shape 50.1 -> 48.5 us against one set
-    // of UV k-blocks loaded and then consumed)
-    const int bpt = nkb / UP;   // batches per tile (even)
-    const int total = live ? NT * bpt : 0;
-    u32x4 a[UP], b[UP];
+  const int bpt = nkb / UP;   // batches per tile (even)
+  const int total = live ? NT * bpt : 0;
+  u32x4 a[UP], b[UP];
 #pragma unroll
-    for (int u = 0; u < UP; ++u) a[u] = live ? __builtin_nontemporal_load(wp + u * 64) : z4;
-    stage_x<RR>(x, R, K, xs);
-    __syncthreads();
-#pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      float acc[RR];
-#pragma unroll
-      for (int r = 0; r < RR; ++r) acc[r] = 0.f;
-      for (int i = 0; i < bpt && live; i += 2) {
-        const int j = n * bpt + i;
-#pragma unroll
-        for (int u = 0; u < UP; ++u) b[u] = __builtin_nontemporal_load(wp + (size_t)(j + 1) * UP * 64 + u * 64);
-        valu_batch_n<RR, UP>(a, i * UP, kq, xs, K, acc);
-        if (j + 2 < total) {
-#pragma unroll
-          for (int u = 0; u < UP; ++u) a[u] = __builtin_nontemporal_load(wp + (size_t)(j + 2) * UP * 64 + u * 64);
-        }
-        valu_batch_n<RR, UP>(b, (i + 1) * UP, kq, xs, K, acc);
-      }
-      out[n] = valu_result<RR>(acc);
-    }
-    return;
-  }
-  u32x4 a[UV];
-#pragma unroll
-  for (int u = 0; u < UV; ++u) a[u] = u < nkb_live ? __builtin_nontemporal_load(wp + u * 64) : z4;
+  for (int u = 0; u < UP; ++u) a[u] = live ? __builtin_nontemporal_load(wp + u * 64) : z4;
   stage_x<RR>(x, R, K, xs);
   __syncthreads();
 #pragma unroll
@@ -381,13 +354,16 @@ __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0
     float acc[RR];
 #pragma unroll
     for (int r = 0; r < RR; ++r) acc[r] = 0.f;
-    for (int kb = 0; kb < nkb_live; kb += UV) {
-      if (n > 0 || kb > 0) {
+    for (int i = 0; i < bpt && live; i += 2) {
+      const int j = n * bpt + i;
 #pragma unroll
-        for (int u = 0; u < UV; ++u) a[u] = __builtin_nontemporal_load(wp + u * 64);
+      for (int u = 0; u < UP; ++u) b[u] = __builtin_nontemporal_load(wp + (size_t)(j + 1) * UP * 64 + u * 64);
+      valu_batch_n<RR, UP>(a, i * UP, kq, xs, K, acc);
+      if (j + 2 < total) {
+#pragma unroll
+        for (int u = 0; u < UP; ++u) a[u] = __builtin_nontemporal_load(wp + (size_t)(j + 2) * UP * 64 + u * 64);
       }
-      valu_batch<RR>(a, UV, kb, kq, xs, K, acc);
-      wp += UV * 64;
+      valu_batch_n<RR, UP>(b, (i + 1) * UP, kq, xs, K, acc);
     }
     out[n] = valu_result<RR>(acc);
   }

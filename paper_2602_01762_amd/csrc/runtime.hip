@@ -679,7 +679,9 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   lmg.V = c->V;
   lmg.topk = p.topk;
   lmg.inv_temp = p.u ? p.inv_temp : 1.f;
-  lmg.gemv = (c->bf16 && R <= LM_GEMV_MAX_ROWS && gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
+  // the GEMV LM head streams whole batches of 16 k-blocks (H a multiple of 512)
+  lmg.gemv = (c->bf16 && R <= LM_GEMV_MAX_ROWS && c->lm.nkb % 16 == 0 &&
+              gemv_lds_bytes(R, H) + 64 * 1024 <= c->lds_limit) ? 1 : 0;
   lmg.nt = 1;
   // one row: four consecutive vocab tiles per wave when that still gives
   // about four waves per CU (longer weight streams, one round of workgroups)

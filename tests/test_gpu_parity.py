@@ -48,6 +48,10 @@ def test_chain_parity_small(cfg):
 @pytest.mark.parametrize("cfg", [
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs1", batch=1),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs2", batch=2),
+    # H = 480: no embedding table (H % 64 != 0), so the GEMV fusion FC gathers
+    # [E(x) ; f] itself, and the one-row LM head takes the MFMA tiles (its
+    # GEMV streams whole batches of 16 k-blocks, H % 512 == 0)
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs1_h480", batch=1, hidden=480),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24", batch=24, vocab=5120),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs40", batch=40, ctx_range=(20, 300)),
 ], ids=lambda c: c.name)
