@@ -104,18 +104,10 @@ __device__ __forceinline__ bool better(float v, int id, float ov, int oid) {
   // bitwise, not short-circuit: lane masks combine without exec-mask branches
   return (v > ov) | ((v == ov) & (id < oid));
 }
-__device__ __forceinline__ void wave_argmax(float &v, int &id) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float ov = __shfl_xor(v, o, 64);
-    int oid = __shfl_xor(id, o, 64);
-    if (better(ov, oid, v, id)) { v = ov; id = oid; }
-  }
-}
 
-// The same over N independent values at once: each butterfly step issues
-// the N cross-lane reads together, so their latencies overlap instead of
-// adding up (the results equal N separate calls)
+// The same over N independent values (the results equal N separate calls;
+// the DPP steps of different values are independent, so the compiler
+// interleaves them)
 template <int N>
 __device__ __forceinline__ void wave_max_n(float (&v)[N]) {
 #pragma unroll
@@ -125,22 +117,6 @@ template <int N>
 __device__ __forceinline__ void wave_sum_n(float (&v)[N]) {
 #pragma unroll
   for (int b = 0; b < N; ++b) v[b] = wave_sum(v[b]);
-}
-template <int N>
-__device__ __forceinline__ void wave_argmax_n(float (&v)[N], int (&id)[N]) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float ov[N];
-    int oid[N];
-#pragma unroll
-    for (int b = 0; b < N; ++b) {
-      ov[b] = __shfl_xor(v[b], o, 64);
-      oid[b] = __shfl_xor(id[b], o, 64);
-    }
-#pragma unroll
-    for (int b = 0; b < N; ++b)
-      if (better(ov[b], oid[b], v[b], id[b])) { v[b] = ov[b]; id[b] = oid[b]; }
-  }
 }
 
 // (value, id) candidates as one 64-bit key whose unsigned order is the
@@ -188,6 +164,16 @@ __device__ __forceinline__ void wave_max_key_n(uint64_t (&k)[N]) {
     const uint64_t m01 = r1 > r0 ? r1 : r0, m23 = r3 > r2 ? r3 : r2;
     k[b] = m23 > m01 ? m23 : m01;
   }
+}
+
+// Arg-max of (value, id) over the wave by the same order as `better`
+// (larger value wins, equal values -> lower id), on candidate keys; every
+// lane ends with the winner.  (NaN ranks lowest here.)
+__device__ __forceinline__ void wave_argmax(float &v, int &id) {
+  uint64_t k[1] = {cand_key(v, id)};
+  wave_max_key_n<1>(k);
+  v = key_value(k[0]);
+  id = key_id(k[0]);
 }
 
 // block-wide (256 threads = 4 waves) reductions through LDS, fixed order

@@ -233,8 +233,8 @@ __device__ __forceinline__ f32x4 valu_result(float (&acc)[RR]) {
   // sum the 4 k-quarters of each tile row (lanes l, l^16, l^32, l^48)
 #pragma unroll
   for (int r = 0; r < RR; ++r) {
-    acc[r] += __shfl_xor(acc[r], 16, 64);
-    acc[r] += __shfl_xor(acc[r], 32, 64);
+    acc[r] += xor16_f(acc[r]);
+    acc[r] += xor32_f(acc[r]);
   }
   // lane l now holds tile row (l & 15); the MFMA layout wants, in lane L,
   // tile rows 4 (L >> 4) + i of batch row (L & 15)
@@ -455,8 +455,8 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
       }
     }
     // tile sum over the 4 lanes holding row r: fixed butterfly order
-    ss += __shfl_xor(ss, 16, 64);
-    ss += __shfl_xor(ss, 32, 64);
+    ss += xor16_f(ss);
+    ss += xor32_f(ss);
     return ss;
   } else if (EPI == EPI_SWIGLU) {
     if (live) {
@@ -472,7 +472,7 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
     // partner values for the rotation (lanes l and l ^ 32 hold the two halves)
     float pv[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) pv[i] = __shfl_xor(v[i], 32, 64);
+    for (int i = 0; i < 4; ++i) pv[i] = xor32_f(v[i]);
     if (!live) return 0.f;
     if (f0 < qd + kd) {
       const bool isq = f0 < qd;
