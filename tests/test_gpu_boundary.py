@@ -161,3 +161,32 @@ def test_bad_host_arguments():
         dr.tree(inp)                               # context created without a tree width
     assert e.value.status == -1
     dr.close()
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_embedding_tables_follow_the_load_order(batch):
+    """The fusion FC's embedding tables (W_fc[:, :H] E[v] per set) are built
+    when both a set and the shared tensors are loaded, in either order, and
+    rebuilt when E is loaded again: a context that loads its sets first, then
+    a wrong E, then the right one, drafts exactly what a context loaded in
+    the usual order drafts (the GEMV path at batch 1, the batched one at 3)."""
+    from paper_2602_01762_amd import binding as B
+    cfg = CFG.with_(batch=batch)
+    w = make_weights(cfg, "cuda")
+    inp = make_inputs(cfg, "cuda")
+    ref = _drafter(cfg)
+    ref.load(w)
+    a = ref.chain(inp, logits=True)
+    other = make_weights(cfg.with_(seed=7), "cuda")
+    dr = _drafter(cfg)
+    for s, ps in enumerate(w.sets):
+        dr.load_set(s, ps)
+    B.prism_draft_load_shared(dr.ctx, other.embed, w.lm_head, w.final_norm)
+    B.prism_draft_load_shared(dr.ctx, w.embed, w.lm_head, w.final_norm)
+    b = dr.chain(inp, logits=True)
+    torch.cuda.synchronize()
+    assert ref.device_status() == 0 and dr.device_status() == 0
+    assert torch.equal(a["tokens"], b["tokens"])
+    assert torch.equal(a["logits"], b["logits"])
+    ref.close()
+    dr.close()
