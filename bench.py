@@ -377,8 +377,8 @@ def cpu_baseline(cfg, w, inp, dr):
     drafted = n * (cfg.n_steps if cfg.mode == "chain" else cfg.tree_nodes)
     return {"value": round(drafted / el, 3), "unit": "drafted tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": "%d full %s calls of sequence 0 (%d draft steps each), fp64 with bf16 "
-                      "roundings emulated, %.1f s" % (n, cfg.mode, cfg.n_steps, el)}
+            "sample": "%d full %s calls of sequence 0 (%d draft steps each), fp64 arithmetic on "
+                      "the stored (bf16) tensors, %.1f s" % (n, cfg.mode, cfg.n_steps, el)}
 
 
 if __name__ == "__main__":
