@@ -18,7 +18,6 @@ namespace prism {
 constexpr int ATT_S = 64;        // slots per step
 constexpr int ATT_MAXG = 8;      // query heads per KV head
 constexpr int ATT_MAXGD = 1024;  // g * d
-constexpr int ATT_MAXD = 256;    // head_dim
 constexpr int ATT_MAXVS = 8;     // slots per thread in P.V: 64 / (256 / (d / 8)) for d <= 256
 constexpr int ATT_MAXCH = 1024;  // chunks per row merged by the combine kernel
 

@@ -132,7 +132,6 @@ template <int KB>
 __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
   constexpr int CL = 16 / KB > 1 ? 16 / KB : 1;   // lists per thread and batch
   __shared__ float shv[8];
-  __shared__ int shi[8];
   const int r = blockIdx.x, tid = threadIdx.x;
   const int k = a.topk;
   const float *pm = a.pmax + (size_t)r * a.n_wg;
