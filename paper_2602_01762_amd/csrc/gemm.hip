@@ -86,6 +86,72 @@ __device__ __forceinline__ void mainloop(const u32x4 *__restrict__ w0, int nkb, 
   }
 }
 
+// The same with two register sets: the k-blocks of batch j + 1 are in flight
+// while batch j is consumed.  Loads past kb1 are clamped to the last k-block
+// (re-read, discarded), so every batch issues the same loads.
+template <typename T, int RT, int NT, bool PAIR>
+__device__ __forceinline__ void mainloop_db(const u32x4 *__restrict__ w0, int nkb, const Act &x,
+                                            int R, int kb0, int kb1, f32x4 (&acc)[NT][RT]) {
+  constexpr int E = Ty<T>::E, KB = Ty<T>::KB;
+  constexpr int U0 = 24 / (NT + (PAIR ? 2 : 1) * RT);
+  constexpr int U = U0 > 8 ? 8 : (U0 < 1 ? 1 : U0);
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15, kq = lane >> 4;
+  const T *xh[RT];
+  const T *xl[RT];
+  bool ok[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = col + 16 * rt;
+    ok[rt] = r < R;
+    const size_t off = (size_t)(ok[rt] ? r : 0) * x.ld + kq * E;
+    xh[rt] = (const T *)x.hi + off;
+    xl[rt] = PAIR ? (const T *)x.lo + off : nullptr;
+  }
+  const u32x4 *wp[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) wp[n] = w0 + (size_t)n * nkb * 64 + lane;
+  const u32x4 z4 = {0, 0, 0, 0};
+  u32x4 a[2][U][NT], bh[2][U][RT], bl[2][U][RT];
+  auto load = [&](int s, int kb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = min(kb + u, kb1 - 1);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) a[s][u][n] = __builtin_nontemporal_load(wp[n] + (size_t)k * 64);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const size_t o = (size_t)k * KB;
+        bh[s][u][rt] = ok[rt] ? *(const u32x4 *)(xh[rt] + o) : z4;
+        if (PAIR) bl[s][u][rt] = ok[rt] ? *(const u32x4 *)(xl[rt] + o) : z4;
+      }
+    }
+  };
+  auto mma = [&](int s, int nb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u < nb) {
+#pragma unroll
+        for (int n = 0; n < NT; ++n)
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) {
+            acc[n][rt] = Ty<T>::mma(a[s][u][n], bh[s][u][rt], acc[n][rt]);
+            if (PAIR) acc[n][rt] = Ty<T>::mma(a[s][u][n], bl[s][u][rt], acc[n][rt]);
+          }
+      }
+    }
+  };
+  if (kb1 <= kb0) return;
+  load(0, kb0);
+  for (int kb = kb0; kb < kb1; kb += 2 * U) {
+    load(1, kb + U);
+    mma(0, kb1 - kb);
+    if (kb + U >= kb1) break;
+    load(0, kb + 2 * U);
+    mma(1, kb1 - kb - U);
+  }
+}
+
 // GEMV main loop for a few rows (R <= RR <= 4) of a bf16 matrix: each wave
 // stages the activation columns of its own K range in LDS as fp32 (hi + lo),
 // then each lane multiplies its 8 weights of a k-block by the matching fp32
@@ -768,8 +834,14 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
 #pragma unroll
     for (int n = 0; n < NT; ++n) acc[n][0] = res[n];
   } else if (live) {
-    mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, 0,
-                              m.nkb, acc);
+    // up to 16 rows the double-buffered loop (16-row LM head 166.3 -> 164.8 us);
+    // at 32 rows it was slower (327 -> 348 us), so those keep one batch at a time
+    if constexpr (RT == 1)
+      mainloop_db<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R,
+                                   0, m.nkb, acc);
+    else
+      mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, 0,
+                                m.nkb, acc);
   }
   if (own_scales) {
     __syncthreads();
