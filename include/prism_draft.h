@@ -32,7 +32,13 @@
  *   - Content that only the device sees (token ids, block-table entries,
  *     context lengths) is bounds-checked by the kernels: an out-of-range
  *     value skips the access and raises a flag that
- *     prism_device_status() reports.
+ *     prism_device_status() reports.  So is a NaN that reaches the logits
+ *     (from a feature row or a weight): the call still completes, and the
+ *     flag is reported as PRISM_ERR_NONFINITE.
+ *   - Device memory: prism_create allocates the workspace, and
+ *     prism_draft_load_shared / prism_draft_load_params allocate the weight
+ *     arena (and the embedding tables, below) on their first call for a
+ *     tensor group.  Drafting and verification calls allocate nothing.
  *   - One context is used by one host thread at a time.  Results are
  *     bit-identical across repeated calls with the same inputs.
  */
@@ -53,7 +59,8 @@ typedef enum {
   PRISM_ERR_UNSUPPORTED = -4,   /* f_map asks one set for two feature widths  */
   PRISM_ERR_OUT_OF_MEMORY = -5, /* device allocation failed                   */
   PRISM_ERR_HIP = -6,           /* a HIP runtime call failed                  */
-  PRISM_ERR_CAPACITY = -7       /* KV block table / pool too small (device)   */
+  PRISM_ERR_CAPACITY = -7,      /* KV block table / pool too small (device)   */
+  PRISM_ERR_NONFINITE = -8      /* NaN logits or tree scores (device)         */
 } prism_status;
 
 typedef enum { PRISM_F32 = 0, PRISM_BF16 = 1 } prism_dtype;
@@ -204,12 +211,13 @@ prism_status prism_draft_load_shared(prism_ctx *ctx, const void *d_embed,
 /* Load parameter set `set` (0..M-1), the weights of processing module
  * set+1 (paper Sec. 3.2: M modules, each a fusion FC and a transformer
  * layer).  Copies and repacks into the step-indexed arena; synchronizes
- * `stream`.  Allocates that set's arena slot on first use.  In bf16
- * contexts of at most two sequences (max_batch <= 2) the slot also holds
- * the set's embedding table, W_fc[:, :H] E[v] for every token v in fp32
- * (V * H * 4 bytes, 2.1 GB at V = 128256, H = 4096), which one- and two-row
- * passes read instead of the FC's embedding columns; it is built here once
- * the shared tensors are loaded. */
+ * `stream`.  Allocates that set's arena slot on first use.  In every bf16
+ * context whose H is a multiple of 64 the slot also holds the set's
+ * embedding table, W_fc[:, :H] E[v] for every token v in fp32: V * H * 4
+ * bytes per set (2.1 GB at V = 128256, H = 4096; 4.2 GB at H = 8192), on
+ * top of the set's weights.  Every pass, whatever its row count, then reads
+ * one table row per row instead of the FC's embedding columns.  The table is
+ * built here once the shared tensors are loaded. */
 prism_status prism_draft_load_params(prism_ctx *ctx, int32_t set,
                                      const prism_param_set *params,
                                      void *stream);
@@ -329,11 +337,13 @@ prism_status prism_verify_tree(prism_ctx *ctx, int32_t batch, int32_t n_nodes,
                                const int32_t *d_parent, int32_t *d_n_accepted,
                                int32_t *d_path, int32_t *d_next_token, void *stream);
 
-/* Synchronize `stream` and report device-side bounds flags raised since
- * the last call: PRISM_ERR_CAPACITY (block table / pool / slot out of
- * range), PRISM_ERR_INVALID_ARG (token id out of range, malformed catch-up
- * offsets), else PRISM_OK.
- * Clears the flags. */
+/* Synchronize `stream` and report device-side flags raised since the last
+ * call, the first that applies of: PRISM_ERR_NONFINITE (a row whose logits
+ * are all NaN, or a NaN tree score: the tokens of such a row are
+ * unspecified and may lie outside 0..V-1; other rows are unaffected),
+ * PRISM_ERR_INVALID_ARG (malformed catch-up offsets), PRISM_ERR_CAPACITY
+ * (block table / pool / slot out of range), PRISM_ERR_INVALID_ARG (token id
+ * out of range), else PRISM_OK.  Clears the flags. */
 prism_status prism_device_status(prism_ctx *ctx, void *stream);
 
 /* Measurement support (not part of the drafting computation).  With
@@ -345,6 +355,14 @@ prism_status prism_device_status(prism_ctx *ctx, void *stream);
  * pairs. */
 prism_status prism_profile_enable(prism_ctx *ctx, int32_t enable);
 prism_status prism_profile_read(prism_ctx *ctx, float *total_ms, int32_t *count);
+
+/* Captured-graph cache of a context.  Chain and tree calls capture one HIP
+ * graph per distinct (call kind, shape, buffer pointers, step map) and
+ * replay it; at most *capacity graphs are kept, and capturing one more
+ * first destroys the least recently used (after a device-wide
+ * synchronization, since it may still be running).  Writes the number held
+ * and the capacity. */
+prism_status prism_graph_cache(const prism_ctx *ctx, int32_t *n_graphs, int32_t *capacity);
 
 #ifdef __cplusplus
 }

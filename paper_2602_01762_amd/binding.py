@@ -15,13 +15,14 @@ LIB_PATH = os.path.join(_HERE, "libprism_draft.so")
 PRISM_F32, PRISM_BF16 = 0, 1
 STATUS = {0: "PRISM_OK", -1: "PRISM_ERR_INVALID_ARG", -2: "PRISM_ERR_SHAPE",
           -3: "PRISM_ERR_NOT_LOADED", -4: "PRISM_ERR_UNSUPPORTED",
-          -5: "PRISM_ERR_OUT_OF_MEMORY", -6: "PRISM_ERR_HIP", -7: "PRISM_ERR_CAPACITY"}
+          -5: "PRISM_ERR_OUT_OF_MEMORY", -6: "PRISM_ERR_HIP", -7: "PRISM_ERR_CAPACITY",
+          -8: "PRISM_ERR_NONFINITE"}
 EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_load_shared",
            "prism_draft_load_params", "prism_set_step_map", "prism_draft_step",
            "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_chain_sample",
            "prism_draft_tree", "prism_verify_chain", "prism_verify_tree",
            "prism_device_status",
-           "prism_profile_enable", "prism_profile_read")
+           "prism_profile_enable", "prism_profile_read", "prism_graph_cache")
 
 c_i32, c_u64, c_f32, c_vp = ctypes.c_int32, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p
 
@@ -106,6 +107,7 @@ def lib():
         L.prism_device_status.argtypes = [c_vp, c_vp]
         L.prism_profile_enable.argtypes = [c_vp, c_i32]
         L.prism_profile_read.argtypes = [c_vp, P(c_f32), P(c_i32)]
+        L.prism_graph_cache.argtypes = [c_vp, P(c_i32), P(c_i32)]
         for n in EXPORTS:
             if n not in ("prism_destroy", "prism_last_error"):
                 getattr(L, n).restype = ctypes.c_int
@@ -221,3 +223,10 @@ def prism_profile_read(ctx):
     ms, n = c_f32(), c_i32()
     _check(lib().prism_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx)
     return ms.value, n.value
+
+
+def prism_graph_cache(ctx):
+    """(graphs held, capacity) of the context's captured-graph cache."""
+    n, cap = c_i32(), c_i32()
+    _check(lib().prism_graph_cache(ctx, ctypes.byref(n), ctypes.byref(cap)), ctx)
+    return n.value, cap.value

@@ -360,7 +360,8 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
       int t = from_lm ? finish_tok(gx.lm, r, tl[r]) : gx.in.tokens[r];
       if (lead && from_lm && gx.lm.rec) gx.lm.rec[(size_t)r * gx.lm.ld_rec] = t;
       if (t < 0 || t >= gx.V) {
-        if (lead) atomicOr(err, ERRF_TOKEN);
+        // from the LM head, only a row of NaN logits leaves no token
+        if (lead) atomicOr(err, from_lm && t == NO_TOKEN ? ERRF_NONFINITE : ERRF_TOKEN);
         t = -1;
       }
       tok[r] = t;
@@ -601,9 +602,9 @@ __device__ __forceinline__ long cache_base(const GemmLaunch &g, int r, int &pos)
 }
 
 // batched variants (more accumulators) run at most 8 waves per workgroup,
-// which leaves them 256 VGPRs
+// which leaves them 256 VGPRs; the planner caps its wave counts the same way
 template <int RT, int NT>
-constexpr int gemm_max_threads() { return RT * NT >= 2 ? 512 : 1024; }
+constexpr int gemm_max_threads() { return 64 * product_max_waves(RT, NT); }
 
 // kernel-only epilogue tag: EPI_NORM on fusion-FC rows that the GEMV main
 // loop gathers itself (no input norm), a separate instantiation so that the
@@ -960,13 +961,9 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
 
 static_assert(GEMV_MAX_ROWS == 2, "GEMV variants cover 1 and 2 rows");
 
-size_t gemv_lds_bytes(int R, int K) {
-  const int vr = R <= 1 ? 1 : 2;
-  return (size_t)vr * K * sizeof(float);
-}
-
 template <typename T, int RT, int NT, bool PAIR, int VR>
-static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
+static bool gemm_epi(const GemmLaunch &g, hipStream_t s) {
+  if (g.kw < 1 || 64 * g.kw > gemm_max_threads<RT, NT>()) return false;
   dim3 grid(g.m.n_tiles / NT);
   size_t lds = (size_t)((g.kw - 1) * NT * RT * 64) * sizeof(f32x4) +
                (size_t)64 * g.kw * sizeof(float);
@@ -974,13 +971,14 @@ static void gemm_epi(const GemmLaunch &g, hipStream_t s) {
   if constexpr (VR > 0) {
     if (g.epi == EPI_NORM && g.gx.embed) {
       hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM_GATHER, VR>), grid, dim3(64 * g.kw), lds, s, g);
-      return;
+      return true;
     }
   }
   if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_NORM, VR>), grid, dim3(64 * g.kw), lds, s, g);
   else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_SWIGLU, VR>), grid, dim3(64 * g.kw), lds, s, g);
   else if constexpr (NT <= 2) hipLaunchKernelGGL((k_gemm<T, RT, NT, PAIR, EPI_QKV, VR>), grid, dim3(64 * g.kw), lds, s, g);
-  // (the planner keeps QKV off the 4- and 8-tile unsplit variants)
+  else return false;   // the planner keeps QKV off the 4- and 8-tile unsplit variants
+  return true;
 }
 
 template <typename T, int RT, int NT, bool PAIR>
@@ -996,7 +994,7 @@ static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
 }
 
 template <typename T, bool PAIR>
-static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
+static bool gemm_rt(const GemmLaunch &g, hipStream_t s) {
   if (g.split > 0) {
     if (g.nt == 8) {
       if (g.R <= 16) gemm_split_launch<T, 1, 8, PAIR>(g, s);
@@ -1014,35 +1012,37 @@ static void gemm_rt(const GemmLaunch &g, hipStream_t s) {
       else if (g.R <= 32) gemm_split_launch<T, 2, 1, PAIR>(g, s);
       else gemm_split_launch<T, 4, 1, PAIR>(g, s);
     }
-    return;
+    return true;
   }
   if constexpr (sizeof(T) == 2) {
     if (g.gemv) {
-      if (g.R <= 1) gemm_epi<T, 1, 1, PAIR, 1>(g, s);
-      else gemm_epi<T, 1, 1, PAIR, 2>(g, s);   // R <= GEMV_MAX_ROWS
-      return;
+      if (g.R <= 1) return gemm_epi<T, 1, 1, PAIR, 1>(g, s);
+      return gemm_epi<T, 1, 1, PAIR, 2>(g, s);   // R <= GEMV_MAX_ROWS
     }
   }
   if (g.nt == 8) {          // batched rows, many tiles: no K slices
-    if (g.R <= 16) gemm_epi<T, 1, 8, PAIR, 0>(g, s);
-    else gemm_epi<T, 2, 8, PAIR, 0>(g, s);
-  } else if (g.nt == 4) {
-    if (g.R <= 16) gemm_epi<T, 1, 4, PAIR, 0>(g, s);
-    else gemm_epi<T, 2, 4, PAIR, 0>(g, s);
-  } else if (g.nt == 2) {
-    if (g.R <= 16) gemm_epi<T, 1, 2, PAIR, 0>(g, s);
-    else if (g.R <= 32) gemm_epi<T, 2, 2, PAIR, 0>(g, s);
-    else gemm_epi<T, 4, 2, PAIR, 0>(g, s);
-  } else {
-    if (g.R <= 16) gemm_epi<T, 1, 1, PAIR, 0>(g, s);
-    else if (g.R <= 32) gemm_epi<T, 2, 1, PAIR, 0>(g, s);
-    else gemm_epi<T, 4, 1, PAIR, 0>(g, s);
+    if (g.R <= 16) return gemm_epi<T, 1, 8, PAIR, 0>(g, s);
+    if (g.R <= 32) return gemm_epi<T, 2, 8, PAIR, 0>(g, s);
+    return false;
   }
+  if (g.nt == 4) {
+    if (g.R <= 16) return gemm_epi<T, 1, 4, PAIR, 0>(g, s);
+    if (g.R <= 32) return gemm_epi<T, 2, 4, PAIR, 0>(g, s);
+    return false;
+  }
+  if (g.nt == 2) {
+    if (g.R <= 16) return gemm_epi<T, 1, 2, PAIR, 0>(g, s);
+    if (g.R <= 32) return gemm_epi<T, 2, 2, PAIR, 0>(g, s);
+    return gemm_epi<T, 4, 2, PAIR, 0>(g, s);
+  }
+  if (g.R <= 16) return gemm_epi<T, 1, 1, PAIR, 0>(g, s);
+  if (g.R <= 32) return gemm_epi<T, 2, 1, PAIR, 0>(g, s);
+  return gemm_epi<T, 4, 1, PAIR, 0>(g, s);
 }
 
-void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s) {
-  if (bf16) gemm_rt<bf16_t, true>(g, s);
-  else gemm_rt<float, false>(g, s);
+bool launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s) {
+  if (bf16) return gemm_rt<bf16_t, true>(g, s);
+  return gemm_rt<float, false>(g, s);
 }
 
 int lm_workgroups(int n_tiles, int nt) { return (n_tiles / nt + 3) / 4; }

@@ -3,23 +3,23 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan.h"
+
 namespace prism {
 
 typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
 
-// device error flags (bit set by kernels on an out-of-range device value)
-enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u, ERRF_ROWS = 4u };
+// device error flags: set by kernels on an out-of-range device value
+// (capacity, token, rows), or on logits that are NaN (nonfinite: every
+// logit of a row NaN, or a NaN tree score)
+enum : uint32_t { ERRF_CAPACITY = 1u, ERRF_TOKEN = 2u, ERRF_ROWS = 4u, ERRF_NONFINITE = 8u };
+// id of an empty (value, id) candidate in the top-k merges: it survives a
+// merge only when no candidate compares above -inf, i.e. every logit is NaN
+constexpr int NO_TOKEN = 0x7fffffff;
 
-// Rows up to which bf16 products (LM head) take the VALU GEMV main loop;
-// above it the staged-activation LDS reads, which grow with the rows, cost
-// more than the MFMA path's fixed 16-row tiles.
-constexpr int GEMV_MAX_ROWS = 2;
-constexpr int LM_GEMV_MAX_ROWS = 1;
 constexpr int MAX_TOPK = 16;
-constexpr int MAX_VERIFY_NODES = 64;   // tree nodes one verification call takes    // largest top-k of the LM-head merge
+constexpr int MAX_VERIFY_NODES = 64;   // tree nodes one verification call takes
 constexpr int MAX_TREE_CAND = 2048;
-constexpr int MAX_ROWS = 64;
-constexpr int MAX_KW = 16;      // waves of one workgroup splitting K
 
 // Tiled weight matrix W[N, K] (y = W x).  Tile t holds 16 output rows;
 // k-block j holds KB consecutive k (KB = 32 for bf16, 16 for fp32).  The
@@ -153,11 +153,11 @@ struct LmLaunch {
 };
 
 // ---- launchers (gemm.hip) -------------------------------------------------
-void launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
+// false (nothing launched): the plan's workgroup exceeds the bound of the
+// kernel instantiation it selects
+bool launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
 int lm_workgroups(int n_tiles, int nt);
-// LDS of the staged activations of the GEMV main loop
-size_t gemv_lds_bytes(int R, int K);
 // partial sums of squares per row that an EPI_NORM launch writes
 int gemm_ss_parts(const GemmLaunch &g);
 // whether the launch (its finish pass, if split) reduces the row scales of
@@ -191,6 +191,7 @@ struct LmSampleArgs {
   float *logp; int ld_logp;        // [R * ld_logp] its log-probability, or NULL
   int *tok_a;                      // optional [R] copy
   int *tok_b; int ld_b;            // optional [R * ld_b] copy
+  uint32_t *err;                   // ERRF_NONFINITE when no id has positive weight
 };
 // whether the sampler takes n_wg LM-head partials per row and groups of
 // `group` ids
@@ -225,7 +226,7 @@ void launch_lm_topk(const LmTopkArgs &a, hipStream_t s);
 // merge LM-head partials: top-k ids, optional log-probs, and the chain's token copies
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
-                       int *tok_b, int ld_b, hipStream_t s);
+                       int *tok_b, int ld_b, uint32_t *err, hipStream_t s);
 void launch_chain_setup(int B, int K, const int32_t *tokens, const int32_t *ctx_lens, int32_t *seq,
                         int32_t *pos, int32_t *tok0, hipStream_t s);
 // catch-up chain: per accepted row its sequence and position; per sequence
@@ -249,6 +250,7 @@ struct TreeWs {
   int32_t *tok, *feat_row, *seq, *pos, *slot; // next-pass rows [B*w]
   uint64_t *bits;                 // next-pass visibility [B*w]
   uint64_t *bits_prev;            // visibility of the pass just run [B*w]
+  uint32_t *err;                  // device error flags
 };
 // after pass d (0 = root): record children, choose the next frontier (if d < D-1),
 // and write the rows of pass d+1

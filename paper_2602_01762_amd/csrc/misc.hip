@@ -2,6 +2,7 @@
 // finalisation with residual + RMSNorm, LM-head partial merge (top-k and
 // log-sum-exp), chain setup, and the draft-tree bookkeeping.
 #include "device.h"
+#include "tree_order.h"
 
 namespace prism {
 
@@ -36,7 +37,8 @@ __global__ __launch_bounds__(256) void k_fc_prep(FcPrepArgs a) {
   }
   const int e0 = (blockIdx.x * 256 + threadIdx.x) * 8;   // 8 consecutive columns
   if (tok < 0 || tok >= a.V) {
-    if (e0 == 0) atomicOr(a.err, ERRF_TOKEN);
+    // from the LM head, only a row of NaN logits leaves no token
+    if (e0 == 0) atomicOr(a.err, a.lm.pval && tok == NO_TOKEN ? ERRF_NONFINITE : ERRF_TOKEN);
     tok = -1;
   }
   if (a.tok_out && e0 == 0) a.tok_out[r] = tok;
@@ -118,6 +120,7 @@ struct LmCombArgs {
   float *logp;
   int *tok_a;          // optional [R]: ids[r][0]
   int *tok_b; int ld_b; // optional [R * ld_b]: ids[r][0]
+  uint32_t *err;        // ERRF_NONFINITE when a row has no token (every logit NaN)
 };
 
 // KB: a power of two >= topk.  Each LM-head workgroup's k candidates come
@@ -237,6 +240,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(LmCombArgs a) {
     }
     ++hd[bw];
     const int id = key_id(best);
+    if (j == 0 && id == NO_TOKEN) atomicOr(a.err, ERRF_NONFINITE);
     a.ids[(size_t)r * k + j] = id;
     if (a.logp) a.logp[(size_t)r * k + j] = key_value(best) - lse;
     if (j == 0) {
@@ -395,6 +399,7 @@ __global__ __launch_bounds__(256) void k_lm_sample(LmSampleArgs a) {
     if (tok < 0) tok = last_nz;
   }
   if (lane == 0) {
+    if (tok < 0) atomicOr(a.err, ERRF_NONFINITE);   // no id of positive weight
     a.ids[r] = tok;
     if (a.logp) {
       const float lt = tok >= 0 ? a.logits[(size_t)r * a.ld_logits + tok] * a.inv_temp : -INFINITY;
@@ -550,8 +555,8 @@ void launch_lm_topk(const LmTopkArgs &a, hipStream_t s) {
 
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
-                       int *tok_b, int ld_b, hipStream_t s) {
-  LmCombArgs a{R, n_wg, topk, V, pmax, psum, pval, pid, ids, logp, tok_a, tok_b, ld_b};
+                       int *tok_b, int ld_b, uint32_t *err, hipStream_t s) {
+  LmCombArgs a{R, n_wg, topk, V, pmax, psum, pval, pid, ids, logp, tok_a, tok_b, ld_b, err};
   if (topk <= 1) hipLaunchKernelGGL(k_lm_combine<1>, dim3(R), dim3(256), 0, s, a);
   else if (topk <= 2) hipLaunchKernelGGL(k_lm_combine<2>, dim3(R), dim3(256), 0, s, a);
   else if (topk <= 4) hipLaunchKernelGGL(k_lm_combine<4>, dim3(R), dim3(256), 0, s, a);
@@ -639,7 +644,9 @@ void launch_rows_gather(int rows, const RowsGather &a, hipStream_t s) {
 // children first (depth 1), then for each later pass the w children of each
 // of the w frontier nodes (frontier rank major, child rank minor).  A score
 // is the parent's score plus the child's log-prob (fp32).  Order key of both
-// the frontier and the output: (score desc, candidate index asc).
+// the frontier and the output: (score desc, candidate index asc), with NaN
+// scores after every number (tree_before), a total order, so that every
+// rank below the cut has exactly one candidate.
 constexpr int TREE_MAXNEW = 256;
 constexpr int TREE_MAXC = MAX_TREE_CAND;
 
@@ -650,10 +657,6 @@ struct TreeExpArgs {
   const int *ids;
   const float *logp;
 };
-
-__device__ __forceinline__ bool rank_before(float sj, int j, float si, int i) {
-  return sj > si || (sj == si && j < i);
-}
 
 __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
   __shared__ float sc[TREE_MAXNEW];
@@ -673,7 +676,7 @@ __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
       row = b * w + pr;
       c = i % w;
       parent = t.front[((size_t)b * (t.D - 1) + (d - 1)) * w + pr];
-      ps = t.cand_score[(size_t)b * t.C + parent];
+      ps = t.cand_score[(size_t)b * t.C + min(max(parent, 0), t.C - 1)];
     }
     const int tok = a.ids[(size_t)row * w + c];
     const float score = ps + a.logp[(size_t)row * w + c];
@@ -689,7 +692,7 @@ __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
   const int L = a.ctx_lens[b];
   for (int i = tid; i < n_new; i += blockDim.x) {
     int rank = 0;
-    for (int j = 0; j < n_new; ++j) rank += rank_before(sc[j], j, sc[i], i);
+    for (int j = 0; j < n_new; ++j) rank += tree_before(sc[j], j, sc[i], i);
     if (rank >= w) continue;
     t.front[((size_t)b * (t.D - 1) + d) * w + rank] = base + i;
     const int nr = b * w + rank;
@@ -775,19 +778,24 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
     }
   }
   __syncthreads();
+  bool nan_seen = false;
   for (int i = tid; i < C; i += blockDim.x) {
     int rank = 0;
-    for (int j = 0; j < C; ++j) rank += rank_before(sc[j], j, sc[i], i);
+    for (int j = 0; j < C; ++j) rank += tree_before(sc[j], j, sc[i], i);
+    nan_seen |= sc[i] != sc[i];
     if (rank < a.v) {
       sel[rank] = i;
       outpos[i] = (short)rank;
     }
   }
+  // a NaN score (from a NaN feature row or weight) is reported; the tree
+  // is still well formed (NaN candidates rank last, parents first)
+  if (nan_seen) atomicOr(t.err, ERRF_NONFINITE);
   __syncthreads();
   if (tid < a.v) {
     const int n = sel[tid];
     const int p = pa[n];
-    const int po = p >= 0 ? outpos[p] : -1;
+    const int po = p >= 0 && p < C ? outpos[p] : -1;
     par[tid] = po;
     const size_t o = (size_t)b * a.v + tid;
     a.tokens[o] = tk[n];
@@ -796,15 +804,7 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
     a.score[o] = sc[n];
   }
   __syncthreads();
-  if (tid < a.v) {
-    uint64_t m = 1ull << tid;
-    int p = par[tid];
-    while (p >= 0) {
-      m |= 1ull << p;
-      p = par[p];
-    }
-    a.mask[(size_t)b * a.v + tid] = m;
-  }
+  if (tid < a.v) a.mask[(size_t)b * a.v + tid] = tree_ancestor_bits(par, tid);
   for (int i = tid; i < C; i += blockDim.x) {
     if (a.c_tok) a.c_tok[(size_t)b * C + i] = tk[i];
     if (a.c_par) a.c_par[(size_t)b * C + i] = pa[i];

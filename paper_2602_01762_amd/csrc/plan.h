@@ -1,0 +1,117 @@
+// Launch plans of the streamed products (host code, plain C++).
+//
+// The runtime plans every product with these functions, and the product
+// kernels take their __launch_bounds__ from product_max_waves, so a plan
+// and the kernel it launches agree by construction.  Nothing here includes a
+// HIP header, so a host unit test compiles this header with g++ and checks
+// the plans of every configured shape.
+#pragma once
+#include <stddef.h>
+
+namespace prism {
+
+// Rows up to which bf16 products take the VALU GEMV main loop (LM head: one
+// row); above it the staged-activation LDS reads, which grow with the rows,
+// cost more than the MFMA path's fixed 16-row tiles.
+constexpr int GEMV_MAX_ROWS = 2;
+constexpr int LM_GEMV_MAX_ROWS = 1;
+constexpr int MAX_ROWS = 64;
+constexpr int MAX_KW = 16;      // waves of one workgroup splitting K
+
+// 16-row tiles of the batch (the MFMA B operand) a product instantiation
+// holds: 1 up to 16 rows, 2 up to 32, else 4.
+constexpr int row_tiles(int R) { return R <= 16 ? 1 : (R <= 32 ? 2 : 4); }
+
+// Waves per workgroup a product instantiation allows (its __launch_bounds__
+// / 64).  Variants with more accumulators (row tiles x tiles per wave >= 2)
+// run at most 8 waves, which leaves them 256 VGPRs.
+constexpr int product_max_waves(int rt, int nt) { return rt * nt >= 2 ? MAX_KW / 2 : MAX_KW; }
+
+// Waves per workgroup of the K-sliced batched product (k_gemm_split).
+constexpr int SPLIT_WAVES = 4;
+
+// LDS of the staged activations of the GEMV main loop (fp32, one or two rows)
+inline size_t gemv_lds_bytes(int R, int K) {
+  const int vr = R <= 1 ? 1 : 2;
+  return (size_t)vr * K * sizeof(float);
+}
+
+struct ProductPlan {
+  int kw = 1;      // waves of one workgroup splitting K
+  int nt = 1;      // output tiles per wave
+  int split = 0;   // > 0: K slices across workgroups (batched path, then a finish pass)
+  int gemv = 0;    // 1: VALU GEMV main loop (bf16, at most GEMV_MAX_ROWS rows)
+};
+
+// Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
+// fragment reuse) and K slices across workgroups: at most one workgroup of
+// 4 waves per CU (longer slices stream better than more of them, and a grid
+// just above the CU count leaves a few CUs with twice the work), at least 4
+// k-blocks per slice, and fp32 slice partials of at most 1/4 of the weight
+// bytes (split * R * N * 4 <= N * K * 2 / 4; at 32 rows the tighter 1/8 cap
+// left the 4096-wide products on 64-128 workgroups: tree 2.695 -> 2.662 ms).
+inline void plan_batched(int n_tiles, int nkb, int K, int R, int &nt, int &split) {
+  nt = n_tiles % 4 == 0 ? 4 : (n_tiles % 2 == 0 ? 2 : 1);
+  if (R > 16 && R <= 32 && n_tiles % 8 == 0) nt = 8;
+  if (R > 32 && nt == 4) nt = 2;
+  const int wgs = (n_tiles / nt + SPLIT_WAVES - 1) / SPLIT_WAVES;
+  int sp = 256 / wgs;
+  if (sp > nkb / 4) sp = nkb / 4;
+  if (sp > K / (8 * R)) sp = K / (8 * R);
+  split = sp < 1 ? 1 : sp;
+}
+
+// Plan of a product of an [N = 16 n_tiles, K] matrix over R rows.  nkb and K
+// are those of the planned k range (the fusion FC may cover its feature
+// columns only); K_full is the width of the staged operand; qkv: the QKV
+// product (its epilogue runs on at most 2 tiles per wave); lds_limit: LDS
+// bytes one workgroup may use.
+inline ProductPlan plan_product(int n_tiles, int nkb, int K, int K_full, int R, bool qkv,
+                                bool bf16, size_t lds_limit) {
+  ProductPlan p;
+  const int rt = row_tiles(R);
+  if (R > GEMV_MAX_ROWS) {
+    plan_batched(n_tiles, nkb, K, R, p.nt, p.split);
+    const int groups = n_tiles / p.nt;
+    if (groups >= 200 && (p.nt == 4 || p.nt == 8) && rt <= 2 && !qkv) {
+      // enough tile groups to fill the chip: K split across the waves of a
+      // workgroup (LDS reduction, epilogue in the kernel), no finish pass;
+      // about 1024 waves in all, within the instantiation's bound
+      p.split = 0;
+      int kw = 1024 / groups;
+      if (kw > product_max_waves(rt, p.nt)) kw = product_max_waves(rt, p.nt);
+      while (kw > 1 && ((kw - 1) * p.nt * rt > 48 || kw > nkb / 4)) --kw;
+      p.kw = kw < 1 ? 1 : kw;
+    }
+    return p;
+  }
+  // 1-2 rows: enough waves to cover HBM latency (about 16 per CU), at least
+  // 4 k-blocks (4 KiB of W) per wave
+  const int groups = n_tiles / p.nt;
+  int kw = (4096 + groups - 1) / groups;
+  if (kw > product_max_waves(rt, p.nt)) kw = product_max_waves(rt, p.nt);
+  // up to 2 workgroups per CU: keep them co-resident (16 waves per CU) so
+  // that a grid of, e.g., 1.5 workgroups per CU runs in one round
+  if (groups <= 512 && groups > 256 && kw > 8) kw = 8;
+  if (kw > nkb / 4) kw = nkb / 4;
+  if (kw < 1) kw = 1;
+  // LDS for the cross-wave sum: (kw - 1) * nt * rt KiB
+  while (kw > 1 && (kw - 1) * p.nt * rt > 48) --kw;
+  p.kw = kw;
+  // GEMV main loop (bf16) when the staged activations fit in the
+  // workgroup's LDS next to the cross-wave partial sums
+  const size_t lds = gemv_lds_bytes(R, K_full) + (size_t)(kw - 1) * 64 * 16 + (size_t)64 * kw * 4;
+  p.gemv = bf16 && lds <= lds_limit ? 1 : 0;
+  if (p.gemv) p.nt = 1;
+  return p;
+}
+
+// Whether a plan's workgroup fits the instantiation it launches (the
+// launcher refuses a plan that does not).
+inline bool plan_fits(const ProductPlan &p, int R) {
+  if (p.split > 0) return true;   // SPLIT_WAVES per workgroup
+  const int rt = p.gemv ? 1 : row_tiles(R);
+  return p.kw >= 1 && p.kw <= product_max_waves(rt, p.gemv ? 1 : p.nt);
+}
+
+}  // namespace prism

@@ -30,10 +30,6 @@ struct Set {
   bool tab_ready = false;
 };
 
-struct Plan {
-  int kw = 1, nt = 1;
-};
-
 struct Pass {            // one forward pass: where its inputs and outputs live
   int set, R, F, topk;
   RowsIn in;
@@ -105,12 +101,19 @@ struct prism_ctx {
 
   hipStream_t cap = nullptr;
   bool use_graph = true;
+  bool enq_bad = false;             // a product plan was refused while enqueueing
   // measurement: event pairs around LM-head launches
   bool profile = false;
   std::vector<hipEvent_t> prof_ev;
   int prof_used = 0;        // pairs recorded by the enqueue in progress
   int prof_last = 0;        // pairs of the last chain/tree call
-  std::map<std::vector<uintptr_t>, hipGraphExec_t> graphs;
+  // captured graphs by key, each with the call count of its last use
+  struct Graph {
+    hipGraphExec_t exec;
+    uint64_t used;
+  };
+  std::map<std::vector<uintptr_t>, Graph> graphs;
+  uint64_t graph_calls = 0;
   std::string msg;
 };
 
@@ -142,46 +145,6 @@ static TiledMat make_tiled(int N, int K, bool bf16) {
   return t;
 }
 static size_t tiled_bytes(const TiledMat &t) { return (size_t)t.n_tiles * t.nkb * 1024; }
-
-// Launch plan of a streamed product: enough waves to cover HBM latency
-// (about 16 per CU), at least 4 k-blocks (4 KiB of W) per wave, and two tiles
-// per wave once batched rows make the B fragments the larger operand stream.
-static Plan plan_for(const TiledMat &t, int R) {
-  Plan p;
-  const int rt = R <= 16 ? 1 : (R <= 32 ? 2 : 4);
-  if (R > 16 && t.n_tiles % 2 == 0 && t.n_tiles >= 1024) p.nt = 2;
-  const int groups = t.n_tiles / p.nt;
-  int kw = (4096 + groups - 1) / groups;
-  const int max_kw = rt * p.nt >= 2 ? MAX_KW / 2 : MAX_KW;   // see gemm_max_threads
-  if (kw > max_kw) kw = max_kw;
-  // up to 2 workgroups per CU: keep them co-resident (16 waves per CU) so
-  // that a grid of, e.g., 1.5 workgroups per CU runs in one round
-  if (groups <= 512 && groups > 256 && kw > 8) kw = 8;
-  if (kw > t.nkb / 4) kw = t.nkb / 4;
-  if (kw < 1) kw = 1;
-  // LDS for the cross-wave sum: (kw - 1) * nt * rt KiB
-  while (kw > 1 && (kw - 1) * p.nt * rt > 48) --kw;
-  p.kw = kw;
-  return p;
-}
-
-// Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
-// fragment reuse) and K slices across workgroups: at most one workgroup of
-// 4 waves per CU (longer slices stream better than more of them, and a grid
-// just above the CU count leaves a few CUs with twice the work), at least 4
-// k-blocks per slice, and fp32 slice partials of at most 1/4 of the weight
-// bytes (split * R * N * 4 <= N * K * 2 / 4; at 32 rows the tighter 1/8 cap
-// left the 4096-wide products on 64-128 workgroups: tree 2.695 -> 2.662 ms).
-static void plan_batched(const TiledMat &t, int R, int &nt, int &split) {
-  nt = t.n_tiles % 4 == 0 ? 4 : (t.n_tiles % 2 == 0 ? 2 : 1);
-  if (R > 16 && R <= 32 && t.n_tiles % 8 == 0) nt = 8;
-  if (R > 32 && nt == 4) nt = 2;
-  const int wgs = (t.n_tiles / nt + 3) / 4;
-  int sp = 256 / wgs;
-  if (sp > t.nkb / 4) sp = t.nkb / 4;
-  if (sp > t.K / (8 * R)) sp = t.K / (8 * R);
-  split = sp < 1 ? 1 : sp;
-}
 
 static void carve(char *&p, void **dst, size_t bytes) {
   *dst = p;
@@ -313,7 +276,8 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
     auto upd = [&](int N, int K) {   // the plan depends on the row count: take every count
       for (int rr = GEMV_MAX_ROWS + 1; rr <= (int)RF; ++rr) {
         int nt, sp;
-        plan_batched(make_tiled(N, K, bf16), rr, nt, sp);
+        const TiledMat t = make_tiled(N, K, bf16);
+        plan_batched(t.n_tiles, t.nkb, t.K, rr, nt, sp);
         if ((size_t)sp * N > pn) pn = (size_t)sp * N;
       }
     };
@@ -385,7 +349,8 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
 }
 
 static void drop_graphs(prism_ctx *c) {
-  for (auto &g : c->graphs) (void)hipGraphExecDestroy(g.second);
+  if (!c->graphs.empty()) (void)hipDeviceSynchronize();   // none may still run
+  for (auto &g : c->graphs) (void)hipGraphExecDestroy(g.second.exec);
   c->graphs.clear();
 }
 
@@ -563,14 +528,6 @@ static RowNorm norm_for(prism_ctx *c, const float *ss, int n_parts, bool own, fl
   return n;
 }
 
-// GEMV main loop (bf16, at most 4 rows) when the staged activations fit in
-// the workgroup's LDS next to the cross-wave partial sums
-static bool use_gemv(const prism_ctx *c, int R, int K, int kw) {
-  if (!c->bf16 || R > GEMV_MAX_ROWS) return false;
-  const size_t lds = gemv_lds_bytes(R, K) + (size_t)(kw - 1) * 64 * 16 + (size_t)64 * kw * 4;
-  return lds <= c->lds_limit;
-}
-
 // kb_lo: the product covers k-blocks [kb_lo, nkb) of m (the fusion FC's
 // feature columns when its embedding half comes from the table)
 static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, int R, int epi,
@@ -581,32 +538,20 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   g.R = R;
   g.epi = epi;
   g.kb_lo = kb_lo;
-  TiledMat pm = m;   // the planned range
-  pm.nkb -= kb_lo;
-  pm.K -= kb_lo * (c->bf16 ? 32 : 16);
-  if (R > GEMV_MAX_ROWS) {
-    plan_batched(pm, R, g.nt, g.split);
-    g.kw = 1;
-    g.part = c->part;
-    const int rt = R <= 16 ? 1 : (R <= 32 ? 2 : 4);
-    const int groups = m.n_tiles / g.nt;
-    if (groups >= 200 && (g.nt == 4 || g.nt == 8) && rt <= 2 && epi != EPI_QKV) {
-      // enough tile groups to fill the chip: K split across the waves of a
-      // workgroup (LDS reduction, epilogue in the kernel), no finish pass;
-      // about 1024 waves in all
-      g.split = 0;
-      int kw = 1024 / groups;
-      while (kw > 1 && ((kw - 1) * g.nt * rt > 48 || kw > pm.nkb / 4)) --kw;
-      g.kw = kw < 1 ? 1 : kw;
-    }
-    return g;
-  }
-  Plan pl = plan_for(pm, R);
+  const int nkb = m.nkb - kb_lo, K = m.K - kb_lo * (c->bf16 ? 32 : 16);
+  const ProductPlan pl =
+      plan_product(m.n_tiles, nkb, K, m.K, R, epi == EPI_QKV, c->bf16, c->lds_limit);
   g.kw = pl.kw;
   g.nt = pl.nt;
-  g.gemv = use_gemv(c, R, m.K, g.kw) ? 1 : 0;
-  if (g.gemv) g.nt = 1;
+  g.split = pl.split;
+  g.gemv = pl.gemv;
+  if (R > GEMV_MAX_ROWS) g.part = c->part;
   return g;
+}
+
+// launch a planned product; a plan the kernels cannot take fails the call
+static void gemm_go(prism_ctx *c, const GemmLaunch &g, hipStream_t s) {
+  if (!launch_gemm(c->bf16, g, s)) c->enq_bad = true;
 }
 
 // Front of a pass: fusion FC and QKV (RoPE, KV append) for p.R rows -> u
@@ -632,14 +577,14 @@ static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStre
                    S.tab_ready ? c->tab_tok : nullptr, S.tab_ready, s);
   }
   g.y = c->u; g.ldy = H; g.gain = S.g1; g.g = c->ug; g.g.ld = H; g.ss = c->ss_u;
-  launch_gemm(bf, g, s);
+  gemm_go(c, g, s);
   const int parts_u = gemm_ss_parts(g);
   // q, k, v = W_qkv RMSNorm(u; g1);  RoPE;  k, v -> cache slot
   g = gemm_of(c, S.qkv, act_of(c->ug, H), R, EPI_QKV);
   g.norm = norm_for(c, c->ss_u, parts_u, gemm_own_scales(g, parts_u), c->sc_u, R, s);
   g.q = c->q; g.nq = c->nq; g.nkv = c->nkv; g.d = c->d;
   g.rows = p.in; g.kv = kv; g.inv_freq = c->inv_freq; g.err = c->err;
-  launch_gemm(bf, g, s);
+  gemm_go(c, g, s);
 }
 
 // Back of a pass, for p.R rows whose q and FC output u are given: attention,
@@ -658,18 +603,18 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   GemmLaunch g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
   g.res = u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
   g.ss = c->ss_r1;
-  launch_gemm(bf, g, s);
+  gemm_go(c, g, s);
   const int parts_r1 = gemm_ss_parts(g);
   // z = SiLU(W_gate m) * (W_up m),  m = RMSNorm(r1; g2)
   g = gemm_of(c, S.gu, act_of(c->r1g, H), R, EPI_SWIGLU);
   g.norm = norm_for(c, c->ss_r1, parts_r1, gemm_own_scales(g, parts_r1), c->sc_r1, R, s);
   g.z = c->z; g.z.ld = c->I;
-  launch_gemm(bf, g, s);
+  gemm_go(c, g, s);
   // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
   g = gemm_of(c, S.down, act_of(c->z, c->I), R, EPI_NORM);
   g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
   g.g.ld = H; g.ss = c->ss_h;
-  launch_gemm(bf, g, s);
+  gemm_go(c, g, s);
   const int parts_h = gemm_ss_parts(g);
   // logits = LM_head RMSNorm(h; g_final)  ->  top-k partials
   LmLaunch lmg{};
@@ -737,10 +682,11 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
     sa.u = p.u; sa.ld_u = p.ld_u;
     sa.ids = p.ids; sa.logp = p.logp_out; sa.ld_logp = p.ld_logp;
     sa.tok_a = p.tok_a; sa.tok_b = p.tok_b; sa.ld_b = p.ld_b;
+    sa.err = c->err;
     launch_lm_sample(sa, s);
   } else if (!p.defer_merge) {
     launch_lm_combine(R, lmg.n_wg, p.topk, c->V, c->lm_max, c->lm_sum, c->lm_val, c->lm_id, p.ids,
-                      p.logp, p.tok_a, p.tok_b, p.ld_b, s);
+                      p.logp, p.tok_a, p.tok_b, p.ld_b, c->err, s);
   }
 }
 
@@ -773,15 +719,23 @@ static prism_status check_batch(prism_ctx *c, const prism_batch *b) {
   return PRISM_OK;
 }
 
+// Graphs kept per context.  Every distinct key (shape, buffers, step map)
+// captures one; past this many the least recently used one is destroyed, so
+// callers that pass fresh output buffers on every call do not grow the
+// cache without bound.
+constexpr size_t GRAPH_CACHE_MAX = 64;
+
 // run `enqueue` directly or through a cached graph keyed by `key`
 template <typename F>
 static prism_status run_graph(prism_ctx *c, const std::vector<uintptr_t> &key, hipStream_t s,
                               F enqueue) {
+  c->enq_bad = false;
   // profiled calls run eagerly: event pairs bracket each LM-head launch on `s`
   if (!c->use_graph || c->profile) {
     c->prof_used = 0;
     enqueue(s);
     c->prof_last = c->prof_used;
+    if (c->enq_bad) return fail(c, PRISM_ERR_SHAPE, "a product plan exceeds its kernel's workgroup bound");
     HIPCHK(c, hipGetLastError());
     return PRISM_OK;
   }
@@ -794,15 +748,27 @@ static prism_status run_graph(prism_ctx *c, const std::vector<uintptr_t> &key, h
     c->prof_last = c->prof_used;
     hipError_t le = hipGetLastError();
     hipError_t ee = hipStreamEndCapture(c->cap, &graph);
+    if (ee == hipSuccess && (le != hipSuccess || c->enq_bad)) (void)hipGraphDestroy(graph);
     if (le != hipSuccess) return fail(c, PRISM_ERR_HIP, "launch during capture: %s", hipGetErrorString(le));
     if (ee != hipSuccess) return fail(c, PRISM_ERR_HIP, "hipStreamEndCapture: %s", hipGetErrorString(ee));
+    if (c->enq_bad) return fail(c, PRISM_ERR_SHAPE, "a product plan exceeds its kernel's workgroup bound");
     hipGraphExec_t exec;
     hipError_t ie = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
     (void)hipGraphDestroy(graph);
     if (ie != hipSuccess) return fail(c, PRISM_ERR_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ie));
-    it = c->graphs.emplace(key, exec).first;
+    if (c->graphs.size() >= GRAPH_CACHE_MAX) {
+      auto lru = c->graphs.begin();
+      for (auto g = c->graphs.begin(); g != c->graphs.end(); ++g)
+        if (g->second.used < lru->second.used) lru = g;
+      // it may still run on some stream of the caller's
+      HIPCHK(c, hipDeviceSynchronize());
+      (void)hipGraphExecDestroy(lru->second.exec);
+      c->graphs.erase(lru);
+    }
+    it = c->graphs.emplace(key, prism_ctx::Graph{exec, 0}).first;
   }
-  HIPCHK(c, hipGraphLaunch(it->second, s));
+  it->second.used = ++c->graph_calls;
+  HIPCHK(c, hipGraphLaunch(it->second.exec, s));
   return PRISM_OK;
 }
 
@@ -848,7 +814,9 @@ prism_status prism_draft_step(prism_ctx *c, int32_t k, const prism_step_io *io, 
   p.ld_logits = c->V;
   p.ids = io->d_topk_ids;
   p.logp = io->d_topk_logp;
+  c->enq_bad = false;
   enqueue_pass(c, p, kv_of(c, b), s);
+  if (c->enq_bad) return fail(c, PRISM_ERR_SHAPE, "a product plan exceeds its kernel's workgroup bound");
   HIPCHK(c, hipGetLastError());
   return PRISM_OK;
 }
@@ -1102,6 +1070,7 @@ prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t de
   t.cand_tok = c->t_ctok; t.cand_par = c->t_cpar; t.cand_score = c->t_cscore;
   t.front = c->t_front;
   t.tok = c->t_tok; t.feat_row = c->t_frow; t.seq = c->t_seq; t.pos = c->t_pos; t.slot = c->t_slot;
+  t.err = c->err;
   auto enqueue = [&](hipStream_t s) {
     launch_tree_setup(B, b.d_tokens, b.d_ctx_lens, c->t_tok, c->t_seq, c->t_pos, c->t_slot,
                       c->t_bits[0], s);
@@ -1172,12 +1141,21 @@ prism_status prism_profile_read(prism_ctx *c, float *total_ms, int32_t *count) {
   return PRISM_OK;
 }
 
+prism_status prism_graph_cache(const prism_ctx *c, int32_t *n_graphs, int32_t *capacity) {
+  if (!c || !n_graphs || !capacity) return PRISM_ERR_INVALID_ARG;
+  *n_graphs = (int32_t)c->graphs.size();
+  *capacity = (int32_t)GRAPH_CACHE_MAX;
+  return PRISM_OK;
+}
+
 prism_status prism_device_status(prism_ctx *c, void *stream) {
   if (!c) return PRISM_ERR_INVALID_ARG;
   HIPCHK(c, hipStreamSynchronize((hipStream_t)stream));
   uint32_t flags = 0, zero = 0;
   HIPCHK(c, hipMemcpy(&flags, c->err, 4, hipMemcpyDeviceToHost));
   HIPCHK(c, hipMemcpy(c->err, &zero, 4, hipMemcpyHostToDevice));
+  if (flags & ERRF_NONFINITE)
+    return fail(c, PRISM_ERR_NONFINITE, "NaN logits or tree scores (NaN in a feature row or a weight)");
   if (flags & ERRF_ROWS) return fail(c, PRISM_ERR_INVALID_ARG, "malformed catch-up offsets");
   if (flags & ERRF_CAPACITY) return fail(c, PRISM_ERR_CAPACITY, "KV slot, block or pool out of range");
   if (flags & ERRF_TOKEN) return fail(c, PRISM_ERR_INVALID_ARG, "token id out of range");

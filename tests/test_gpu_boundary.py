@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from synth import SMALL_BF16_CHAIN, make_inputs, make_weights
+from synth import SMALL_BF16_CHAIN, SMALL_BF16_TREE, make_inputs, make_weights
 from harness import gpu_setup
 
 pytestmark = [pytest.mark.gpu,
@@ -189,4 +189,89 @@ def test_embedding_tables_follow_the_load_order(batch):
     assert torch.equal(a["tokens"], b["tokens"])
     assert torch.equal(a["logits"], b["logits"])
     ref.close()
+    dr.close()
+
+
+def test_tree_with_nan_feature_row_completes_and_is_reported():
+    """A NaN in one sequence's target feature makes every logit and score of
+    that sequence NaN.  The tree call still completes: NaN candidates rank
+    after every number (by creation index among themselves), and the
+    ancestor walk follows only parents that come first.  The flag is reported
+    as PRISM_ERR_NONFINITE.  The other sequence's tree is bit-identical to a
+    clean run, and the NaN sequence's tree is still well formed."""
+    cfg = SMALL_BF16_TREE
+    dr, w, inp = gpu_setup(cfg)
+    ref = {k: v.clone() for k, v in dr.tree(inp).items()}
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    inp.features[0, 5] = float("nan")
+    out = dr.tree(inp)
+    torch.cuda.synchronize()
+    assert dr.device_status() == -8          # PRISM_ERR_NONFINITE
+    assert dr.device_status() == 0
+    for k in ("tokens", "parent", "depth", "score", "mask", "cand_tokens", "cand_score"):
+        assert torch.equal(out[k][1:], ref[k][1:]), k
+    assert torch.isnan(out["score"][0]).all()
+    par = out["parent"][0].cpu().numpy()
+    mask = [int(m) & (2 ** 64 - 1) for m in out["mask"][0].cpu().numpy()]
+    for i in range(cfg.tree_nodes):
+        assert -1 <= par[i] < i
+        assert mask[i] == (1 << i) | (mask[par[i]] if par[i] >= 0 else 0)
+    # a clean call afterwards is unaffected
+    inp.features[0, 5] = 0.0
+    inp2 = make_inputs(cfg, "cuda")
+    out = dr.tree(inp2)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    for k in ("tokens", "parent", "score", "mask"):
+        assert torch.equal(out[k], ref[k]), k
+    dr.close()
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_chain_with_nan_feature_row_completes_and_is_reported(batch):
+    """The same for a greedy chain, at one row (GEMV products, the token
+    taken from the LM-head partials inside the next FC) and three rows
+    (MFMA products, a prep kernel): the NaN row has no arg-max, which is
+    reported; the other rows are bit-identical to a clean run."""
+    cfg = SMALL_BF16_CHAIN.with_(batch=batch)
+    dr, w, inp = gpu_setup(cfg)
+    ref = dr.chain(inp, logits=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    bad = batch - 1
+    inp.features[bad, 3] = float("nan")
+    out = dr.chain(inp, logits=True)
+    torch.cuda.synchronize()
+    assert dr.device_status() == -8          # PRISM_ERR_NONFINITE
+    keep = [b for b in range(batch) if b != bad]
+    assert torch.equal(out["tokens"][keep], ref["tokens"][keep])
+    assert torch.equal(out["logits"][keep], ref["logits"][keep])
+    assert torch.isnan(out["logits"][bad]).all()
+    dr.close()
+
+
+def test_graph_cache_is_bounded():
+    """Every distinct set of output buffers captures a graph; past the
+    cache's capacity the least recently used one is dropped, and every call
+    still drafts the same tokens."""
+    from paper_2602_01762_amd import binding as B
+    cfg = SMALL_BF16_CHAIN.with_(batch=1)
+    dr, w, inp = gpu_setup(cfg)
+    b = dr.batch(inp)
+    ref = dr.chain(inp, K=2, batch=b)["tokens"].clone()
+    n0, cap = B.prism_graph_cache(dr.ctx)
+    assert n0 == 1 and cap >= 8
+    outs = [dr.chain(inp, K=2, batch=b) for _ in range(cap + 6)]   # all buffers kept alive
+    torch.cuda.synchronize()
+    n, _ = B.prism_graph_cache(dr.ctx)
+    assert n == cap
+    for o in outs:
+        assert torch.equal(o["tokens"], ref)
+    # the first buffers were evicted; using them again recaptures correctly
+    again = dr.chain(inp, K=2, out=outs[0], batch=b)
+    torch.cuda.synchronize()
+    assert torch.equal(again["tokens"], ref)
+    assert B.prism_graph_cache(dr.ctx)[0] == cap
+    assert dr.device_status() == 0
     dr.close()

@@ -1,0 +1,180 @@
+"""Host unit tests of the library's plain-C++ rules, compiled with g++ (no GPU).
+
+* tree_order.h: the candidate order of the draft tree and the ancestor walk,
+  on NaN, infinity and tie inputs.  The kernels rank candidates by it, so
+  ranks must form a permutation whatever the scores are.  If they do not,
+  two candidates share a slot and another slot is never written.
+* plan.h: the launch plan of every product of every configured shape and row
+  count fits the kernel instantiation that it selects.
+"""
+import itertools
+import math
+import os
+import struct
+import subprocess
+
+import pytest
+
+from synth import CONFIGS, SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2602_01762_amd", "csrc")
+
+DRIVER = r"""
+#define __host__
+#define __device__
+#include <cstdio>
+#include <cstring>
+#include <cstdint>
+#include "tree_order.h"
+#include "plan.h"
+using namespace prism;
+
+static float f_of(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
+
+int main() {
+  char cmd[16];
+  while (std::scanf("%15s", cmd) == 1) {
+    if (!std::strcmp(cmd, "rank")) {          // n, then n float bit patterns
+      int n; std::scanf("%d", &n);
+      float s[4096];
+      for (int i = 0; i < n; ++i) { unsigned u; std::scanf("%x", &u); s[i] = f_of(u); }
+      for (int i = 0; i < n; ++i) {
+        int r = 0;
+        for (int j = 0; j < n; ++j) r += tree_before(s[j], j, s[i], i);
+        std::printf("%d ", r);
+      }
+      std::printf("\n");
+    } else if (!std::strcmp(cmd, "anc")) {    // n, then n parents
+      int n; std::scanf("%d", &n);
+      int par[64];
+      for (int i = 0; i < n; ++i) std::scanf("%d", &par[i]);
+      for (int i = 0; i < n; ++i) std::printf("%llx ", (unsigned long long)tree_ancestor_bits(par, i));
+      std::printf("\n");
+    } else if (!std::strcmp(cmd, "plan")) {   // n_tiles nkb K K_full R qkv bf16 lds
+      int nt, nkb, K, Kf, R, qkv, bf; long lds;
+      std::scanf("%d %d %d %d %d %d %d %ld", &nt, &nkb, &K, &Kf, &R, &qkv, &bf, &lds);
+      ProductPlan p = plan_product(nt, nkb, K, Kf, R, qkv != 0, bf != 0, (size_t)lds);
+      const int rt = p.gemv ? 1 : row_tiles(R);
+      std::printf("%d %d %d %d %d %d\n", p.kw, p.nt, p.split, p.gemv, plan_fits(p, R) ? 1 : 0,
+                  product_max_waves(rt, p.gemv ? 1 : p.nt));
+    }
+  }
+  return 0;
+}
+"""
+
+
+@pytest.fixture(scope="module")
+def driver(tmp_path_factory):
+    d = tmp_path_factory.mktemp("rules")
+    src = d / "rules.cpp"
+    src.write_text(DRIVER)
+    exe = d / "rules"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-Wall", "-Werror", "-Wno-unused-result", "-I", CSRC, str(src), "-o",
+                    str(exe)], check=True)
+
+    def run(text):
+        return subprocess.run([str(exe)], input=text, check=True, capture_output=True,
+                              text=True).stdout.split("\n")
+    return run
+
+
+def bits(x):
+    return "%08x" % struct.unpack("<I", struct.pack("<f", x))[0]
+
+
+def ranks(driver, scores):
+    line = "rank %d %s\n" % (len(scores), " ".join(bits(s) for s in scores))
+    return [int(t) for t in driver(line)[0].split()]
+
+
+def expected_ranks(scores):
+    """Rank of each candidate by sorting (score desc, index asc) with NaN last."""
+    key = lambda i: (1, 0.0, i) if math.isnan(scores[i]) else (0, -scores[i], i)
+    order = sorted(range(len(scores)), key=key)
+    r = [0] * len(scores)
+    for pos, i in enumerate(order):
+        r[i] = pos
+    return r
+
+
+NAN, INF = float("nan"), float("inf")
+NEG_NAN = struct.unpack("<f", struct.pack("<I", 0xffc00001))[0]
+
+
+@pytest.mark.parametrize("scores", [
+    [0.0, -1.0, -0.5, -1.0, -2.0],                 # exact tie
+    [NAN, -1.0, NAN, 0.0],                         # NaN last, among them by index
+    [NAN] * 7,                                     # every score NaN
+    [-INF, NAN, -INF, -3.0, INF],                  # infinities around NaN
+    [-0.0, 0.0, -0.0],                             # signed zeros compare equal
+    [NEG_NAN, NAN, -INF],                          # NaN of either sign
+    [1e-45, -1e-45, 0.0, 3.4e38, -3.4e38],         # denormals, extremes
+])
+def test_tree_order_is_a_total_order(driver, scores):
+    got = ranks(driver, scores)
+    assert sorted(got) == list(range(len(scores))), "ranks must be a permutation"
+    assert got == expected_ranks(scores)
+
+
+def test_tree_order_random_with_nan_and_ties(driver):
+    import numpy as np
+    rng = np.random.default_rng(0)
+    for trial in range(20):
+        n = int(rng.integers(1, 400))
+        s = rng.choice([-1.0, -0.5, 0.0, NAN, -INF], size=n).astype(np.float32)
+        s = np.where(rng.random(n) < 0.5, s, rng.normal(size=n).astype(np.float32))
+        scores = [float(x) for x in s]
+        got = ranks(driver, scores)
+        assert got == expected_ranks(scores)
+
+
+def test_ancestor_walk_is_bounded_and_exact(driver):
+    # a valid tree: 0 and 1 under the root, 2 under 0, 3 under 2, 4 under 1
+    out = driver("anc 5 -1 -1 0 2 1\n")[0].split()
+    assert [int(x, 16) for x in out] == [0b1, 0b10, 0b101, 0b1101, 0b10010]
+    # corrupt parents (self loop, cycle, forward link, out of range) stop the walk
+    out = driver("anc 5 0 2 1 7 -9\n")[0].split()
+    assert [int(x, 16) for x in out] == [0b1, 0b10, 0b110, 0b1000, 0b10000]
+
+
+def _products(cfg):
+    """(n_tiles, nkb, K, K_full, qkv) of every product a pass of cfg runs."""
+    bf = cfg.dtype == "bf16"
+    kq = 32 if bf else 16
+    H, I = cfg.hidden, cfg.ffn
+    tab = bf and H % 64 == 0
+    out = []
+    for F in {cfg.feat_width, H}:
+        lo = H // kq if tab else 0
+        out.append((H // 16, (H + F) // kq - lo, H + F - lo * kq, H + F, False))
+    out.append((cfg.qkv_dim // 16, H // kq, H, H, True))
+    out.append((H // 16, cfg.n_q_heads * cfg.head_dim // kq, cfg.n_q_heads * cfg.head_dim,
+                cfg.n_q_heads * cfg.head_dim, False))
+    out.append((2 * I // 16, H // kq, H, H, False))
+    out.append((H // 16, I // kq, I, I, False))
+    return out
+
+
+def test_every_plan_fits_its_kernel(driver):
+    cfgs = list(CONFIGS.values()) + [SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN]
+    # the parity tests' wide-FFN and odd-hidden variants
+    cfgs += [SMALL_BF16_CHAIN.with_(ffn=6400), SMALL_BF16_CHAIN.with_(ffn=12800),
+             SMALL_BF16_CHAIN.with_(hidden=480, feat_width=1440)]
+    lines, cases = [], []
+    for cfg in cfgs:
+        bf = 1 if cfg.dtype == "bf16" else 0
+        for (nt, nkb, K, Kf, qkv), R, lds in itertools.product(
+                _products(cfg), range(1, 65), (65536, 163840)):
+            lines.append("plan %d %d %d %d %d %d %d %d" % (nt, nkb, K, Kf, R, qkv, bf, lds))
+            cases.append((cfg.name, nt, nkb, R, qkv, lds))
+    out = driver("\n".join(lines) + "\n")
+    assert len([o for o in out if o]) == len(cases)
+    for case, o in zip(cases, out):
+        kw, nt, split, gemv, fits, maxw = (int(x) for x in o.split())
+        assert fits == 1 and 1 <= kw <= maxw, (case, o)
+        if split == 0 and not gemv:
+            assert 64 * kw <= 64 * maxw
+        if gemv:
+            assert case[3] <= 2 and nt == 1
