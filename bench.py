@@ -7,10 +7,14 @@ vocab 128256, step-1 feature 3 x 4096), batch 1, prior context 2048, bf16,
 every step with its own parameter set.  Weights and inputs are seeded
 synthetic tensors already resident in HBM when timing starts.
 
-Printed (one JSON line): drafted tokens/s, per-draft-step microseconds, the
-roofline of the dominant kernel (the LM-head GEMV with fused top-k, timed
-with HIP events around each of its launches), and the CPU oracle timed on a
-bounded sample of the same workload.
+Printed (one JSON line): drafted tokens/s, per-draft-step microseconds (the
+call time / K, and each step between its own HIP events), the roofline of
+the dominant kernel (the LM-head GEMV with fused top-k, timed with HIP
+events around each of its launches), and the CPU oracle timed on a bounded
+sample of the same workload.  The same line carries, under "bs16", the
+batch-16 half of the metric (same weights, ragged contexts 512-4096, paged
+KV), and under "llama3_70b_bs32" the 70B-shaped batch-32 chain with the
+bf16 MFMA fraction of its weight products.
 """
 import argparse
 import json
@@ -33,7 +37,7 @@ def kernel_source_digest(read=None):
     not with its documentation."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("gemm.hip", "device.h", "internal.h"):
+    for f in ("gemm.hip", "device.h", "internal.h", "plan.h"):
         if read is None:
             with open(os.path.join(ROOT, "paper_2602_01762_amd", "csrc", f)) as fh:
                 text = fh.read()
@@ -206,58 +210,82 @@ def verify_bench(args):
     print(json.dumps(res), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS) + sorted(VERIFY_WORKLOADS))
-    ap.add_argument("--cpu-baseline", type=int, default=1,
-                    help="time the CPU oracle on a bounded sample (0 = skip)")
-    ap.add_argument("--calibrate-copy", type=int, default=0,
-                    help="also run a plain 256 MiB device copy (counter calibration)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py measures the single-GPU drafting path; --gpus %d is not supported "
-              "(the path has no cross-GPU component)." % args.gpus, file=sys.stderr)
-        sys.exit(2)
+def product_flops(cfg, s, rows):
+    """Multiply-add flops (2 per weight element per row) of the weight
+    products of one pass of set s over `rows` rows, as the method defines
+    them: the whole fusion FC, QKV, O, gate/up, down and the LM head."""
+    es = 2 if cfg.dtype == "bf16" else 4
+    return 2 * rows * step_weight_bytes(cfg, s) // es
 
-    if args.workload in VERIFY_WORKLOADS:
-        return verify_bench(args)
 
+def mfma_ceiling(rows):
+    """Largest bf16 MFMA fraction a product can reach while it streams each
+    weight from HBM once: 2 * rows flops per 2-byte weight = rows flop/B,
+    times 8 TB/s, over the 2.5 PFLOP/s dense peak."""
+    return rows * HBM_PEAK_GBS * 1e9 / (BF16_PEAK_TFLOPS * 1e12)
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def make_call(cfg, dr, inp):
+    """The drafting call of a workload on preallocated outputs."""
+    import torch
+    tree = cfg.mode == "tree"
+    b = dr.batch(inp)
+    out = dr.tree_buffers(cfg.batch, cfg.n_steps, debug=False) if tree else \
+        dr.chain_buffers(cfg.batch, cfg.n_steps)
+    if tree:
+        return lambda: dr.tree(inp, out=out, batch=b)
+    if cfg.n_new:      # step 1 prefills every accepted token
+        return lambda: dr.chain_catchup(inp, out=out, batch=b)
+    if cfg.temperature:    # stochastic drafting: draws and their log p_draft
+        out["logp"] = torch.empty((cfg.batch, cfg.n_steps), dtype=torch.float32, device="cuda")
+        return lambda: dr.chain_sample(inp, cfg.temperature, out=out, batch=b)
+    return lambda: dr.chain(inp, out=out, batch=b)
+
+
+def profiled(dr, call, what, steps):
+    """Per-call lists of event-pair milliseconds of the classes `what`
+    (eager launches on the stream, each pair around one launch or pass)."""
+    import torch
+    from paper_2602_01762_amd import binding
+    binding.prism_profile_enable(dr.ctx, what)
+    call()
+    torch.cuda.synchronize()
+    runs = []
+    for _ in range(steps):
+        call()
+        runs.append(binding.prism_profile_pairs(dr.ctx))
+    binding.prism_profile_enable(dr.ctx, 0)
+    return runs
+
+
+def measure(cfg, w, inp, args, gemm=False):
+    """Time one workload: the timed region, per-call spread, per-step and
+    LM-head event timings, and (gemm) the weight products' time."""
     import numpy as np
     import torch
-    from synth import CONFIGS, make_inputs, make_weights
     from paper_2602_01762_amd import Drafter, binding
-
-    cfg = CONFIGS[WORKLOADS[args.workload]]
-    torch.cuda.set_device(0)
-    print("bench: %s, generating weights" % cfg.name, file=sys.stderr, flush=True)
-    w = make_weights(cfg, "cuda")
-    inp = make_inputs(cfg, "cuda")
     dr = Drafter(cfg)
     if cfg.f_map is not None:
         dr.set_step_map(cfg.fmap)
     dr.load(w)
     torch.cuda.synchronize()
     tree = cfg.mode == "tree"
-    b = dr.batch(inp)
-    out = dr.tree_buffers(cfg.batch, cfg.n_steps, debug=False) if tree else \
-        dr.chain_buffers(cfg.batch, cfg.n_steps)
-    if tree:
-        call = lambda: dr.tree(inp, out=out, batch=b)
-    elif cfg.n_new:      # step 1 prefills every accepted token
-        call = lambda: dr.chain_catchup(inp, out=out, batch=b)
-    elif cfg.temperature:    # stochastic drafting: draws and their log p_draft
-        out["logp"] = torch.empty((cfg.batch, cfg.n_steps), dtype=torch.float32, device="cuda")
-        call = lambda: dr.chain_sample(inp, cfg.temperature, out=out, batch=b)
-    else:
-        call = lambda: dr.chain(inp, out=out, batch=b)
-
+    call = make_call(cfg, dr, inp)
     for _ in range(args.warmup):
         call()
     torch.cuda.synchronize()
-    print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    print("bench: %s: timing %d calls" % (cfg.name, args.steps), file=sys.stderr, flush=True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record()
@@ -267,11 +295,12 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     total_ms = e0.elapsed_time(e1)
-    ms_per_step = total_ms / args.steps
+    ms_per_call = total_ms / args.steps
     K = cfg.n_steps
     drafted = cfg.batch * K if not tree else cfg.batch * cfg.tree_nodes
-    value = drafted * args.steps / (total_ms / 1e3)
     assert dr.device_status() == 0
+    m = {"ms_per_call": ms_per_call, "value": drafted * args.steps / (total_ms / 1e3),
+         "wall_s": t_wall}
 
     # per-call distribution: a second pass of the same number of calls, each
     # between its own pair of events (kept out of the timed region above)
@@ -283,40 +312,105 @@ def main():
         a1.record()
     torch.cuda.synchronize()
     per_call = np.array([a0.elapsed_time(a1) for a0, a1 in ev])
-    call_ms = {"median": round(float(np.median(per_call)), 4),
-               "p10": round(float(np.percentile(per_call, 10)), 4),
-               "p90": round(float(np.percentile(per_call, 90)), 4)}
+    m["call_ms"] = {"median": round(float(np.median(per_call)), 4),
+                    "p10": round(float(np.percentile(per_call, 10)), 4),
+                    "p90": round(float(np.percentile(per_call, 90)), 4)}
 
+    # each forward pass between its own events (eager launches): per-step us
+    runs = profiled(dr, call, binding.PRISM_PROFILE_PASSES, args.steps)
+    m["per_step_us"] = [round(float(np.mean([r[k] for r in runs])) * 1e3, 2) for k in range(K)]
     # dominant kernel: HIP events around every LM-head launch (same kernels,
     # launched directly on the stream so the events bracket each launch)
-    binding.prism_profile_enable(dr.ctx, True)
-    call()
-    torch.cuda.synchronize()
-    lm_ms, lm_n = 0.0, 0
-    for _ in range(args.steps):
-        call()
-        ms, n = binding.prism_profile_read(dr.ctx)
-        lm_ms += ms
-        lm_n += n
-    binding.prism_profile_enable(dr.ctx, False)
+    runs = profiled(dr, call, binding.PRISM_PROFILE_LMHEAD, args.steps)
+    lm_ms = [x for r in runs for x in r]
     rows = cfg.batch if not tree else cfg.batch * cfg.tree_width
-    lm_us = lm_ms * 1e3 / max(lm_n, 1)
+    lm_us = float(np.mean(lm_ms)) * 1e3
     lm_b = lm_head_bytes(cfg, rows)
     achieved = lm_b / (lm_us * 1e-6) / 1e9
     kname = ("k_lmhead (LM head, fp32 logits stored; top-k by k_lm_topk)" if lm_topk_pass(cfg, rows)
              else "k_lmhead (LM head GEMV + fused top-k partials)" if rows == 1 and cfg.dtype == "bf16"
              else "k_lmhead (LM head MFMA tiles + fused top-k partials)")
-    roofline = {"kernel": kname, "bound": "hbm",
-                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "avg_launch_us": round(lm_us, 2), "launches_timed": lm_n,
-                "algorithmic_bytes_per_launch": lm_b}
+    m["roofline"] = {"kernel": kname, "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": lm_traffic(cfg),
+                     "avg_launch_us": round(lm_us, 2), "launches_timed": len(lm_ms),
+                     "algorithmic_bytes_per_launch": lm_b}
     chain_bytes = sum(step_weight_bytes(cfg, cfg.fmap[k]) for k in range(K))
     streamed = sum(step_streamed_bytes(cfg, cfg.fmap[k], pass_rows(cfg, k)) for k in range(K))
+    m["weight_bytes_per_step_call"] = chain_bytes
+    m["weight_bytes_streamed_per_step_call"] = streamed
+    m["whole_call_hbm_frac_weights_only"] = round(streamed / (ms_per_call * 1e-3) / 1e9
+                                                  / HBM_PEAK_GBS, 4)
+    if gemm:
+        # the weight products (LM head included) between their own events
+        runs = profiled(dr, call, binding.PRISM_PROFILE_PRODUCTS | binding.PRISM_PROFILE_LMHEAD,
+                        args.steps)
+        g_ms = float(np.mean([sum(r) for r in runs]))
+        flops = sum(product_flops(cfg, cfg.fmap[k], pass_rows(cfg, k)) for k in range(K))
+        tf = flops / (g_ms * 1e-3) / 1e12
+        m["gemm"] = {"flops_per_call": flops, "ms_per_call": round(g_ms, 4),
+                     "launches_per_call": len(runs[0]), "achieved_tflops": round(tf, 1),
+                     "peak_tflops": BF16_PEAK_TFLOPS, "mfma_frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                     "mfma_frac_ceiling_at_hbm_peak": round(mfma_ceiling(cfg.batch), 4),
+                     "note": "algorithmic flops (2 per weight element per row, the whole fusion "
+                             "FC) over the summed event time of the product and LM-head "
+                             "launches; streaming each weight once caps MFMA use at the "
+                             "ceiling given"}
+    dr.close()
+    return m
+
+
+def sub_result(cfg, m):
+    """A secondary workload's figures inside the one JSON line."""
+    out = {"workload": cfg.name, "batch": cfg.batch, "draft_steps": cfg.n_steps,
+           "prior_context": cfg.max_ctx if cfg.ctx_range is None else list(cfg.ctx_range),
+           "ms_per_call": round(m["ms_per_call"], 4),
+           "per_draft_step_us": round(m["ms_per_call"] * 1e3 / cfg.n_steps, 2),
+           "per_step_us": m["per_step_us"], "value": round(m["value"], 1),
+           "unit": "drafted tokens/s", "call_ms": m["call_ms"],
+           "whole_call_hbm_frac_weights_only": m["whole_call_hbm_frac_weights_only"],
+           "roofline": m["roofline"]}
+    if "gemm" in m:
+        out["gemm"] = m["gemm"]
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS) + sorted(VERIFY_WORKLOADS))
+    ap.add_argument("--cpu-baseline", type=int, default=1,
+                    help="time the CPU oracle on a bounded sample (0 = skip)")
+    ap.add_argument("--secondary", type=int, default=1,
+                    help="with the default workload, also time the batch-16 chain and the "
+                         "70B batch-32 chain (0 = skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="also run a plain 256 MiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures the single-GPU drafting path; --gpus %d is not supported "
+              "(the path has no cross-GPU component)." % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    if args.workload in VERIFY_WORKLOADS:
+        return verify_bench(args)
+
+    import torch
+    from synth import CONFIGS, L3_70B_BS32, L3_8B_BS16, make_inputs, make_weights
+
+    cfg = CONFIGS[WORKLOADS[args.workload]]
+    torch.cuda.set_device(0)
+    print("bench: %s, generating weights" % cfg.name, file=sys.stderr, flush=True)
+    w = make_weights(cfg, "cuda")
+    inp = make_inputs(cfg, "cuda")
+    m = measure(cfg, w, inp, args, gemm=cfg.batch >= 16)
+    K = cfg.n_steps
     res = {
         "metric": "drafted tokens/s + per-draft-step µs (8B shape, bs=1/16); % HBM/MFMA peak",
-        "value": round(value, 1), "unit": "drafted tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "value": round(m["value"], 1), "unit": "drafted tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(m["ms_per_call"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
         "data": "synthetic (seeded random-init weights N(0,0.02), features N(0,1), prior KV N(0,1))",
         "config": {"workload": cfg.name, "batch": cfg.batch, "draft_steps": K,
@@ -324,16 +418,18 @@ def main():
                    "kv_block": cfg.kv_block_size, "mode": cfg.mode,
                    "accepted_tokens_step1": list(cfg.n_new) if cfg.n_new else 1,
                    "temperature": cfg.temperature or 0.0},
-        "per_draft_step_us": round(ms_per_step * 1e3 / K, 2),
-        "call_ms": call_ms,
-        "weight_bytes_per_step_call": chain_bytes,
-        "weight_bytes_streamed_per_step_call": streamed,
-        "whole_call_hbm_frac_weights_only": round(streamed / (ms_per_step * 1e-3) / 1e9
-                                                  / HBM_PEAK_GBS, 4),
-        "wall_s": round(t_wall, 4),
-        "roofline": roofline,
+        "per_draft_step_us": round(m["ms_per_call"] * 1e3 / K, 2),
+        "per_step_us": m["per_step_us"],
+        "call_ms": m["call_ms"],
+        "weight_bytes_per_step_call": m["weight_bytes_per_step_call"],
+        "weight_bytes_streamed_per_step_call": m["weight_bytes_streamed_per_step_call"],
+        "whole_call_hbm_frac_weights_only": m["whole_call_hbm_frac_weights_only"],
+        "wall_s": round(m["wall_s"], 4),
+        "roofline": m["roofline"],
     }
-    print("bench: gpu done %.3f ms/step" % ms_per_step, file=sys.stderr, flush=True)
+    if "gemm" in m:
+        res["gemm"] = m["gemm"]
+    print("bench: gpu done %.3f ms/call" % m["ms_per_call"], file=sys.stderr, flush=True)
     if args.calibrate_copy:
         # a copy of known size: its FETCH_SIZE / WRITE_SIZE counters give the
         # KiB-per-byte scale of the same counters on the LM-head kernel
@@ -342,15 +438,24 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-    res["roofline"]["traffic"] = lm_traffic(cfg)
-
     if args.cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(cfg, w, inp, dr)
-    dr.close()
+        res["cpu_baseline"] = cpu_baseline(cfg, w, inp)
+    if args.secondary and args.workload == "8b_bs1":
+        # the other half of the metric (batch 16, same weights) and the 70B
+        # batch-32 chain whose products the MFMA figure is quoted on
+        inp16 = make_inputs(L3_8B_BS16, "cuda")
+        res["bs16"] = sub_result(L3_8B_BS16, measure(L3_8B_BS16, w, inp16, args))
+        del w, inp, inp16
+        torch.cuda.empty_cache()
+        print("bench: %s, generating weights" % L3_70B_BS32.name, file=sys.stderr, flush=True)
+        w70 = make_weights(L3_70B_BS32, "cuda")
+        inp70 = make_inputs(L3_70B_BS32, "cuda")
+        res["llama3_70b_bs32"] = sub_result(L3_70B_BS32, measure(L3_70B_BS32, w70, inp70, args,
+                                                                 gemm=True))
     print(json.dumps(res), flush=True)
 
 
-def cpu_baseline(cfg, w, inp, dr):
+def cpu_baseline(cfg, w, inp):
     """The oracle, as it is, on the host cores: full drafting calls of one
     sequence of the same workload, repeated until about 10 s have passed."""
     import numpy as np
@@ -376,7 +481,7 @@ def cpu_baseline(cfg, w, inp, dr):
             break
     drafted = n * (cfg.n_steps if cfg.mode == "chain" else cfg.tree_nodes)
     return {"value": round(drafted / el, 3), "unit": "drafted tokens/s", "cores": threads,
-            "kind": "oracle",
+            "cpu_model": cpu_model(), "kind": "oracle",
             "sample": "%d full %s calls of sequence 0 (%d draft steps each), fp64 arithmetic on "
                       "the stored (bf16) tensors, %.1f s" % (n, cfg.mode, cfg.n_steps, el)}
 

@@ -347,14 +347,22 @@ prism_status prism_verify_tree(prism_ctx *ctx, int32_t batch, int32_t n_nodes,
 prism_status prism_device_status(prism_ctx *ctx, void *stream);
 
 /* Measurement support (not part of the drafting computation).  With
- * enable != 0, chain and tree calls launch their kernels directly on
- * `stream` instead of replaying a graph, and record a pair of HIP events on
- * that stream around every LM-head launch (the largest product of a step).
- * prism_profile_read() waits for the events of the last chain or tree call
- * and returns the summed milliseconds between each pair and the number of
- * pairs. */
-prism_status prism_profile_enable(prism_ctx *ctx, int32_t enable);
+ * what != 0, drafting calls launch their kernels directly on `stream`
+ * instead of replaying a graph, and record a pair of HIP events on that
+ * stream around every launch of the classes selected by the bits of `what`:
+ * PRISM_PROFILE_LMHEAD each LM-head launch, PRISM_PROFILE_PRODUCTS each
+ * other weight product (fusion FC, QKV, O, gate/up, down; a K-split
+ * product with its finish pass), PRISM_PROFILE_PASSES each whole forward
+ * pass (a chain step, a tree level; the catch-up prefill with its front).
+ * At most 8 pairs per pass are kept.  what = 0 turns profiling off.
+ * prism_profile_read() waits for the event pairs of the last drafting call
+ * and returns their summed milliseconds and their number;
+ * prism_profile_pairs() writes the milliseconds of each pair, in launch
+ * order, to ms[0 .. min(cap, count) - 1] and their number to *count. */
+enum { PRISM_PROFILE_LMHEAD = 1, PRISM_PROFILE_PRODUCTS = 2, PRISM_PROFILE_PASSES = 4 };
+prism_status prism_profile_enable(prism_ctx *ctx, int32_t what);
 prism_status prism_profile_read(prism_ctx *ctx, float *total_ms, int32_t *count);
+prism_status prism_profile_pairs(prism_ctx *ctx, float *ms, int32_t cap, int32_t *count);
 
 /* Captured-graph cache of a context.  Chain and tree calls capture one HIP
  * graph per distinct (call kind, shape, buffer pointers, step map) and

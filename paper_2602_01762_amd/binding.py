@@ -22,7 +22,8 @@ EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_loa
            "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_chain_sample",
            "prism_draft_tree", "prism_verify_chain", "prism_verify_tree",
            "prism_device_status",
-           "prism_profile_enable", "prism_profile_read", "prism_graph_cache")
+           "prism_profile_enable", "prism_profile_read", "prism_profile_pairs",
+           "prism_graph_cache")
 
 c_i32, c_u64, c_f32, c_vp = ctypes.c_int32, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p
 
@@ -107,6 +108,7 @@ def lib():
         L.prism_device_status.argtypes = [c_vp, c_vp]
         L.prism_profile_enable.argtypes = [c_vp, c_i32]
         L.prism_profile_read.argtypes = [c_vp, P(c_f32), P(c_i32)]
+        L.prism_profile_pairs.argtypes = [c_vp, P(c_f32), c_i32, P(c_i32)]
         L.prism_graph_cache.argtypes = [c_vp, P(c_i32), P(c_i32)]
         for n in EXPORTS:
             if n not in ("prism_destroy", "prism_last_error"):
@@ -214,8 +216,12 @@ def prism_device_status(ctx, stream=None) -> int:
     return lib().prism_device_status(ctx, cur_stream() if stream is None else stream)
 
 
-def prism_profile_enable(ctx, enable: bool = True):
-    _check(lib().prism_profile_enable(ctx, 1 if enable else 0), ctx)
+PRISM_PROFILE_LMHEAD, PRISM_PROFILE_PRODUCTS, PRISM_PROFILE_PASSES = 1, 2, 4
+
+
+def prism_profile_enable(ctx, what=PRISM_PROFILE_LMHEAD):
+    """what: PRISM_PROFILE_* bits (True = the LM head), 0 / False = off."""
+    _check(lib().prism_profile_enable(ctx, int(what)), ctx)
 
 
 def prism_profile_read(ctx):
@@ -223,6 +229,13 @@ def prism_profile_read(ctx):
     ms, n = c_f32(), c_i32()
     _check(lib().prism_profile_read(ctx, ctypes.byref(ms), ctypes.byref(n)), ctx)
     return ms.value, n.value
+
+
+def prism_profile_pairs(ctx, cap: int = 512):
+    """Milliseconds of each event pair of the last drafting call, in launch order."""
+    arr, n = (c_f32 * cap)(), c_i32()
+    _check(lib().prism_profile_pairs(ctx, arr, cap, ctypes.byref(n)), ctx)
+    return list(arr[:min(n.value, cap)])
 
 
 def prism_graph_cache(ctx):

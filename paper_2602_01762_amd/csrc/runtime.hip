@@ -104,6 +104,7 @@ struct prism_ctx {
   bool enq_bad = false;             // a product plan was refused while enqueueing
   // measurement: event pairs around LM-head launches
   bool profile = false;
+  int prof_what = 0;        // PRISM_PROFILE_* bits
   std::vector<hipEvent_t> prof_ev;
   int prof_used = 0;        // pairs recorded by the enqueue in progress
   int prof_last = 0;        // pairs of the last chain/tree call
@@ -549,9 +550,23 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   return g;
 }
 
+// measurement: an event pair around the next launches of class `what`
+// (-1: not profiled, or no event pair left)
+static int prof_begin(prism_ctx *c, int what, hipStream_t s) {
+  if (!c->profile || !(c->prof_what & what) || 2 * c->prof_used + 1 >= (int)c->prof_ev.size())
+    return -1;
+  (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
+  return c->prof_used++;
+}
+static void prof_end(prism_ctx *c, int pair, hipStream_t s) {
+  if (pair >= 0) (void)hipEventRecord(c->prof_ev[2 * pair + 1], s);
+}
+
 // launch a planned product; a plan the kernels cannot take fails the call
 static void gemm_go(prism_ctx *c, const GemmLaunch &g, hipStream_t s) {
+  const int pr = prof_begin(c, PRISM_PROFILE_PRODUCTS, s);
   if (!launch_gemm(c->bf16, g, s)) c->enq_bad = true;
+  prof_end(c, pr, s);
 }
 
 // Front of a pass: fusion FC and QKV (RoPE, KV append) for p.R rows -> u
@@ -659,10 +674,9 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
     }
     lmg.no_part = 1;
   }
-  const bool prof = c->profile && c->prof_used * 2 + 1 < (int)c->prof_ev.size();
-  if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
+  const int pr = prof_begin(c, PRISM_PROFILE_LMHEAD, s);
   launch_lmhead(bf, lmg, s);
-  if (prof) (void)hipEventRecord(c->prof_ev[2 * c->prof_used++ + 1], s);
+  prof_end(c, pr, s);
   if (topk_pass) {
     LmTopkArgs ta{};
     ta.logits = lmg.logits; ta.ld = lmg.ld_logits;
@@ -691,8 +705,10 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
 }
 
 static void enqueue_pass(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStream_t s) {
+  const int pr = prof_begin(c, PRISM_PROFILE_PASSES, s);
   enqueue_front(c, p, kv, s);
   enqueue_back(c, p, kv, c->q, c->u, s);
+  prof_end(c, pr, s);
 }
 
 static prism_status check_set(prism_ctx *c, int step, int want_F) {
@@ -815,7 +831,9 @@ prism_status prism_draft_step(prism_ctx *c, int32_t k, const prism_step_io *io, 
   p.ids = io->d_topk_ids;
   p.logp = io->d_topk_logp;
   c->enq_bad = false;
+  c->prof_used = 0;
   enqueue_pass(c, p, kv_of(c, b), s);
+  c->prof_last = c->prof_used;
   if (c->enq_bad) return fail(c, PRISM_ERR_SHAPE, "a product plan exceeds its kernel's workgroup bound");
   HIPCHK(c, hipGetLastError());
   return PRISM_OK;
@@ -874,6 +892,7 @@ static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, 
     p.tok_b = d_out_tokens + (k - 1);
     p.ld_b = K;
     if (k == 1 && cu) {
+      const int pr = prof_begin(c, PRISM_PROFILE_PASSES, s);
       Pass f = p;                 // front over every accepted row
       f.R = cu->total_rows;
       f.in.tokens = cu->d_tokens;
@@ -890,6 +909,7 @@ static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, 
       rg.src[1] = c->u; rg.dst[1] = c->u2; rg.n[1] = H;
       launch_rows_gather(B, rg, s);
       enqueue_back(c, p, kv, c->q2, c->u2, s);
+      prof_end(c, pr, s);
     } else {
       enqueue_pass(c, p, kv, s);
     }
@@ -1109,12 +1129,18 @@ prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t de
   return run_graph(c, key, (hipStream_t)stream, enqueue);
 }
 
-prism_status prism_profile_enable(prism_ctx *c, int32_t enable) {
+prism_status prism_profile_enable(prism_ctx *c, int32_t what) {
   if (!c) return PRISM_ERR_INVALID_ARG;
+  if (what & ~(PRISM_PROFILE_LMHEAD | PRISM_PROFILE_PRODUCTS | PRISM_PROFILE_PASSES))
+    return fail(c, PRISM_ERR_INVALID_ARG, "unknown profile bits 0x%x", (unsigned)what);
   drop_graphs(c);
-  c->profile = enable != 0;
+  c->profile = what != 0;
+  c->prof_what = what;
   if (c->profile && c->prof_ev.empty()) {
-    const int pairs = c->cfg.max_steps;
+    // per pass: one pair for the pass, five products (a split one counted
+    // once) and the LM head; a tree or catch-up call runs at most max_steps
+    // passes
+    const int pairs = c->cfg.max_steps * 8;
     for (int i = 0; i < 2 * pairs; ++i) {
       hipEvent_t e;
       HIPCHK(c, hipEventCreate(&e));
@@ -1122,6 +1148,19 @@ prism_status prism_profile_enable(prism_ctx *c, int32_t enable) {
     }
   }
   c->prof_last = 0;
+  return PRISM_OK;
+}
+
+prism_status prism_profile_pairs(prism_ctx *c, float *ms, int32_t cap, int32_t *count) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  if (!count || (cap > 0 && !ms)) return fail(c, PRISM_ERR_INVALID_ARG, "NULL output");
+  *count = 0;
+  if (!c->profile) return fail(c, PRISM_ERR_INVALID_ARG, "profiling is not enabled");
+  for (int i = 0; i < c->prof_last && i < cap; ++i) {
+    HIPCHK(c, hipEventSynchronize(c->prof_ev[2 * i + 1]));
+    HIPCHK(c, hipEventElapsedTime(&ms[i], c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+  }
+  *count = c->prof_last;
   return PRISM_OK;
 }
 

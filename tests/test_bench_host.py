@@ -70,3 +70,13 @@ def test_several_gpus_are_refused():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode != 0
     assert "single-GPU" in r.stdout + r.stderr
+
+
+def test_mfma_figures():
+    # streaming each weight once: rows flop per byte at 8 TB/s over 2.5 PF
+    assert abs(bench.mfma_ceiling(32) - 32 * 8e12 / 2.5e15) < 1e-12
+    assert abs(bench.mfma_ceiling(32) - 0.1024) < 1e-12
+    # 2 flops per weight element per row; a later step's FC is [H, 2H]
+    H, I, V = 8192, 28672, 128256
+    params = H * 2 * H + (64 + 16) * 128 * H + H * 64 * 128 + 3 * H * I + V * H
+    assert bench.product_flops(L3_70B_BS32, 1, 32) == 2 * 32 * params

@@ -256,6 +256,38 @@ def run_tree_parity(cfg, seqs=None):
     dr.close()
 
 
+# An empty prior context (L_b = 0: the first pass starts from an empty KV
+# cache, Sec. 3.2): the first row attends to its own slot only.  All
+# sequences empty at one row (GEMV) and three rows (MFMA), a ragged batch
+# with one empty sequence among short ones, catch-up prefills from an empty
+# cache, and a tree.
+CTX0 = dict(ctx_range=None, ctx_len=0)
+
+
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_ctx0", **CTX0),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs1_ctx0", batch=1, **CTX0),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_ctx0_mixed", batch=6, ctx_range=(0, 3)),
+    SMALL_F32_CHAIN.with_(name="small_f32_chain_ctx0", **CTX0),
+], ids=lambda c: c.name)
+def test_chain_parity_empty_context(cfg):
+    from synth import ctx_lengths
+    assert (ctx_lengths(cfg) == 0).any()
+    run_chain_parity(cfg)
+
+
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs1_n4_ctx0", batch=1, n_new=(4, 4), **CTX0),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs3_ctx0", batch=3, n_new=(2, 5), **CTX0),
+], ids=lambda c: c.name)
+def test_chain_catchup_parity_empty_context(cfg):
+    test_chain_catchup_parity(cfg)
+
+
+def test_tree_parity_empty_context():
+    run_tree_parity(SMALL_BF16_TREE.with_(name="small_bf16_tree_ctx0", **CTX0))
+
+
 def test_tree_parity_small():
     run_tree_parity(SMALL_BF16_TREE)
 

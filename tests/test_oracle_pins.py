@@ -248,6 +248,83 @@ def test_sampled_chain_equals_brute_force(cfg):
     assert np.max(np.abs(inc["logp"] - (picked - lse))) < 1e-12
 
 
+# ------------------------------------------------------------------ T1d empty prior context
+# The prefill from an initial KV cache that holds nothing yet (Sec. 3.2: the
+# first draft pass starts from KV_(0)): every sequence, or some of a ragged
+# batch, has L_b = 0, so its first row attends to its own slot only.
+TINY_EMPTY = TINY.with_(name="pin_tiny_empty", ctx_range=None, ctx_len=0)
+TINY_MIXED = TINY.with_(name="pin_tiny_mixed", batch=6, ctx_range=(0, 3))   # L_b = 1 2 3 1 3 0
+
+
+@pytest.mark.parametrize("cfg", [TINY_EMPTY, TINY_EMPTY.with_(dtype="bf16"), TINY_MIXED],
+                         ids=["f32", "bf16", "mixed"])
+def test_empty_prior_context_chain_equals_brute_force(cfg):
+    hw, hi = build(cfg)
+    assert (hi["ctx_lens"] == 0).any()
+    orc = Oracle(cfg, hw)
+    inc = orc.chain(hi)
+    bf = brute_chain(orc, hi, cfg.n_steps)
+    assert np.array_equal(inc["tokens"], bf["tokens"])
+    assert np.max(np.abs(inc["hidden"] - bf["hidden"])) < 1e-12
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_empty_prior_context_catchup_equals_brute_force(dtype):
+    cfg = TINY_EMPTY.with_(batch=3, n_new=(2, 4), dtype=dtype)
+    hw, hi = build(cfg)
+    orc = Oracle(cfg, hw)
+    inc = orc.chain(hi, catchup=True)
+    bf = brute_chain(orc, hi, cfg.n_steps, catchup=True)
+    assert np.array_equal(inc["tokens"], bf["tokens"])
+    assert np.max(np.abs(inc["hidden"] - bf["hidden"])) < 1e-12
+    # the accepted rows sit at slots 0 .. n_b - 1, the chain right after them
+    for b in range(cfg.batch):
+        n = int(hi["new_offsets"][b + 1] - hi["new_offsets"][b])
+        assert sorted(inc["draft_kv"][b]) == list(range(n + cfg.n_steps - 1))
+
+
+def test_empty_prior_context_first_step_attends_to_itself():
+    # with L_b = 0 the first row sees one key, its own, so each head's
+    # attention output is its KV head's stored value: o_h = v_(h // g), and
+    # the first step equals a forward pass whose attention is replaced by
+    # that copy (a different computation of the same quantity)
+    cfg = TINY_EMPTY
+    hw, hi = build(cfg)
+    orc = Oracle(cfg, hw)
+    ch = orc.chain(hi, K=1)
+    P = hw["sets"][cfg.fmap[0]]
+    g = cfg.n_q_heads // cfg.n_kv_heads
+    for b in range(cfg.batch):
+        x = np.concatenate([widen(hw["embed"][int(hi["tokens"][b])]), widen(hi["features"][b])])
+        u = widen(P["w_fc"]) @ x
+        a = rmsnorm(u, widen(P["g1"]), cfg.rms_eps)
+        v = orc.store(widen(P["w_v"]) @ a).reshape(cfg.n_kv_heads, cfg.head_dim)
+        o = np.concatenate([v[h // g] for h in range(cfg.n_q_heads)])
+        r1 = u + widen(P["w_o"]) @ o
+        m = rmsnorm(r1, widen(P["g2"]), cfg.rms_eps)
+        hid = r1 + widen(P["w_down"]) @ (silu(widen(P["w_gate"]) @ m) * (widen(P["w_up"]) @ m))
+        assert np.max(np.abs(hid - ch["hidden"][b, 0])) < 1e-12
+
+
+@pytest.mark.parametrize("cfg", [TINY_EMPTY, TINY_EMPTY.with_(dtype="bf16")], ids=["f32", "bf16"])
+def test_empty_prior_context_tree_nodes_equal_forced_chains(cfg):
+    tcfg = cfg.with_(mode="tree", n_steps=3, tree_width=3, tree_nodes=10)
+    hw, hi = build(tcfg)
+    orc = Oracle(tcfg, hw)
+    tr = orc.tree(hi)
+    for b in range(tcfg.batch):
+        c = tr[b]["cand"]
+        for ps in tr[b]["passes"]:
+            d, n, path = ps["depth"], ps["cand"], []
+            while n >= 0:
+                path.append(int(c["token"][n]))
+                n = int(c["parent"][n])
+            forced = np.zeros((tcfg.batch, d + 1), dtype=np.int64)
+            forced[b, :d] = path[::-1]
+            ch = orc.chain(hi, K=d + 1, forced=forced, seqs=[b])
+            assert np.max(np.abs(ch["logits"][b, d] - ps["logits"])) < 1e-12
+
+
 # ------------------------------------------------------------------ T2 tree = chains
 @pytest.mark.parametrize("cfg", [TINY, TINY_BF16], ids=lambda c: c.dtype)
 def test_tree_nodes_equal_forced_chains(cfg):
@@ -316,6 +393,74 @@ def test_tree_frontier_is_topw_of_children():
         # every child score is parent score + a log-prob (<= parent score)
         for n in kids:
             assert c["score"][n] <= c["score"][c["parent"][n]] + 1e-15
+
+
+# ------------------------------------------------------------------ T2b the final cut
+def _cut_by_brute_force(c, v):
+    """The final top-v of a candidate list, from the definitions alone.
+
+    Rank = number of candidates that come first under (score desc, creation
+    index asc), counted pair by pair.  Each kept candidate's path is walked
+    explicitly through the candidate parents; its output parent is the
+    output position of the path's second node, its depth the path's length,
+    its mask the output positions of the whole path.  Returns the kept
+    candidates in rank order and, for each, (token, parent, depth, score,
+    mask), plus whether every kept node's ancestors were kept."""
+    n = len(c["score"])
+    sc = [float(x) for x in c["score"]]
+    rank = [sum(1 for j in range(n) if sc[j] > sc[i] or (sc[j] == sc[i] and j < i))
+            for i in range(n)]
+    kept = sorted((i for i in range(n) if rank[i] < v), key=lambda i: rank[i])
+    pos = {cand: k for k, cand in enumerate(kept)}
+    rows, closed = [], True
+    for cand in kept:
+        path = []
+        x = cand
+        while x >= 0:
+            path.append(x)
+            x = int(c["parent"][x])
+        closed &= all(a in pos for a in path)
+        parent = pos.get(path[1], -99) if len(path) > 1 else -1
+        mask = sum(1 << pos[a] for a in path if a in pos)
+        rows.append((int(c["token"][cand]), parent, len(path), sc[cand], mask))
+    return kept, rows, closed
+
+
+@pytest.mark.parametrize("cfg", [TINY, TINY_BF16, TINY_EMPTY], ids=["f32", "bf16", "empty"])
+@pytest.mark.parametrize("v", [5, 8, 17])
+def test_tree_cut_equals_brute_force(cfg, v):
+    # w = 3, D = 3: 3 + 2 * 9 = 21 candidates, cut to v < 21
+    tcfg = cfg.with_(mode="tree", n_steps=3, tree_width=3, tree_nodes=v)
+    hw, hi = build(tcfg)
+    orc = Oracle(tcfg, hw)
+    tr = orc.tree(hi)
+    for b in range(tcfg.batch):
+        c = tr[b]["cand"]
+        assert len(c["score"]) == tcfg.n_candidates == 21
+        kept, rows, closed = _cut_by_brute_force(c, v)
+        assert closed, "the cut must keep every ancestor of a kept node"
+        assert [int(x) for x in tr[b]["nodes"]] == kept
+        got = list(zip([int(x) for x in tr[b]["tokens"]], [int(x) for x in tr[b]["parent"]],
+                       [int(x) for x in tr[b]["depth"]], [float(x) for x in tr[b]["score"]],
+                       [int(x) for x in tr[b]["mask"]]))
+        assert got == rows
+        # the cut reaches below depth 1 and is not the whole list
+        assert max(r[2] for r in rows) >= 2 and len(kept) < 21
+        # every candidate's score is the sum of its path's log-probs, each
+        # taken from a chain forced along the path
+        for cand in range(21):
+            path, x = [], cand
+            while x >= 0:
+                path.append(x)
+                x = int(c["parent"][x])
+            path = path[::-1]
+            toks = [int(c["token"][a]) for a in path]
+            forced = np.zeros((tcfg.batch, len(path)), dtype=np.int64)
+            forced[b, :] = toks
+            ch = orc.chain(hi, K=len(path), forced=forced, seqs=[b])
+            lp = sum(ch["logits"][b, k, toks[k]] - logsumexp(ch["logits"][b, k])
+                     for k in range(len(path)))
+            assert abs(lp - c["score"][cand]) < 1e-12
 
 
 # ------------------------------------------------------------------ T3 set isolation
