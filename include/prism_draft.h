@@ -88,12 +88,11 @@ typedef struct {
   int32_t tree_nodes;    /* v output nodes of a tree call, <= 64             */
   int32_t max_new_rows;  /* largest total of new accepted tokens in one
                             prism_draft_chain_catchup call (0 = no such
-                            calls), <= 64                                   */
+                            calls), <= 4096                                 */
 } prism_config;
 /* Kernel tiling requires: H, n_q_heads*d, I multiples of 32 (bf16) or 16
  * (fp32); H + F_t likewise; rows per pass (max_batch, or max_batch*w for
- * trees, or max_new_rows) <= 64.  prism_create returns PRISM_ERR_SHAPE
- * otherwise. */
+ * trees) <= 64.  prism_create returns PRISM_ERR_SHAPE otherwise. */
 
 /* Weights of one processing module, as device tensors in the context dtype.
  * Layouts follow y = W x with W row-major [out, in].  The call copies them
@@ -277,7 +276,10 @@ prism_status prism_draft_chain_sample(prism_ctx *ctx, const prism_batch *batch,
  * batch->batch sequences (a malformed table raises PRISM_ERR_INVALID_ARG in
  * prism_device_status and leaves the outputs unspecified).  Outputs as in
  * prism_draft_chain; d_out_logits and d_out_hidden hold the last row's
- * values for step 1.  Requires max_new_rows >= total_rows. */
+ * values for step 1.  Requires max_new_rows >= total_rows.  The fusion FC
+ * and QKV of the accepted rows run in chunks of up to 64 rows (a row's KV
+ * depends on no other row, and the attention runs once every chunk has
+ * written its KV), so a call may take more rows than one pass. */
 prism_status prism_draft_chain_catchup(prism_ctx *ctx, const prism_batch *batch,
                                        const prism_catchup *catchup, int32_t K,
                                        int32_t *d_out_tokens, float *d_out_logits,

@@ -20,6 +20,7 @@ constexpr int NO_TOKEN = 0x7fffffff;
 constexpr int MAX_TOPK = 16;
 constexpr int MAX_VERIFY_NODES = 64;   // tree nodes one verification call takes
 constexpr int MAX_TREE_CAND = 2048;
+constexpr int MAX_NEW_ROWS = 4096;     // accepted rows of one catch-up call
 
 // Tiled weight matrix W[N, K] (y = W x).  Tile t holds 16 output rows;
 // k-block j holds KB consecutive k (KB = 32 for bf16, 16 for fp32).  The
@@ -234,8 +235,13 @@ void launch_chain_setup(int B, int K, const int32_t *tokens, const int32_t *ctx_
 void launch_catchup_setup(int B, int T, int K, const int32_t *offsets, const int32_t *ctx_lens,
                           int32_t *rseq, int32_t *rpos, int32_t *last, int32_t *seq, int32_t *pos,
                           uint32_t *err, hipStream_t s);
-struct RowsGather {              // two dense fp32 matrices [*, n[m]]
-  const int32_t *idx;            // [rows] source row of each destination row, -1: zeros
+// Two dense fp32 matrices [*, n[m]]: destination row b takes source row
+// idx[b] - r0 when r0 <= idx[b] < r0 + n_src (the source holds rows r0 ..
+// r0 + n_src - 1 of a longer list), is left as it is when idx[b] falls
+// outside, and is zeroed when idx[b] = -1 (on the call with r0 = 0).
+struct RowsGather {
+  const int32_t *idx;            // [rows]
+  int r0, n_src;
   const float *src[2];
   float *dst[2];
   int n[2];

@@ -624,14 +624,19 @@ void launch_catchup_setup(int B, int T, int K, const int32_t *offsets, const int
                      ctx_lens, rseq, rpos, last, seq, pos, err);
 }
 
-// For each of two dense fp32 matrices m (blockIdx.z): dst_m[b][0..n_m) =
-// src_m[idx[b]][0..n_m) for b < rows; idx -1 gives zeros.
+// For each of two dense fp32 matrices m (blockIdx.z), destination row b <
+// rows: the source row idx[b] - r0 if it is one of the n_src source rows,
+// zeros if idx[b] = -1 (first chunk only), else nothing.
 __global__ void k_rows_gather(RowsGather a) {
   const int b = blockIdx.y, m = blockIdx.z;
-  const int r = a.idx[b];
+  const int i = a.idx[b];
+  const int r = i - a.r0;
+  const bool take = i >= 0 && r >= 0 && r < a.n_src;
+  const bool zero = i < 0 && a.r0 == 0;
+  if (!take && !zero) return;
   const int n = a.n[m];
   for (int c = blockIdx.x * blockDim.x + threadIdx.x; c < n; c += gridDim.x * blockDim.x)
-    a.dst[m][(size_t)b * n + c] = r >= 0 ? a.src[m][(size_t)r * n + c] : 0.f;
+    a.dst[m][(size_t)b * n + c] = take ? a.src[m][(size_t)r * n + c] : 0.f;
 }
 
 void launch_rows_gather(int rows, const RowsGather &a, hipStream_t s) {

@@ -90,6 +90,7 @@ struct prism_ctx {
   int nsub = 1;                     // attention: 64-slot steps per workgroup
   int lm_nwg_last = 0;              // LM-head partial count of the pass last enqueued
   int new_max = 0;                  // catch-up rows capacity
+  int front_max = 0;                // rows of one catch-up front chunk
   int32_t *c_rseq = nullptr, *c_rpos = nullptr, *c_last = nullptr;   // catch-up rows
   float *q2 = nullptr, *u2 = nullptr;   // q and u of each sequence's last accepted row
   float *samp_logits = nullptr;     // [rows, V] fp32 logits kept for the sampler
@@ -186,8 +187,9 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   if (((k.n_q_heads + 2 * k.n_kv_heads) * k.head_dim + k.head_dim) > 16384)
     return fail(nullptr, PRISM_ERR_SHAPE, "q/k/v width too large");
   if (k.max_steps > 63) return fail(nullptr, PRISM_ERR_SHAPE, "max_steps > 63");
-  if (k.max_new_rows < 0 || k.max_new_rows > MAX_ROWS)
-    return fail(nullptr, PRISM_ERR_SHAPE, "max_new_rows %d out of 0..%d", k.max_new_rows, MAX_ROWS);
+  if (k.max_new_rows < 0 || k.max_new_rows > MAX_NEW_ROWS)
+    return fail(nullptr, PRISM_ERR_SHAPE, "max_new_rows %d out of 0..%d", k.max_new_rows,
+                MAX_NEW_ROWS);
   const int w = k.tree_width;
   const int rows = k.max_batch * (w > 1 ? w : 1);
   if (rows > MAX_ROWS) return fail(nullptr, PRISM_ERR_SHAPE, "rows per pass %d > %d", rows, MAX_ROWS);
@@ -239,11 +241,13 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->n_wg_lm = lm_workgroups(c->lm.n_tiles, 1);
   if (const char *e = getenv("PRISM_NO_GRAPH")) c->use_graph = !(e[0] == '1');
 
-  // rows of a full pass (R) and of the fusion FC / QKV front of a catch-up
-  // step (RF: every accepted token)
+  // rows of a full pass (R) and of one chunk of the fusion FC / QKV front of
+  // a catch-up step (RF: the accepted tokens, at most MAX_ROWS per chunk)
   const size_t R = rows, es = c->esz;
-  const size_t RF = rows > k.max_new_rows ? rows : k.max_new_rows;
+  const int front_rows = k.max_new_rows < MAX_ROWS ? k.max_new_rows : MAX_ROWS;
+  const size_t RF = rows > front_rows ? rows : front_rows;
   c->new_max = k.max_new_rows;
+  c->front_max = (int)RF;
   size_t total = 0;
   std::vector<std::pair<void **, size_t>> L;
   auto add = [&](void **p, size_t b) { L.push_back({p, b}); total += (b + 255) & ~(size_t)255; };
@@ -893,21 +897,32 @@ static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, 
     p.ld_b = K;
     if (k == 1 && cu) {
       const int pr = prof_begin(c, PRISM_PROFILE_PASSES, s);
-      Pass f = p;                 // front over every accepted row
-      f.R = cu->total_rows;
-      f.in.tokens = cu->d_tokens;
-      f.in.feat = cu->d_features;
-      f.in.feat_bf16 = (int)c->bf16;
-      f.in.feat_ld = c->cfg.feat_width;
-      f.in.seq = c->c_rseq;
-      f.in.pos = c->c_rpos;
-      f.in.slot = c->c_rpos;
-      enqueue_front(c, f, kv, s);
-      RowsGather rg{};
-      rg.idx = c->c_last;
-      rg.src[0] = c->q; rg.dst[0] = c->q2; rg.n[0] = c->nq * c->d;
-      rg.src[1] = c->u; rg.dst[1] = c->u2; rg.n[1] = H;
-      launch_rows_gather(B, rg, s);
+      // front over every accepted row, in chunks of at most front_max rows:
+      // the front (FC, QKV, KV append) of one row depends on no other row,
+      // and only each sequence's last row runs the attention, after every
+      // chunk has written its KV; that row's q and u are kept as its chunk
+      // passes
+      const size_t fb = (size_t)c->cfg.feat_width * c->esz;
+      for (int r0 = 0; r0 < cu->total_rows; r0 += c->front_max) {
+        const int n = cu->total_rows - r0 < c->front_max ? cu->total_rows - r0 : c->front_max;
+        Pass f = p;
+        f.R = n;
+        f.in.tokens = cu->d_tokens + r0;
+        f.in.feat = (const char *)cu->d_features + (size_t)r0 * fb;
+        f.in.feat_bf16 = (int)c->bf16;
+        f.in.feat_ld = c->cfg.feat_width;
+        f.in.seq = c->c_rseq + r0;
+        f.in.pos = c->c_rpos + r0;
+        f.in.slot = c->c_rpos + r0;
+        enqueue_front(c, f, kv, s);
+        RowsGather rg{};
+        rg.idx = c->c_last;
+        rg.r0 = r0;
+        rg.n_src = n;
+        rg.src[0] = c->q; rg.dst[0] = c->q2; rg.n[0] = c->nq * c->d;
+        rg.src[1] = c->u; rg.dst[1] = c->u2; rg.n[1] = H;
+        launch_rows_gather(B, rg, s);
+      }
       enqueue_back(c, p, kv, c->q2, c->u2, s);
       prof_end(c, pr, s);
     } else {

@@ -140,11 +140,10 @@ L3_70B_BS32 = DraftConfig(
 
 # Catch-up chains: step 1 prefills every token accepted in the last
 # verification (the paper's S_acc; with K = 5 drafts, up to K + 1 = 6 tokens
-# can be accepted per cycle; the batch-16 shape keeps the total within the
-# 64-row pass capacity).
+# can be accepted per cycle, so batch 16 brings up to 96 rows).
 L3_8B_BS1_CATCHUP = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_catchup4", n_new=(4, 4))
 L3_8B_BS16_CATCHUP = L3_8B_BS16.with_(name="llama3_8b_bf16_chain_bs16_paged_catchup",
-                                      n_new=(1, 4))
+                                      n_new=(1, 6))
 
 # The paper's second target family (Sec. 4 "Target LLMs": Llama-2 7B; MHA,
 # vocabulary 32000).  The draft fuses only the target's last-layer hidden

@@ -92,7 +92,7 @@ def _cfg(**kw):
     (dict(max_batch=65), -2),            # more than 64 rows per pass
     (dict(tree_width=8, tree_nodes=0, max_steps=3), -2),
     (dict(tree_width=8, tree_nodes=60, max_steps=9, max_batch=1), -2),  # > 64 draft slots
-    (dict(max_new_rows=65), -2),         # more than 64 catch-up rows
+    (dict(max_new_rows=4097), -2),       # more than 4096 catch-up rows
     (dict(max_new_rows=-1), -2),
 ])
 def test_create_rejects_bad_config(bad, code):

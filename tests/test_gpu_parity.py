@@ -81,6 +81,12 @@ def test_chain_parity_unsplit_products(cfg):
     SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs3", batch=3, n_new=(1, 5)),
     SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs12", batch=12, n_new=(1, 4)),
     SMALL_F32_CHAIN.with_(name="small_f32_catchup", n_new=(1, 4)),
+    # more accepted rows than one pass takes: the front runs in chunks of 64
+    # rows, a sequence's rows may straddle two chunks
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs16_n1to6", batch=16, n_new=(1, 6)),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs1_n70", batch=1, n_new=(70, 70),
+                           ctx_range=(37, 100)),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs5_n30to40", batch=5, n_new=(30, 40)),
 ], ids=lambda c: c.name)
 def test_chain_catchup_parity(cfg):
     log("catch-up parity", cfg.name)
