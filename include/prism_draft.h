@@ -194,7 +194,8 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out);
 void prism_destroy(prism_ctx *ctx);
 
 /* Message of the last failed call on ctx (empty if none); valid until the
- * next call on ctx.  With ctx == NULL: the last prism_create failure. */
+ * next call on ctx.  With ctx == NULL: the last failure of a call that takes
+ * no context (prism_create, prism_verify_chain_static). */
 const char *prism_last_error(const prism_ctx *ctx);
 
 /* Load the frozen shared tensors (paper Table 2: E and LM_head are frozen
@@ -321,6 +322,27 @@ prism_status prism_verify_chain(prism_ctx *ctx, int32_t batch, int32_t K, float 
                                 const float *d_target_logits, const float *d_draft_logits,
                                 const int32_t *d_draft_tokens, const float *d_uniforms,
                                 int32_t *d_n_accepted, int32_t *d_next_token, void *stream);
+
+/* prism_verify_chain for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same verification and kernels, with no context and no
+ * allocation.  The statistics of the logits rows live in a fixed device
+ * array of the library, one copy per GPU (1 MiB + 256 B, held until the
+ * process ends), whose address is resolved once per device (by
+ * prism_create, or by the first call on that device).  vocab is V (a
+ * multiple of 16); batch * (K + 1) rows, plus batch * K when sampled, may
+ * not exceed 8192 (PRISM_ERR_SHAPE otherwise); K <= 63.  Other arguments,
+ * outputs and draws are those of prism_verify_chain.  Every call on one GPU
+ * shares that array: calls that overlap on one GPU (other streams, other
+ * threads) race and must be serialised by the caller.  An out-of-range draft
+ * id is not kept, as in prism_verify_chain, but raises no flag (there is no
+ * context to report it).  Errors: prism_last_error(NULL). */
+prism_status prism_verify_chain_static(int32_t vocab, int32_t batch, int32_t K,
+                                       float temperature, const float *d_target_logits,
+                                       const float *d_draft_logits,
+                                       const int32_t *d_draft_tokens, const float *d_uniforms,
+                                       int32_t *d_n_accepted, int32_t *d_next_token,
+                                       void *stream);
 
 /* Greedy verification of a draft tree (paper Sec. 2, tree verification
  * under a tree attention mask): target logits row 0 is for the token after

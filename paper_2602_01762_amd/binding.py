@@ -20,7 +20,8 @@ STATUS = {0: "PRISM_OK", -1: "PRISM_ERR_INVALID_ARG", -2: "PRISM_ERR_SHAPE",
 EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_load_shared",
            "prism_draft_load_params", "prism_set_step_map", "prism_draft_step",
            "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_chain_sample",
-           "prism_draft_tree", "prism_verify_chain", "prism_verify_tree",
+           "prism_draft_tree", "prism_verify_chain", "prism_verify_chain_static",
+           "prism_verify_tree",
            "prism_device_status",
            "prism_profile_enable", "prism_profile_read", "prism_profile_pairs",
            "prism_graph_cache")
@@ -103,6 +104,8 @@ def lib():
         L.prism_draft_tree.argtypes = [c_vp, P(prism_batch), c_i32, P(prism_tree_out), c_vp]
         L.prism_verify_chain.argtypes = [c_vp, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                          c_vp, c_vp]
+        L.prism_verify_chain_static.argtypes = [c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp,
+                                                c_vp, c_vp, c_vp, c_vp]
         L.prism_verify_tree.argtypes = [c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp,
                                         c_vp]
         L.prism_device_status.argtypes = [c_vp, c_vp]
@@ -202,6 +205,16 @@ def prism_verify_chain(ctx, batch: int, K: int, temperature: float, target_logit
                                     ptr(draft_logits), ptr(draft_tokens), ptr(uniforms),
                                     ptr(n_accepted), ptr(next_token),
                                     cur_stream() if stream is None else stream), ctx)
+
+
+def prism_verify_chain_static(vocab: int, batch: int, K: int, temperature: float, target_logits,
+                              draft_logits, draft_tokens, uniforms, n_accepted, next_token,
+                              stream=None):
+    _check(lib().prism_verify_chain_static(vocab, batch, K, float(temperature),
+                                           ptr(target_logits), ptr(draft_logits),
+                                           ptr(draft_tokens), ptr(uniforms), ptr(n_accepted),
+                                           ptr(next_token),
+                                           cur_stream() if stream is None else stream), None)
 
 
 def prism_verify_tree(ctx, batch: int, n_nodes: int, target_logits, tokens, parent, n_accepted,

@@ -9,6 +9,10 @@ namespace prism {
 
 typedef uint16_t bf16_t;  // bf16 storage (bit pattern)
 
+// message of the last failed call that takes no context (prism_create, the
+// static verification), read by prism_last_error(NULL)
+void set_global_error(const char *msg);
+
 // device error flags: set by kernels on an out-of-range device value
 // (capacity, token, rows), or on logits that are NaN (nonfinite: every
 // logit of a row NaN, or a NaN tree score)
@@ -199,6 +203,9 @@ struct LmSampleArgs {
 bool lm_sample_fits(int n_wg, int group);
 void launch_lm_sample(const LmSampleArgs &a, hipStream_t s);
 // ---- launchers (verify.hip) -----------------------------------------------
+// device address of the static verification scratch on the current device
+// (resolved once per device)
+hipError_t verify_scratch(void **out);
 // workspace for the per-slice statistics of `rows` logits rows
 size_t verify_stats_bytes(int rows);
 void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, const float *dl,

@@ -49,6 +49,8 @@ std::string g_create_error;
 
 }  // namespace
 
+void prism::set_global_error(const char *msg) { g_create_error = msg; }
+
 struct prism_ctx {
   prism_config cfg{};
   bool bf16 = true;
@@ -344,6 +346,15 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   std::vector<double> inv(c->d / 2);
   for (int i = 0; i < c->d / 2; ++i) inv[i] = std::pow((double)k.rope_theta, -2.0 * i / c->d);
   (void)hipMemcpy(c->inv_freq, inv.data(), inv.size() * 8, hipMemcpyHostToDevice);
+  {   // the static verification scratch of this device, resolved at set-up
+    void *vs = nullptr;
+    const hipError_t e = verify_scratch(&vs);
+    if (e != hipSuccess) {
+      (void)hipFree(c->ws);
+      delete c;
+      return fail(nullptr, PRISM_ERR_HIP, "hipGetSymbolAddress: %s", hipGetErrorString(e));
+    }
+  }
   if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) {
     (void)hipFree(c->ws);
     delete c;

@@ -12,7 +12,12 @@
 // logits), z = logit / T; one workgroup per sequence then merges the slices
 // in order and takes the decisions.  Draws use the drafter's inverse CDF
 // in token-id order.
+#include <cstdarg>
+#include <cstdio>
+#include <mutex>
+
 #include "device.h"
+#include "prism_draft.h"
 
 namespace prism {
 
@@ -322,6 +327,92 @@ __global__ __launch_bounds__(64) void k_verify_tree(VerifyTreeArgs a) {
 }
 
 size_t verify_stats_bytes(int rows) { return (size_t)rows * VSPLIT * sizeof(RowStat); }
+
+// ---------------------------------------------------------------------------
+// Chain verification that allocates nothing, for callers that cannot call
+// hipMalloc (graph capture, serving loops): the per-slice row statistics and
+// the kernels' error word live in this file-scope device array, one copy per
+// GPU, held until the process ends.  Its device address comes from
+// hipGetSymbolAddress, once per device (in prism_create, or at the first
+// call on a device); host code never passes the array's own name.
+constexpr int VSTATIC_ROWS = 8192;   // logits rows statistics are kept for
+constexpr size_t VSTATIC_BYTES = 256 + (size_t)VSTATIC_ROWS * VSPLIT * sizeof(RowStat);
+static __device__ __align__(256) unsigned char scratch[VSTATIC_BYTES];
+
+namespace {
+constexpr int SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[SCRATCH_DEVICES] = {};
+
+prism_status static_fail(prism_status st, const char *fmt, ...) {
+  char buf[256];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  set_global_error(buf);
+  return st;
+}
+}  // namespace
+
+hipError_t verify_scratch(void **out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= SCRATCH_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace prism
+
+extern "C" prism_status prism_verify_chain_static(int32_t vocab, int32_t batch, int32_t K,
+                                                  float temperature, const float *d_target_logits,
+                                                  const float *d_draft_logits,
+                                                  const int32_t *d_draft_tokens,
+                                                  const float *d_uniforms, int32_t *d_n_accepted,
+                                                  int32_t *d_next_token, void *stream) {
+  using namespace prism;
+  if (vocab < 16 || vocab % 16)
+    return static_fail(PRISM_ERR_SHAPE, "vocab %d must be a positive multiple of 16", vocab);
+  if (batch < 1 || K < 1 || K >= VER_MAXK)
+    return static_fail(PRISM_ERR_INVALID_ARG, "batch %d / K %d out of range (K < %d)", batch,
+                       K, VER_MAXK);
+  if (!(temperature >= 0.f) || (temperature > 0.f && !std::isfinite(1.f / temperature)))
+    return static_fail(PRISM_ERR_INVALID_ARG, "temperature %g", (double)temperature);
+  const bool sampled = temperature > 0.f;
+  if (!d_target_logits || !d_draft_tokens || !d_n_accepted || !d_next_token ||
+      (sampled && (!d_draft_logits || !d_uniforms)))
+    return static_fail(PRISM_ERR_INVALID_ARG, "NULL pointer");
+  const long rows = (long)batch * (K + 1) + (sampled ? (long)batch * K : 0);
+  if (rows > VSTATIC_ROWS)
+    return static_fail(PRISM_ERR_SHAPE,
+                       "%ld logits rows exceed the %d the static scratch holds "
+                       "(batch * (K + 1), plus batch * K when sampled)",
+                       rows, VSTATIC_ROWS);
+  void *base = nullptr;
+  hipError_t e = verify_scratch(&base);
+  if (e != hipSuccess)
+    return static_fail(PRISM_ERR_HIP, "hipGetSymbolAddress: %s", hipGetErrorString(e));
+  uint32_t *err = (uint32_t *)base;                    // written by the kernels, never read
+  void *stats = (unsigned char *)base + 256;
+  launch_verify_chain(batch, K, vocab, sampled ? 1.f / temperature : 0.f, d_target_logits,
+                      d_draft_logits, d_draft_tokens, d_uniforms, d_n_accepted, d_next_token,
+                      stats, err, (hipStream_t)stream);
+  e = hipGetLastError();
+  if (e != hipSuccess) return static_fail(PRISM_ERR_HIP, "launch: %s", hipGetErrorString(e));
+  return PRISM_OK;
+}
+
+namespace prism {
 
 void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, const float *dl,
                          const int32_t *drafts, const float *u, int32_t *n_acc, int32_t *next,
