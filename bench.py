@@ -375,12 +375,74 @@ def sub_result(cfg, m):
     return out
 
 
+def tree_cycle_bench(args):
+    """One tree speculation cycle on the 8B shapes: the drafter's tree call
+    (batch 4, D 6, w 8, v 60), the target model's pass over the root and the
+    60 nodes of each tree under the tree mask (one transformer layer of the
+    8B shape with its own weights and the shared-shape LM head, 4 x 61 rows
+    in passes of up to 64), and greedy tree verification of its logits."""
+    import numpy as np
+    import torch
+    from synth import L3_8B_TREE, make_inputs, make_weights, scoring_target
+    from paper_2602_01762_amd import Drafter
+    torch.cuda.set_device(0)
+    cfg, tcfg = L3_8B_TREE, scoring_target(L3_8B_TREE)
+    print("bench: %s + %s, generating weights" % (cfg.name, tcfg.name), file=sys.stderr, flush=True)
+    w, inp = make_weights(cfg, "cuda"), make_inputs(cfg, "cuda")
+    wt, it = make_weights(tcfg.with_(seed=7), "cuda"), make_inputs(tcfg, "cuda")
+    it.features.zero_()
+    dr, tdr = Drafter(cfg), Drafter(tcfg, max_batch=64)
+    dr.load(w)
+    tdr.load(wt)
+    tree = dr.tree_buffers(cfg.batch, cfg.n_steps, debug=False)
+    b, tb = dr.batch(inp), tdr.batch(it)
+    lg = torch.empty((cfg.batch, cfg.tree_nodes + 1, cfg.vocab), dtype=torch.float32, device="cuda")
+    parts = {"draft": lambda: dr.tree(inp, out=tree, batch=b),
+             "score": lambda: tdr.score_tree(it, tree["tokens"], tree["depth"], tree["mask"],
+                                             out=lg, batch=tb),
+             "verify": lambda: tdr.verify_tree(lg, tree["tokens"], tree["parent"])}
+    cycle = lambda: [f() for f in parts.values()]
+    for _ in range(args.warmup):
+        cycle()
+    torch.cuda.synchronize()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    t = {}
+    for name, f in list(parts.items()) + [("cycle", cycle)]:
+        e0, e1 = ev(), ev()
+        e0.record()
+        for _ in range(args.steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        t[name] = e0.elapsed_time(e1) * 1e3 / args.steps
+    assert dr.device_status() == 0 and tdr.device_status() == 0
+    rows = cfg.batch * (cfg.tree_nodes + 1)
+    # the scoring passes: per pass the layer's weights (FC over [E(x) ; 0],
+    # QKV, O, gate/up, down) and the LM head, plus the logits rows written
+    npass = -(-rows // 64)
+    score_bytes = npass * (step_weight_bytes(tcfg, 0) - 2 * tcfg.hidden * tcfg.hidden) \
+        + rows * cfg.vocab * 4
+    res = {"metric": "tree speculation cycle latency (draft tree + target scoring + verify)",
+           "value": round(t["cycle"], 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(t["cycle"] / 1e3, 5),
+           "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded random-init drafter and one-layer target)",
+           "config": {"workload": "llama3_8b_tree_bs4_score_verify", "batch": cfg.batch,
+                      "depth": cfg.n_steps, "width": cfg.tree_width, "nodes": cfg.tree_nodes,
+                      "target_rows": rows, "target_passes": npass},
+           "part_us": {k: round(v, 2) for k, v in t.items() if k != "cycle"},
+           "score_hbm_frac": round(score_bytes / (t["score"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "score_bytes_per_call": score_bytes}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="8b_bs1", choices=sorted(WORKLOADS) + sorted(VERIFY_WORKLOADS))
+    ap.add_argument("--workload", default="8b_bs1",
+                    choices=sorted(WORKLOADS) + sorted(VERIFY_WORKLOADS) + ["8b_tree_cycle"])
     ap.add_argument("--cpu-baseline", type=int, default=1,
                     help="time the CPU oracle on a bounded sample (0 = skip)")
     ap.add_argument("--secondary", type=int, default=1,
@@ -396,6 +458,8 @@ def main():
 
     if args.workload in VERIFY_WORKLOADS:
         return verify_bench(args)
+    if args.workload == "8b_tree_cycle":
+        return tree_cycle_bench(args)
 
     import torch
     from synth import CONFIGS, L3_70B_BS32, L3_8B_BS16, make_inputs, make_weights

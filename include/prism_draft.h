@@ -299,6 +299,31 @@ prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
                               int32_t depth, const prism_tree_out *out,
                               void *stream);
 
+/* Target-side scoring of draft trees (paper Sec. 2: the target model scores
+ * every candidate of a draft tree in one forward pass under a tree attention
+ * mask; the logits then go to prism_verify_tree).  ctx holds the scoring
+ * model in the layer structure of this library (one transformer layer with
+ * its own weights, the set of step 1, its own frozen embedding, LM head and
+ * KV cache).  For sequence b (prior context L_b = batch->d_ctx_lens[b] in the
+ * scoring model's cache):
+ *   row 0      the root, batch->d_tokens[b], at position and KV slot L_b;
+ *   row 1 + j  tree node j, d_tokens[b*n_nodes + j], at position
+ *              L_b + d_depth[b*n_nodes + j] and slot L_b + 1 + j, attending to
+ *              the prior context, the root and the nodes of
+ *              d_mask[b*n_nodes + j] (its ancestors and itself);
+ * every row fuses batch->d_features row b.  d_tokens, d_depth and d_mask are
+ * [B, n_nodes] as prism_draft_tree writes them (node order: every parent
+ * before its children).  Writes d_logits [B, n_nodes + 1, V] fp32 (row 0:
+ * the token after the root; row 1 + j: after node j) and the KV slots
+ * L_b .. L_b + n_nodes.  The rows run in passes of up to max_batch *
+ * max(1, tree_width) rows (at most 64), in tree order.  n_nodes <= 63.  A
+ * depth outside 1..n_nodes, or a mask without the node's own bit or naming a
+ * later node, is clamped and raises PRISM_ERR_INVALID_ARG in
+ * prism_device_status. */
+prism_status prism_score_tree(prism_ctx *ctx, const prism_batch *batch, int32_t n_nodes,
+                              const int32_t *d_tokens, const int32_t *d_depth,
+                              const uint64_t *d_mask, float *d_logits, void *stream);
+
 /* Verification of drafted chains (paper Sec. 2, speculative decoding): the
  * target model has scored the K drafts of each sequence in one pass, giving
  * logits row i for the token after i drafts (i = 0..K).  Greedy
@@ -365,7 +390,8 @@ prism_status prism_verify_tree(prism_ctx *ctx, int32_t batch, int32_t n_nodes,
  * call, the first that applies of: PRISM_ERR_NONFINITE (a row whose logits
  * are all NaN, or a NaN tree score: the tokens of such a row are
  * unspecified and may lie outside 0..V-1; other rows are unaffected),
- * PRISM_ERR_INVALID_ARG (malformed catch-up offsets), PRISM_ERR_CAPACITY
+ * PRISM_ERR_INVALID_ARG (malformed catch-up offsets or tree-scoring rows),
+ * PRISM_ERR_CAPACITY
  * (block table / pool / slot out of range), PRISM_ERR_INVALID_ARG (token id
  * out of range), else PRISM_OK.  Clears the flags. */
 prism_status prism_device_status(prism_ctx *ctx, void *stream);

@@ -21,7 +21,10 @@ What is computed (PRISM, Sec. 3.2 "Draft with PRISM"; notation of Table 2):
     Fig. 3(b) caption: the KV cache passes from one module to the next);
   * the same steps laid out as a draft tree with a tree attention mask
     (Sec. 2 "SoTA Draft Models"; Sec. 3.2 says PRISM is compatible with tree
-    drafts; Sec. 4.1 and 4.3 give the depth / width / verified-node topology).
+    drafts; Sec. 4.1 and 4.3 give the depth / width / verified-node topology);
+  * the target's side of tree verification: one pass of a scoring model
+    over the root and every node of a drafted tree under its ancestor mask
+    (Sec. 2, speculative decoding with tree attention).
 
 Readings where the paper is silent:
 the decode equation is read as H_in = F(E(x_{k-1}), h_{k-2})
@@ -420,6 +423,43 @@ class Oracle:
                       "nodes": order, "tokens": c["token"][order], "parent": par,
                       "depth": c["depth"][order], "score": c["score"][order], "mask": mask}
         return out
+
+    # target-side tree scoring ------------------------------------------------
+    def score_tree(self, hi: dict, tokens: np.ndarray, depth: np.ndarray, mask: np.ndarray,
+                   seqs: Optional[Sequence[int]] = None) -> dict:
+        """The target model's pass over draft trees (Sec. 2: the target
+        scores every candidate of the tree in one forward pass under a tree
+        attention mask), with this oracle's weights as the scoring model
+        (set f_map(1), every row fusing the sequence's feature row).
+
+        Sequence b: row 0 is the root (hi["tokens"][b]) at position and slot
+        L_b; row 1 + j is node j (tokens[b, j]) at position L_b + depth[b, j]
+        and slot L_b + 1 + j, seeing the prior context, the root and the
+        slots of the nodes in mask[b, j] (its ancestors and itself).
+        Returns logits [B, n+1, V] (sequences not in `seqs` left NaN) and the
+        KV each sequence wrote ("draft_kv")."""
+        cfg = self.cfg
+        B, n = tokens.shape
+        seqs = list(range(B)) if seqs is None else list(seqs)
+        logits = np.full((B, n + 1, cfg.vocab), np.nan)
+        kv = {}
+        for b in seqs:
+            cache = self.new_cache(hi, b)
+            L = cache["L"]
+            toks, pos, slots, vis = [int(hi["tokens"][b])], [L], [L], [list(range(L + 1))]
+            for j in range(n):
+                m = int(mask[b, j]) & ((1 << 64) - 1)
+                nodes = [a for a in range(n) if (m >> a) & 1]
+                toks.append(int(tokens[b, j]))
+                pos.append(L + int(depth[b, j]))
+                slots.append(L + 1 + j)
+                vis.append(list(range(L + 1)) + [L + 1 + a for a in nodes])
+            feats = np.stack([widen(hi["features"][b])] * (n + 1))
+            _, lg = self.forward(cfg.fmap[0], toks, feats, pos, {b: cache}, [b] * (n + 1), slots,
+                                 vis)
+            logits[b] = lg
+            kv[b] = cache["draft"]
+        return {"logits": logits, "draft_kv": kv}
 
     @staticmethod
     def _frontier(c: dict, lo: int, w: int, forced) -> List[int]:

@@ -20,7 +20,8 @@ STATUS = {0: "PRISM_OK", -1: "PRISM_ERR_INVALID_ARG", -2: "PRISM_ERR_SHAPE",
 EXPORTS = ("prism_create", "prism_destroy", "prism_last_error", "prism_draft_load_shared",
            "prism_draft_load_params", "prism_set_step_map", "prism_draft_step",
            "prism_draft_chain", "prism_draft_chain_catchup", "prism_draft_chain_sample",
-           "prism_draft_tree", "prism_verify_chain", "prism_verify_chain_static",
+           "prism_draft_tree", "prism_score_tree", "prism_verify_chain",
+           "prism_verify_chain_static",
            "prism_verify_tree",
            "prism_device_status",
            "prism_profile_enable", "prism_profile_read", "prism_profile_pairs",
@@ -102,6 +103,7 @@ def lib():
         L.prism_draft_chain_sample.argtypes = [c_vp, P(prism_batch), c_i32, c_f32, c_vp, c_vp,
                                                c_vp, c_vp, c_vp, c_vp]
         L.prism_draft_tree.argtypes = [c_vp, P(prism_batch), c_i32, P(prism_tree_out), c_vp]
+        L.prism_score_tree.argtypes = [c_vp, P(prism_batch), c_i32, c_vp, c_vp, c_vp, c_vp, c_vp]
         L.prism_verify_chain.argtypes = [c_vp, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp, c_vp, c_vp,
                                          c_vp, c_vp]
         L.prism_verify_chain_static.argtypes = [c_i32, c_i32, c_i32, c_f32, c_vp, c_vp, c_vp,
@@ -196,6 +198,13 @@ def prism_draft_chain_sample(ctx, batch: prism_batch, K: int, temperature: float
 
 def prism_draft_tree(ctx, batch: prism_batch, depth: int, out: prism_tree_out, stream=None):
     _check(lib().prism_draft_tree(ctx, ctypes.byref(batch), depth, ctypes.byref(out),
+                                  cur_stream() if stream is None else stream), ctx)
+
+
+def prism_score_tree(ctx, batch: prism_batch, n_nodes: int, tokens, depth, mask, logits,
+                     stream=None):
+    _check(lib().prism_score_tree(ctx, ctypes.byref(batch), n_nodes, ptr(tokens), ptr(depth),
+                                  ptr(mask), ptr(logits),
                                   cur_stream() if stream is None else stream), ctx)
 
 

@@ -25,6 +25,7 @@ constexpr int MAX_TOPK = 16;
 constexpr int MAX_VERIFY_NODES = 64;   // tree nodes one verification call takes
 constexpr int MAX_TREE_CAND = 2048;
 constexpr int MAX_NEW_ROWS = 4096;     // accepted rows of one catch-up call
+constexpr int MAX_SCORE_NODES = 63;    // nodes of one scored tree (visibility bits 1..63)
 
 // Tiled weight matrix W[N, K] (y = W x).  Tile t holds 16 output rows;
 // k-block j holds KB consecutive k (KB = 32 for bf16, 16 for fp32).  The
@@ -269,6 +270,11 @@ struct TreeWs {
 // and write the rows of pass d+1
 void launch_tree_expand(int d, const TreeWs &t, const int32_t *ctx_lens, const int *ids,
                         const float *logp, hipStream_t s);
+// rows of a tree-scoring pass: root and nodes of each of B trees of n nodes
+void launch_score_setup(int B, int n, const int32_t *root_tok, const int32_t *ctx_lens,
+                        const int32_t *tokens, const int32_t *depth, const uint64_t *mask,
+                        int32_t *tok, int32_t *seq, int32_t *pos, int32_t *slot, uint64_t *bits,
+                        uint32_t *err, hipStream_t s);
 void launch_tree_setup(int B, const int32_t *tokens, const int32_t *ctx_lens, int32_t *tok,
                        int32_t *seq, int32_t *pos, int32_t *slot, uint64_t *bits, hipStream_t s);
 void launch_tree_final(const TreeWs &t, int v, int32_t *tokens, int32_t *parent, int32_t *depth,

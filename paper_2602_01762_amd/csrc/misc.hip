@@ -718,6 +718,52 @@ void launch_tree_expand(int d, const TreeWs &t, const int32_t *ctx_lens, const i
   hipLaunchKernelGGL(k_tree_expand, dim3(t.B), dim3(256), 0, s, a);
 }
 
+// Rows of a tree-scoring pass (the target model's side of tree
+// verification): sequence b owns rows b * (n + 1) .. b * (n + 1) + n.  Row 0
+// is the root (the last accepted token) at position and slot L_b; row 1 + j
+// is node j at position L_b + depth_j and slot L_b + 1 + j, seeing the root
+// (bit 0) and its ancestor mask shifted by one.  A depth outside 1..n or a
+// mask that lacks the node's own bit or names a later node is clamped to a
+// well-formed row and raises ERRF_ROWS.
+__global__ void k_score_setup(int B, int n, const int32_t *root_tok, const int32_t *ctx_lens,
+                              const int32_t *tokens, const int32_t *depth, const uint64_t *mask,
+                              int32_t *tok, int32_t *seq, int32_t *pos, int32_t *slot,
+                              uint64_t *bits, uint32_t *err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * (n + 1)) return;
+  const int b = i / (n + 1), r = i % (n + 1);
+  const int L = ctx_lens[b];
+  seq[i] = b;
+  if (r == 0) {
+    tok[i] = root_tok[b];
+    pos[i] = L;
+    slot[i] = L;
+    bits[i] = 1ull;
+    return;
+  }
+  const int j = r - 1;                     // j <= 62
+  const size_t o = (size_t)b * n + j;
+  int dp = depth[o];
+  uint64_t m = mask[o];
+  const uint64_t keep = (2ull << j) - 1;   // bits 0..j
+  if (dp < 1 || dp > n || (m & ~keep) || !((m >> j) & 1ull)) atomicOr(err, ERRF_ROWS);
+  dp = dp < 1 ? 1 : (dp > n ? n : dp);
+  m = (m & keep) | (1ull << j);
+  tok[i] = tokens[o];
+  pos[i] = L + dp;
+  slot[i] = L + 1 + j;
+  bits[i] = 1ull | (m << 1);
+}
+
+void launch_score_setup(int B, int n, const int32_t *root_tok, const int32_t *ctx_lens,
+                        const int32_t *tokens, const int32_t *depth, const uint64_t *mask,
+                        int32_t *tok, int32_t *seq, int32_t *pos, int32_t *slot, uint64_t *bits,
+                        uint32_t *err, hipStream_t s) {
+  const int rows = B * (n + 1);
+  hipLaunchKernelGGL(k_score_setup, dim3((rows + 255) / 256), dim3(256), 0, s, B, n, root_tok,
+                     ctx_lens, tokens, depth, mask, tok, seq, pos, slot, bits, err);
+}
+
 // Root-pass rows: sequence b at position and slot L_b, visibility bit 0.
 __global__ void k_tree_setup(int B, const int32_t *tokens, const int32_t *ctx_lens, int32_t *tok,
                              int32_t *seq, int32_t *pos, int32_t *slot, uint64_t *bits) {

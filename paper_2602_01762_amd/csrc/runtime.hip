@@ -94,6 +94,10 @@ struct prism_ctx {
   int new_max = 0;                  // catch-up rows capacity
   int front_max = 0;                // rows of one catch-up front chunk
   int32_t *c_rseq = nullptr, *c_rpos = nullptr, *c_last = nullptr;   // catch-up rows
+  // tree scoring: the rows of every tree, [max_batch * (MAX_SCORE_NODES + 1)]
+  int32_t *s_tok = nullptr, *s_seq = nullptr, *s_pos = nullptr, *s_slot = nullptr;
+  uint64_t *s_bits = nullptr;
+  int score_rows = 0;
   float *q2 = nullptr, *u2 = nullptr;   // q and u of each sequence's last accepted row
   float *samp_logits = nullptr;     // [rows, V] fp32 logits kept for the sampler
   void *vstats = nullptr;           // verification: per-slice statistics of logits rows
@@ -331,6 +335,12 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->t_seq, R * 4);
   add((void **)&c->t_pos, R * 4);
   add((void **)&c->t_slot, R * 4);
+  c->score_rows = k.max_batch * (MAX_SCORE_NODES + 1);
+  add((void **)&c->s_tok, (size_t)c->score_rows * 4);
+  add((void **)&c->s_seq, (size_t)c->score_rows * 4);
+  add((void **)&c->s_pos, (size_t)c->score_rows * 4);
+  add((void **)&c->s_slot, (size_t)c->score_rows * 4);
+  add((void **)&c->s_bits, (size_t)c->score_rows * 8);
   add((void **)&c->t_bits[0], R * 8);
   add((void **)&c->t_bits[1], R * 8);
   add((void **)&c->err, 256);
@@ -1155,6 +1165,59 @@ prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t de
   return run_graph(c, key, (hipStream_t)stream, enqueue);
 }
 
+prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_nodes,
+                              const int32_t *d_tokens, const int32_t *d_depth,
+                              const uint64_t *d_mask, float *d_logits, void *stream) {
+  if (!c) return PRISM_ERR_INVALID_ARG;
+  prism_status st = check_batch(c, batch);
+  if (st) return st;
+  if (n_nodes < 1 || n_nodes > MAX_SCORE_NODES)
+    return fail(c, PRISM_ERR_INVALID_ARG, "n_nodes %d out of 1..%d", n_nodes, MAX_SCORE_NODES);
+  if (!d_tokens || !d_depth || !d_mask || !d_logits)
+    return fail(c, PRISM_ERR_INVALID_ARG, "NULL tree or logits pointer");
+  if ((st = check_set(c, 1, c->cfg.feat_width))) return st;
+  const prism_batch b = *batch;
+  const KvArgs kv = kv_of(c, &b);
+  const int B = b.batch, V = c->V, rows = B * (n_nodes + 1);
+  std::vector<uintptr_t> key = {5, (uintptr_t)B, (uintptr_t)n_nodes, (uintptr_t)b.d_tokens,
+                                (uintptr_t)b.d_features, (uintptr_t)b.d_ctx_lens,
+                                (uintptr_t)b.d_k_pool, (uintptr_t)b.d_v_pool,
+                                (uintptr_t)b.d_block_table, (uintptr_t)b.n_pool_blocks,
+                                (uintptr_t)d_tokens, (uintptr_t)d_depth, (uintptr_t)d_mask,
+                                (uintptr_t)d_logits, (uintptr_t)c->fmap[0]};
+  const int set = c->fmap[0];
+  return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
+    launch_score_setup(B, n_nodes, b.d_tokens, b.d_ctx_lens, d_tokens, d_depth, d_mask, c->s_tok,
+                       c->s_seq, c->s_pos, c->s_slot, c->s_bits, c->err, s);
+    // rows in tree order, in passes of up to rows_max: a node's ancestors
+    // come before it, so their KV is written by this pass or an earlier one
+    for (int r0 = 0; r0 < rows; r0 += c->rows_max) {
+      const int n = rows - r0 < c->rows_max ? rows - r0 : c->rows_max;
+      Pass p{};
+      p.set = set;
+      p.R = n;
+      p.F = c->sets[set].F;
+      p.topk = 1;
+      p.defer_merge = true;        // the logits are the output
+      p.in.tokens = c->s_tok + r0;
+      p.in.feat = b.d_features;
+      p.in.feat_bf16 = (int)c->bf16;
+      p.in.feat_ld = c->cfg.feat_width;
+      p.in.feat_rows = c->s_seq + r0;
+      p.in.seq = c->s_seq + r0;
+      p.in.pos = c->s_pos + r0;
+      p.in.slot = c->s_slot + r0;
+      p.in.bits = c->s_bits + r0;
+      p.hid_out = c->hid[0];
+      p.ld_hid = c->H;
+      p.logits = d_logits + (size_t)r0 * V;
+      p.ld_logits = V;
+      p.ids = c->ids;
+      enqueue_pass(c, p, kv, s);
+    }
+  });
+}
+
 prism_status prism_profile_enable(prism_ctx *c, int32_t what) {
   if (!c) return PRISM_ERR_INVALID_ARG;
   if (what & ~(PRISM_PROFILE_LMHEAD | PRISM_PROFILE_PRODUCTS | PRISM_PROFILE_PASSES))
@@ -1221,7 +1284,8 @@ prism_status prism_device_status(prism_ctx *c, void *stream) {
   HIPCHK(c, hipMemcpy(c->err, &zero, 4, hipMemcpyHostToDevice));
   if (flags & ERRF_NONFINITE)
     return fail(c, PRISM_ERR_NONFINITE, "NaN logits or tree scores (NaN in a feature row or a weight)");
-  if (flags & ERRF_ROWS) return fail(c, PRISM_ERR_INVALID_ARG, "malformed catch-up offsets");
+  if (flags & ERRF_ROWS)
+    return fail(c, PRISM_ERR_INVALID_ARG, "malformed catch-up offsets or tree-scoring rows");
   if (flags & ERRF_CAPACITY) return fail(c, PRISM_ERR_CAPACITY, "KV slot, block or pool out of range");
   if (flags & ERRF_TOKEN) return fail(c, PRISM_ERR_INVALID_ARG, "token id out of range");
   return PRISM_OK;

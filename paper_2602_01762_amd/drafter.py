@@ -177,6 +177,19 @@ class Drafter:
         B.prism_draft_tree(self.ctx, b, depth, t)
         return out
 
+    def score_tree(self, inp, tokens, depth, mask, out=None, batch=None):
+        """Target-side scoring of B draft trees (this context holds the
+        scoring model): logits [B, v+1, V] of the root and every node under
+        the tree mask.  inp describes the scoring model's own sequences
+        (root tokens, features, prior KV)."""
+        b = batch if batch is not None else self.batch(inp)
+        Bn, v = int(tokens.shape[0]), int(tokens.shape[1])
+        if out is None:
+            out = torch.empty((Bn, v + 1, self.shape.vocab), dtype=torch.float32,
+                              device=self.device)
+        B.prism_score_tree(self.ctx, b, v, tokens, depth, mask, out)
+        return out
+
     def verify_chain(self, target_logits, draft_tokens, temperature: float = 0.0,
                      draft_logits=None, uniforms=None):
         """Sec. 2 verification of B chains of K drafts; returns kept counts

@@ -45,6 +45,9 @@ class DraftConfig:
     # stochastic drafting: tokens drawn from softmax(logits / T) with seeded
     # uniforms (None: greedy)
     temperature: Optional[float] = None
+    # KV slots appended after the prior context, when not those of the
+    # chain or tree (a target model scoring a tree of v nodes needs 1 + v)
+    draft_slots: Optional[int] = None
 
     # ---- derived -------------------------------------------------------
     @property
@@ -80,6 +83,8 @@ class DraftConfig:
     @property
     def n_draft_slots(self) -> int:
         """KV slots the drafting call appends after the prior context."""
+        if self.draft_slots is not None:
+            return self.draft_slots
         if self.mode == "chain":
             return self.n_steps + (self.n_new[1] - 1 if self.n_new else 0)
         return 1 + (self.n_steps - 1) * self.tree_width
@@ -159,6 +164,17 @@ L2_7B_BS1_M2 = L2_7B_BS1.with_(name="llama2_7b_bf16_chain_bs1_m2", f_map=(0, 1, 
 
 # Stochastic drafting at T = 1 (the paper's T = 1 rows, Tables 4-5).
 L3_8B_BS1_T1 = L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_t1", temperature=1.0)
+
+# A target model for tree verification (Sec. 2: the target scores every
+# candidate of a draft tree in one pass under a tree attention mask): one
+# transformer layer of the drafter's shape with its own weights, fed the
+# token embeddings (its feature input is zero, width H), scoring the root
+# and the v nodes of each drafted tree.
+def scoring_target(cfg: DraftConfig) -> DraftConfig:
+    return cfg.with_(name=cfg.name + "_target1", n_steps=1, feat_width=cfg.hidden, mode="chain",
+                     tree_width=0, tree_nodes=0, f_map=None, n_sets=1,
+                     draft_slots=1 + cfg.tree_nodes)
+
 
 CONFIGS = {c.name: c for c in (TINY_F32, L3_8B_BS1, L3_8B_BS16, L3_8B_TREE, L3_70B_BS32,
                                L3_8B_BS1_CATCHUP, L3_8B_BS16_CATCHUP, L3_8B_BS1_T1,

@@ -9,9 +9,10 @@ import pytest
 import torch
 
 from oracle import softmax_t, verify_chain_greedy, verify_chain_sample, verify_tree_greedy
-from synth import (L3_8B_BS16, L3_8B_TREE, SMALL_BF16_CHAIN, SMALL_BF16_TREE, make_verify_chain,
-                   make_verify_tree_targets)
-from harness import gpu_setup, log
+from synth import (L3_8B_BS16, L3_8B_TREE, SMALL_BF16_CHAIN, SMALL_BF16_TREE, host_inputs,
+                   host_weights, make_inputs, make_verify_chain, make_verify_tree_targets,
+                   make_weights, scoring_target)
+from harness import LOGIT_TOL, MARGIN, check_draft_kv, check_token, gpu_setup, log
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -133,3 +134,111 @@ def test_verify_tree_full_vocab():
         ref = verify_tree_greedy(tln[b], tokens[b].cpu().numpy(), parent[b].cpu().numpy())
         assert int(out["n"][b]) == ref["n"] and int(out["next"][b]) == ref["next"]
     dr.close()
+
+
+def run_score_tree(cfg, seqs=None):
+    """Draft a tree with the GPU drafter, score it with a GPU target model
+    (one layer of the drafter's shape with its own weights, its feature input
+    zero) under the tree mask, verify it greedily, and compare with the
+    oracle: the target's logits of every row (root and nodes), the target KV
+    it wrote, and the accepted path."""
+    from oracle import Oracle
+    from paper_2602_01762_amd import Drafter
+    log("score tree", cfg.name)
+    dr, w, inp = gpu_setup(cfg)
+    tr = dr.tree(inp, debug=False)
+    torch.cuda.synchronize()
+    assert dr.device_status() == 0
+    tcfg = scoring_target(cfg)
+    wt = make_weights(tcfg.with_(seed=7), "cuda")
+    it = make_inputs(tcfg, "cuda")
+    it.features.zero_()
+    assert torch.equal(it.tokens, inp.tokens) and torch.equal(it.ctx_lens, inp.ctx_lens)
+    tdr = Drafter(tcfg, max_batch=64)        # passes of up to 64 rows
+    tdr.load(wt)
+    lg = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"])
+    again = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"])
+    ver = tdr.verify_tree(lg, tr["tokens"], tr["parent"])
+    torch.cuda.synchronize()
+    assert tdr.device_status() == 0
+    assert torch.equal(lg, again)
+    seqs = list(range(cfg.batch)) if seqs is None else seqs
+    toks, depth = tr["tokens"].cpu().numpy(), tr["depth"].cpu().numpy()
+    mask, parent = tr["mask"].cpu().numpy(), tr["parent"].cpu().numpy()
+    ref = Oracle(tcfg, host_weights(wt)).score_tree(host_inputs(it, tcfg, seqs), toks, depth,
+                                                    mask, seqs)
+    g = lg.cpu().numpy().astype(np.float64)
+    err, lens = 0.0, []
+    for b in seqs:
+        e = float(np.max(np.abs(g[b] - ref["logits"][b])))
+        assert e <= LOGIT_TOL[cfg.dtype], "seq %d: logits max-abs %.3g" % (b, e)
+        err = max(err, e)
+        for r in range(cfg.tree_nodes + 1):
+            check_token(ref["logits"][b, r], int(np.argmax(g[b, r])), "seq %d row %d" % (b, r))
+        # verification of the GPU's logits is exact; on the oracle's logits it
+        # agrees unless a choice on the path is a near tie
+        mine = verify_tree_greedy(g[b], toks[b], parent[b])
+        n = int(ver["n"][b])
+        assert (n, int(ver["next"][b])) == (mine["n"], mine["next"])
+        assert list(ver["path"][b].cpu().numpy()[:n]) == mine["path"]
+        theirs = verify_tree_greedy(ref["logits"][b], toks[b], parent[b])
+        if theirs["path"] != mine["path"]:
+            at = -1
+            for node in mine["path"] + [None]:
+                row = ref["logits"][b, at + 1]
+                top = np.sort(row)[::-1]
+                if top[0] - top[1] <= MARGIN:
+                    break
+                assert node is not None, "seq %d: paths differ without a near tie" % b
+                at = node
+        lens.append(n)
+    check_draft_kv(tcfg, it, ref["draft_kv"], seqs)
+    log(cfg.name, "target logits max-abs %.3g, accepted %s" % (err, lens))
+    tdr.close()
+    dr.close()
+    return lens
+
+
+def test_score_tree_and_verify_small():
+    lens = run_score_tree(SMALL_BF16_TREE)
+    assert len(lens) == SMALL_BF16_TREE.batch
+
+
+def test_score_tree_and_verify_small_empty_context():
+    run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_ctx0", ctx_range=None, ctx_len=0))
+
+
+def test_score_tree_rows_are_checked():
+    """A mask that names a later node or lacks the node's own bit, and a
+    depth out of range, are clamped to well-formed rows and reported."""
+    from paper_2602_01762_amd import Drafter
+    cfg = SMALL_BF16_TREE
+    tcfg = scoring_target(cfg)
+    it = make_inputs(tcfg, "cuda")
+    tdr = Drafter(tcfg, max_batch=64)
+    tdr.load(make_weights(tcfg.with_(seed=7), "cuda"))
+    v = cfg.tree_nodes
+    toks = torch.zeros((cfg.batch, v), dtype=torch.int32, device="cuda")
+    depth = torch.ones((cfg.batch, v), dtype=torch.int32, device="cuda")
+    mask = (torch.ones((cfg.batch, v), dtype=torch.int64, device="cuda")
+            << torch.arange(v, device="cuda"))
+    tdr.score_tree(it, toks, depth, mask)
+    torch.cuda.synchronize()
+    assert tdr.device_status() == 0
+    for bad in ("mask_later", "mask_self", "depth"):
+        m, dp = mask.clone(), depth.clone()
+        if bad == "mask_later":
+            m[0, 3] |= 1 << 5
+        elif bad == "mask_self":
+            m[1, 4] = 1
+        else:
+            dp[0, 2] = v + 1
+        tdr.score_tree(it, toks, dp, m)
+        torch.cuda.synchronize()
+        assert tdr.device_status() == -1, bad
+    tdr.close()
+
+
+@pytest.mark.slow
+def test_score_tree_and_verify_full_8b():
+    run_score_tree(L3_8B_TREE, seqs=[0])

@@ -463,6 +463,41 @@ def test_tree_cut_equals_brute_force(cfg, v):
             assert abs(lp - c["score"][cand]) < 1e-12
 
 
+# ------------------------------------------------------------------ T2c target-side tree scoring
+@pytest.mark.parametrize("cfg", [TINY, TINY_BF16, TINY_EMPTY], ids=["f32", "bf16", "empty"])
+def test_scored_tree_rows_equal_causal_paths(cfg):
+    # the scoring model's row for node j equals a plain causal pass over the
+    # root and the path to j (positions L_b, L_b + 1, ...), and its root row a
+    # one-row pass at L_b: the tree mask, slots and positions reproduce every
+    # branch run on its own
+    tcfg = cfg.with_(mode="tree", n_steps=4, tree_width=2, tree_nodes=12)
+    hw, hi = build(tcfg)
+    tr = Oracle(tcfg, hw).tree(hi)
+    assert max(int(x) for b in range(tcfg.batch) for x in tr[b]["depth"]) >= 3
+    scfg = tcfg.with_(mode="chain", n_steps=1, feat_width=tcfg.hidden, tree_width=0,
+                      tree_nodes=0, draft_slots=1 + tcfg.tree_nodes)
+    hs = host_weights(make_weights(scfg.with_(seed=5)))
+    feats = np.random.default_rng(2).standard_normal((tcfg.batch, tcfg.hidden))
+    his = dict(hi, features=feats)
+    sc = Oracle(scfg, hs)
+    toks = np.stack([tr[b]["tokens"] for b in range(tcfg.batch)])
+    depth = np.stack([tr[b]["depth"] for b in range(tcfg.batch)])
+    mask = np.stack([tr[b]["mask"] for b in range(tcfg.batch)])
+    got = sc.score_tree(his, toks, depth, mask)["logits"]
+    for b in range(tcfg.batch):
+        L = int(hi["ctx_lens"][b])
+        for j in range(-1, tcfg.tree_nodes):
+            path = [] if j < 0 else [a for a in range(j + 1) if (int(mask[b, j]) >> a) & 1]
+            rows = [int(hi["tokens"][b])] + [int(toks[b, a]) for a in path]
+            n = len(rows)
+            assert j < 0 or n - 1 == int(depth[b, j])
+            cache = {b: sc.new_cache(his, b)}
+            pos = [L + i for i in range(n)]
+            _, lg = sc.forward(0, rows, np.stack([feats[b]] * n), pos, cache, [b] * n, pos,
+                               [list(range(p + 1)) for p in pos])
+            assert np.max(np.abs(lg[-1] - got[b, j + 1])) < 1e-12, (b, j)
+
+
 # ------------------------------------------------------------------ T3 set isolation
 def test_step_k_uses_only_set_k():
     hw, hi = build(TINY)
