@@ -85,7 +85,7 @@ def lm_workgroups(cfg, rows):
         nt = 4 if tiles % 16 == 0 and nkb % 16 == 0 and tiles // 4 >= 1024 else 1
     elif rows <= 32 and tiles % 8 == 0:
         nt = 8
-    elif rows <= 32 and tiles % 4 == 0:
+    elif tiles % 4 == 0:
         nt = 4
     else:
         nt = 2 if tiles % 2 == 0 else 1

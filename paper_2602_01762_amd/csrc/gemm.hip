@@ -998,11 +998,12 @@ static bool gemm_rt(const GemmLaunch &g, hipStream_t s) {
   if (g.split > 0) {
     if (g.nt == 8) {
       if (g.R <= 16) gemm_split_launch<T, 1, 8, PAIR>(g, s);
-      else gemm_split_launch<T, 2, 8, PAIR>(g, s);
+      else if (g.R <= 32) gemm_split_launch<T, 2, 8, PAIR>(g, s);
+      else gemm_split_launch<T, 4, 8, PAIR>(g, s);
     } else if (g.nt == 4) {
       if (g.R <= 16) gemm_split_launch<T, 1, 4, PAIR>(g, s);
       else if (g.R <= 32) gemm_split_launch<T, 2, 4, PAIR>(g, s);
-      else gemm_split_launch<T, 4, 2, PAIR>(g, s);
+      else gemm_split_launch<T, 4, 4, PAIR>(g, s);
     } else if (g.nt == 2) {
       if (g.R <= 16) gemm_split_launch<T, 1, 2, PAIR>(g, s);
       else if (g.R <= 32) gemm_split_launch<T, 2, 2, PAIR>(g, s);
@@ -1070,14 +1071,16 @@ static void lm_rt(const LmLaunch &g, hipStream_t s) {
       return;
     }
   }
-  if (g.nt == 8) {   // eight tiles per wave share each B fragment (up to 32 rows)
+  if (g.nt == 8) {   // eight tiles per wave share each B fragment
     if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 8, PAIR, 0>), grid, blk, 0, s, g);
-    else hipLaunchKernelGGL((k_lmhead<T, 2, 8, PAIR, 0>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 8, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 8, PAIR, 0>), grid, blk, 0, s, g);
     return;
   }
   if (g.nt == 4) {   // four tiles per wave share each B fragment (batched rows)
     if (g.R <= 16) hipLaunchKernelGGL((k_lmhead<T, 1, 4, PAIR, 0>), grid, blk, 0, s, g);
-    else hipLaunchKernelGGL((k_lmhead<T, 2, 4, PAIR, 0>), grid, blk, 0, s, g);
+    else if (g.R <= 32) hipLaunchKernelGGL((k_lmhead<T, 2, 4, PAIR, 0>), grid, blk, 0, s, g);
+    else hipLaunchKernelGGL((k_lmhead<T, 4, 4, PAIR, 0>), grid, blk, 0, s, g);
     return;
   }
   if (g.nt == 2) {

@@ -44,16 +44,17 @@ struct ProductPlan {
 };
 
 // Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
-// fragment reuse) and K slices across workgroups: at most one workgroup of
-// 4 waves per CU (longer slices stream better than more of them, and a grid
-// just above the CU count leaves a few CUs with twice the work), at least 4
-// k-blocks per slice, and fp32 slice partials of at most 1/4 of the weight
-// bytes (split * R * N * 4 <= N * K * 2 / 4; at 32 rows the tighter 1/8 cap
-// left the 4096-wide products on 64-128 workgroups: tree 2.695 -> 2.662 ms).
+// fragment reuse: 4, or 8 at 17-32 rows, so that the activation fragments a
+// wave loads stay within twice its weight fragments) and K slices across
+// workgroups: at most one workgroup of 4 waves per CU (longer slices stream
+// better than more of them, and a grid just above the CU count leaves a few
+// CUs with twice the work), at least 4 k-blocks per slice, and fp32 slice
+// partials of at most 1/4 of the weight bytes (split * R * N * 4 <= N * K * 2
+// / 4; at 32 rows the tighter 1/8 cap left the 4096-wide products on 64-128
+// workgroups: tree 2.695 -> 2.662 ms).
 inline void plan_batched(int n_tiles, int nkb, int K, int R, int &nt, int &split) {
   nt = n_tiles % 4 == 0 ? 4 : (n_tiles % 2 == 0 ? 2 : 1);
-  if (R > 16 && R <= 32 && n_tiles % 8 == 0) nt = 8;
-  if (R > 32 && nt == 4) nt = 2;
+  if (R > 16 && n_tiles % 8 == 0) nt = 8;
   const int wgs = (n_tiles / nt + SPLIT_WAVES - 1) / SPLIT_WAVES;
   int sp = 256 / wgs;
   if (sp > nkb / 4) sp = nkb / 4;

@@ -674,10 +674,10 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
     lmg.nt = 4;
   // batched rows: several vocab tiles per wave share B fragments; 8 up to
   // 32 rows (at 16 rows: 176 -> 166 us against 4 tiles, the B stream being
-  // half as large per weight byte)
+  // half as large per weight byte), 4 above
   if (!lmg.gemv && R > LM_GEMV_MAX_ROWS) {
-    if (R <= 32 && c->lm.n_tiles % 8 == 0) lmg.nt = 8;
-    else if (R <= 32 && c->lm.n_tiles % 4 == 0) lmg.nt = 4;
+    if (c->lm.n_tiles % 8 == 0) lmg.nt = 8;
+    else if (c->lm.n_tiles % 4 == 0) lmg.nt = 4;
     else if (c->lm.n_tiles % 2 == 0) lmg.nt = 2;
   }
   lmg.n_wg = lm_workgroups(c->lm.n_tiles, lmg.nt);
