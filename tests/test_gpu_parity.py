@@ -369,6 +369,24 @@ def test_full_8b_bs1_catchup():
     run_catchup_parity(L3_8B_BS1_CATCHUP, [0])
 
 
+def test_catchup_at_the_row_limit():
+    """4096 accepted rows (64 sequences x 64 tokens, the largest catch-up
+    call): 64 front chunks of 64 rows, every sequence in a chunk of its own
+    at a chunk border."""
+    cfg = SMALL_BF16_CHAIN.with_(name="small_bf16_catchup_bs64_n64", batch=64, n_new=(64, 64),
+                                 ctx_range=(37, 100))
+    assert cfg.max_new_rows == 4096
+    test_chain_catchup_parity(cfg)
+
+
+@pytest.mark.slow
+def test_full_8b_bs1_catchup_two_chunks():
+    """The 8B shape with 70 accepted tokens: the front runs in two chunks
+    (64 + 6 rows), the last row in the second."""
+    run_catchup_parity(L3_8B_BS1.with_(name="llama3_8b_bf16_chain_bs1_catchup70", n_new=(70, 70)),
+                       [0])
+
+
 @pytest.mark.slow
 def test_full_8b_bs16_catchup():
     from synth import new_counts
