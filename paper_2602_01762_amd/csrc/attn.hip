@@ -15,11 +15,11 @@
 
 namespace prism {
 
-constexpr int ATT_S = 64;        // slots per step
+constexpr int ATT_S = ATT_STEP;  // slots per step
 constexpr int ATT_MAXG = 8;      // query heads per KV head
 constexpr int ATT_MAXGD = 1024;  // g * d
 constexpr int ATT_MAXVS = 8;     // slots per thread in P.V: 64 / (256 / (d / 8)) for d <= 256
-constexpr int ATT_MAXCH = 1024;  // chunks per row merged by the combine kernel
+constexpr int ATT_MAXCH = ATT_MAX_CHUNKS;  // chunks per row merged by the combine kernel
 
 struct AttnArgs {
   const float *q;             // [R, nq*d] fp32, RoPE applied
@@ -27,6 +27,7 @@ struct AttnArgs {
   const uint64_t *bits;
   KvArgs kv;
   int R, nq, nkv, d, nch, nsub;
+  int grp;                    // rows per workgroup of the grouped MFMA kernel (one sequence's tree rows)
   float scale;
   float *pm, *pl, *po;        // [R, nq, nch] / [R, nq, nch, d]
   ActOut o;                   // [R, nq*d]
@@ -268,37 +269,68 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
 // waves stream independently.  Each wave keeps its own softmax state; the 4
 // waves merge in LDS at the end and write the same per-chunk partials as the
 // VALU kernel.
+//
+// Grouped form (GRP, tree rows): a workgroup takes grp rows of one sequence,
+// and score column col is (row col / g of the group, head col % g), so the
+// 16 columns hold grp * g query rows instead of g.  The rows share the prior
+// context [0, L) and differ only in which of the 64 tree slots after it they
+// see, so each context slot's K/V is read once for the group instead of once
+// per row.  A slot is loaded if any row of the group sees it and masked per
+// column; the partials are written per row as in the ungrouped form.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return f2bf(lo) | (f2bf(hi) << 16);
 }
 
-constexpr int ATT_MAXSUB = 16;    // 64-slot steps per workgroup
+constexpr int ATT_MAXSUB = ATT_MAX_SUB;    // 64-slot steps per workgroup
 
-template <int DK, bool NTL>   // head_dim / 32; NTL: K/V rows read with streaming (nontemporal) loads
+// DK: head_dim / 32; NTL: K/V rows read with streaming (nontemporal) loads;
+// GRP: grouped form (a.grp rows of one sequence per workgroup, tree bits)
+template <int DK, bool NTL, bool GRP>
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   constexpr int ATT_MAXDK = DK, ATT_MAXDT = 2 * DK;
-  const int c = blockIdx.z, j = blockIdx.x, r = blockIdx.y;
+  const int c = blockIdx.z, j = blockIdx.x;
+  const int gs = GRP ? a.grp : 1;
+  const int r = blockIdx.y * gs;             // the workgroup's (first) row
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, q4 = lane >> 4;
   int b, L, prefix, total;
   uint64_t bits;
-  if (!row_range(a, r, b, L, prefix, total, bits)) {
+  if (!row_range(a, r, b, L, prefix, total, bits) || (GRP && !a.bits)) {
     if (c == 0 && j == 0 && tid == 0) atomicOr(a.err, ERRF_CAPACITY);
     return;
+  }
+  const int g = a.nq / a.nkv;
+  // column col: query head col (ungrouped), or row r + col / g, head col % g;
+  // its own tree bits (grouped)
+  bool cvalid = col < g;
+  uint64_t cbits = 0ull;
+  if constexpr (GRP) {
+    // every row of the group must belong to the row-r sequence (the launcher
+    // groups the rows of one tree); another row's columns stay masked
+    uint64_t ub = 0ull;
+    for (int i = 0; i < gs; ++i) {
+      if (a.seq[r + i] == b) ub |= a.bits[r + i];
+      else if (c == 0 && j == 0 && tid == 0) atomicOr(a.err, ERRF_ROWS);
+    }
+    const int rc = r + col / g;
+    cvalid = col < gs * g && a.seq[rc < r + gs ? rc : r] == b;
+    cbits = cvalid ? a.bits[rc] : 0ull;
+    bits = ub;                                 // slots loaded: seen by any row
+    total = L + (ub ? 64 - __clzll((long long)ub) : 0);
   }
   const int span = ATT_S * a.nsub;
   const int tbeg = c * span;
   if (tbeg >= total) return;                 // uniform across the workgroup
   // the launcher instantiates DK = d / 32, so every head-dim loop below is full
   constexpr int d = 32 * DK;
-  const int g = a.nq / a.nkv;
+  constexpr int NCOLD = GRP ? 16 * d : ATT_MAXGD;   // merge buffer: columns x dims
   const int bs = a.kv.bs;
 
   __shared__ bf16_t vt[4][32 * DK][16];     // per wave: V tile as [dim][slot]
   __shared__ float mg_m[4][16], mg_l[4][16];
-  __shared__ float mg_o[4][ATT_MAXGD];
+  __shared__ float mg_o[4][NCOLD];
   __shared__ int s_blk[ATT_S * ATT_MAXSUB];  // physical blocks of the chunk's slots
 
   // block-table entries of the chunk (at most one per slot)
@@ -315,8 +347,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
   for (int kk = 0; kk < ATT_MAXDK; ++kk) {
     qh[kk] = ql[kk] = u32x4{0, 0, 0, 0};
-    if (col < g) {
-      const float *qp = a.q + (size_t)r * a.nq * d + (size_t)(j * g + col) * d + 32 * kk + 8 * q4;
+    if (cvalid) {
+      const int rq = GRP ? r + col / g : r, hq = GRP ? col % g : col;
+      const float *qp = a.q + (size_t)rq * a.nq * d + (size_t)(j * g + hq) * d + 32 * kk + 8 * q4;
       const f32x4 x0 = *(const f32x4 *)qp, x1 = *(const f32x4 *)(qp + 4);
       const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
       float hi[8], lo[8];
@@ -357,14 +390,15 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     }
   };
 
-  float m_run = -INFINITY, l_run = 0.f;      // softmax state of head `col`
+  float m_run = -INFINITY, l_run = 0.f;      // softmax state of column `col`
   f32x4 o[ATT_MAXDT];                         // O[head 4 q4 + i][dim 16 dt + col]
 #pragma unroll
   for (int dt = 0; dt < ATT_MAXDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // One 64-slot step of the wave's 16 slots t0 + 16 wave + [0, 16): lane
-  // (col, q4) holds the K/V rows of slot col (offset off, -1 = invisible).
-  auto step = [&](long off, const u32x4 (&ka)[ATT_MAXDK], const u32x4 (&va)[ATT_MAXDK]) {
+  // One 64-slot step of the wave's 16 slots tb + [0, 16) (tb = t0 + 16 wave):
+  // lane (col, q4) holds the K/V rows of slot tb + col (offset off, -1 =
+  // invisible).
+  auto step = [&](int tb, long off, const u32x4 (&ka)[ATT_MAXDK], const u32x4 (&va)[ATT_MAXDK]) {
     // scores S[slot 4 q4 + i][head col]
     f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -379,13 +413,21 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     const uint64_t vmask = __ballot(vis);
     float sv[4] = {sc.x, sc.y, sc.z, sc.w};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sv[i] = (vmask >> (4 * q4 + i)) & 1ull ? sv[i] * a.scale : -INFINITY;
-    // online softmax of head col over these 16 slots (lanes col, col^16, ...)
+    for (int i = 0; i < 4; ++i) {
+      bool v = (vmask >> (4 * q4 + i)) & 1ull;
+      if constexpr (GRP) {   // the column's row: the prior context and its own tree slots
+        const int sh = tb + 4 * q4 + i - L;
+        v = v && cvalid && (sh < 0 || (sh < 64 && ((cbits >> (sh & 63)) & 1ull)));
+      }
+      sv[i] = v ? sv[i] * a.scale : -INFINITY;
+    }
+    // online softmax of column col over these 16 slots (lanes col, col^16, ...)
     float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
     mx = fmaxf(mx, xor16_f(mx));
     mx = fmaxf(mx, xor32_f(mx));
     const float mn = fmaxf(m_run, mx);
-    const float al = m_run == -INFINITY ? 0.f : expf(m_run - mn);
+    // alpha = 1 while nothing has accumulated (O and l are still zero)
+    const float al = m_run == -INFINITY ? 1.f : expf(m_run - mn);
     float p[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) p[i] = sv[i] == -INFINITY ? 0.f : expf(sv[i] - mn);
@@ -406,8 +448,8 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       }
     }
     wave_lds_sync();
-    // rescale O rows (heads 4 q4 + i) by their alpha, which is exactly 1
-    // for every head once its running max stops moving (most steps of a
+    // rescale O rows (columns 4 q4 + i) by their alpha, which is exactly 1
+    // for every column once its running max stops moving (most steps of a
     // long context): the wave then skips the broadcasts and multiplies
     if (__ballot(al != 1.f)) {
       float ah[4];
@@ -446,13 +488,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     if (t0 >= tend) break;                    // uniform
     off1 = sub + 1 < a.nsub ? slot_off(slot0 + (sub + 1) * ATT_S) : -1;
     load_kv(off1, k1, v1);
-    step(off0, k0, v0);
+    step(t0 + 16 * wave, off0, k0, v0);
     if (sub + 1 >= a.nsub || t0 + ATT_S >= tend) break;   // uniform
     off0 = sub + 2 < a.nsub ? slot_off(slot0 + (sub + 2) * ATT_S) : -1;
     load_kv(off0, k0, v0);
-    step(off1, k1, v1);
+    step(t0 + ATT_S + 16 * wave, off1, k1, v1);
   }
   // merge the 4 waves' states and write this chunk's partials
+  const int ncol = GRP ? gs * g : g;
   if (q4 == 0) {
     mg_m[wave][col] = m_run;
     mg_l[wave][col] = l_run;
@@ -463,12 +506,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int h = 4 * q4 + i;
-      if (h < g) mg_o[wave][h * d + 16 * dt + col] = ov[i];
+      if (h < ncol) mg_o[wave][h * d + 16 * dt + col] = ov[i];
     }
   }
   __syncthreads();
-  for (int e = tid; e < g * d; e += 256) {
-    const int h = e / d, dim = e % d;
+  for (int e = tid; e < ncol * d; e += 256) {
+    const int h = e / d, dim = e % d;        // h: column
+    const int rr = GRP ? r + h / g : r, hh = GRP ? h % g : h;
+    if (GRP && a.seq[rr] != b) continue;     // another sequence's row (flagged above)
     float M = -INFINITY;
     for (int w = 0; w < 4; ++w) M = fmaxf(M, mg_m[w][h]);
     float lsum = 0.f, osum = 0.f;
@@ -477,7 +522,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
       lsum += mg_l[w][h] * wt;
       osum += mg_o[w][e] * wt;
     }
-    const size_t pi = ((size_t)r * a.nq + j * g + h) * a.nch + c;
+    const size_t pi = ((size_t)rr * a.nq + j * g + hh) * a.nch + c;
     a.po[pi * d + dim] = osum;
     if (dim == 0) {
       a.pm[pi] = M;
@@ -553,12 +598,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   }
 }
 
-int attention_chunks(int max_slots, int nsub) {
-  return (max_slots + ATT_S * nsub - 1) / (ATT_S * nsub);
-}
-
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
-                      const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
+                      const KvArgs &kv, int max_slots, int grp, float *pm, float *pl, float *po,
                       ActOut o, uint32_t *err, hipStream_t s) {
   AttnArgs a;
   a.q = q;
@@ -570,35 +611,44 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   a.nq = nq;
   a.nkv = nkv;
   a.d = d;
-  a.nsub = nsub;
-  a.nch = attention_chunks(max_slots, nsub);
   a.scale = 1.0f / sqrtf((float)d);
   a.pm = pm;
   a.pl = pl;
   a.po = po;
   a.o = o;
   a.err = err;
+  // grouped rows: tree rows (bits), bf16, head_dim 64 or 128, the group's
+  // query rows within the 16 score columns, whole groups
+  const int g = nq / nkv;
+  a.grp = grp > 1 && bf16 && in.bits && (d == 64 || d == 128) && grp * g <= 16 && R % grp == 0
+              ? grp : 1;
+  // steps per workgroup for this pass's rows (or row groups)
+  a.nsub = attention_nsub(R / a.grp, nkv, max_slots);
+  a.nch = attention_chunks(max_slots, a.nsub);
   // chunk index slowest: every row's first chunks are dispatched before any
   // row's later ones, so the last workgroups to start are the short tails
-  dim3 g1(nkv, R, a.nch), g2(nq, R);
+  dim3 g1(nkv, R / a.grp, a.nch), g2(nq, R);
   // K/V that one pass requests at capacity (R rows of max_slots slots):
   // beyond 1.5 times the 256 MiB infinity cache the rows are streamed with
   // nontemporal loads (70B batch 32, 539 MB: 5.917 -> 5.847 ms); below it
   // ordinary loads let the cache keep the prior context from one step to the
   // next (batch 16 paged, 269 MB at capacity and 151 MB on average:
   // nontemporal loads were 3.7% slower; the tree, 140 MB: 0.6% slower)
-  const double kv_bytes = (double)R * max_slots * nkv * d * 2 * (bf16 ? 2 : 4);
+  const double kv_bytes = (double)R / a.grp * max_slots * nkv * d * 2 * (bf16 ? 2 : 4);
   const bool ntl = kv_bytes > 1.5 * 256 * 1024 * 1024;
   if (bf16) {
-    if (d == 64) {
-      if (ntl) hipLaunchKernelGGL((k_attn_mfma<2, true>), g1, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn_mfma<2, false>), g1, dim3(256), 0, s, a);
+    if (a.grp > 1) {
+      if (d == 64) hipLaunchKernelGGL((k_attn_mfma<2, false, true>), g1, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_mfma<4, false, true>), g1, dim3(256), 0, s, a);
+    } else if (d == 64) {
+      if (ntl) hipLaunchKernelGGL((k_attn_mfma<2, true, false>), g1, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_mfma<2, false, false>), g1, dim3(256), 0, s, a);
     } else if (d == 128) {
-      if (ntl) hipLaunchKernelGGL((k_attn_mfma<4, true>), g1, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn_mfma<4, false>), g1, dim3(256), 0, s, a);
+      if (ntl) hipLaunchKernelGGL((k_attn_mfma<4, true, false>), g1, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_mfma<4, false, false>), g1, dim3(256), 0, s, a);
     } else if (d == 256) {
-      if (ntl) hipLaunchKernelGGL((k_attn_mfma<8, true>), g1, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn_mfma<8, false>), g1, dim3(256), 0, s, a);
+      if (ntl) hipLaunchKernelGGL((k_attn_mfma<8, true, false>), g1, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_mfma<8, false, false>), g1, dim3(256), 0, s, a);
     } else {
       hipLaunchKernelGGL(k_attn_partial<bf16_t>, g1, dim3(256), 0, s, a);
     }

@@ -179,10 +179,14 @@ void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_st
 // ---- launchers (misc.hip) -------------------------------------------------
 void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
                     int V, int H, int F, ActOut X, uint32_t *err, int32_t *tok_out, bool feat_only, hipStream_t s);
+// grp > 1: rows r .. r + grp - 1 (r a multiple of grp) belong to one sequence
+// and carry tree bits; the launch groups them when the kernel allows it
+// The partials pm, pl, po hold R * attention_chunks(max_slots, nsub) rows
+// x chunks for the steps per workgroup that attention_nsub gives this pass
+// (attention_partial_rows bounds them over every pass).
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
-                      const KvArgs &kv, int max_slots, int nsub, float *pm, float *pl, float *po,
+                      const KvArgs &kv, int max_slots, int grp, float *pm, float *pl, float *po,
                       ActOut o, uint32_t *err, hipStream_t s);
-int attention_chunks(int max_slots, int nsub);
 // Draw each row's token from softmax(logits * inv_temp) by inverse CDF in
 // id order with the row's uniform u[r * ld_u]: the LM head's per-group
 // (max, sum) of the scaled logits locate the group where the running sum

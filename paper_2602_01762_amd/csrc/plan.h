@@ -1,4 +1,5 @@
-// Launch plans of the streamed products (host code, plain C++).
+// Launch plans of the streamed products and the tree attention's row
+// groups (host code, plain C++).
 //
 // The runtime plans every product with these functions, and the product
 // kernels take their __launch_bounds__ from product_max_waves, so a plan
@@ -113,6 +114,58 @@ inline bool plan_fits(const ProductPlan &p, int R) {
   if (p.split > 0) return true;   // SPLIT_WAVES per workgroup
   const int rt = p.gemv ? 1 : row_tiles(R);
   return p.kw >= 1 && p.kw <= product_max_waves(rt, p.gemv ? 1 : p.nt);
+}
+
+// Rows per workgroup of the grouped tree attention (rows of one sequence
+// at tree width w): the largest divisor of w whose query rows, g = nq / nkv
+// heads each, fit the 16 score columns of the MFMA tile; 1 = no grouping
+// (fp32 caches and head dims other than 64 and 128 run ungrouped).
+inline int attention_group(bool bf16, int nq, int nkv, int d, int w) {
+  if (!bf16 || (d != 64 && d != 128) || nkv <= 0 || nq % nkv) return 1;
+  const int g = nq / nkv;
+  int gs = 1;
+  for (int k = 2; k <= w && k * g <= 16; ++k)
+    if (w % k == 0) gs = k;
+  return gs;
+}
+
+constexpr int ATT_STEP = 64;          // KV slots per attention step
+constexpr int ATT_MAX_SUB = 16;       // steps per attention workgroup
+constexpr int ATT_MAX_CHUNKS = 1024;  // chunks per row the attention merge takes
+
+// Chunks (of nsub steps) that cover max_slots slots.
+inline int attention_chunks(int max_slots, int nsub) {
+  return (max_slots + ATT_STEP * nsub - 1) / (ATT_STEP * nsub);
+}
+
+// Steps per workgroup of a pass with `units` workgroups per KV head and
+// chunk (rows, or row groups): the fewest (a power of two up to ATT_MAX_SUB)
+// that keep the grid at about 512 workgroups at capacity (two resident per
+// CU), so that each streams several steps after its dependent lookups.  A
+// pass with few rows gets short chunks and still fills the chip.
+inline int attention_nsub(int units, int nkv, int max_slots) {
+  int nsub = 1;
+  while (nsub < ATT_MAX_SUB && (long)units * nkv * attention_chunks(max_slots, nsub) > 512) nsub *= 2;
+  return nsub;
+}
+
+// Rows x chunks of the attention partials that any pass of 1..rows_max rows
+// writes (row groups of grp rows where rows_max allows them), and the most
+// chunks of any one row; the partial buffers are sized from the first, and
+// the second must not exceed ATT_MAX_CHUNKS.
+inline long attention_partial_rows(int rows_max, int grp, int nkv, int max_slots, int &max_chunks) {
+  long most = 0;
+  max_chunks = 0;
+  for (int R = 1; R <= rows_max; ++R) {
+    const int groups[2] = {1, grp};   // rows per workgroup: single rows, whole groups
+    for (int gs : groups) {
+      if (gs < 1 || R % gs) continue;
+      const int ch = attention_chunks(max_slots, attention_nsub(R / gs, nkv, max_slots));
+      if ((long)R * ch > most) most = (long)R * ch;
+      if (ch > max_chunks) max_chunks = ch;
+    }
+  }
+  return most;
 }
 
 }  // namespace prism

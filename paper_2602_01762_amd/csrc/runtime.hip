@@ -32,6 +32,7 @@ struct Set {
 
 struct Pass {            // one forward pass: where its inputs and outputs live
   int set, R, F, topk;
+  int grp;                // > 1: attention over groups of grp rows of one sequence (tree levels)
   RowsIn in;
   TokFromLm lm_in;        // tokens from the previous pass's LM partials (pval != NULL)
   bool defer_merge;       // leave the LM partials to the next pass (chain, top-1)
@@ -57,7 +58,7 @@ struct prism_ctx {
   size_t esz = 2;
   int dev = 0;
   int H = 0, nq = 0, nkv = 0, d = 0, I = 0, V = 0, QKV = 0;
-  int rows_max = 0, max_slots = 0, nch = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
+  int rows_max = 0, max_slots = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
   int feat_max = 0;
   // passes take the fusion FC's embedding half from a per-set table (bf16)
   bool use_tab = false;
@@ -89,7 +90,7 @@ struct prism_ctx {
   float *t_cscore = nullptr;
   int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
   uint64_t *t_bits[2] = {nullptr, nullptr};
-  int nsub = 1;                     // attention: 64-slot steps per workgroup
+  int att_grp = 1;                  // tree levels: rows per attention workgroup
   int lm_nwg_last = 0;              // LM-head partial count of the pass last enqueued
   int new_max = 0;                  // catch-up rows capacity
   int front_max = 0;                // rows of one catch-up front chunk
@@ -225,14 +226,12 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->I = k.ffn; c->V = k.vocab; c->QKV = (c->nq + 2 * c->nkv) * c->d;
   c->rows_max = rows;
   c->max_slots = k.max_blocks_per_seq * k.kv_block_size;
-  // attention steps per workgroup: at most about 512 (row, head, chunk)
-  // units (two resident workgroups per CU), so that each workgroup streams
-  // several steps after its dependent lookups
-  c->nsub = 1;
-  while (c->nsub < 16 && (long)rows * k.n_kv_heads * attention_chunks(c->max_slots, c->nsub) > 512)
-    c->nsub *= 2;
-  c->nch = attention_chunks(c->max_slots, c->nsub);
-  if (c->nch > 1024) {
+  // attention partials: rows x chunks of the largest pass (chunks per pass
+  // from its row count); tree levels group att_grp rows of one sequence
+  c->att_grp = w > 1 ? attention_group(bf16, k.n_q_heads, k.n_kv_heads, k.head_dim, w) : 1;
+  int max_chunks = 0;
+  const long part_rc = attention_partial_rows(rows, c->att_grp, k.n_kv_heads, c->max_slots, max_chunks);
+  if (max_chunks > ATT_MAX_CHUNKS) {
     delete c;
     return fail(nullptr, PRISM_ERR_SHAPE, "KV capacity per sequence too large for the attention merge");
   }
@@ -275,9 +274,9 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->sc_r1, R * 4);
   add((void **)&c->sc_h, R * 4);
   add((void **)&c->q, RF * c->nq * c->d * 4);
-  add((void **)&c->pm, R * c->nq * c->nch * 4);
-  add((void **)&c->pl, R * c->nq * c->nch * 4);
-  add((void **)&c->po, R * c->nq * c->nch * c->d * 4);
+  add((void **)&c->pm, part_rc * c->nq * 4);
+  add((void **)&c->pl, part_rc * c->nq * 4);
+  add((void **)&c->po, part_rc * c->nq * c->d * 4);
   planes(c->o, R * c->nq * c->d);
   planes(c->z, R * c->I);
   add((void **)&c->hid[0], R * c->H * 4);
@@ -637,8 +636,8 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   // attention over the visible slots -> o
   ActOut o = c->o;
   o.ld = c->nq * c->d;
-  launch_attention(bf, R, c->nq, c->nkv, c->d, q, p.in, kv, c->max_slots, c->nsub, c->pm,
-                   c->pl, c->po, o, c->err, s);
+  launch_attention(bf, R, c->nq, c->nkv, c->d, q, p.in, kv, c->max_slots, p.grp, c->pm, c->pl,
+                   c->po, o, c->err, s);
   // r1 = u + W_o o  ->  r1, (r1 * g2), sums of squares
   GemmLaunch g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
   g.res = u; g.ldres = H; g.y = c->r1; g.ldy = H; g.gain = S.g2; g.g = c->r1g; g.g.ld = H;
@@ -1134,6 +1133,7 @@ prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t de
       Pass p{};
       p.set = c->fmap[d];
       p.R = d == 0 ? B : B * w;
+      p.grp = d == 0 ? 1 : c->att_grp;   // level d > 0: sequence b owns rows b w .. b w + w - 1
       p.F = d == 0 ? c->cfg.feat_width : H;
       p.topk = w;
       p.in.tokens = c->t_tok;

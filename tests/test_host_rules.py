@@ -5,7 +5,8 @@
   ranks must form a permutation whatever the scores are.  If they do not,
   two candidates share a slot and another slot is never written.
 * plan.h: the launch plan of every product of every configured shape and row
-  count fits the kernel instantiation that it selects.
+  count fits the kernel instantiation that it selects, and the tree
+  attention's row groups divide the tree width and fit the 16 score columns.
 """
 import itertools
 import math
@@ -58,6 +59,20 @@ int main() {
       const int rt = p.gemv ? 1 : row_tiles(R);
       std::printf("%d %d %d %d %d %d\n", p.kw, p.nt, p.split, p.gemv, plan_fits(p, R) ? 1 : 0,
                   product_max_waves(rt, p.gemv ? 1 : p.nt));
+    } else if (!std::strcmp(cmd, "grp")) {    // bf16 nq nkv d w
+      int bf, nq, nkv, d, w;
+      std::scanf("%d %d %d %d %d", &bf, &nq, &nkv, &d, &w);
+      std::printf("%d\n", attention_group(bf != 0, nq, nkv, d, w));
+    } else if (!std::strcmp(cmd, "nsub")) {   // units nkv max_slots
+      int u, nkv, ms;
+      std::scanf("%d %d %d", &u, &nkv, &ms);
+      const int ns = attention_nsub(u, nkv, ms);
+      std::printf("%d %d\n", ns, attention_chunks(ms, ns));
+    } else if (!std::strcmp(cmd, "part")) {   // rows_max grp nkv max_slots
+      int rm, gp, nkv, ms, mc;
+      std::scanf("%d %d %d %d", &rm, &gp, &nkv, &ms);
+      const long p = attention_partial_rows(rm, gp, nkv, ms, mc);
+      std::printf("%ld %d\n", p, mc);
     }
   }
   return 0;
@@ -178,3 +193,51 @@ def test_every_plan_fits_its_kernel(driver):
             assert 64 * kw <= 64 * maxw
         if gemv:
             assert case[3] <= 2 and nt == 1
+
+
+def test_tree_attention_groups(driver):
+    cfgs = list(CONFIGS.values()) + [SMALL_BF16_TREE, SMALL_BF16_CHAIN]
+    cases = [(1 if c.dtype == "bf16" else 0, c.n_q_heads, c.n_kv_heads, c.head_dim, w)
+             for c in cfgs for w in range(1, 17)]
+    cases += [(1, 32, 8, 256, 8), (0, 32, 8, 128, 8), (1, 64, 8, 128, 6), (1, 32, 32, 64, 12)]
+    out = driver("".join("grp %d %d %d %d %d\n" % c for c in cases))
+    for (bf, nq, nkv, d, w), o in zip(cases, out):
+        gs = int(o)
+        g = nq // nkv
+        assert gs >= 1 and w % gs == 0 and gs * g <= 16 or gs == 1, (bf, nq, nkv, d, w, gs)
+        if not bf or d not in (64, 128):
+            assert gs == 1
+        else:   # the largest such divisor
+            best = max(k for k in range(1, w + 1) if w % k == 0 and (k * g <= 16 or k == 1))
+            assert gs == best, (nq, nkv, d, w, gs)
+    # the workloads' trees: 4 rows of 4 query heads per workgroup
+    assert driver("grp 1 32 8 128 8\n")[0] == "4"
+    t = SMALL_BF16_TREE
+    assert driver("grp 1 %d %d %d %d\n" % (t.n_q_heads, t.n_kv_heads, t.head_dim,
+                                           t.tree_width))[0] == "4"
+
+
+@pytest.mark.parametrize("rows_max,grp,nkv,max_slots", [
+    (32, 4, 8, 1152), (4, 1, 8, 1152), (1, 1, 8, 4096), (32, 1, 8, 4096), (16, 1, 8, 4096),
+    (2, 4, 2, 448), (64, 2, 8, 131072), (8, 8, 1, 64), (32, 4, 8, 16)])
+def test_attention_partials_cover_every_pass(driver, rows_max, grp, nkv, max_slots):
+    """Steps per workgroup: a power of two up to 16, the fewest that keep a
+    pass at most 512 workgroups; the partial buffers hold rows x chunks of
+    every pass of 1..rows_max rows, grouped or not."""
+    part, most_ch = (int(x) for x in driver("part %d %d %d %d\n" % (rows_max, grp, nkv,
+                                                                      max_slots))[0].split())
+    seen_rc, seen_ch = 0, 0
+    for R in range(1, rows_max + 1):
+        for gs in {1, grp}:
+            if R % gs:
+                continue
+            units = R // gs
+            ns, ch = (int(x) for x in driver("nsub %d %d %d\n" % (units, nkv, max_slots))[0].split())
+            assert ns in (1, 2, 4, 8, 16)
+            assert ch == -(-max_slots // (64 * ns))
+            assert units * nkv * ch <= 512 or ns == 16
+            if ns > 1:   # the fewest such steps
+                assert units * nkv * -(-max_slots // (64 * (ns // 2))) > 512
+            assert R * ch <= part
+            seen_rc, seen_ch = max(seen_rc, R * ch), max(seen_ch, ch)
+    assert (part, most_ch) == (seen_rc, seen_ch)
