@@ -1021,6 +1021,11 @@ static bool gemm_rt(const GemmLaunch &g, hipStream_t s) {
       return gemm_epi<T, 1, 1, PAIR, 2>(g, s);   // R <= GEMV_MAX_ROWS
     }
   }
+  if (g.nt == 7) {          // gate/up shapes whose tile count is a multiple of 7 * 256
+    if (g.R <= 16) return gemm_epi<T, 1, 7, PAIR, 0>(g, s);
+    if (g.R <= 32) return gemm_epi<T, 2, 7, PAIR, 0>(g, s);
+    return false;
+  }
   if (g.nt == 8) {          // batched rows, many tiles: no K slices
     if (g.R <= 16) return gemm_epi<T, 1, 8, PAIR, 0>(g, s);
     if (g.R <= 32) return gemm_epi<T, 2, 8, PAIR, 0>(g, s);

@@ -44,24 +44,46 @@ struct ProductPlan {
   int gemv = 0;    // 1: VALU GEMV main loop (bf16, at most GEMV_MAX_ROWS rows)
 };
 
-// Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
-// fragment reuse: 4, or 8 at 17-32 rows, so that the activation fragments a
-// wave loads stay within twice its weight fragments) and K slices across
-// workgroups: at most one workgroup of 4 waves per CU (longer slices stream
-// better than more of them, and a grid just above the CU count leaves a few
-// CUs with twice the work), at least 4 k-blocks per slice, and fp32 slice
-// partials of at most 1/4 of the weight bytes (split * R * N * 4 <= N * K * 2
-// / 4; at 32 rows the tighter 1/8 cap left the 4096-wide products on 64-128
-// workgroups: tree 2.695 -> 2.662 ms).
-inline void plan_batched(int n_tiles, int nkb, int K, int R, int &nt, int &split) {
-  nt = n_tiles % 4 == 0 ? 4 : (n_tiles % 2 == 0 ? 2 : 1);
-  if (R > 16 && n_tiles % 8 == 0) nt = 8;
+// K slices of a batched product at nt tiles per wave: at most one workgroup
+// of 4 waves per CU (longer slices stream better than more of them, and a
+// grid just above the CU count leaves a few CUs with twice the work), at
+// least 4 k-blocks per slice, and fp32 slice partials of at most 1/4 of the
+// weight bytes (split * R * N * 4 <= N * K * 2 / 4; at 32 rows the tighter
+// 1/8 cap left the 4096-wide products on 64-128 workgroups: tree 2.695 ->
+// 2.662 ms; a 1/2 cap was 1.5% slower on the tree).
+inline int batched_split(int n_tiles, int nt, int nkb, int K, int R) {
   const int wgs = (n_tiles / nt + SPLIT_WAVES - 1) / SPLIT_WAVES;
   int sp = 256 / wgs;
   if (sp > nkb / 4) sp = nkb / 4;
   if (sp > K / (8 * R)) sp = K / (8 * R);
-  split = sp < 1 ? 1 : sp;
+  return sp < 1 ? 1 : sp;
 }
+
+// Batched products (more than GEMV_MAX_ROWS rows): tiles per wave (B
+// fragment reuse: 4, or 8 at 17-32 rows, so that the activation fragments a
+// wave loads stay within twice its weight fragments) and K slices across
+// workgroups.  At 17-32 rows 8 tiles are taken unless the slice cap leaves
+// their grid smaller than the 4-tile one (the tree's 4096-wide products:
+// 128 workgroups at 8 tiles, 256 at 4; tree 2.342 -> 2.313 ms; at 70B both
+// fill the chip, and 4 tiles there were 2.5% slower).
+inline void plan_batched(int n_tiles, int nkb, int K, int R, int &nt, int &split) {
+  nt = n_tiles % 4 == 0 ? 4 : (n_tiles % 2 == 0 ? 2 : 1);
+  split = batched_split(n_tiles, nt, nkb, K, R);
+  if (R > 16 && n_tiles % 8 == 0) {
+    const int s8 = batched_split(n_tiles, 8, nkb, K, R);
+    const long w8 = (long)(n_tiles / 8 + SPLIT_WAVES - 1) / SPLIT_WAVES * s8;
+    const long w4 = (long)(n_tiles / nt + SPLIT_WAVES - 1) / SPLIT_WAVES * split;
+    if (w8 >= w4) {
+      nt = 8;
+      split = s8;
+    }
+  }
+}
+
+// Rounds of a grid of `groups` workgroups over the 256 CUs, times the tiles
+// each one streams: the relative time of an unsplit product at nt tiles per
+// wave.
+inline int unsplit_cost(int n_tiles, int nt) { return (n_tiles / nt + 255) / 256 * nt; }
 
 // Plan of a product of an [N = 16 n_tiles, K] matrix over R rows.  nkb and K
 // are those of the planned k range (the fusion FC may cover its feature
@@ -78,8 +100,13 @@ inline ProductPlan plan_product(int n_tiles, int nkb, int K, int K_full, int R, 
     if (groups >= 200 && (p.nt == 4 || p.nt == 8) && rt <= 2 && !qkv) {
       // enough tile groups to fill the chip: K split across the waves of a
       // workgroup (LDS reduction, epilogue in the kernel), no finish pass;
-      // about 1024 waves in all, within the instantiation's bound
+      // about 1024 waves in all, within the instantiation's bound.  7 tiles
+      // per wave where that fills whole rounds of the CUs and 4 or 8 do not
+      // (gate/up, 1792 and 3584 tiles: 256 and 512 groups instead of 224 and
+      // 448; batch 16 1.813 -> 1.790 ms, 70B 5.873 -> 5.838, tree -0.4%)
       p.split = 0;
+      if (n_tiles % 7 == 0 && unsplit_cost(n_tiles, 7) < unsplit_cost(n_tiles, p.nt)) p.nt = 7;
+      const int groups = n_tiles / p.nt;
       int kw = 1024 / groups;
       if (kw > product_max_waves(rt, p.nt)) kw = product_max_waves(rt, p.nt);
       while (kw > 1 && ((kw - 1) * p.nt * rt > 48 || kw > nkb / 4)) --kw;

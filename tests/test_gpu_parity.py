@@ -61,10 +61,14 @@ def test_chain_parity_row_counts(cfg):
 
 # A wide FFN gives the gate/up product at least 200 groups of 4 (16 rows) or
 # 8 (24 rows) tiles, which takes the unsplit batched path (K shared by the
-# waves of a workgroup, epilogue in the kernel).
+# waves of a workgroup, epilogue in the kernel).  At the 8B FFN width (1792
+# gate/up tiles) it runs 7 tiles per wave, at 16 and 32 rows.
 @pytest.mark.parametrize("cfg", [
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs16_ffn6400", batch=16, ffn=6400),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24_ffn12800", batch=24, ffn=12800, vocab=5120),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs16_ffn14336", batch=16, ffn=14336),
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs32_ffn14336", batch=32, ffn=14336,
+                           ctx_range=(20, 200)),
 ], ids=lambda c: c.name)
 def test_chain_parity_unsplit_products(cfg):
     run_chain_parity(cfg)

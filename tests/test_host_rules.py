@@ -191,6 +191,12 @@ def test_every_plan_fits_its_kernel(driver):
         assert fits == 1 and 1 <= kw <= maxw, (case, o)
         if split == 0 and not gemv:
             assert 64 * kw <= 64 * maxw
+            # instantiations the launcher dispatches unsplit
+            assert nt in (1, 2, 4, 7, 8), (case, o)
+            if nt in (4, 7, 8):
+                assert case[3] <= 32 and not case[4], (case, o)
+        if split > 0:
+            assert nt in (1, 2, 4, 8), (case, o)
         if gemv:
             assert case[3] <= 2 and nt == 1
 
@@ -241,3 +247,15 @@ def test_attention_partials_cover_every_pass(driver, rows_max, grp, nkv, max_slo
             assert R * ch <= part
             seen_rc, seen_ch = max(seen_rc, R * ch), max(seen_ch, ch)
     assert (part, most_ch) == (seen_rc, seen_ch)
+
+
+def test_gate_up_tiles_fill_whole_rounds(driver):
+    """The 8B gate/up (1792 tiles) at 16 and 32 rows and the 70B one (3584
+    tiles) at 32 rows run unsplit at 7 tiles per wave: 256 and 512 tile
+    groups, whole rounds of the 256 CUs."""
+    for n_tiles, K, R, groups in ((1792, 4096, 16, 256), (1792, 4096, 32, 256),
+                                  (3584, 8192, 32, 512)):
+        o = driver("plan %d %d %d %d %d 0 1 163840\n" % (n_tiles, K // 32, K, K, R))[0]
+        kw, nt, split, gemv, fits, maxw = (int(x) for x in o.split())
+        assert (nt, split, gemv, fits) == (7, 0, 0, 1), o
+        assert n_tiles // nt == groups
