@@ -491,16 +491,53 @@ __device__ __forceinline__ void finish_scales(const RowNorm &nm, int nr, const S
   __syncthreads();
 }
 
+// Operands of one lane's epilogue that do not depend on the product: the
+// residual and gain values (EPI_NORM) or the RoPE inverse frequencies
+// (EPI_QKV) of its 4 outputs.  The finish pass loads them before the slice
+// sums, so that they do not add a round trip after them.
+struct EpiPre {
+  f32x4 res;
+  float gain[4];
+  float freq[4];
+};
+
+template <typename T, int EPI>
+__device__ __forceinline__ EpiPre epilogue_prefetch(const GemmLaunch &g, int tile, int r) {
+  const int n0 = tile * 16 + 4 * ((threadIdx.x & 63) >> 4);
+  EpiPre p;
+  p.res = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p.gain[i] = p.freq[i] = 0.f;
+  if (r >= g.R) return p;
+  if (EPI == EPI_NORM) {
+    if (g.res) p.res = *(const f32x4 *)(g.res + (size_t)r * g.ldres + n0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p.gain[i] = Ty<T>::ld((const T *)g.gain, n0 + i);
+  } else if (EPI == EPI_QKV) {
+    const int f0 = tile * 16, d = g.d;
+    const int qd = g.nq * d, kd = g.nkv * d;
+    if (f0 < qd + kd) {
+      const int fr = f0 < qd ? f0 : f0 - qd;
+      const int dim0 = 8 * ((fr % d) / 16) + 4 * ((threadIdx.x & 63) >> 4 & 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p.freq[i] = g.inv_freq[dim0 + i];
+    }
+  }
+  return p;
+}
+
 // Epilogue of one 16x16 accumulator tile in the MFMA layout: the lane holds
 // output rows n0..n0+3 (tiled order) of batch row r = (lane & 15) + 16 rt.
 // Every lane of the wave must call it (it shuffles).  scale: the row's
 // RMSNorm scale (1 if none); cbase / rpos: the row's cache slot and position
-// (QKV only).  EPI_NORM returns the tile's sum of squares of row r (valid in
-// lanes 0..15); the caller stores it.
+// (QKV only); pre: the lane's prefetched operands (else loaded here).
+// EPI_NORM returns the tile's sum of squares of row r (valid in lanes
+// 0..15); the caller stores it.
 template <typename T, int EPI>
 __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, int r, f32x4 a,
                                                float scale, long cbase, int rpos,
-                                               f32x4 tadd = f32x4{0.f, 0.f, 0.f, 0.f}) {
+                                               f32x4 tadd = f32x4{0.f, 0.f, 0.f, 0.f},
+                                               const EpiPre *pre = nullptr) {
   const int lane = threadIdx.x & 63, q4 = lane >> 4;
   const int n0 = tile * 16 + 4 * q4;
   const bool live = r < g.R;
@@ -508,7 +545,9 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
   if (EPI == EPI_NORM) {
     float ss = 0.f;
     if (live) {
-      if (g.res) {
+      if (pre) {
+        v[0] += pre->res.x; v[1] += pre->res.y; v[2] += pre->res.z; v[3] += pre->res.w;
+      } else if (g.res) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[i] += g.res[(size_t)r * g.ldres + n0 + i];
       }
@@ -517,7 +556,8 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
       *(f32x4 *)(g.y + (size_t)r * g.ldy + n0) = f32x4{v[0], v[1], v[2], v[3]};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * Ty<T>::ld((const T *)g.gain, n0 + i));
+        const float gn = pre ? pre->gain[i] : Ty<T>::ld((const T *)g.gain, n0 + i);
+        put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * gn);
         ss += v[i] * v[i];
       }
     }
@@ -552,7 +592,7 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         // angle in fp64, reduced to [-pi, pi] in fp64, cos/sin in fp32
-        const double ang = (double)rpos * g.inv_freq[dim0 + i];
+        const double ang = (double)rpos * (pre ? pre->freq[i] : g.inv_freq[dim0 + i]);
         const double red = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
         float sn, cs;
         sincosf((float)red, &sn, &cs);
@@ -731,11 +771,17 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
     }
 }
 
-// Tiles per workgroup of the finish pass (a divisor of n_tiles, at most 8).
-static int finish_tiles(int n_tiles) {
-  for (int f = 8; f > 1; f >>= 1)
-    if (n_tiles % f == 0) return f;
-  return 1;
+// Tiles per workgroup of the finish pass (a divisor of n_tiles, at most 8):
+// few, so that the pass spreads over many CUs, but for EPI_NORM enough that
+// a row's sums-of-squares parts (n_tiles / ft) stay within FIN_PARTS, which
+// the consumers reduce themselves.
+constexpr int FIN_TILES = 2, FIN_TILES_NORM = 2, FIN_PARTS = 128;
+static int finish_tiles(int n_tiles, int epi) {
+  int f = epi == EPI_NORM ? FIN_TILES_NORM : FIN_TILES;
+  if (epi == EPI_NORM)
+    while (f < 8 && n_tiles / f > FIN_PARTS) f *= 2;
+  while (f > 1 && n_tiles % f) f >>= 1;
+  return f;
 }
 
 // One wave per (tile, 16-row group), FT = blockDim.x / 64 consecutive tiles
@@ -744,7 +790,7 @@ static int finish_tiles(int n_tiles) {
 // here from the producer's partials (or come precomputed).  EPI_NORM sums of
 // squares are added over the workgroup's tiles in wave order, which leaves
 // one partial per workgroup and row (n_tiles / FT per row in all).
-constexpr int FIN_UNROLL = 8;
+constexpr int FIN_UNROLL = 16;
 template <typename T, int EPI>
 __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   __shared__ float rowscale[16];
@@ -762,6 +808,8 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   f32x4 tadd = f32x4{0.f, 0.f, 0.f, 0.f};   // fusion FC: the row's embedding-table term
   long cbase = -1;
   int rpos = 0;
+  // operands that do not depend on the slices go out before them
+  const EpiPre pre = epilogue_prefetch<T, EPI>(g, tile, r);
   if (r < g.R) {
     if (EPI == EPI_QKV) cbase = cache_base(g, r, rpos);
     // the row's token goes out first, its table row right after the first
@@ -789,7 +837,7 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   } else if (g.norm.scale && r < g.R) {
     sc = g.norm.scale[r];
   }
-  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos, tadd);
+  const float ss = epilogue_tile<T, EPI>(g, tile, r, a, sc, cbase, rpos, tadd, &pre);
   if constexpr (EPI == EPI_NORM) {
     if (lane < 16) ssw[wave][lane] = ss;
     __syncthreads();
@@ -986,7 +1034,7 @@ static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
   const int groups = g.m.n_tiles / NT;
   hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), dim3((groups + 3) / 4, g.split), dim3(256), 0,
                      s, g);
-  const int ft = finish_tiles(g.m.n_tiles);
+  const int ft = finish_tiles(g.m.n_tiles, g.epi);
   const dim3 fg(g.m.n_tiles / ft, (g.R + 15) / 16), fb(64 * ft);
   if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, fb, 0, s, g);
   else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, fb, 0, s, g);
@@ -1054,11 +1102,11 @@ bool launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s) {
 int lm_workgroups(int n_tiles, int nt) { return (n_tiles / nt + 3) / 4; }
 
 int gemm_ss_parts(const GemmLaunch &g) {
-  return g.split > 0 ? g.m.n_tiles / finish_tiles(g.m.n_tiles) : g.m.n_tiles;
+  return g.split > 0 ? g.m.n_tiles / finish_tiles(g.m.n_tiles, g.epi) : g.m.n_tiles;
 }
 
 bool gemm_own_scales(const GemmLaunch &g, int n_parts) {
-  if (g.split > 0) return scales_fit(64 * finish_tiles(g.m.n_tiles), g.R < 16 ? g.R : 16, n_parts);
+  if (g.split > 0) return scales_fit(64 * finish_tiles(g.m.n_tiles, g.epi), g.R < 16 ? g.R : 16, n_parts);
   return g.R <= MAX_ROWS && scales_fit(64 * g.kw, g.R, n_parts);
 }
 
