@@ -698,8 +698,15 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     mainloop_valu<VR, GX>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, g.x, g.R, m.K, xs, kb0,
                           kb1, acc[0][0], g.gx, g.err, g.tab, m.N, t0, &tv);
   } else {
-    mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
-                              kb1, acc);
+    // up to 16 rows (7 or more tiles: registers) the next batch of k-blocks
+    // is in flight while one is consumed: batch 16 -0.7%; at 32 rows the
+    // second register set spills (tree +5%)
+    if constexpr (RT == 1 && NT >= 7 && sizeof(T) == 2)
+      mainloop_db<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R,
+                                   kb0, kb1, acc);
+    else
+      mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
+                                kb1, acc);
   }
   if (kw > 1) {
     if (wave > 0) {
@@ -758,8 +765,14 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
   for (int n = 0; n < NT; ++n)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0, kb1,
-                            acc);
+  // up to 16 rows with two register sets of k-blocks (batch 16 -0.8%); at
+  // 32 rows it was slower (70B +0.6%)
+  if constexpr (RT == 1 && sizeof(T) == 2)
+    mainloop_db<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
+                                 kb1, acc);
+  else
+    mainloop<T, RT, NT, PAIR>((const u32x4 *)m.w + (size_t)t0 * m.nkb * 64, m.nkb, g.x, g.R, kb0,
+                              kb1, acc);
   const int q4 = lane >> 4;
 #pragma unroll
   for (int n = 0; n < NT; ++n)
