@@ -302,6 +302,21 @@ def test_tree_parity_small():
     run_tree_parity(SMALL_BF16_TREE)
 
 
+# Head geometries of the grouped tree attention (a workgroup takes the
+# largest divisor of w whose rows x query heads fit 16 score columns): 6 rows
+# of 2 heads, 2 rows of 8 heads, 4 rows of 4 heads at head_dim 128, and a
+# width with no such divisor (ungrouped).
+@pytest.mark.parametrize("cfg", [
+    SMALL_BF16_TREE.with_(name="small_bf16_tree_g2_w6", n_q_heads=8, n_kv_heads=4,
+                          tree_width=6, n_steps=3, tree_nodes=20),
+    SMALL_BF16_TREE.with_(name="small_bf16_tree_g8_w4", n_q_heads=8, n_kv_heads=1),
+    SMALL_BF16_TREE.with_(name="small_bf16_tree_d128", n_q_heads=4, n_kv_heads=1, head_dim=128),
+    SMALL_BF16_TREE.with_(name="small_bf16_tree_w5", tree_width=5, n_steps=3, tree_nodes=14),
+], ids=lambda c: c.name)
+def test_tree_parity_head_geometries(cfg):
+    run_tree_parity(cfg)
+
+
 def test_tree_width_one_equals_chain():
     tcfg = SMALL_BF16_TREE.with_(tree_width=1, tree_nodes=SMALL_BF16_TREE.n_steps)
     dr, w, inp = gpu_setup(tcfg)
