@@ -452,10 +452,12 @@ __device__ __forceinline__ void put_act(const ActOut &o, size_t i, float v) {
 // producer's partial sums of squares (layout [part][R]).  Thread t serves row
 // r0 + t / tpr and adds parts t % tpr, t % tpr + tpr, ... in that order; the
 // tpr threads of a row (adjacent lanes of one wave) then meet in a fixed
-// butterfly, so the result does not depend on scheduling.  The loads are
-// issued before the main loop (issue_scales) and reduced after it
-// (finish_scales).
+// butterfly, so the result does not depend on scheduling.  The first
+// SS_PER_THREAD parts of each thread are requested before the main loop
+// (issue_scales); finish_scales adds them and loads any further ones (up to
+// SS_MAX_ROUNDS times as many) after it.
 constexpr int SS_PER_THREAD = 16;
+constexpr int SS_MAX_ROUNDS = 4;
 struct ScaleLoads {
   float v[SS_PER_THREAD];
 };
@@ -465,7 +467,7 @@ __host__ __device__ inline int scale_tpr(int threads, int nr) {
   return t;
 }
 __host__ __device__ inline bool scales_fit(int threads, int nr, int n_parts) {
-  return nr <= threads && n_parts <= SS_PER_THREAD * scale_tpr(threads, nr);
+  return nr <= threads && n_parts <= SS_MAX_ROUNDS * SS_PER_THREAD * scale_tpr(threads, nr);
 }
 __device__ __forceinline__ ScaleLoads issue_scales(const RowNorm &nm, int R, int r0, int nr) {
   ScaleLoads s;
@@ -479,12 +481,17 @@ __device__ __forceinline__ ScaleLoads issue_scales(const RowNorm &nm, int R, int
   return s;
 }
 // every thread of the block calls it (barrier); rowscale[0 .. nr - 1]
-__device__ __forceinline__ void finish_scales(const RowNorm &nm, int nr, const ScaleLoads &s,
-                                              float *rowscale) {
+__device__ __forceinline__ void finish_scales(const RowNorm &nm, int R, int r0, int nr,
+                                              const ScaleLoads &s, float *rowscale) {
   const int tpr = scale_tpr(blockDim.x, nr);
   float acc = 0.f;
 #pragma unroll
   for (int j = 0; j < SS_PER_THREAD; ++j) acc += s.v[j];
+  {
+    const int r = threadIdx.x / tpr;
+    for (int p = threadIdx.x % tpr + SS_PER_THREAD * tpr; r < nr && p < nm.n_parts; p += tpr)
+      acc += nm.ss[(size_t)p * R + r0 + r];
+  }
   for (int o = 1; o < tpr; o <<= 1) acc += __shfl_xor(acc, o, 64);
   const int r = threadIdx.x / tpr;
   if (r < nr && threadIdx.x % tpr == 0) rowscale[r] = 1.0f / sqrtf(acc / (float)nm.n + nm.eps);
@@ -718,7 +725,7 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
   }
   if (own_scales) {
     __syncthreads();
-    finish_scales(g.norm, g.R, sl, rowscale);
+    finish_scales(g.norm, g.R, 0, g.R, sl, rowscale);
   } else if (kw > 1) {
     __syncthreads();
   }
@@ -845,7 +852,7 @@ __global__ __launch_bounds__(512) void k_gemm_finish(GemmLaunch g) {
   }
   float sc = 1.f;
   if (own) {
-    finish_scales(g.norm, nr, sl, rowscale);
+    finish_scales(g.norm, g.R, r0, nr, sl, rowscale);
     if (r < g.R) sc = rowscale[r - r0];
   } else if (g.norm.scale && r < g.R) {
     sc = g.norm.scale[r];
@@ -907,7 +914,7 @@ __global__ __launch_bounds__(256) void k_lmhead(LmLaunch g) {
   }
   if (own_scales) {
     __syncthreads();
-    finish_scales(g.norm, g.R, sc, rowscale);
+    finish_scales(g.norm, g.R, 0, g.R, sc, rowscale);
   }
   const int q4 = lane >> 4;
 #pragma unroll
