@@ -791,6 +791,105 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
     }
 }
 
+// The same for bf16 with the slice's activation fragments staged in LDS once
+// per workgroup: the 4 waves share the K slice, so instead of each wave
+// loading every B fragment, the workgroup loads each once and the waves read
+// them from LDS.  Layout xs[(k-block, plane, row tile)][lane], the B operand
+// order, so each ds_read_b128 is one contiguous, conflict-free KiB.  The
+// first batch of weight loads is issued right after the staging loads, so
+// the two overlap; only weight fragments occupy registers in the loop (two
+// sets, the next batch in flight while one is consumed).  The launcher takes
+// this path when a wave stages at most SPLIT_LDS_FRAGS / 4 fragments.
+constexpr int SPLIT_LDS_FRAGS = 64;   // staged fragments per workgroup (64 KiB)
+template <int RT, int NT>
+__global__ __launch_bounds__(256) void k_gemm_split_lds(GemmLaunch g) {
+  extern __shared__ u32x4 xs_split[];    // [nf][64]
+  constexpr int SF = SPLIT_LDS_FRAGS / 4;  // fragments per wave
+  constexpr int U = 16 / NT > 0 ? 16 / NT : 1;   // k-blocks per batch
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const TiledMat &m = g.m;
+  const int t0 = (blockIdx.x * 4 + wave) * NT;
+  const bool live = t0 < m.n_tiles;       // n_tiles is a multiple of NT
+  const int S = gridDim.y, sl = blockIdx.y;
+  const int nk = m.nkb - g.kb_lo;
+  const int kb0 = g.kb_lo + (int)((long)sl * nk / S), kb1 = g.kb_lo + (int)((long)(sl + 1) * nk / S);
+  const int nf = (kb1 - kb0) * 2 * RT;    // <= SPLIT_LDS_FRAGS (checked by the launcher)
+  // staging loads: fragment f = (k-block i, plane p, row tile rt), lane (row
+  // 16 rt + (lane & 15), k 8 (lane >> 4)); unconditional (clamped) so that
+  // the weight loads issued after them stay in flight
+  u32x4 sv[SF];
+#pragma unroll
+  for (int i = 0; i < SF; ++i) {
+    const int f = max(min(wave + 4 * i, nf - 1), 0);
+    const int kbi = f / (2 * RT), pl = (f / RT) & 1, rt = f % RT;
+    const int r = (lane & 15) + 16 * rt;
+    const int kb = min(kb0 + kbi, m.nkb - 1);
+    const bf16_t *src = (const bf16_t *)(pl ? g.x.lo : g.x.hi) + (size_t)(r < g.R ? r : 0) * g.x.ld +
+                        (size_t)kb * 32 + 8 * (lane >> 4);
+    sv[i] = *(const u32x4 *)src;
+    if (r >= g.R) sv[i] = u32x4{0, 0, 0, 0};
+  }
+  const u32x4 *wp[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) wp[n] = (const u32x4 *)m.w + ((size_t)(live ? t0 : 0) + n) * m.nkb * 64 + lane;
+  u32x4 a[2][U][NT];
+  auto loadw = [&](int st, int kb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = min(kb + u, kb1 - 1);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) a[st][u][n] = __builtin_nontemporal_load(wp[n] + (size_t)k * 64);
+    }
+  };
+  if (live && kb1 > kb0) loadw(0, kb0);
+#pragma unroll
+  for (int i = 0; i < SF; ++i) {
+    const int f = wave + 4 * i;
+    if (f < nf) xs_split[f * 64 + lane] = sv[i];
+  }
+  __syncthreads();
+  if (!live || kb1 <= kb0) return;        // no barriers below
+  f32x4 acc[NT][RT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](int st, int kb, int nb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (u < nb) {
+        const int kbi = kb + u - kb0;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const u32x4 bh = xs_split[((kbi * 2 + 0) * RT + rt) * 64 + lane];
+          const u32x4 bl = xs_split[((kbi * 2 + 1) * RT + rt) * 64 + lane];
+#pragma unroll
+          for (int n = 0; n < NT; ++n) {
+            acc[n][rt] = Ty<bf16_t>::mma(a[st][u][n], bh, acc[n][rt]);
+            acc[n][rt] = Ty<bf16_t>::mma(a[st][u][n], bl, acc[n][rt]);
+          }
+        }
+      }
+    }
+  };
+  for (int kb = kb0; kb < kb1; kb += 2 * U) {
+    loadw(1, kb + U);
+    mma(0, kb, kb1 - kb);
+    if (kb + U >= kb1) break;
+    loadw(0, kb + 2 * U);
+    mma(1, kb + U, kb1 - kb - U);
+  }
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int n = 0; n < NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const int r = (lane & 15) + 16 * rt;
+      if (r < g.R)
+        *(f32x4 *)(g.part + ((size_t)sl * g.R + r) * m.N + (t0 + n) * 16 + 4 * q4) = acc[n][rt];
+    }
+}
+
 // Tiles per workgroup of the finish pass (a divisor of n_tiles, at most 8):
 // few, so that the pass spreads over many CUs, but for EPI_NORM enough that
 // a row's sums-of-squares parts (n_tiles / ft) stay within FIN_PARTS, which
@@ -1052,8 +1151,18 @@ static bool gemm_epi(const GemmLaunch &g, hipStream_t s) {
 template <typename T, int RT, int NT, bool PAIR>
 static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
   const int groups = g.m.n_tiles / NT;
-  hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), dim3((groups + 3) / 4, g.split), dim3(256), 0,
-                     s, g);
+  const dim3 grid((groups + 3) / 4, g.split);
+  bool staged = false;
+  if constexpr (sizeof(T) == 2 && RT <= 2) {
+    const int nk = g.m.nkb - g.kb_lo;
+    const int nk_max = (nk + g.split - 1) / g.split;   // the longest slice
+    if (nk_max * 2 * RT <= SPLIT_LDS_FRAGS) {
+      hipLaunchKernelGGL((k_gemm_split_lds<RT, NT>), grid, dim3(256),
+                         (size_t)nk_max * 2 * RT * 64 * sizeof(u32x4), s, g);
+      staged = true;
+    }
+  }
+  if (!staged) hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), grid, dim3(256), 0, s, g);
   const int ft = finish_tiles(g.m.n_tiles, g.epi);
   const dim3 fg(g.m.n_tiles / ft, (g.R + 15) / 16), fb(64 * ft);
   if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, fb, 0, s, g);
