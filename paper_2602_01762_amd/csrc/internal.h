@@ -265,6 +265,7 @@ struct TreeWs {
   int32_t *cand_tok, *cand_par;   // [B, C]
   float *cand_score;              // [B, C]
   int32_t *front;                 // [B, D-1, w] candidate index of frontier nodes
+  float *front_score;             // [B, D-1, w] their scores
   int32_t *tok, *feat_row, *seq, *pos, *slot; // next-pass rows [B*w]
   uint64_t *bits;                 // next-pass visibility [B*w]
   uint64_t *bits_prev;            // visibility of the pass just run [B*w]

@@ -496,6 +496,7 @@ __global__ __launch_bounds__(256) void k_lm_topk(LmTopkArgs a) {
     if (tid < n) {
       const uint64_t mine = s_cand[tid];
       int rank = 0;
+#pragma unroll 8
       for (int i = 0; i < n; ++i) rank += s_cand[i] > mine ? 1 : 0;
       if (rank < k) {
         a.pval[pi * k + rank] = key_value(mine);
@@ -650,10 +651,20 @@ void launch_rows_gather(int rows, const RowsGather &a, hipStream_t s) {
 // of the w frontier nodes (frontier rank major, child rank minor).  A score
 // is the parent's score plus the child's log-prob (fp32).  Order key of both
 // the frontier and the output: (score desc, candidate index asc), with NaN
-// scores after every number (tree_before), a total order, so that every
-// rank below the cut has exactly one candidate.
+// scores after every number (tree_before; tree_rank_key as one integer), a
+// total order, so that every rank below the cut has exactly one candidate.
 constexpr int TREE_MAXNEW = 256;
 constexpr int TREE_MAXC = MAX_TREE_CAND;
+
+// Rank of candidate key k among n keys in LDS: the number of greater keys.
+// Unrolled so that the LDS reads of a batch are in flight together (one
+// read at a time waits its full latency per candidate: 30 us for 328).
+__device__ __forceinline__ int tree_rank(const uint64_t *keys, int n, uint64_t k) {
+  int r = 0;
+#pragma unroll 16
+  for (int j = 0; j < n; ++j) r += keys[j] > k ? 1 : 0;
+  return r;
+}
 
 struct TreeExpArgs {
   TreeWs t;
@@ -664,6 +675,7 @@ struct TreeExpArgs {
 };
 
 __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
+  __shared__ uint64_t rk[TREE_MAXNEW];
   __shared__ float sc[TREE_MAXNEW];
   __shared__ int tk[TREE_MAXNEW];
   const TreeWs &t = a.t;
@@ -677,11 +689,14 @@ __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
     if (d == 0) {
       row = b; c = i; parent = -1; ps = 0.f;
     } else {
+      // the parent's index and score, both recorded with the frontier (no
+      // load that waits on another)
       const int pr = i / w;
       row = b * w + pr;
       c = i % w;
-      parent = t.front[((size_t)b * (t.D - 1) + (d - 1)) * w + pr];
-      ps = t.cand_score[(size_t)b * t.C + min(max(parent, 0), t.C - 1)];
+      const size_t fi = ((size_t)b * (t.D - 1) + (d - 1)) * w + pr;
+      parent = t.front[fi];
+      ps = t.front_score[fi];
     }
     const int tok = a.ids[(size_t)row * w + c];
     const float score = ps + a.logp[(size_t)row * w + c];
@@ -689,6 +704,7 @@ __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
     t.cand_tok[ci] = tok;
     t.cand_par[ci] = parent;
     t.cand_score[ci] = score;
+    rk[i] = tree_rank_key(score, i);
     sc[i] = score;
     tk[i] = tok;
   }
@@ -696,10 +712,10 @@ __global__ __launch_bounds__(256) void k_tree_expand(TreeExpArgs a) {
   __syncthreads();
   const int L = a.ctx_lens[b];
   for (int i = tid; i < n_new; i += blockDim.x) {
-    int rank = 0;
-    for (int j = 0; j < n_new; ++j) rank += tree_before(sc[j], j, sc[i], i);
+    const int rank = tree_rank(rk, n_new, rk[i]);
     if (rank >= w) continue;
     t.front[((size_t)b * (t.D - 1) + d) * w + rank] = base + i;
+    t.front_score[((size_t)b * (t.D - 1) + d) * w + rank] = sc[i];
     const int nr = b * w + rank;
     const int prow = d == 0 ? b : b * w + i / w;
     t.tok[nr] = tk[i];
@@ -799,6 +815,7 @@ struct TreeFinArgs {
 __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
   constexpr int PER = (TREE_MAXC + 255) / 256;
   __shared__ float sc[TREE_MAXC];
+  __shared__ uint64_t rk[TREE_MAXC];
   __shared__ int tk[TREE_MAXC], pa[TREE_MAXC];
   __shared__ short outpos[TREE_MAXC];
   __shared__ int sel[64];
@@ -806,6 +823,12 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
   const TreeWs &t = a.t;
   const int b = blockIdx.x, tid = threadIdx.x;
   const int C = t.C, w = t.w;
+  // the frontier copy is requested with the candidates, not after the
+  // ranking: (D - 1) w <= 63 entries (the context admits at most 64 draft
+  // slots), one per thread
+  const int nf = a.front_out ? (t.D - 1) * w : 0;
+  const int fr = tid < nf ? t.front[(size_t)b * nf + tid] : 0;
+  bool nan_seen = false;
   {
     float vs[PER];
     int vt[PER], vp[PER];
@@ -822,18 +845,17 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
       const int i = tid + 256 * q;
       if (i < C) {
         sc[i] = vs[q];
+        rk[i] = tree_rank_key(vs[q], i);
         tk[i] = vt[q];
         pa[i] = vp[q];
         outpos[i] = -1;
+        nan_seen |= vs[q] != vs[q];
       }
     }
   }
   __syncthreads();
-  bool nan_seen = false;
   for (int i = tid; i < C; i += blockDim.x) {
-    int rank = 0;
-    for (int j = 0; j < C; ++j) rank += tree_before(sc[j], j, sc[i], i);
-    nan_seen |= sc[i] != sc[i];
+    const int rank = tree_rank(rk, C, rk[i]);
     if (rank < a.v) {
       sel[rank] = i;
       outpos[i] = (short)rank;
@@ -861,11 +883,7 @@ __global__ __launch_bounds__(256) void k_tree_final(TreeFinArgs a) {
     if (a.c_par) a.c_par[(size_t)b * C + i] = pa[i];
     if (a.c_score) a.c_score[(size_t)b * C + i] = sc[i];
   }
-  if (a.front_out) {
-    const int nf = (t.D - 1) * w;
-    for (int i = tid; i < nf; i += blockDim.x)
-      a.front_out[(size_t)b * nf + i] = t.front[(size_t)b * nf + i];
-  }
+  if (tid < nf) a.front_out[(size_t)b * nf + tid] = fr;
 }
 
 void launch_tree_final(const TreeWs &t, int v, int32_t *tokens, int32_t *parent, int32_t *depth,

@@ -87,6 +87,7 @@ struct prism_ctx {
   int *lm_id = nullptr, *ids = nullptr, *tokbuf = nullptr;
   int32_t *c_seq = nullptr, *c_pos = nullptr, *c_tok0 = nullptr;
   int32_t *t_ctok = nullptr, *t_cpar = nullptr, *t_front = nullptr;
+  float *t_fscore = nullptr;
   float *t_cscore = nullptr;
   int32_t *t_tok = nullptr, *t_frow = nullptr, *t_seq = nullptr, *t_pos = nullptr, *t_slot = nullptr;
   uint64_t *t_bits[2] = {nullptr, nullptr};
@@ -329,6 +330,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->t_cpar, tb * 4);
   add((void **)&c->t_cscore, tb * 4);
   add((void **)&c->t_front, (size_t)k.max_batch * (k.max_steps > 1 ? k.max_steps - 1 : 1) * (w > 0 ? w : 1) * 4);
+  add((void **)&c->t_fscore, (size_t)k.max_batch * (k.max_steps > 1 ? k.max_steps - 1 : 1) * (w > 0 ? w : 1) * 4);
   add((void **)&c->t_tok, R * 4);
   add((void **)&c->t_frow, R * 4);
   add((void **)&c->t_seq, R * 4);
@@ -1123,7 +1125,7 @@ prism_status prism_draft_tree(prism_ctx *c, const prism_batch *batch, int32_t de
   TreeWs t{};
   t.B = B; t.w = w; t.D = depth; t.C = C;
   t.cand_tok = c->t_ctok; t.cand_par = c->t_cpar; t.cand_score = c->t_cscore;
-  t.front = c->t_front;
+  t.front = c->t_front; t.front_score = c->t_fscore;
   t.tok = c->t_tok; t.feat_row = c->t_frow; t.seq = c->t_seq; t.pos = c->t_pos; t.slot = c->t_slot;
   t.err = c->err;
   auto enqueue = [&](hipStream_t s) {

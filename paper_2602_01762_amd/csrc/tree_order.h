@@ -28,6 +28,14 @@ __host__ __device__ inline bool tree_before(float sj, int j, float si, int i) {
   return kj > ki || (kj == ki && j < i);
 }
 
+// The same order as one integer compare: tree_before(sj, j, si, i) holds
+// exactly when tree_rank_key(sj, j) > tree_rank_key(si, i) (score key in the
+// high half; the complemented index in the low half, so that of two equal
+// scores the lower index compares higher).  i >= 0.
+__host__ __device__ inline uint64_t tree_rank_key(float s, int i) {
+  return ((uint64_t)tree_score_key(s) << 32) | (uint64_t)(~(uint32_t)i);
+}
+
 // Ancestor bitset of output node i (i < 64): bit i and the bit of every
 // node on its path to the root.  par[n] is the output position of n's
 // parent (-1: the root).  A selected tree has par[n] < n, because a parent

@@ -1,7 +1,7 @@
 """Host unit tests of the library's plain-C++ rules, compiled with g++ (no GPU).
 
-* tree_order.h: the candidate order of the draft tree and the ancestor walk,
-  on NaN, infinity and tie inputs.  The kernels rank candidates by it, so
+* tree_order.h: the candidate order of the draft tree (as a comparison and as
+  integer keys) and the ancestor walk, on NaN, infinity and tie inputs.  The kernels rank candidates by it, so
   ranks must form a permutation whatever the scores are.  If they do not,
   two candidates share a slot and another slot is never written.
 * plan.h: the launch plan of every product of every configured shape and row
@@ -43,6 +43,16 @@ int main() {
       for (int i = 0; i < n; ++i) {
         int r = 0;
         for (int j = 0; j < n; ++j) r += tree_before(s[j], j, s[i], i);
+        std::printf("%d ", r);
+      }
+      std::printf("\n");
+    } else if (!std::strcmp(cmd, "rankk")) {  // the same ranks by the integer keys
+      int n; std::scanf("%d", &n);
+      uint64_t k[4096];
+      for (int i = 0; i < n; ++i) { unsigned u; std::scanf("%x", &u); k[i] = tree_rank_key(f_of(u), i); }
+      for (int i = 0; i < n; ++i) {
+        int r = 0;
+        for (int j = 0; j < n; ++j) r += k[j] > k[i] ? 1 : 0;
         std::printf("%d ", r);
       }
       std::printf("\n");
@@ -99,8 +109,8 @@ def bits(x):
     return "%08x" % struct.unpack("<I", struct.pack("<f", x))[0]
 
 
-def ranks(driver, scores):
-    line = "rank %d %s\n" % (len(scores), " ".join(bits(s) for s in scores))
+def ranks(driver, scores, cmd="rank"):
+    line = "%s %d %s\n" % (cmd, len(scores), " ".join(bits(s) for s in scores))
     return [int(t) for t in driver(line)[0].split()]
 
 
@@ -127,8 +137,9 @@ NEG_NAN = struct.unpack("<f", struct.pack("<I", 0xffc00001))[0]
     [NEG_NAN, NAN, -INF],                          # NaN of either sign
     [1e-45, -1e-45, 0.0, 3.4e38, -3.4e38],         # denormals, extremes
 ])
-def test_tree_order_is_a_total_order(driver, scores):
-    got = ranks(driver, scores)
+@pytest.mark.parametrize("cmd", ["rank", "rankk"])
+def test_tree_order_is_a_total_order(driver, scores, cmd):
+    got = ranks(driver, scores, cmd)
     assert sorted(got) == list(range(len(scores))), "ranks must be a permutation"
     assert got == expected_ranks(scores)
 
@@ -141,8 +152,9 @@ def test_tree_order_random_with_nan_and_ties(driver):
         s = rng.choice([-1.0, -0.5, 0.0, NAN, -INF], size=n).astype(np.float32)
         s = np.where(rng.random(n) < 0.5, s, rng.normal(size=n).astype(np.float32))
         scores = [float(x) for x in s]
-        got = ranks(driver, scores)
-        assert got == expected_ranks(scores)
+        want = expected_ranks(scores)
+        assert ranks(driver, scores) == want
+        assert ranks(driver, scores, "rankk") == want
 
 
 def test_ancestor_walk_is_bounded_and_exact(driver):
