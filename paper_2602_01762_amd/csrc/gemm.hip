@@ -565,6 +565,7 @@ __device__ __forceinline__ float epilogue_tile(const GemmLaunch &g, int tile, in
       for (int i = 0; i < 4; ++i) {
         const float gn = pre ? pre->gain[i] : Ty<T>::ld((const T *)g.gain, n0 + i);
         put_act<T>(g.g, (size_t)r * g.g.ld + n0 + i, v[i] * gn);
+        if (g.yx.hi) put_act<T>(g.yx, (size_t)r * g.yx.ld + n0 + i, v[i]);
         ss += v[i] * v[i];
       }
     }
@@ -752,6 +753,39 @@ __global__ __launch_bounds__((gemm_max_threads<RT, NT>())) void k_gemm(GemmLaunc
     }
 }
 
+// Token of row i for a K-split fusion FC that has no prep pass: wave 0 of
+// the workgroup with linear index i resolves it, its loads of the previous
+// LM head's top-1 partials issued at the start of the kernel and reduced
+// after them, so that the other loads of the workgroup do not wait.
+constexpr int SPLIT_TOK_PRE = 4;
+struct SplitTok {
+  int row = -1;                  // wave-uniform; -1: this wave resolves none
+  int tok = -1;
+  TokLoads<SPLIT_TOK_PRE> l;
+};
+__device__ __forceinline__ SplitTok split_tok_issue(const GemmLaunch &g) {
+  SplitTok st;
+  const int i = blockIdx.y * gridDim.x + blockIdx.x;
+  if (!g.tok_out || (threadIdx.x >> 6) != 0 || i >= g.R) return st;
+  st.row = i;
+  if (g.gx.lm.pval) st.l = issue_tok<SPLIT_TOK_PRE>(g.gx.lm, i);
+  else st.tok = g.gx.in.tokens[i];
+  return st;
+}
+__device__ __forceinline__ void split_tok_store(const GemmLaunch &g, const SplitTok &st) {
+  if (st.row < 0) return;
+  const bool from_lm = g.gx.lm.pval != nullptr;
+  int t = from_lm ? finish_tok<SPLIT_TOK_PRE>(g.gx.lm, st.row, st.l) : st.tok;
+  if ((threadIdx.x & 63) != 0) return;
+  if (from_lm && g.gx.lm.rec) g.gx.lm.rec[(size_t)st.row * g.gx.lm.ld_rec] = t;
+  if (t < 0 || t >= g.gx.V) {
+    // from the LM head, only a row of NaN logits leaves no token
+    atomicOr(g.err, from_lm && t == NO_TOKEN ? ERRF_NONFINITE : ERRF_TOKEN);
+    t = -1;
+  }
+  g.tok_out[st.row] = t;
+}
+
 // Batched products (R > 4 rows): the 4 waves of a workgroup take 4
 // consecutive groups of NT tiles over the same K slice (slice blockIdx.y of
 // gridDim.y), so the B fragments a wave loads are the ones its neighbours
@@ -764,6 +798,9 @@ __global__ __launch_bounds__(256) void k_gemm_split(GemmLaunch g) {
   const TiledMat &m = g.m;
   const int t0 = (blockIdx.x * 4 + wave) * NT;
   if (t0 >= m.n_tiles) return;   // n_tiles is a multiple of NT; no barriers below
+  // (resolved before the main loop: kept across it, its registers lowered
+  // the occupancy of some instantiations)
+  split_tok_store(g, split_tok_issue(g));   // wave 0 is never idle
   const int S = gridDim.y, sl = blockIdx.y;
   const int nk = m.nkb - g.kb_lo;
   const int kb0 = g.kb_lo + (int)((long)sl * nk / S), kb1 = g.kb_lo + (int)((long)(sl + 1) * nk / S);
@@ -814,6 +851,7 @@ __global__ __launch_bounds__(256) void k_gemm_split_lds(GemmLaunch g) {
   const int nk = m.nkb - g.kb_lo;
   const int kb0 = g.kb_lo + (int)((long)sl * nk / S), kb1 = g.kb_lo + (int)((long)(sl + 1) * nk / S);
   const int nf = (kb1 - kb0) * 2 * RT;    // <= SPLIT_LDS_FRAGS (checked by the launcher)
+  const SplitTok stok = split_tok_issue(g);   // wave 0 is live in every workgroup
   // staging loads: fragment f = (k-block i, plane p, row tile rt), lane (row
   // 16 rt + (lane & 15), k 8 (lane >> 4)); unconditional (clamped) so that
   // the weight loads issued after them stay in flight
@@ -848,6 +886,7 @@ __global__ __launch_bounds__(256) void k_gemm_split_lds(GemmLaunch g) {
     if (f < nf) xs_split[f * 64 + lane] = sv[i];
   }
   __syncthreads();
+  split_tok_store(g, stok);               // its loads returned before the staging ones
   if (!live || kb1 <= kb0) return;        // no barriers below
   f32x4 acc[NT][RT];
 #pragma unroll

@@ -141,6 +141,12 @@ struct GemmLaunch {
   const float *tab;
   int kb_lo;
   const int32_t *tab_tok;   // batched path: each row's token (-1: none), written by the FC prep
+  // chain steps >= 2 without an FC prep pass: the previous step's down
+  // product also writes its output y as operand planes (yx.hi != NULL), and
+  // wave 0 of K-split workgroup i < R resolves row i's token (from gx.lm, or
+  // gx.in.tokens; -1 if out of range) into tok_out for the finish pass
+  ActOut yx;
+  int32_t *tok_out;
 };
 
 struct LmLaunch {

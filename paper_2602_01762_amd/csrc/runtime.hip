@@ -44,6 +44,10 @@ struct Pass {            // one forward pass: where its inputs and outputs live
   float *logits; long ld_logits;
   int *ids; float *logp;
   int *tok_a; int *tok_b; int ld_b;
+  // chain steps: this pass's FC takes its feature operand from the previous
+  // pass's down product and its tokens in its own K-split kernel (no prep
+  // pass); this pass's down product writes that operand for the next pass
+  bool op_in, op_out;
 };
 
 std::string g_create_error;
@@ -612,6 +616,13 @@ static void enqueue_front(prism_ctx *c, const Pass &p, const KvArgs &kv, hipStre
   if (g.gemv) {   // the GEMV stages [E(x) ; f] (or f) itself
     g.gx.embed = c->embed; g.gx.V = c->V; g.gx.H = H; g.gx.in = p.in; g.gx.lm = p.lm_in;
     g.err = c->err;
+  } else if (p.op_in) {
+    // the feature columns were written by the previous down product; the
+    // K-split kernel resolves the tokens for its finish pass
+    g.tab_tok = c->tab_tok;
+    g.tok_out = c->tab_tok;
+    g.gx.V = c->V; g.gx.in = p.in; g.gx.lm = p.lm_in;
+    g.err = c->err;
   } else {
     if (S.tab_ready) g.tab_tok = c->tab_tok;
     launch_fc_prep(bf, R, p.in, p.lm_in, c->embed, c->V, H, p.F, X, c->err,
@@ -655,6 +666,11 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   g = gemm_of(c, S.down, act_of(c->z, c->I), R, EPI_NORM);
   g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
   g.g.ld = H; g.ss = c->ss_h;
+  if (p.op_out) {   // h as the next pass's FC feature columns (X[:, H:2H])
+    g.yx.hi = (bf16_t *)c->xfc.hi + H;
+    g.yx.lo = (bf16_t *)c->xfc.lo + H;
+    g.yx.ld = 2 * H;
+  }
   gemm_go(c, g, s);
   const int parts_h = gemm_ss_parts(g);
   // logits = LM_head RMSNorm(h; g_final)  ->  top-k partials
@@ -882,10 +898,21 @@ static void enqueue_chain(prism_ctx *c, const prism_batch &b, const KvArgs &kv, 
                          c->c_last, c->c_seq, c->c_pos, c->err, s);
   else
     launch_chain_setup(B, K, b.d_tokens, b.d_ctx_lens, c->c_seq, c->c_pos, c->c_tok0, s);
+  // step k >= 2 skips the FC prep pass when its FC is a K-split product over
+  // the feature columns (bf16, embedding table) with a workgroup per row
+  auto direct = [&](int k) -> bool {
+    if (k < 2 || k > K || !c->bf16 || B <= GEMV_MAX_ROWS) return false;
+    const Set &S = c->sets[c->fmap[k - 1]];
+    if (!S.tab_ready || S.F != H) return false;
+    const GemmLaunch g = gemm_of(c, S.fc, Act{}, B, EPI_NORM, H / 32);
+    return g.split > 0 && !g.gemv && (long)((S.fc.n_tiles / g.nt + 3) / 4) * g.split >= B;
+  };
   const float *prev = nullptr;
   int ld_prev = 0;
   for (int k = 1; k <= K; ++k) {
     Pass p{};
+    p.op_in = direct(k);
+    p.op_out = direct(k + 1);
     p.set = c->fmap[k - 1];
     p.R = B;
     p.F = k == 1 ? c->cfg.feat_width : H;
