@@ -54,6 +54,12 @@ def test_chain_parity_small(cfg):
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs1_h480", batch=1, hidden=480),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24", batch=24, vocab=5120),
     SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs40", batch=40, ctx_range=(20, 300)),
+    # H = 2048 at 24 rows: the fusion FC's K-split grid (80 workgroups) has one
+    # per row, so steps >= 2 take their feature operand from the previous
+    # down product and resolve their tokens in the K-split kernel (no prep
+    # pass), with two row tiles
+    SMALL_BF16_CHAIN.with_(name="small_bf16_chain_bs24_h2048", batch=24, hidden=2048,
+                           ctx_range=(20, 200)),
 ], ids=lambda c: c.name)
 def test_chain_parity_row_counts(cfg):
     run_chain_parity(cfg)
