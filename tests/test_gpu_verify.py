@@ -208,6 +208,13 @@ def test_score_tree_and_verify_small_empty_context():
     run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_ctx0", ctx_range=None, ctx_len=0))
 
 
+def test_score_tree_and_verify_small_two_passes():
+    """4 trees x 21 rows = 84 rows: two scoring passes of up to 64 rows, the
+    second one's nodes attending to KV that the first one wrote."""
+    lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_b4", batch=4))
+    assert len(lens) == 4
+
+
 def test_score_tree_rows_are_checked():
     """A mask that names a later node or lacks the node's own bit, and a
     depth out of range, are clamped to well-formed rows and reported."""
