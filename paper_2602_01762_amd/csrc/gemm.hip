@@ -1320,6 +1320,126 @@ void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
   else lm_rt<float, false>(g, s);
 }
 
+// LM head over many rows at once, logits only (the target's tree-scoring
+// pass: up to LMR_MAX_ROWS rows in one launch instead of one launch per
+// pass, each weight read once from HBM).  Workgroup (vocab group x, row
+// group y) takes 16 vocab tiles (4 per wave) against 64 rows (4 row tiles);
+// the row groups of one vocab group are consecutive in launch order, so they
+// run together and the later ones find the weights in the infinity cache.
+// The 8 activation fragments of a k-block (4 row tiles, hi and lo) are
+// staged in LDS once per workgroup: each wave loads 2 of them LMR_D k-blocks
+// ahead into registers and stores them one k-block ahead of use
+// (double-buffered LDS, one barrier per k-block); the weight fragments come
+// LMR_D k-blocks ahead too.  Each weight fragment feeds 8 MFMAs, each
+// activation fragment 4 (the wave's tiles).  Rows r >= R read as zero; the
+// row scale (the final RMSNorm) comes precomputed.
+constexpr int LMR_NT = 4, LMR_RT = 4, LMR_D = 4;
+__global__ __launch_bounds__(256) void k_lmhead_rows(LmRowsArgs g) {
+  __shared__ u32x4 xs[2][2 * LMR_RT][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const TiledMat &m = g.m;
+  // workgroup id -> (vocab group, row group): the row groups of a vocab group
+  // take ids 8 apart, so the hardware's round-robin places them on one XCD
+  // (one L2) and dispatches them together; the later ones find the weights
+  // in that L2
+  const int n_rg = (g.R + 16 * LMR_RT - 1) / (16 * LMR_RT);
+  const int id = blockIdx.x, blk = id / (8 * n_rg), in = id % (8 * n_rg);
+  const int xg = blk * 8 + in % 8, yg = in / 8;
+  if (xg * 4 * LMR_NT >= m.n_tiles) return;   // padding workgroup (uniform)
+  const int t0 = (xg * 4 + wave) * LMR_NT;
+  const bool live = t0 < m.n_tiles;           // the wave's first tile exists
+  const int r0 = yg * 16 * LMR_RT;
+  const int nkb = m.nkb;                      // a multiple of LMR_D (host check)
+  const u32x4 z4 = {0, 0, 0, 0};
+  // staging: wave w loads fragments (row tile w, hi) and (row tile w, lo)
+  const int sr = r0 + 16 * wave + (lane & 15);
+  const bool sok = sr < g.R;
+  const bf16_t *sh = (const bf16_t *)g.x.hi + (size_t)(sok ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+  const bf16_t *sl = (const bf16_t *)g.x.lo + (size_t)(sok ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+  const u32x4 *wp[LMR_NT];
+#pragma unroll
+  for (int n = 0; n < LMR_NT; ++n) {   // a tile past the end streams the wave's first (discarded)
+    const int t = t0 + n < m.n_tiles ? t0 + n : (live ? t0 : 0);
+    wp[n] = (const u32x4 *)m.w + (size_t)t * nkb * 64 + lane;
+  }
+  u32x4 a[LMR_D][LMR_NT], sv[LMR_D][2];
+#pragma unroll
+  for (int u = 0; u < LMR_D; ++u) {
+    sv[u][0] = *(const u32x4 *)(sh + (size_t)u * 32);
+    sv[u][1] = *(const u32x4 *)(sl + (size_t)u * 32);
+#pragma unroll
+    for (int n = 0; n < LMR_NT; ++n) a[u][n] = live ? wp[n][(size_t)u * 64] : z4;
+  }
+  xs[0][2 * wave][lane] = sok ? sv[0][0] : z4;
+  xs[0][2 * wave + 1][lane] = sok ? sv[0][1] : z4;
+  __syncthreads();
+  f32x4 acc[LMR_NT][LMR_RT];
+#pragma unroll
+  for (int n = 0; n < LMR_NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < LMR_RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int kb0 = 0; kb0 < nkb; kb0 += LMR_D) {
+#pragma unroll
+    for (int u = 0; u < LMR_D; ++u) {
+      const int kb = kb0 + u, buf = kb & 1;
+      if (live) {
+#pragma unroll
+        for (int rt = 0; rt < LMR_RT; ++rt) {
+          const u32x4 bh = xs[buf][2 * rt][lane];
+          const u32x4 bl = xs[buf][2 * rt + 1][lane];
+#pragma unroll
+          for (int n = 0; n < LMR_NT; ++n) {
+            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bh, acc[n][rt]);
+            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bl, acc[n][rt]);
+          }
+        }
+      }
+      // k-block kb + 1 (loaded LMR_D - 1 steps ago) into the other buffer;
+      // k-block kb + LMR_D into the registers it leaves (loads past the end
+      // re-read the last k-block and are discarded)
+      const int un = (u + 1) % LMR_D;   // a constant once the loop is unrolled
+      if (kb + 1 < nkb) {   // uniform
+        xs[buf ^ 1][2 * wave][lane] = sok ? sv[un][0] : z4;
+        xs[buf ^ 1][2 * wave + 1][lane] = sok ? sv[un][1] : z4;
+      }
+      const int kn = min(kb + LMR_D, nkb - 1);
+      sv[u][0] = *(const u32x4 *)(sh + (size_t)kn * 32);
+      sv[u][1] = *(const u32x4 *)(sl + (size_t)kn * 32);
+      if (live) {
+#pragma unroll
+        for (int n = 0; n < LMR_NT; ++n) a[u][n] = wp[n][(size_t)kn * 64];   // cached: shared
+      }
+      __syncthreads();
+    }
+  }
+  if (!live) return;
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int rt = 0; rt < LMR_RT; ++rt) {
+    const int r = r0 + 16 * rt + (lane & 15);
+    if (r >= g.R) continue;
+    const float sc = g.scale ? g.scale[r] : 1.f;
+#pragma unroll
+    for (int n = 0; n < LMR_NT; ++n) {
+      if (t0 + n >= m.n_tiles) continue;
+      const f32x4 v = acc[n][rt];
+      *(f32x4 *)(g.logits + (size_t)r * g.ld_logits + (t0 + n) * 16 + 4 * q4) =
+          f32x4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
+    }
+  }
+}
+
+bool lmhead_rows_fits(const TiledMat &m, int R) {
+  return R >= 1 && R <= LMR_MAX_ROWS && m.nkb % LMR_D == 0 && m.nkb >= LMR_D;
+}
+
+void launch_lmhead_rows(const LmRowsArgs &g, hipStream_t s) {
+  const int xg = (g.m.n_tiles + 4 * LMR_NT - 1) / (4 * LMR_NT);
+  const int n_rg = (g.R + 16 * LMR_RT - 1) / (16 * LMR_RT);
+  const int xg8 = (xg + 7) / 8 * 8;   // whole groups of 8 vocab groups (padding exits)
+  hipLaunchKernelGGL(k_lmhead_rows, dim3(xg8 * n_rg), dim3(256), 0, s, g);
+}
+
 // Embedding half of a fusion FC for every token: T[v][n] = sum_{k < H}
 // W[n][k] E[v][k].  Wave w of workgroup (x, y) takes feature tile 4 x + w
 // against vocab rows 64 y .. 64 y + 63: W's tiled blocks are the A operand

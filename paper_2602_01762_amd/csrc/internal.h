@@ -169,6 +169,18 @@ struct LmLaunch {
 // kernel instantiation it selects
 bool launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
+// LM head over up to LMR_MAX_ROWS rows in one launch, logits only (bf16):
+// logits[r][v] = scale[r] * (W x_r)[v]
+constexpr int LMR_MAX_ROWS = 256;
+struct LmRowsArgs {
+  TiledMat m;
+  Act x;                  // [R, H] hi/lo planes
+  int R;
+  const float *scale;     // [R] row scales, or NULL
+  float *logits; long ld_logits;
+};
+bool lmhead_rows_fits(const TiledMat &m, int R);
+void launch_lmhead_rows(const LmRowsArgs &g, hipStream_t s);
 int lm_workgroups(int n_tiles, int nt);
 // partial sums of squares per row that an EPI_NORM launch writes
 int gemm_ss_parts(const GemmLaunch &g);

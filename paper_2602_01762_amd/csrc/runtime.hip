@@ -48,6 +48,10 @@ struct Pass {            // one forward pass: where its inputs and outputs live
   // pass's down product and its tokens in its own K-split kernel (no prep
   // pass); this pass's down product writes that operand for the next pass
   bool op_in, op_out;
+  // tree scoring (lm_rows_x.hi != NULL): no LM head in the pass; its
+  // operand rows and row scales go here, for one LM head over several passes
+  ActOut lm_rows_x;
+  float *lm_rows_scale;
 };
 
 std::string g_create_error;
@@ -79,6 +83,8 @@ struct prism_ctx {
   ActOut xfc;                       // FC operand planes [R, H + feat_max]
   float *u = nullptr, *r1 = nullptr;  // residual stream rows [R, H]
   ActOut ug, r1g, hg;               // (x * gain) operand planes [R, H]
+  ActOut lmr_x;                     // bf16: LM-head operand rows of a tree-scoring group [LMR_MAX_ROWS, H]
+  float *lmr_scale = nullptr;       // and their row scales
   float *ss_u = nullptr, *ss_r1 = nullptr, *ss_h = nullptr;  // [parts <= H/16][R]
   float *sc_u = nullptr, *sc_r1 = nullptr, *sc_h = nullptr;  // row scales [R]
   float *q = nullptr;               // [R, nq*d] fp32
@@ -272,6 +278,10 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   planes(c->ug, RF * c->H);
   planes(c->r1g, R * c->H);
   planes(c->hg, R * c->H);
+  if (bf16) {
+    planes(c->lmr_x, (size_t)LMR_MAX_ROWS * c->H);
+    add((void **)&c->lmr_scale, LMR_MAX_ROWS * 4);
+  }
   add((void **)&c->ss_u, nth * RF * 4);
   add((void **)&c->ss_r1, nth * R * 4);
   add((void **)&c->ss_h, nth * R * 4);
@@ -664,7 +674,8 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   gemm_go(c, g, s);
   // h = r1 + W_down z  ->  h (output), (h * g_final), sums of squares
   g = gemm_of(c, S.down, act_of(c->z, c->I), R, EPI_NORM);
-  g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf; g.g = c->hg;
+  g.res = c->r1; g.ldres = H; g.y = p.hid_out; g.ldy = p.ld_hid; g.gain = c->gf;
+  g.g = p.lm_rows_x.hi ? p.lm_rows_x : c->hg;
   g.g.ld = H; g.ss = c->ss_h;
   if (p.op_out) {   // h as the next pass's FC feature columns (X[:, H:2H])
     g.yx.hi = (bf16_t *)c->xfc.hi + H;
@@ -673,6 +684,10 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   }
   gemm_go(c, g, s);
   const int parts_h = gemm_ss_parts(g);
+  if (p.lm_rows_x.hi) {   // the caller runs the LM head over several passes' rows
+    launch_rowscale(R, c->ss_h, parts_h, H, c->cfg.rms_eps, p.lm_rows_scale, s);
+    return;
+  }
   // logits = LM_head RMSNorm(h; g_final)  ->  top-k partials
   LmLaunch lmg{};
   lmg.m = c->lm;
@@ -1215,6 +1230,12 @@ prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_
                                 (uintptr_t)d_tokens, (uintptr_t)d_depth, (uintptr_t)d_mask,
                                 (uintptr_t)d_logits, (uintptr_t)c->fmap[0]};
   const int set = c->fmap[0];
+  // more rows than one pass takes (bf16): the passes of each group of up to
+  // LMR_MAX_ROWS rows leave their LM-head operand rows, and one LM head over
+  // the group streams the weights once instead of once per pass
+  const int grp_rows = LMR_MAX_ROWS / c->rows_max * c->rows_max;
+  const bool grouped = c->bf16 && rows > c->rows_max && grp_rows > 0 && c->lmr_x.hi &&
+                       lmhead_rows_fits(c->lm, grp_rows);
   return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
     launch_score_setup(B, n_nodes, b.d_tokens, b.d_ctx_lens, d_tokens, d_depth, d_mask, c->s_tok,
                        c->s_seq, c->s_pos, c->s_slot, c->s_bits, c->err, s);
@@ -1222,6 +1243,7 @@ prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_
     // come before it, so their KV is written by this pass or an earlier one
     for (int r0 = 0; r0 < rows; r0 += c->rows_max) {
       const int n = rows - r0 < c->rows_max ? rows - r0 : c->rows_max;
+      const int g0 = grouped ? r0 / grp_rows * grp_rows : r0;   // the pass's group
       Pass p{};
       p.set = set;
       p.R = n;
@@ -1242,7 +1264,25 @@ prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_
       p.logits = d_logits + (size_t)r0 * V;
       p.ld_logits = V;
       p.ids = c->ids;
+      if (grouped) {
+        const size_t off = (size_t)(r0 - g0) * c->H;
+        p.lm_rows_x.hi = (bf16_t *)c->lmr_x.hi + off;
+        p.lm_rows_x.lo = (bf16_t *)c->lmr_x.lo + off;
+        p.lm_rows_x.ld = c->H;
+        p.lm_rows_scale = c->lmr_scale + (r0 - g0);
+      }
       enqueue_pass(c, p, kv, s);
+      const int gn = rows - g0 < grp_rows ? rows - g0 : grp_rows;
+      if (grouped && r0 + n == g0 + gn) {   // the group's last pass: its LM head
+        LmRowsArgs a{};
+        a.m = c->lm;
+        a.x = act_of(c->lmr_x, c->H);
+        a.R = gn;
+        a.scale = c->lmr_scale;
+        a.logits = d_logits + (size_t)g0 * V;
+        a.ld_logits = V;
+        launch_lmhead_rows(a, s);
+      }
     }
   });
 }
