@@ -418,10 +418,14 @@ def tree_cycle_bench(args):
     assert dr.device_status() == 0 and tdr.device_status() == 0
     rows = cfg.batch * (cfg.tree_nodes + 1)
     # the scoring passes: per pass the layer's weights (FC over [E(x) ; 0],
-    # QKV, O, gate/up, down) and the LM head, plus the logits rows written
+    # QKV, O, gate/up, down); the LM head once per pass, or (bf16, more rows
+    # than one pass) once per group of up to 256 rows; the logits rows written
     npass = -(-rows // 64)
-    score_bytes = npass * (step_weight_bytes(tcfg, 0) - 2 * tcfg.hidden * tcfg.hidden) \
-        + rows * cfg.vocab * 4
+    es = 2 if tcfg.dtype == "bf16" else 4
+    lm_bytes = es * tcfg.vocab * tcfg.hidden
+    n_lm = -(-rows // 256) if tcfg.dtype == "bf16" and npass > 1 else npass
+    score_bytes = npass * (step_weight_bytes(tcfg, 0) - 2 * tcfg.hidden * tcfg.hidden - lm_bytes) \
+        + n_lm * lm_bytes + rows * cfg.vocab * 4
     res = {"metric": "tree speculation cycle latency (draft tree + target scoring + verify)",
            "value": round(t["cycle"], 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(t["cycle"] / 1e3, 5),
@@ -429,7 +433,7 @@ def tree_cycle_bench(args):
            "data": "synthetic (seeded random-init drafter and one-layer target)",
            "config": {"workload": "llama3_8b_tree_bs4_score_verify", "batch": cfg.batch,
                       "depth": cfg.n_steps, "width": cfg.tree_width, "nodes": cfg.tree_nodes,
-                      "target_rows": rows, "target_passes": npass},
+                      "target_rows": rows, "target_passes": npass, "target_lm_head_launches": n_lm},
            "part_us": {k: round(v, 2) for k, v in t.items() if k != "cycle"},
            "score_hbm_frac": round(score_bytes / (t["score"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
            "score_bytes_per_call": score_bytes}

@@ -1333,7 +1333,7 @@ void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
 // LMR_D k-blocks ahead too.  Each weight fragment feeds 8 MFMAs, each
 // activation fragment 4 (the wave's tiles).  Rows r >= R read as zero; the
 // row scale (the final RMSNorm) comes precomputed.
-constexpr int LMR_NT = 4, LMR_RT = 4, LMR_D = 4;
+constexpr int LMR_NT = 4, LMR_RT = 4, LMR_D = 2;
 __global__ __launch_bounds__(256) void k_lmhead_rows(LmRowsArgs g) {
   __shared__ u32x4 xs[2][2 * LMR_RT][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -1351,27 +1351,39 @@ __global__ __launch_bounds__(256) void k_lmhead_rows(LmRowsArgs g) {
   const int r0 = yg * 16 * LMR_RT;
   const int nkb = m.nkb;                      // a multiple of LMR_D (host check)
   const u32x4 z4 = {0, 0, 0, 0};
-  // staging: wave w loads fragments (row tile w, hi) and (row tile w, lo)
-  const int sr = r0 + 16 * wave + (lane & 15);
-  const bool sok = sr < g.R;
-  const bf16_t *sh = (const bf16_t *)g.x.hi + (size_t)(sok ? sr : 0) * g.x.ld + 8 * (lane >> 4);
-  const bf16_t *sl = (const bf16_t *)g.x.lo + (size_t)(sok ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+  // staging: wave w loads the hi and lo fragments of row tiles w, w + 4, ...
+  constexpr int SJ = LMR_RT / 4;
+  bool sok[SJ];
+  const bf16_t *sh[SJ], *sl[SJ];
+#pragma unroll
+  for (int jj = 0; jj < SJ; ++jj) {
+    const int sr = r0 + 16 * (wave + 4 * jj) + (lane & 15);
+    sok[jj] = sr < g.R;
+    sh[jj] = (const bf16_t *)g.x.hi + (size_t)(sok[jj] ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+    sl[jj] = (const bf16_t *)g.x.lo + (size_t)(sok[jj] ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+  }
   const u32x4 *wp[LMR_NT];
 #pragma unroll
   for (int n = 0; n < LMR_NT; ++n) {   // a tile past the end streams the wave's first (discarded)
     const int t = t0 + n < m.n_tiles ? t0 + n : (live ? t0 : 0);
     wp[n] = (const u32x4 *)m.w + (size_t)t * nkb * 64 + lane;
   }
-  u32x4 a[LMR_D][LMR_NT], sv[LMR_D][2];
+  u32x4 a[LMR_D][LMR_NT], sv[LMR_D][SJ][2];
 #pragma unroll
   for (int u = 0; u < LMR_D; ++u) {
-    sv[u][0] = *(const u32x4 *)(sh + (size_t)u * 32);
-    sv[u][1] = *(const u32x4 *)(sl + (size_t)u * 32);
+#pragma unroll
+    for (int jj = 0; jj < SJ; ++jj) {
+      sv[u][jj][0] = *(const u32x4 *)(sh[jj] + (size_t)u * 32);
+      sv[u][jj][1] = *(const u32x4 *)(sl[jj] + (size_t)u * 32);
+    }
 #pragma unroll
     for (int n = 0; n < LMR_NT; ++n) a[u][n] = live ? wp[n][(size_t)u * 64] : z4;
   }
-  xs[0][2 * wave][lane] = sok ? sv[0][0] : z4;
-  xs[0][2 * wave + 1][lane] = sok ? sv[0][1] : z4;
+#pragma unroll
+  for (int jj = 0; jj < SJ; ++jj) {
+    xs[0][2 * (wave + 4 * jj)][lane] = sok[jj] ? sv[0][jj][0] : z4;
+    xs[0][2 * (wave + 4 * jj) + 1][lane] = sok[jj] ? sv[0][jj][1] : z4;
+  }
   __syncthreads();
   f32x4 acc[LMR_NT][LMR_RT];
 #pragma unroll
@@ -1399,12 +1411,18 @@ __global__ __launch_bounds__(256) void k_lmhead_rows(LmRowsArgs g) {
       // re-read the last k-block and are discarded)
       const int un = (u + 1) % LMR_D;   // a constant once the loop is unrolled
       if (kb + 1 < nkb) {   // uniform
-        xs[buf ^ 1][2 * wave][lane] = sok ? sv[un][0] : z4;
-        xs[buf ^ 1][2 * wave + 1][lane] = sok ? sv[un][1] : z4;
+#pragma unroll
+        for (int jj = 0; jj < SJ; ++jj) {
+          xs[buf ^ 1][2 * (wave + 4 * jj)][lane] = sok[jj] ? sv[un][jj][0] : z4;
+          xs[buf ^ 1][2 * (wave + 4 * jj) + 1][lane] = sok[jj] ? sv[un][jj][1] : z4;
+        }
       }
       const int kn = min(kb + LMR_D, nkb - 1);
-      sv[u][0] = *(const u32x4 *)(sh + (size_t)kn * 32);
-      sv[u][1] = *(const u32x4 *)(sl + (size_t)kn * 32);
+#pragma unroll
+      for (int jj = 0; jj < SJ; ++jj) {
+        sv[u][jj][0] = *(const u32x4 *)(sh[jj] + (size_t)kn * 32);
+        sv[u][jj][1] = *(const u32x4 *)(sl[jj] + (size_t)kn * 32);
+      }
       if (live) {
 #pragma unroll
         for (int n = 0; n < LMR_NT; ++n) a[u][n] = wp[n][(size_t)kn * 64];   // cached: shared
