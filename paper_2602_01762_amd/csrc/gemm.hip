@@ -1322,10 +1322,10 @@ void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
 
 // LM head over many rows at once, logits only (the target's tree-scoring
 // pass: up to LMR_MAX_ROWS rows in one launch instead of one launch per
-// pass, each weight read once from HBM).  Workgroup (vocab group x, row
-// group y) takes 16 vocab tiles (4 per wave) against 64 rows (4 row tiles);
-// the row groups of one vocab group are consecutive in launch order, so they
-// run together and the later ones find the weights in the infinity cache.
+// pass).  Workgroup (vocab group x, row group y) takes 16 vocab tiles (4 per
+// wave) against 64 rows (4 row tiles); the row groups of one vocab group run
+// together on one XCD (see the id mapping below), so the later ones find the
+// weights in its L2 and HBM serves each weight about once.
 // The 8 activation fragments of a k-block (4 row tiles, hi and lo) are
 // staged in LDS once per workgroup: each wave loads 2 of them LMR_D k-blocks
 // ahead into registers and stores them one k-block ahead of use
