@@ -400,7 +400,10 @@ __device__ __forceinline__ void mainloop_valu(const u32x4 *__restrict__ w0, cons
 // wave.  Two register sets of UV / 2 k-blocks: batch j + 1 is in flight
 // while batch j is consumed, so the stream has no gap between batches (8B
 // LM head 163.0 -> 161.3 us, Llama-2 shape 50.1 -> 48.5 us against one set
-// of UV k-blocks loaded and then consumed).
+// of UV k-blocks loaded and then consumed).  With several tiles per wave the
+// stream's last pair is peeled, so every other load is unconditional: with a
+// conditional one the compiler's wait counts drained every load at each pair
+// (8B LM head 161.2 -> 160.8 us).
 template <int RR, int NT>
 __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0, int nkb,
                                                     const Act &x, int R, int K, float *xs,
@@ -421,15 +424,28 @@ __device__ __forceinline__ void mainloop_valu_tiles(const u32x4 *__restrict__ w0
     float acc[RR];
 #pragma unroll
     for (int r = 0; r < RR; ++r) acc[r] = 0.f;
-    for (int i = 0; i < bpt && live; i += 2) {
+    // every pair but the stream's last loads the next one unconditionally,
+    // so that the compiler counts the loads in flight exactly (several
+    // tiles; a one-tile stream keeps the conditional load, which measured
+    // faster there: Llama-2 shape 48.2 against 50.4 us)
+    const int iend = NT > 1 && n == NT - 1 ? bpt - 2 : bpt;
+    int i = 0;
+    for (; i < iend && live; i += 2) {
       const int j = n * bpt + i;
 #pragma unroll
       for (int u = 0; u < UP; ++u) b[u] = __builtin_nontemporal_load(wp + (size_t)(j + 1) * UP * 64 + u * 64);
       valu_batch_n<RR, UP>(a, i * UP, kq, xs, K, acc);
-      if (j + 2 < total) {
+      if (NT > 1 || j + 2 < total) {
 #pragma unroll
         for (int u = 0; u < UP; ++u) a[u] = __builtin_nontemporal_load(wp + (size_t)(j + 2) * UP * 64 + u * 64);
       }
+      valu_batch_n<RR, UP>(b, (i + 1) * UP, kq, xs, K, acc);
+    }
+    if (NT > 1 && n == NT - 1 && live) {
+      const int j = n * bpt + i;
+#pragma unroll
+      for (int u = 0; u < UP; ++u) b[u] = __builtin_nontemporal_load(wp + (size_t)(j + 1) * UP * 64 + u * 64);
+      valu_batch_n<RR, UP>(a, i * UP, kq, xs, K, acc);
       valu_batch_n<RR, UP>(b, (i + 1) * UP, kq, xs, K, acc);
     }
     out[n] = valu_result<RR>(acc);
