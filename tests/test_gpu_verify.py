@@ -215,6 +215,13 @@ def test_score_tree_and_verify_small_two_passes():
     assert len(lens) == 4
 
 
+def test_score_tree_and_verify_small_two_groups():
+    """13 trees x 21 rows = 273 rows: five scoring passes, their LM-head rows
+    in two launches (256 rows, then 17)."""
+    lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_b13", batch=13))
+    assert len(lens) == 13
+
+
 def test_score_tree_rows_are_checked():
     """A mask that names a later node or lacks the node's own bit, and a
     depth out of range, are clamped to well-formed rows and reported."""
