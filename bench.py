@@ -379,8 +379,8 @@ def tree_cycle_bench(args):
     """One tree speculation cycle on the 8B shapes: the drafter's tree call
     (batch 4, D 6, w 8, v 60), the target model's pass over the root and the
     60 nodes of each tree under the tree mask (one transformer layer of the
-    8B shape with its own weights and the shared-shape LM head, 4 x 61 rows
-    in passes of up to 64), and greedy tree verification of its logits."""
+    8B shape with its own weights and the shared-shape LM head, the 4 x 61
+    rows in one pass), and greedy tree verification of its logits."""
     import numpy as np
     import torch
     from synth import L3_8B_TREE, make_inputs, make_weights, scoring_target
@@ -416,16 +416,19 @@ def tree_cycle_bench(args):
         torch.cuda.synchronize()
         t[name] = e0.elapsed_time(e1) * 1e3 / args.steps
     assert dr.device_status() == 0 and tdr.device_status() == 0
-    rows = cfg.batch * (cfg.tree_nodes + 1)
-    # the scoring passes: per pass the layer's weights (FC over [E(x) ; 0],
-    # QKV, O, gate/up, down); the LM head once per pass, or (bf16, more rows
-    # than one pass) once per group of up to 256 rows; the logits rows written
-    npass = -(-rows // 64)
+    rps = cfg.tree_nodes + 1
+    rows = cfg.batch * rps
+    # the scoring passes (bf16: whole trees, up to 256 rows each): per pass
+    # the layer's weights (FC over [E(x) ; 0], QKV, O, gate/up, down) and the
+    # LM head; the logits rows written
+    per_pass = 256 // rps * rps if tcfg.dtype == "bf16" else 64
+    npass = -(-rows // per_pass)
     es = 2 if tcfg.dtype == "bf16" else 4
     lm_bytes = es * tcfg.vocab * tcfg.hidden
-    n_lm = -(-rows // 256) if tcfg.dtype == "bf16" and npass > 1 else npass
-    score_bytes = npass * (step_weight_bytes(tcfg, 0) - 2 * tcfg.hidden * tcfg.hidden - lm_bytes) \
-        + n_lm * lm_bytes + rows * cfg.vocab * 4
+    n_lm = npass
+    layer_bytes = step_weight_bytes(tcfg, 0) - 2 * tcfg.hidden * tcfg.hidden - lm_bytes
+    score_bytes = npass * layer_bytes + n_lm * lm_bytes + rows * cfg.vocab * 4
+    score_params = (layer_bytes + lm_bytes) // es
     res = {"metric": "tree speculation cycle latency (draft tree + target scoring + verify)",
            "value": round(t["cycle"], 2), "unit": "us", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(t["cycle"] / 1e3, 5),
@@ -436,6 +439,11 @@ def tree_cycle_bench(args):
                       "target_rows": rows, "target_passes": npass, "target_lm_head_launches": n_lm},
            "part_us": {k: round(v, 2) for k, v in t.items() if k != "cycle"},
            "score_hbm_frac": round(score_bytes / (t["score"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           # the passes are MFMA work (244 rows): every row meets every weight
+           # of the layer and the LM head once, as an exact hi/lo bf16 pair of
+           # activations, so the MFMAs execute 4 flops per row and weight
+           "score_mfma_frac_executed": round(4 * rows * score_params / (t["score"] * 1e-6) / 1e12
+                                             / BF16_PEAK_TFLOPS, 4),
            "score_bytes_per_call": score_bytes}
     print(json.dumps(res), flush=True)
 

@@ -28,6 +28,8 @@ struct AttnArgs {
   KvArgs kv;
   int R, nq, nkv, d, nch, nsub;
   int grp;                    // rows per workgroup of the grouped MFMA kernel (one sequence's tree rows)
+  int rps;                    // > 0: rows come in runs of rps rows of one tree each, grouped from
+                              // each run's first row (its last group may be shorter)
   float scale;
   float *pm, *pl, *po;        // [R, nq, nch] / [R, nq, nch, d]
   ActOut o;                   // [R, nq*d]
@@ -291,8 +293,13 @@ template <int DK, bool NTL, bool GRP>
 __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   constexpr int ATT_MAXDK = DK, ATT_MAXDT = 2 * DK;
   const int c = blockIdx.z, j = blockIdx.x;
-  const int gs = GRP ? a.grp : 1;
-  const int r = blockIdx.y * gs;             // the workgroup's (first) row
+  int gs = GRP ? a.grp : 1;
+  int r = blockIdx.y * gs;                   // the workgroup's (first) row
+  if (GRP && a.rps > 0) {                    // runs of rps rows: ceil(rps / grp) groups each
+    const int gpr = (a.rps + a.grp - 1) / a.grp, gi = blockIdx.y % gpr;
+    r = blockIdx.y / gpr * a.rps + gi * a.grp;
+    gs = min(a.grp, a.rps - gi * a.grp);
+  }
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, q4 = lane >> 4;
   int b, L, prefix, total;
@@ -599,8 +606,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
 }
 
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
-                      const KvArgs &kv, int max_slots, int grp, float *pm, float *pl, float *po,
-                      ActOut o, uint32_t *err, hipStream_t s) {
+                      const KvArgs &kv, int max_slots, int grp, int rps, float *pm, float *pl,
+                      float *po, ActOut o, uint32_t *err, hipStream_t s) {
   AttnArgs a;
   a.q = q;
   a.seq = in.seq;
@@ -618,23 +625,26 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   a.o = o;
   a.err = err;
   // grouped rows: tree rows (bits), bf16, head_dim 64 or 128, the group's
-  // query rows within the 16 score columns, whole groups
+  // query rows within the 16 score columns, whole groups (or whole runs)
   const int g = nq / nkv;
-  a.grp = grp > 1 && bf16 && in.bits && (d == 64 || d == 128) && grp * g <= 16 && R % grp == 0
-              ? grp : 1;
+  const bool grouped = grp > 1 && bf16 && in.bits && (d == 64 || d == 128) && grp * g <= 16 &&
+                       (rps > 0 ? R % rps == 0 : R % grp == 0);
+  a.grp = grouped ? grp : 1;
+  a.rps = grouped ? rps : 0;
+  const int units = !grouped ? R : rps > 0 ? R / rps * ((rps + grp - 1) / grp) : R / grp;
   // steps per workgroup for this pass's rows (or row groups)
-  a.nsub = attention_nsub(R / a.grp, nkv, max_slots);
+  a.nsub = attention_nsub(units, nkv, max_slots);
   a.nch = attention_chunks(max_slots, a.nsub);
   // chunk index slowest: every row's first chunks are dispatched before any
   // row's later ones, so the last workgroups to start are the short tails
-  dim3 g1(nkv, R / a.grp, a.nch), g2(nq, R);
+  dim3 g1(nkv, units, a.nch), g2(nq, R);
   // K/V that one pass requests at capacity (R rows of max_slots slots):
   // beyond 1.5 times the 256 MiB infinity cache the rows are streamed with
   // nontemporal loads (70B batch 32, 539 MB: 5.917 -> 5.847 ms); below it
   // ordinary loads let the cache keep the prior context from one step to the
   // next (batch 16 paged, 269 MB at capacity and 151 MB on average:
   // nontemporal loads were 3.7% slower; the tree, 140 MB: 0.6% slower)
-  const double kv_bytes = (double)R / a.grp * max_slots * nkv * d * 2 * (bf16 ? 2 : 4);
+  const double kv_bytes = (double)units * max_slots * nkv * d * 2 * (bf16 ? 2 : 4);
   const bool ntl = kv_bytes > 1.5 * 256 * 1024 * 1024;
   if (bf16) {
     if (a.grp > 1) {

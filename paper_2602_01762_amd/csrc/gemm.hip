@@ -1203,6 +1203,184 @@ static bool gemm_epi(const GemmLaunch &g, hipStream_t s) {
   return true;
 }
 
+// Products over more rows than the 16-row-tile kernels take (tree-scoring
+// passes of up to ROWGRP_MAX_ROWS rows, bf16).  A workgroup takes
+// ROWGRP_TILES output tiles (4 per wave) against one group of ROWGRP_ROWS
+// rows over one K slice.  The row group's hi and lo B fragments of each
+// k-block are staged in LDS once for the 4 waves (two buffers, one barrier
+// per k-block), so each weight fragment feeds 4 row tiles x 2 planes from
+// registers and LDS.  The row groups of one (tile group, slice) pair take
+// workgroup ids 8 apart: the hardware's round-robin places them on one XCD
+// and dispatches them together, and the later ones find the weights in that
+// XCD's L2.  Slice partial sums go to part[s][r][n] as in k_gemm_split, and
+// k_gemm_finish applies the epilogue.
+constexpr int RG_NT = 4, RG_RT = 4, RG_D = 2;
+static_assert(4 * RG_NT == ROWGRP_TILES && 16 * RG_RT == ROWGRP_ROWS, "row-group tiling");
+__global__ __launch_bounds__(256) void k_gemm_rows(GemmLaunch g) {
+  __shared__ u32x4 xs[2][2 * RG_RT][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const TiledMat &m = g.m;
+  const int n_rg = (g.R + ROWGRP_ROWS - 1) / ROWGRP_ROWS;
+  const int n_xg = (m.n_tiles + ROWGRP_TILES - 1) / ROWGRP_TILES;
+  const int S = g.split;
+  const int id = blockIdx.x, blk = id / (8 * n_rg), in = id % (8 * n_rg);
+  const int pair = blk * 8 + in % 8, yg = in / 8;
+  if (pair >= n_xg * S) return;               // padding workgroup (uniform)
+  const int xg = pair % n_xg, sl = pair / n_xg;
+  const int t0 = (xg * 4 + wave) * RG_NT;
+  const bool live = t0 < m.n_tiles;           // the wave's first tile exists
+  const int r0 = yg * ROWGRP_ROWS;
+  const int nk = m.nkb - g.kb_lo;
+  // S <= nk (host check): every slice has at least one k-block
+  const int kb0 = g.kb_lo + (int)((long)sl * nk / S), kb1 = g.kb_lo + (int)((long)(sl + 1) * nk / S);
+  const u32x4 z4 = {0, 0, 0, 0};
+  // staging: wave w loads the hi and lo fragments of row tiles w, w + 4, ...
+  // A row past the last one stages row 0 instead: B column j of the product
+  // only reaches output row j, which is not stored
+  constexpr int SJ = RG_RT / 4;
+  const bf16_t *sh[SJ], *sw[SJ];
+#pragma unroll
+  for (int j = 0; j < SJ; ++j) {
+    const int sr = r0 + 16 * (wave + 4 * j) + (lane & 15);
+    sh[j] = (const bf16_t *)g.x.hi + (size_t)(sr < g.R ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+    sw[j] = (const bf16_t *)g.x.lo + (size_t)(sr < g.R ? sr : 0) * g.x.ld + 8 * (lane >> 4);
+  }
+  const u32x4 *wp[RG_NT];
+#pragma unroll
+  for (int n = 0; n < RG_NT; ++n) {   // a tile past the end streams the wave's first (discarded)
+    const int t = t0 + n < m.n_tiles ? t0 + n : (live ? t0 : 0);
+    wp[n] = (const u32x4 *)m.w + (size_t)t * m.nkb * 64 + lane;
+  }
+  u32x4 a[RG_D][RG_NT], sv[RG_D][SJ][2];
+#pragma unroll
+  for (int u = 0; u < RG_D; ++u) {
+    const int k = min(kb0 + u, kb1 - 1);
+#pragma unroll
+    for (int j = 0; j < SJ; ++j) {
+      sv[u][j][0] = *(const u32x4 *)(sh[j] + (size_t)k * 32);
+      sv[u][j][1] = *(const u32x4 *)(sw[j] + (size_t)k * 32);
+    }
+#pragma unroll
+    for (int n = 0; n < RG_NT; ++n) a[u][n] = wp[n][(size_t)k * 64];
+  }
+#pragma unroll
+  for (int j = 0; j < SJ; ++j) {
+    xs[0][2 * (wave + 4 * j)][lane] = sv[0][j][0];
+    xs[0][2 * (wave + 4 * j) + 1][lane] = sv[0][j][1];
+  }
+  __syncthreads();
+  f32x4 acc[RG_NT][RG_RT];
+#pragma unroll
+  for (int n = 0; n < RG_NT; ++n)
+#pragma unroll
+    for (int rt = 0; rt < RG_RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // the slice in whole pairs of k-blocks: an odd slice ends with a k-block
+  // of zero activations (its weight loads re-read the last one), so that
+  // the loop has no exit in its middle and the accumulators stay in place
+  const int kb_end = kb0 + ((kb1 - kb0 + 1) & ~1);
+  for (int kb = kb0; kb < kb_end; kb += RG_D) {
+#pragma unroll
+    for (int u = 0; u < RG_D; ++u) {
+      const int k = kb + u;                   // staged in buffer u (kb - kb0 is even)
+      // every global load below is unconditional (a wave past the last tile
+      // streams tile 0 and discards it), so that the compiler can count the
+      // loads in flight and wait only for the ones each step consumes.  (The
+      // products sit in a branch: without it the compiler rotated the
+      // accumulators through other registers and copied them back every
+      // iteration.)
+      if (live) {
+        u32x4 bx[2 * RG_RT];
+#pragma unroll
+        for (int i = 0; i < 2 * RG_RT; ++i) bx[i] = xs[u][i][lane];
+#pragma unroll
+        for (int rt = 0; rt < RG_RT; ++rt) {
+#pragma unroll
+          for (int n = 0; n < RG_NT; ++n) {
+            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bx[2 * rt], acc[n][rt]);
+            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bx[2 * rt + 1], acc[n][rt]);
+          }
+        }
+      }
+      // k-block k + 1 (loaded RG_D - 1 steps ago; zeros past the slice) into
+      // the other buffer, which every wave has read before the last barrier;
+      // k-block k + RG_D into the registers this one leaves (loads past the
+      // slice re-read its last k-block)
+      const int un = (u + 1) % RG_D;          // a constant once the loop is unrolled
+#pragma unroll
+      for (int j = 0; j < SJ; ++j) {
+        xs[u ^ 1][2 * (wave + 4 * j)][lane] = sv[un][j][0];
+        xs[u ^ 1][2 * (wave + 4 * j) + 1][lane] = sv[un][j][1];
+      }
+      if (k + 1 == kb1) {                     // uniform: the zero k-block of an odd slice
+#pragma unroll
+        for (int j = 0; j < SJ; ++j) {
+          xs[u ^ 1][2 * (wave + 4 * j)][lane] = z4;
+          xs[u ^ 1][2 * (wave + 4 * j) + 1][lane] = z4;
+        }
+      }
+      const int kn = min(k + RG_D, kb1 - 1);
+#pragma unroll
+      for (int j = 0; j < SJ; ++j) {
+        sv[u][j][0] = *(const u32x4 *)(sh[j] + (size_t)kn * 32);
+        sv[u][j][1] = *(const u32x4 *)(sw[j] + (size_t)kn * 32);
+      }
+#pragma unroll
+      for (int n = 0; n < RG_NT; ++n) a[u][n] = wp[n][(size_t)kn * 64];   // cached: shared
+      __syncthreads();
+    }
+  }
+  if (!live) return;
+  const int q4 = lane >> 4;
+#pragma unroll
+  for (int rt = 0; rt < RG_RT; ++rt) {
+    const int r = r0 + 16 * rt + (lane & 15);
+    if (r >= g.R) continue;
+    if (g.part) {   // slice partials for the finish pass
+#pragma unroll
+      for (int n = 0; n < RG_NT; ++n) {
+        if (t0 + n >= m.n_tiles) continue;
+        *(f32x4 *)(g.part + ((size_t)sl * g.R + r) * m.N + (t0 + n) * 16 + 4 * q4) = acc[n][rt];
+      }
+    } else {        // one slice, stored scaled (the LM head): y[r][n] = scale[r] acc
+      const float sc = g.norm.scale ? g.norm.scale[r] : 1.f;
+#pragma unroll
+      for (int n = 0; n < RG_NT; ++n) {
+        if (t0 + n >= m.n_tiles) continue;
+        const f32x4 v = acc[n][rt];
+        *(f32x4 *)(g.y + (size_t)r * g.ldy + (t0 + n) * 16 + 4 * q4) =
+            f32x4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
+      }
+    }
+  }
+}
+
+// the finish pass of a K-split product: one wave per (tile, 16 rows)
+template <typename T>
+static void finish_launch(const GemmLaunch &g, hipStream_t s) {
+  const int ft = finish_tiles(g.m.n_tiles, g.epi);
+  const dim3 fg(g.m.n_tiles / ft, (g.R + 15) / 16), fb(64 * ft);
+  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, fb, 0, s, g);
+  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, fb, 0, s, g);
+  else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, fb, 0, s, g);
+}
+
+// Row-group product and, with slice partials, its finish pass; without them
+// (one slice) the kernel stores y = scale * acc itself.  false (nothing
+// launched): rows or slices out of the kernel's range, a token resolution it
+// does not do, or a direct store without its output.
+static bool gemm_rows_launch(const GemmLaunch &g, hipStream_t s) {
+  const int nk = g.m.nkb - g.kb_lo;
+  if (g.R < 1 || g.R > ROWGRP_MAX_ROWS || g.split < 1 || g.split > nk || g.tok_out || !g.x.lo ||
+      (!g.part && (g.split != 1 || !g.y)))
+    return false;
+  const long n_xg = (g.m.n_tiles + ROWGRP_TILES - 1) / ROWGRP_TILES;
+  const long n_rg = (g.R + ROWGRP_ROWS - 1) / ROWGRP_ROWS;
+  const long pairs = n_xg * g.split;
+  hipLaunchKernelGGL(k_gemm_rows, dim3((unsigned)((pairs + 7) / 8 * 8 * n_rg)), dim3(256), 0, s, g);
+  if (g.part) finish_launch<bf16_t>(g, s);
+  return true;
+}
+
 template <typename T, int RT, int NT, bool PAIR>
 static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
   const int groups = g.m.n_tiles / NT;
@@ -1218,15 +1396,16 @@ static void gemm_split_launch(const GemmLaunch &g, hipStream_t s) {
     }
   }
   if (!staged) hipLaunchKernelGGL((k_gemm_split<T, RT, NT, PAIR>), grid, dim3(256), 0, s, g);
-  const int ft = finish_tiles(g.m.n_tiles, g.epi);
-  const dim3 fg(g.m.n_tiles / ft, (g.R + 15) / 16), fb(64 * ft);
-  if (g.epi == EPI_NORM) hipLaunchKernelGGL((k_gemm_finish<T, EPI_NORM>), fg, fb, 0, s, g);
-  else if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((k_gemm_finish<T, EPI_SWIGLU>), fg, fb, 0, s, g);
-  else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, fb, 0, s, g);
+  finish_launch<T>(g, s);
 }
 
 template <typename T, bool PAIR>
 static bool gemm_rt(const GemmLaunch &g, hipStream_t s) {
+  if (g.rowgrp) {
+    if constexpr (sizeof(T) == 2) return gemm_rows_launch(g, s);
+    return false;
+  }
+  if (g.R > MAX_ROWS) return false;   // the kernels below hold at most 4 row tiles
   if (g.split > 0) {
     if (g.nt == 8) {
       if (g.R <= 16) gemm_split_launch<T, 1, 8, PAIR>(g, s);
@@ -1337,141 +1516,25 @@ void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s) {
 }
 
 // LM head over many rows at once, logits only (the target's tree-scoring
-// pass: up to LMR_MAX_ROWS rows in one launch instead of one launch per
-// pass).  Workgroup (vocab group x, row group y) takes 16 vocab tiles (4 per
-// wave) against 64 rows (4 row tiles); the row groups of one vocab group run
-// together on one XCD (see the id mapping below), so the later ones find the
-// weights in its L2 and HBM serves each weight about once.
-// The 8 activation fragments of a k-block (4 row tiles, hi and lo) are
-// staged in LDS once per workgroup: each wave loads 2 of them LMR_D k-blocks
-// ahead into registers and stores them one k-block ahead of use
-// (double-buffered LDS, one barrier per k-block); the weight fragments come
-// LMR_D k-blocks ahead too.  Each weight fragment feeds 8 MFMAs, each
-// activation fragment 4 (the wave's tiles).  Rows r >= R read as zero; the
-// row scale (the final RMSNorm) comes precomputed.
-constexpr int LMR_NT = 4, LMR_RT = 4, LMR_D = 2;
-__global__ __launch_bounds__(256) void k_lmhead_rows(LmRowsArgs g) {
-  __shared__ u32x4 xs[2][2 * LMR_RT][64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const TiledMat &m = g.m;
-  // workgroup id -> (vocab group, row group): the row groups of a vocab group
-  // take ids 8 apart, so the hardware's round-robin places them on one XCD
-  // (one L2) and dispatches them together; the later ones find the weights
-  // in that L2
-  const int n_rg = (g.R + 16 * LMR_RT - 1) / (16 * LMR_RT);
-  const int id = blockIdx.x, blk = id / (8 * n_rg), in = id % (8 * n_rg);
-  const int xg = blk * 8 + in % 8, yg = in / 8;
-  if (xg * 4 * LMR_NT >= m.n_tiles) return;   // padding workgroup (uniform)
-  const int t0 = (xg * 4 + wave) * LMR_NT;
-  const bool live = t0 < m.n_tiles;           // the wave's first tile exists
-  const int r0 = yg * 16 * LMR_RT;
-  const int nkb = m.nkb;                      // a multiple of LMR_D (host check)
-  const u32x4 z4 = {0, 0, 0, 0};
-  // staging: wave w loads the hi and lo fragments of row tiles w, w + 4, ...
-  constexpr int SJ = LMR_RT / 4;
-  bool sok[SJ];
-  const bf16_t *sh[SJ], *sl[SJ];
-#pragma unroll
-  for (int jj = 0; jj < SJ; ++jj) {
-    const int sr = r0 + 16 * (wave + 4 * jj) + (lane & 15);
-    sok[jj] = sr < g.R;
-    sh[jj] = (const bf16_t *)g.x.hi + (size_t)(sok[jj] ? sr : 0) * g.x.ld + 8 * (lane >> 4);
-    sl[jj] = (const bf16_t *)g.x.lo + (size_t)(sok[jj] ? sr : 0) * g.x.ld + 8 * (lane >> 4);
-  }
-  const u32x4 *wp[LMR_NT];
-#pragma unroll
-  for (int n = 0; n < LMR_NT; ++n) {   // a tile past the end streams the wave's first (discarded)
-    const int t = t0 + n < m.n_tiles ? t0 + n : (live ? t0 : 0);
-    wp[n] = (const u32x4 *)m.w + (size_t)t * nkb * 64 + lane;
-  }
-  u32x4 a[LMR_D][LMR_NT], sv[LMR_D][SJ][2];
-#pragma unroll
-  for (int u = 0; u < LMR_D; ++u) {
-#pragma unroll
-    for (int jj = 0; jj < SJ; ++jj) {
-      sv[u][jj][0] = *(const u32x4 *)(sh[jj] + (size_t)u * 32);
-      sv[u][jj][1] = *(const u32x4 *)(sl[jj] + (size_t)u * 32);
-    }
-#pragma unroll
-    for (int n = 0; n < LMR_NT; ++n) a[u][n] = live ? wp[n][(size_t)u * 64] : z4;
-  }
-#pragma unroll
-  for (int jj = 0; jj < SJ; ++jj) {
-    xs[0][2 * (wave + 4 * jj)][lane] = sok[jj] ? sv[0][jj][0] : z4;
-    xs[0][2 * (wave + 4 * jj) + 1][lane] = sok[jj] ? sv[0][jj][1] : z4;
-  }
-  __syncthreads();
-  f32x4 acc[LMR_NT][LMR_RT];
-#pragma unroll
-  for (int n = 0; n < LMR_NT; ++n)
-#pragma unroll
-    for (int rt = 0; rt < LMR_RT; ++rt) acc[n][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int kb0 = 0; kb0 < nkb; kb0 += LMR_D) {
-#pragma unroll
-    for (int u = 0; u < LMR_D; ++u) {
-      const int kb = kb0 + u, buf = kb & 1;
-      if (live) {
-#pragma unroll
-        for (int rt = 0; rt < LMR_RT; ++rt) {
-          const u32x4 bh = xs[buf][2 * rt][lane];
-          const u32x4 bl = xs[buf][2 * rt + 1][lane];
-#pragma unroll
-          for (int n = 0; n < LMR_NT; ++n) {
-            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bh, acc[n][rt]);
-            acc[n][rt] = Ty<bf16_t>::mma(a[u][n], bl, acc[n][rt]);
-          }
-        }
-      }
-      // k-block kb + 1 (loaded LMR_D - 1 steps ago) into the other buffer;
-      // k-block kb + LMR_D into the registers it leaves (loads past the end
-      // re-read the last k-block and are discarded)
-      const int un = (u + 1) % LMR_D;   // a constant once the loop is unrolled
-      if (kb + 1 < nkb) {   // uniform
-#pragma unroll
-        for (int jj = 0; jj < SJ; ++jj) {
-          xs[buf ^ 1][2 * (wave + 4 * jj)][lane] = sok[jj] ? sv[un][jj][0] : z4;
-          xs[buf ^ 1][2 * (wave + 4 * jj) + 1][lane] = sok[jj] ? sv[un][jj][1] : z4;
-        }
-      }
-      const int kn = min(kb + LMR_D, nkb - 1);
-#pragma unroll
-      for (int jj = 0; jj < SJ; ++jj) {
-        sv[u][jj][0] = *(const u32x4 *)(sh[jj] + (size_t)kn * 32);
-        sv[u][jj][1] = *(const u32x4 *)(sl[jj] + (size_t)kn * 32);
-      }
-      if (live) {
-#pragma unroll
-        for (int n = 0; n < LMR_NT; ++n) a[u][n] = wp[n][(size_t)kn * 64];   // cached: shared
-      }
-      __syncthreads();
-    }
-  }
-  if (!live) return;
-  const int q4 = lane >> 4;
-#pragma unroll
-  for (int rt = 0; rt < LMR_RT; ++rt) {
-    const int r = r0 + 16 * rt + (lane & 15);
-    if (r >= g.R) continue;
-    const float sc = g.scale ? g.scale[r] : 1.f;
-#pragma unroll
-    for (int n = 0; n < LMR_NT; ++n) {
-      if (t0 + n >= m.n_tiles) continue;
-      const f32x4 v = acc[n][rt];
-      *(f32x4 *)(g.logits + (size_t)r * g.ld_logits + (t0 + n) * 16 + 4 * q4) =
-          f32x4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
-    }
-  }
-}
-
+// pass: up to LMR_MAX_ROWS rows in one launch): the row-group product with
+// one K slice, its epilogue storing logits[r][v] = scale[r] * acc (the final
+// RMSNorm's row scale comes precomputed).
 bool lmhead_rows_fits(const TiledMat &m, int R) {
-  return R >= 1 && R <= LMR_MAX_ROWS && m.nkb % LMR_D == 0 && m.nkb >= LMR_D;
+  return R >= 1 && R <= LMR_MAX_ROWS && R <= ROWGRP_MAX_ROWS && m.nkb >= 1;
 }
 
-void launch_lmhead_rows(const LmRowsArgs &g, hipStream_t s) {
-  const int xg = (g.m.n_tiles + 4 * LMR_NT - 1) / (4 * LMR_NT);
-  const int n_rg = (g.R + 16 * LMR_RT - 1) / (16 * LMR_RT);
-  const int xg8 = (xg + 7) / 8 * 8;   // whole groups of 8 vocab groups (padding exits)
-  hipLaunchKernelGGL(k_lmhead_rows, dim3(xg8 * n_rg), dim3(256), 0, s, g);
+void launch_lmhead_rows(const LmRowsArgs &a, hipStream_t s) {
+  GemmLaunch g{};
+  g.m = a.m;
+  g.x = a.x;
+  g.R = a.R;
+  g.split = 1;
+  g.rowgrp = 1;
+  g.part = nullptr;          // the epilogue stores y directly
+  g.y = a.logits;
+  g.ldy = a.ld_logits;
+  g.norm.scale = a.scale;
+  gemm_rows_launch(g, s);
 }
 
 // Embedding half of a fusion FC for every token: T[v][n] = sum_{k < H}

@@ -116,6 +116,7 @@ struct GemmLaunch {
   int nt;          // tiles per workgroup (1 or 2)
   int gemv;        // 1: VALU GEMV main loop (bf16, R <= 4, staged fp32 activations)
   int split;       // > 0: batched path, K split over `split` workgroup slices
+  int rowgrp;      // 1: more than MAX_ROWS rows: the row-group kernel (k_gemm_rows), split slices
   float *part;     // batched path: slice partial sums [split][R][N]
   int epi;
   RowNorm norm;    // scale rows of the result (SWIGLU, QKV); n_parts = 0: none
@@ -169,8 +170,8 @@ struct LmLaunch {
 // kernel instantiation it selects
 bool launch_gemm(bool bf16, const GemmLaunch &g, hipStream_t s);
 void launch_lmhead(bool bf16, const LmLaunch &g, hipStream_t s);
-// LM head over up to LMR_MAX_ROWS rows in one launch, logits only (bf16):
-// logits[r][v] = scale[r] * (W x_r)[v]
+// LM head over up to LMR_MAX_ROWS rows in one launch, logits only (bf16,
+// the row-group product kernel): logits[r][v] = scale[r] * (W x_r)[v]
 constexpr int LMR_MAX_ROWS = 256;
 struct LmRowsArgs {
   TiledMat m;
@@ -198,13 +199,15 @@ void launch_repack(bool bf16, const void *src, int n_src_rows, int K, int row_st
 void launch_fc_prep(bool bf16, int R, const RowsIn &in, const TokFromLm &lm, const void *embed,
                     int V, int H, int F, ActOut X, uint32_t *err, int32_t *tok_out, bool feat_only, hipStream_t s);
 // grp > 1: rows r .. r + grp - 1 (r a multiple of grp) belong to one sequence
-// and carry tree bits; the launch groups them when the kernel allows it
+// and carry tree bits; the launch groups them when the kernel allows it.
+// rps > 0 (with grp > 1): the rows come in runs of rps rows of one tree each,
+// grouped in grp rows from each run's first row.
 // The partials pm, pl, po hold R * attention_chunks(max_slots, nsub) rows
 // x chunks for the steps per workgroup that attention_nsub gives this pass
 // (attention_partial_rows bounds them over every pass).
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
-                      const KvArgs &kv, int max_slots, int grp, float *pm, float *pl, float *po,
-                      ActOut o, uint32_t *err, hipStream_t s);
+                      const KvArgs &kv, int max_slots, int grp, int rps, float *pm, float *pl,
+                      float *po, ActOut o, uint32_t *err, hipStream_t s);
 // Draw each row's token from softmax(logits * inv_temp) by inverse CDF in
 // id order with the row's uniform u[r * ld_u]: the LM head's per-group
 // (max, sum) of the scaled logits locate the group where the running sum

@@ -42,7 +42,24 @@ struct ProductPlan {
   int nt = 1;      // output tiles per wave
   int split = 0;   // > 0: K slices across workgroups (batched path, then a finish pass)
   int gemv = 0;    // 1: VALU GEMV main loop (bf16, at most GEMV_MAX_ROWS rows)
+  int rowgrp = 0;  // 1: row-group kernel (more than MAX_ROWS rows, bf16), K slices, finish pass
 };
+
+// Products over more than MAX_ROWS rows (tree-scoring passes of whole trees,
+// bf16, up to ROWGRP_MAX_ROWS rows): workgroups of 4 waves take
+// ROWGRP_TILES output tiles against one group of ROWGRP_ROWS rows over one K
+// slice.  Slices: about ROWGRP_WGS workgroups in all (two per CU), at least
+// 4 k-blocks each.
+constexpr int ROWGRP_MAX_ROWS = 256;
+constexpr int ROWGRP_TILES = 16;
+constexpr int ROWGRP_ROWS = 64;
+constexpr int ROWGRP_WGS = 512;
+inline int rowgrp_split(int n_tiles, int nkb, int R) {
+  const int base = (n_tiles + ROWGRP_TILES - 1) / ROWGRP_TILES * ((R + ROWGRP_ROWS - 1) / ROWGRP_ROWS);
+  int sp = (ROWGRP_WGS + base / 2) / base;
+  if (sp > nkb / 4) sp = nkb / 4;
+  return sp < 1 ? 1 : sp;
+}
 
 // K slices of a batched product at nt tiles per wave: at most one workgroup
 // of 4 waves per CU (longer slices stream better than more of them, and a
@@ -94,6 +111,12 @@ inline ProductPlan plan_product(int n_tiles, int nkb, int K, int K_full, int R, 
                                 bool bf16, size_t lds_limit) {
   ProductPlan p;
   const int rt = row_tiles(R);
+  if (R > MAX_ROWS) {   // the row-group kernel (bf16 only: fp32 passes stay within MAX_ROWS)
+    p.rowgrp = bf16 ? 1 : 0;
+    p.nt = 4;
+    p.split = rowgrp_split(n_tiles, nkb, R);
+    return p;
+  }
   if (R > GEMV_MAX_ROWS) {
     plan_batched(n_tiles, nkb, K, R, p.nt, p.split);
     const int groups = n_tiles / p.nt;
@@ -176,18 +199,31 @@ inline int attention_nsub(int units, int nkv, int max_slots) {
   return nsub;
 }
 
+// Rows per workgroup of the tree-scoring attention (grouped from each
+// tree's first row, the tree's last group possibly shorter): as many rows
+// as fit the 16 score columns at g = nq / nkv query heads each; 1 = no
+// grouping (fp32 caches and head dims other than 64 and 128).
+inline int score_attention_group(bool bf16, int nq, int nkv, int d) {
+  if (!bf16 || (d != 64 && d != 128) || nkv <= 0 || nq % nkv) return 1;
+  const int g = nq / nkv;
+  return g >= 16 ? 1 : 16 / g;
+}
+
 // Rows x chunks of the attention partials that any pass of 1..rows_max rows
-// writes (row groups of grp rows where rows_max allows them), and the most
-// chunks of any one row; the partial buffers are sized from the first, and
-// the second must not exceed ATT_MAX_CHUNKS.
-inline long attention_partial_rows(int rows_max, int grp, int nkv, int max_slots, int &max_chunks) {
+// writes, single rows or in groups of grp or grp2 rows, and the most chunks
+// of any one row; the partial buffers are sized from the first, and the
+// second must not exceed ATT_MAX_CHUNKS.  A pass of R rows in groups of gs
+// has at least ceil(R / gs) workgroup rows (more where groups restart at
+// each tree), and the chunks per row do not grow with them.
+inline long attention_partial_rows(int rows_max, int grp, int grp2, int nkv, int max_slots,
+                                   int &max_chunks) {
   long most = 0;
   max_chunks = 0;
   for (int R = 1; R <= rows_max; ++R) {
-    const int groups[2] = {1, grp};   // rows per workgroup: single rows, whole groups
+    const int groups[3] = {1, grp, grp2};   // rows per workgroup
     for (int gs : groups) {
-      if (gs < 1 || R % gs) continue;
-      const int ch = attention_chunks(max_slots, attention_nsub(R / gs, nkv, max_slots));
+      if (gs < 1) continue;
+      const int ch = attention_chunks(max_slots, attention_nsub((R + gs - 1) / gs, nkv, max_slots));
       if ((long)R * ch > most) most = (long)R * ch;
       if (ch > max_chunks) max_chunks = ch;
     }

@@ -3,6 +3,7 @@
 // chain and the tree.  Implements include/prism_draft.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -33,6 +34,7 @@ struct Set {
 struct Pass {            // one forward pass: where its inputs and outputs live
   int set, R, F, topk;
   int grp;                // > 1: attention over groups of grp rows of one sequence (tree levels)
+  int rps;                // > 0 (with grp): rows in runs of rps rows of one tree (tree scoring)
   RowsIn in;
   TokFromLm lm_in;        // tokens from the previous pass's LM partials (pval != NULL)
   bool defer_merge;       // leave the LM partials to the next pass (chain, top-1)
@@ -67,6 +69,11 @@ struct prism_ctx {
   int dev = 0;
   int H = 0, nq = 0, nkv = 0, d = 0, I = 0, V = 0, QKV = 0;
   int rows_max = 0, max_slots = 0, kmax = 1, n_wg_lm = 0, Cmax = 0;
+  // rows of the largest pass: tree scoring (bf16) runs whole trees in passes
+  // of up to LMR_MAX_ROWS rows (the row-group products and one LM head per
+  // pass); other passes take at most rows_max
+  int pass_max = 0;
+  int score_grp = 1;                // tree scoring: rows per attention workgroup
   int feat_max = 0;
   // passes take the fusion FC's embedding half from a per-set table (bf16)
   bool use_tab = false;
@@ -240,8 +247,11 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   // attention partials: rows x chunks of the largest pass (chunks per pass
   // from its row count); tree levels group att_grp rows of one sequence
   c->att_grp = w > 1 ? attention_group(bf16, k.n_q_heads, k.n_kv_heads, k.head_dim, w) : 1;
+  c->pass_max = bf16 && rows < LMR_MAX_ROWS ? LMR_MAX_ROWS : rows;
+  c->score_grp = score_attention_group(bf16, k.n_q_heads, k.n_kv_heads, k.head_dim);
   int max_chunks = 0;
-  const long part_rc = attention_partial_rows(rows, c->att_grp, k.n_kv_heads, c->max_slots, max_chunks);
+  const long part_rc = attention_partial_rows(c->pass_max, c->att_grp, c->score_grp, k.n_kv_heads,
+                                              c->max_slots, max_chunks);
   if (max_chunks > ATT_MAX_CHUNKS) {
     delete c;
     return fail(nullptr, PRISM_ERR_SHAPE, "KV capacity per sequence too large for the attention merge");
@@ -257,11 +267,12 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   c->n_wg_lm = lm_workgroups(c->lm.n_tiles, 1);
   if (const char *e = getenv("PRISM_NO_GRAPH")) c->use_graph = !(e[0] == '1');
 
-  // rows of a full pass (R) and of one chunk of the fusion FC / QKV front of
-  // a catch-up step (RF: the accepted tokens, at most MAX_ROWS per chunk)
-  const size_t R = rows, es = c->esz;
+  // rows of a drafting pass (R), of any pass (RP: tree scoring), and of one
+  // chunk of the fusion FC / QKV front of a catch-up step too (RF: the
+  // accepted tokens, at most MAX_ROWS per chunk)
+  const size_t R = rows, RP = c->pass_max, es = c->esz;
   const int front_rows = k.max_new_rows < MAX_ROWS ? k.max_new_rows : MAX_ROWS;
-  const size_t RF = rows > front_rows ? rows : front_rows;
+  const size_t RF = (int)RP > front_rows ? RP : front_rows;
   c->new_max = k.max_new_rows;
   c->front_max = (int)RF;
   size_t total = 0;
@@ -274,36 +285,43 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   const size_t nth = (size_t)c->H / 16;
   planes(c->xfc, RF * (c->H + c->feat_max));
   add((void **)&c->u, RF * c->H * 4);
-  add((void **)&c->r1, R * c->H * 4);
+  add((void **)&c->r1, RP * c->H * 4);
   planes(c->ug, RF * c->H);
-  planes(c->r1g, R * c->H);
-  planes(c->hg, R * c->H);
+  planes(c->r1g, RP * c->H);
+  planes(c->hg, RP * c->H);
   if (bf16) {
     planes(c->lmr_x, (size_t)LMR_MAX_ROWS * c->H);
     add((void **)&c->lmr_scale, LMR_MAX_ROWS * 4);
   }
   add((void **)&c->ss_u, nth * RF * 4);
-  add((void **)&c->ss_r1, nth * R * 4);
-  add((void **)&c->ss_h, nth * R * 4);
+  add((void **)&c->ss_r1, nth * RP * 4);
+  add((void **)&c->ss_h, nth * RP * 4);
   add((void **)&c->sc_u, RF * 4);
-  add((void **)&c->sc_r1, R * 4);
-  add((void **)&c->sc_h, R * 4);
+  add((void **)&c->sc_r1, RP * 4);
+  add((void **)&c->sc_h, RP * 4);
   add((void **)&c->q, RF * c->nq * c->d * 4);
   add((void **)&c->pm, part_rc * c->nq * 4);
   add((void **)&c->pl, part_rc * c->nq * 4);
   add((void **)&c->po, part_rc * c->nq * c->d * 4);
-  planes(c->o, R * c->nq * c->d);
-  planes(c->z, R * c->I);
-  add((void **)&c->hid[0], R * c->H * 4);
+  planes(c->o, RP * c->nq * c->d);
+  planes(c->z, RP * c->I);
+  add((void **)&c->hid[0], RP * c->H * 4);
   add((void **)&c->hid[1], R * c->H * 4);
-  if ((int)RF > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums
+  if ((int)RF > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums [split][rows][N]
     size_t pn = 0;
-    auto upd = [&](int N, int K) {   // the plan depends on the row count: take every count
+    // the slices depend on the row count and tiles per wave, and grow with
+    // K: every count, every tile count, the full K of each matrix
+    auto upd = [&](int N, int K) {
+      const TiledMat t = make_tiled(N, K, bf16);
       for (int rr = GEMV_MAX_ROWS + 1; rr <= (int)RF; ++rr) {
-        int nt, sp;
-        const TiledMat t = make_tiled(N, K, bf16);
-        plan_batched(t.n_tiles, t.nkb, t.K, rr, nt, sp);
-        if ((size_t)sp * N > pn) pn = (size_t)sp * N;
+        int sp = 0;
+        if (rr > MAX_ROWS) {
+          sp = rowgrp_split(t.n_tiles, t.nkb, rr);
+        } else {
+          for (int nt = 1; nt <= 8; nt *= 2)
+            if (t.n_tiles % nt == 0) sp = std::max(sp, batched_split(t.n_tiles, nt, t.nkb, t.K, rr));
+        }
+        pn = std::max(pn, (size_t)rr * sp * N);
       }
     };
     upd(c->H, c->H + k.feat_width);
@@ -312,7 +330,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
     upd(c->H, c->nq * c->d);
     upd(2 * c->I, c->H);
     upd(c->H, c->I);
-    add((void **)&c->part, RF * pn * 4);
+    add((void **)&c->part, pn * 4);
   }
   add((void **)&c->lm_max, R * c->n_wg_lm * 4);
   add((void **)&c->lm_sum, R * c->n_wg_lm * 4);
@@ -321,7 +339,7 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->ids, R * c->kmax * 4);
   add((void **)&c->logp, R * c->kmax * 4);
   add((void **)&c->tokbuf, R * 4);
-  add((void **)&c->tab_tok, R * 4);
+  add((void **)&c->tab_tok, RF * 4);
   add((void **)&c->samp_logits, R * c->V * 4);
   {   // verification rows: target and draft rows of a chain, or every node of a tree
     const int chain_rows = k.max_batch * (2 * k.max_steps + 1);
@@ -586,6 +604,7 @@ static GemmLaunch gemm_of(const prism_ctx *c, const TiledMat &m, const Act &x, i
   g.nt = pl.nt;
   g.split = pl.split;
   g.gemv = pl.gemv;
+  g.rowgrp = pl.rowgrp;
   if (R > GEMV_MAX_ROWS) g.part = c->part;
   return g;
 }
@@ -659,7 +678,7 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   // attention over the visible slots -> o
   ActOut o = c->o;
   o.ld = c->nq * c->d;
-  launch_attention(bf, R, c->nq, c->nkv, c->d, q, p.in, kv, c->max_slots, p.grp, c->pm, c->pl,
+  launch_attention(bf, R, c->nq, c->nkv, c->d, q, p.in, kv, c->max_slots, p.grp, p.rps, c->pm, c->pl,
                    c->po, o, c->err, s);
   // r1 = u + W_o o  ->  r1, (r1 * g2), sums of squares
   GemmLaunch g = gemm_of(c, S.o, act_of(o, c->nq * c->d), R, EPI_NORM);
@@ -1230,20 +1249,21 @@ prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_
                                 (uintptr_t)d_tokens, (uintptr_t)d_depth, (uintptr_t)d_mask,
                                 (uintptr_t)d_logits, (uintptr_t)c->fmap[0]};
   const int set = c->fmap[0];
-  // more rows than one pass takes (bf16): the passes of each group of up to
-  // LMR_MAX_ROWS rows leave their LM-head operand rows, and one LM head over
-  // the group streams the weights once instead of once per pass
-  const int grp_rows = LMR_MAX_ROWS / c->rows_max * c->rows_max;
-  const bool grouped = c->bf16 && rows > c->rows_max && grp_rows > 0 && c->lmr_x.hi &&
-                       lmhead_rows_fits(c->lm, grp_rows);
+  const int rps = n_nodes + 1;   // each tree's rows: its root, then its nodes
+  // bf16: passes of whole trees, up to pass_max rows (the row-group
+  // products), the tree's rows grouped in the attention, and one LM head over
+  // each pass's rows; otherwise passes of up to rows_max rows with their own
+  // LM heads
+  const bool wide = c->bf16 && c->pass_max > c->rows_max && c->lmr_x.hi &&
+                    lmhead_rows_fits(c->lm, c->pass_max) && rps <= c->pass_max;
+  const int per_pass = wide ? c->pass_max / rps * rps : c->rows_max;
   return run_graph(c, key, (hipStream_t)stream, [&](hipStream_t s) {
     launch_score_setup(B, n_nodes, b.d_tokens, b.d_ctx_lens, d_tokens, d_depth, d_mask, c->s_tok,
                        c->s_seq, c->s_pos, c->s_slot, c->s_bits, c->err, s);
-    // rows in tree order, in passes of up to rows_max: a node's ancestors
-    // come before it, so their KV is written by this pass or an earlier one
-    for (int r0 = 0; r0 < rows; r0 += c->rows_max) {
-      const int n = rows - r0 < c->rows_max ? rows - r0 : c->rows_max;
-      const int g0 = grouped ? r0 / grp_rows * grp_rows : r0;   // the pass's group
+    // rows in tree order: a node's ancestors come before it, so their KV is
+    // written by this pass or an earlier one
+    for (int r0 = 0; r0 < rows; r0 += per_pass) {
+      const int n = rows - r0 < per_pass ? rows - r0 : per_pass;
       Pass p{};
       p.set = set;
       p.R = n;
@@ -1264,22 +1284,21 @@ prism_status prism_score_tree(prism_ctx *c, const prism_batch *batch, int32_t n_
       p.logits = d_logits + (size_t)r0 * V;
       p.ld_logits = V;
       p.ids = c->ids;
-      if (grouped) {
-        const size_t off = (size_t)(r0 - g0) * c->H;
-        p.lm_rows_x.hi = (bf16_t *)c->lmr_x.hi + off;
-        p.lm_rows_x.lo = (bf16_t *)c->lmr_x.lo + off;
+      if (wide) {
+        p.grp = c->score_grp;
+        p.rps = rps;
+        p.lm_rows_x = c->lmr_x;
         p.lm_rows_x.ld = c->H;
-        p.lm_rows_scale = c->lmr_scale + (r0 - g0);
+        p.lm_rows_scale = c->lmr_scale;
       }
       enqueue_pass(c, p, kv, s);
-      const int gn = rows - g0 < grp_rows ? rows - g0 : grp_rows;
-      if (grouped && r0 + n == g0 + gn) {   // the group's last pass: its LM head
+      if (wide) {   // the pass's LM head
         LmRowsArgs a{};
         a.m = c->lm;
         a.x = act_of(c->lmr_x, c->H);
-        a.R = gn;
+        a.R = n;
         a.scale = c->lmr_scale;
-        a.logits = d_logits + (size_t)g0 * V;
+        a.logits = d_logits + (size_t)r0 * V;
         a.ld_logits = V;
         launch_lmhead_rows(a, s);
       }

@@ -154,7 +154,7 @@ def run_score_tree(cfg, seqs=None):
     it = make_inputs(tcfg, "cuda")
     it.features.zero_()
     assert torch.equal(it.tokens, inp.tokens) and torch.equal(it.ctx_lens, inp.ctx_lens)
-    tdr = Drafter(tcfg, max_batch=64)        # passes of up to 64 rows
+    tdr = Drafter(tcfg, max_batch=64)        # bf16: passes of whole trees, up to 256 rows
     tdr.load(wt)
     lg = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"])
     again = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"])
@@ -209,17 +209,29 @@ def test_score_tree_and_verify_small_empty_context():
 
 
 def test_score_tree_and_verify_small_two_passes():
-    """4 trees x 21 rows = 84 rows: two scoring passes of up to 64 rows, the
-    second one's nodes attending to KV that the first one wrote."""
+    """4 trees x 21 rows = 84 rows: one scoring pass of more than 64 rows
+    (the row-group products over a full and a ragged row group, the trees'
+    rows grouped by 4 in the attention, 5 groups per tree, the last of one
+    row)."""
     lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_b4", batch=4))
     assert len(lens) == 4
 
 
 def test_score_tree_and_verify_small_two_groups():
-    """13 trees x 21 rows = 273 rows: five scoring passes, their LM-head rows
-    in two launches (256 rows, then 17)."""
+    """13 trees x 21 rows = 273 rows: two scoring passes of whole trees (12
+    trees in 252 rows, then one in 21), the second one's nodes attending to
+    KV that the first one wrote."""
     lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_b13", batch=13))
     assert len(lens) == 13
+
+
+def test_score_tree_and_verify_small_mha():
+    """One query head per KV head: 16 rows per attention workgroup, so each
+    21-row tree is a group of 16 and one of 5; 5 trees = 105 rows in one
+    row-group pass."""
+    lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_mha_b5", batch=5,
+                                                n_kv_heads=8))
+    assert len(lens) == 5
 
 
 def test_score_tree_rows_are_checked():

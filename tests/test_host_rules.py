@@ -67,8 +67,8 @@ int main() {
       std::scanf("%d %d %d %d %d %d %d %ld", &nt, &nkb, &K, &Kf, &R, &qkv, &bf, &lds);
       ProductPlan p = plan_product(nt, nkb, K, Kf, R, qkv != 0, bf != 0, (size_t)lds);
       const int rt = p.gemv ? 1 : row_tiles(R);
-      std::printf("%d %d %d %d %d %d\n", p.kw, p.nt, p.split, p.gemv, plan_fits(p, R) ? 1 : 0,
-                  product_max_waves(rt, p.gemv ? 1 : p.nt));
+      std::printf("%d %d %d %d %d %d %d\n", p.kw, p.nt, p.split, p.gemv, plan_fits(p, R) ? 1 : 0,
+                  product_max_waves(rt, p.gemv ? 1 : p.nt), p.rowgrp);
     } else if (!std::strcmp(cmd, "grp")) {    // bf16 nq nkv d w
       int bf, nq, nkv, d, w;
       std::scanf("%d %d %d %d %d", &bf, &nq, &nkv, &d, &w);
@@ -78,11 +78,15 @@ int main() {
       std::scanf("%d %d %d", &u, &nkv, &ms);
       const int ns = attention_nsub(u, nkv, ms);
       std::printf("%d %d\n", ns, attention_chunks(ms, ns));
-    } else if (!std::strcmp(cmd, "part")) {   // rows_max grp nkv max_slots
-      int rm, gp, nkv, ms, mc;
-      std::scanf("%d %d %d %d", &rm, &gp, &nkv, &ms);
-      const long p = attention_partial_rows(rm, gp, nkv, ms, mc);
+    } else if (!std::strcmp(cmd, "part")) {   // rows_max grp grp2 nkv max_slots
+      int rm, gp, gp2, nkv, ms, mc;
+      std::scanf("%d %d %d %d %d", &rm, &gp, &gp2, &nkv, &ms);
+      const long p = attention_partial_rows(rm, gp, gp2, nkv, ms, mc);
       std::printf("%ld %d\n", p, mc);
+    } else if (!std::strcmp(cmd, "sgrp")) {   // bf16 nq nkv d
+      int bf, nq, nkv, d;
+      std::scanf("%d %d %d %d", &bf, &nq, &nkv, &d);
+      std::printf("%d\n", score_attention_group(bf != 0, nq, nkv, d));
     }
   }
   return 0;
@@ -199,8 +203,8 @@ def test_every_plan_fits_its_kernel(driver):
     out = driver("\n".join(lines) + "\n")
     assert len([o for o in out if o]) == len(cases)
     for case, o in zip(cases, out):
-        kw, nt, split, gemv, fits, maxw = (int(x) for x in o.split())
-        assert fits == 1 and 1 <= kw <= maxw, (case, o)
+        kw, nt, split, gemv, fits, maxw, rowgrp = (int(x) for x in o.split())
+        assert fits == 1 and 1 <= kw <= maxw and rowgrp == 0, (case, o)
         if split == 0 and not gemv:
             assert 64 * kw <= 64 * maxw
             # instantiations the launcher dispatches unsplit
@@ -235,30 +239,41 @@ def test_tree_attention_groups(driver):
                                            t.tree_width))[0] == "4"
 
 
-@pytest.mark.parametrize("rows_max,grp,nkv,max_slots", [
-    (32, 4, 8, 1152), (4, 1, 8, 1152), (1, 1, 8, 4096), (32, 1, 8, 4096), (16, 1, 8, 4096),
-    (2, 4, 2, 448), (64, 2, 8, 131072), (8, 8, 1, 64), (32, 4, 8, 16)])
-def test_attention_partials_cover_every_pass(driver, rows_max, grp, nkv, max_slots):
+@pytest.mark.parametrize("rows_max,grp,grp2,nkv,max_slots", [
+    (32, 4, 4, 8, 1152), (4, 1, 4, 8, 1152), (1, 1, 1, 8, 4096), (32, 1, 4, 8, 4096),
+    (16, 1, 16, 8, 4096), (2, 4, 1, 2, 448), (64, 2, 4, 8, 131072), (8, 8, 1, 1, 64),
+    (32, 4, 4, 8, 16), (256, 4, 4, 8, 1152), (256, 1, 16, 32, 4096), (256, 2, 2, 8, 131072)])
+def test_attention_partials_cover_every_pass(driver, rows_max, grp, grp2, nkv, max_slots):
     """Steps per workgroup: a power of two up to 16, the fewest that keep a
     pass at most 512 workgroups; the partial buffers hold rows x chunks of
-    every pass of 1..rows_max rows, grouped or not."""
-    part, most_ch = (int(x) for x in driver("part %d %d %d %d\n" % (rows_max, grp, nkv,
-                                                                      max_slots))[0].split())
+    every pass of 1..rows_max rows: single rows, groups of grp or grp2 rows,
+    and runs of rps rows (trees) grouped from each run's first row."""
+    part, most_ch = (int(x) for x in driver("part %d %d %d %d %d\n" % (
+        rows_max, grp, grp2, nkv, max_slots))[0].split())
+
+    def chunks(units):
+        ns, ch = (int(x) for x in driver("nsub %d %d %d\n" % (units, nkv, max_slots))[0].split())
+        assert ns in (1, 2, 4, 8, 16)
+        assert ch == -(-max_slots // (64 * ns))
+        assert units * nkv * ch <= 512 or ns == 16
+        if ns > 1:   # the fewest such steps
+            assert units * nkv * -(-max_slots // (64 * (ns // 2))) > 512
+        return ch
+
     seen_rc, seen_ch = 0, 0
     for R in range(1, rows_max + 1):
-        for gs in {1, grp}:
-            if R % gs:
-                continue
-            units = R // gs
-            ns, ch = (int(x) for x in driver("nsub %d %d %d\n" % (units, nkv, max_slots))[0].split())
-            assert ns in (1, 2, 4, 8, 16)
-            assert ch == -(-max_slots // (64 * ns))
-            assert units * nkv * ch <= 512 or ns == 16
-            if ns > 1:   # the fewest such steps
-                assert units * nkv * -(-max_slots // (64 * (ns // 2))) > 512
+        for gs in {1, grp, grp2}:
+            ch = chunks(-(-R // gs))
             assert R * ch <= part
             seen_rc, seen_ch = max(seen_rc, R * ch), max(seen_ch, ch)
     assert (part, most_ch) == (seen_rc, seen_ch)
+    # runs of rps rows (trees of rps - 1 nodes) in groups of grp2: more
+    # workgroup rows than ceil(R / grp2), never more chunks per row
+    for rps in (2, 5, 17, 61, 64):
+        for n_runs in range(1, rows_max // rps + 1, 3):
+            R = n_runs * rps
+            units = n_runs * -(-rps // grp2)
+            assert R * chunks(units) <= part
 
 
 def test_gate_up_tiles_fill_whole_rounds(driver):
@@ -268,6 +283,49 @@ def test_gate_up_tiles_fill_whole_rounds(driver):
     for n_tiles, K, R, groups in ((1792, 4096, 16, 256), (1792, 4096, 32, 256),
                                   (3584, 8192, 32, 512)):
         o = driver("plan %d %d %d %d %d 0 1 163840\n" % (n_tiles, K // 32, K, K, R))[0]
-        kw, nt, split, gemv, fits, maxw = (int(x) for x in o.split())
-        assert (nt, split, gemv, fits) == (7, 0, 0, 1), o
+        kw, nt, split, gemv, fits, maxw, rowgrp = (int(x) for x in o.split())
+        assert (nt, split, gemv, fits, rowgrp) == (7, 0, 0, 1, 0), o
         assert n_tiles // nt == groups
+
+
+def test_row_group_plans_for_scoring_passes(driver):
+    """Passes of more than 64 rows (tree scoring, whole trees up to 256 rows)
+    take the row-group kernel in bf16: at least one K slice, at most a
+    quarter of the k-blocks (so every slice has k-blocks), about 512
+    workgroups of 16 tiles x 64 rows in all.  fp32 contexts never plan them
+    (their passes stay within 64 rows; the launcher refuses such a plan)."""
+    cfgs = list(CONFIGS.values()) + [SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN,
+                                     SMALL_BF16_CHAIN.with_(hidden=480, feat_width=1440)]
+    lines, cases = [], []
+    for cfg in cfgs:
+        bf = 1 if cfg.dtype == "bf16" else 0
+        for (nt, nkb, K, Kf, qkv), R in itertools.product(_products(cfg), (65, 100, 183, 244, 256)):
+            lines.append("plan %d %d %d %d %d %d %d 163840" % (nt, nkb, K, Kf, R, qkv, bf))
+            cases.append((cfg.name, bf, nt, nkb, R))
+    out = driver("\n".join(lines) + "\n")
+    for (name, bf, n_tiles, nkb, R), o in zip(cases, out):
+        kw, nt, split, gemv, fits, maxw, rowgrp = (int(x) for x in o.split())
+        assert rowgrp == bf and gemv == 0, (name, n_tiles, nkb, R, o)
+        if not bf:
+            continue
+        assert 1 <= split <= max(1, nkb // 4), (name, n_tiles, nkb, R, o)
+        base = -(-n_tiles // 16) * -(-R // 64)
+        if nkb // 4 >= split + 1:   # not capped by the k-blocks: the nearest count to 512
+            assert abs(base * split - 512) <= base / 2 + 1e-9, (name, n_tiles, nkb, R, o)
+    # the 8B scoring passes (4 trees of 61 rows): FC 8, QKV 5, O 8, gate/up 1, down 8 slices
+    o = [driver("plan %d %d %d %d 244 %d 1 163840\n" % c)[0].split()[2] for c in (
+        (256, 384, 12288, 16384, 0), (384, 128, 4096, 4096, 1), (256, 128, 4096, 4096, 0),
+        (1792, 128, 4096, 4096, 0), (256, 448, 14336, 14336, 0))]
+    assert o == ["8", "5", "8", "1", "8"]
+
+
+@pytest.mark.parametrize("bf,nq,nkv,d,want", [
+    (1, 32, 8, 128, 4), (1, 32, 32, 128, 16), (1, 64, 8, 128, 2), (1, 24, 8, 64, 5),
+    (1, 32, 8, 256, 1), (0, 32, 8, 128, 1), (1, 32, 2, 128, 1), (1, 30, 8, 128, 1)])
+def test_scoring_attention_groups(driver, bf, nq, nkv, d, want):
+    """Tree-scoring rows per attention workgroup: as many rows of g = nq / nkv
+    query heads as fit the 16 score columns (bf16, head dims 64 and 128)."""
+    gs = int(driver("sgrp %d %d %d %d\n" % (bf, nq, nkv, d))[0])
+    assert gs == want
+    if gs > 1:
+        assert gs * (nq // nkv) <= 16 < (gs + 1) * (nq // nkv)
