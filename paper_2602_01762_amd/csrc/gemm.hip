@@ -1204,9 +1204,9 @@ static bool gemm_epi(const GemmLaunch &g, hipStream_t s) {
 }
 
 // Products over more rows than the 16-row-tile kernels take (tree-scoring
-// passes of up to ROWGRP_MAX_ROWS rows, bf16).  A workgroup takes
-// ROWGRP_TILES output tiles (4 per wave) against one group of ROWGRP_ROWS
-// rows over one K slice.  The row group's hi and lo B fragments of each
+// passes of up to ROWGRP_MAX_ROWS rows, bf16).  A workgroup takes 4 RG_NT
+// output tiles (RG_NT per wave) against one group of ROWGRP_ROWS rows over
+// one K slice.  The row group's hi and lo B fragments of each
 // k-block are staged in LDS once for the 4 waves (two buffers, one barrier
 // per k-block), so each weight fragment feeds 4 row tiles x 2 planes from
 // registers and LDS.  The row groups of one (tile group, slice) pair take
@@ -1214,14 +1214,15 @@ static bool gemm_epi(const GemmLaunch &g, hipStream_t s) {
 // and dispatches them together, and the later ones find the weights in that
 // XCD's L2.  Slice partial sums go to part[s][r][n] as in k_gemm_split, and
 // k_gemm_finish applies the epilogue.
-constexpr int RG_NT = 4, RG_RT = 4, RG_D = 2;
-static_assert(4 * RG_NT == ROWGRP_TILES && 16 * RG_RT == ROWGRP_ROWS, "row-group tiling");
-__global__ __launch_bounds__(256) void k_gemm_rows(GemmLaunch g) {
+constexpr int RG_RT = 4, RG_D = 2;
+static_assert(16 * RG_RT == ROWGRP_ROWS, "row-group tiling");
+template <int RG_NT>
+__device__ __forceinline__ void gemm_rows_body(const GemmLaunch &g) {
   __shared__ u32x4 xs[2][2 * RG_RT][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const TiledMat &m = g.m;
   const int n_rg = (g.R + ROWGRP_ROWS - 1) / ROWGRP_ROWS;
-  const int n_xg = (m.n_tiles + ROWGRP_TILES - 1) / ROWGRP_TILES;
+  const int n_xg = (m.n_tiles + 4 * RG_NT - 1) / (4 * RG_NT);
   const int S = g.split;
   const int id = blockIdx.x, blk = id / (8 * n_rg), in = id % (8 * n_rg);
   const int pair = blk * 8 + in % 8, yg = in / 8;
@@ -1341,18 +1342,34 @@ __global__ __launch_bounds__(256) void k_gemm_rows(GemmLaunch g) {
         if (t0 + n >= m.n_tiles) continue;
         *(f32x4 *)(g.part + ((size_t)sl * g.R + r) * m.N + (t0 + n) * 16 + 4 * q4) = acc[n][rt];
       }
-    } else {        // one slice, stored scaled (the LM head): y[r][n] = scale[r] acc
+    } else {        // one slice, the epilogue here (row scales precomputed)
       const float sc = g.norm.scale ? g.norm.scale[r] : 1.f;
 #pragma unroll
       for (int n = 0; n < RG_NT; ++n) {
         if (t0 + n >= m.n_tiles) continue;
-        const f32x4 v = acc[n][rt];
-        *(f32x4 *)(g.y + (size_t)r * g.ldy + (t0 + n) * 16 + 4 * q4) =
-            f32x4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
+        if (g.epi == EPI_SWIGLU) {   // z = SiLU(gate) * up; no shuffles, r < R
+          (void)epilogue_tile<bf16_t, EPI_SWIGLU>(g, t0 + n, r, acc[n][rt], sc, -1, 0);
+        } else {                     // EPI_STORE (the LM head): y[r][n] = scale[r] acc
+          const f32x4 v = acc[n][rt];
+          *(f32x4 *)(g.y + (size_t)r * g.ldy + (t0 + n) * 16 + 4 * q4) =
+              f32x4{v.x * sc, v.y * sc, v.z * sc, v.w * sc};
+        }
       }
     }
   }
 }
+
+// The products: 4 tiles per wave (ROWGRP_TILES per workgroup), up to 3
+// workgroups per CU.
+static_assert(4 * 4 == ROWGRP_TILES, "row-group tiling");
+__global__ __launch_bounds__(256) void k_gemm_rows(GemmLaunch g) { gemm_rows_body<4>(g); }
+
+// The LM head (one slice, EPI_STORE): 8 tiles per wave, which halves the LDS
+// reads per MFMA; its 128 accumulators leave room for two waves per SIMD
+// only if they share the VGPRs (LM head of the 8B scoring pass 504 -> 454 us).
+constexpr int LMR_NT = 8;
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_lmhead_rows(GemmLaunch g) { gemm_rows_body<LMR_NT>(g); }
 
 // the finish pass of a K-split product: one wave per (tile, 16 rows)
 template <typename T>
@@ -1364,20 +1381,34 @@ static void finish_launch(const GemmLaunch &g, hipStream_t s) {
   else hipLaunchKernelGGL((k_gemm_finish<T, EPI_QKV>), fg, fb, 0, s, g);
 }
 
-// Row-group product and, with slice partials, its finish pass; without them
-// (one slice) the kernel stores y = scale * acc itself.  false (nothing
-// launched): rows or slices out of the kernel's range, a token resolution it
-// does not do, or a direct store without its output.
-static bool gemm_rows_launch(const GemmLaunch &g, hipStream_t s) {
+// Whether a row-group product applies its epilogue in the kernel: the LM
+// head's store, and a SwiGLU product of one slice (its row scales
+// precomputed); the others write slice partials for the finish pass.
+static bool rows_direct(const GemmLaunch &g) {
+  return g.epi == EPI_STORE || (g.epi == EPI_SWIGLU && g.split == 1);
+}
+
+// Row-group product and, with slice partials, its finish pass.  false
+// (nothing launched): rows or slices out of the kernel's range, a token
+// resolution it does not do, or a direct epilogue without its operands.
+static bool gemm_rows_launch(GemmLaunch g, hipStream_t s) {
   const int nk = g.m.nkb - g.kb_lo;
+  const bool direct = rows_direct(g);
   if (g.R < 1 || g.R > ROWGRP_MAX_ROWS || g.split < 1 || g.split > nk || g.tok_out || !g.x.lo ||
-      (!g.part && (g.split != 1 || !g.y)))
+      (direct && (g.split != 1 || (g.epi == EPI_STORE && !g.y) ||
+                  (g.epi == EPI_SWIGLU && (!g.z.hi || (g.norm.n_parts > 0 && !g.norm.scale))))) ||
+      (!direct && !g.part))
     return false;
-  const long n_xg = (g.m.n_tiles + ROWGRP_TILES - 1) / ROWGRP_TILES;
+  if (direct) g.part = nullptr;
+  const bool lm = g.epi == EPI_STORE;
+  const int tiles = lm ? 4 * LMR_NT : ROWGRP_TILES;   // per workgroup
+  const long n_xg = (g.m.n_tiles + tiles - 1) / tiles;
   const long n_rg = (g.R + ROWGRP_ROWS - 1) / ROWGRP_ROWS;
   const long pairs = n_xg * g.split;
-  hipLaunchKernelGGL(k_gemm_rows, dim3((unsigned)((pairs + 7) / 8 * 8 * n_rg)), dim3(256), 0, s, g);
-  if (g.part) finish_launch<bf16_t>(g, s);
+  const dim3 grid((unsigned)((pairs + 7) / 8 * 8 * n_rg));
+  if (lm) hipLaunchKernelGGL(k_lmhead_rows, grid, dim3(256), 0, s, g);
+  else hipLaunchKernelGGL(k_gemm_rows, grid, dim3(256), 0, s, g);
+  if (!direct) finish_launch<bf16_t>(g, s);
   return true;
 }
 
@@ -1469,6 +1500,7 @@ int gemm_ss_parts(const GemmLaunch &g) {
 }
 
 bool gemm_own_scales(const GemmLaunch &g, int n_parts) {
+  if (g.rowgrp && rows_direct(g)) return false;   // no finish pass: scales precomputed
   if (g.split > 0) return scales_fit(64 * finish_tiles(g.m.n_tiles, g.epi), g.R < 16 ? g.R : 16, n_parts);
   return g.R <= MAX_ROWS && scales_fit(64 * g.kw, g.R, n_parts);
 }
@@ -1530,7 +1562,7 @@ void launch_lmhead_rows(const LmRowsArgs &a, hipStream_t s) {
   g.R = a.R;
   g.split = 1;
   g.rowgrp = 1;
-  g.part = nullptr;          // the epilogue stores y directly
+  g.epi = EPI_STORE;         // the kernel stores y itself
   g.y = a.logits;
   g.ldy = a.ld_logits;
   g.norm.scale = a.scale;

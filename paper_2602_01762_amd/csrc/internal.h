@@ -86,7 +86,9 @@ struct RowsIn {
   const uint64_t *bits;
 };
 
-enum Epi { EPI_NORM = 0, EPI_SWIGLU = 1, EPI_QKV = 2 };
+// EPI_STORE (row-group kernel only): y = scale * acc, nothing else (the LM
+// head of a tree-scoring pass)
+enum Epi { EPI_NORM = 0, EPI_SWIGLU = 1, EPI_QKV = 2, EPI_STORE = 3 };
 
 // Token of each row taken straight from the previous LM head's top-1
 // partials ([R][n_wg] values and ids; larger value wins, ties -> lower id),
