@@ -225,6 +225,16 @@ def test_score_tree_and_verify_small_two_groups():
     assert len(lens) == 13
 
 
+def test_score_tree_and_verify_small_h480():
+    """Hidden size 480: 15 k-blocks per row (odd, so the LM head's single K
+    slice ends with a k-block of zero activations), 30 output tiles in the
+    480-wide products (a tile group with waves past the last tile), no
+    embedding table; 5 trees = 105 rows in one row-group pass."""
+    lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_bf16_tree_h480_b5", batch=5,
+                                                hidden=480, feat_width=1440))
+    assert len(lens) == 5
+
+
 def test_score_tree_and_verify_small_mha():
     """One query head per KV head: 16 rows per attention workgroup, so each
     21-row tree is a group of 16 and one of 5; 5 trees = 105 rows in one
