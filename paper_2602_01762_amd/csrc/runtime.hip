@@ -51,7 +51,7 @@ struct Pass {            // one forward pass: where its inputs and outputs live
   // pass); this pass's down product writes that operand for the next pass
   bool op_in, op_out;
   // tree scoring (lm_rows_x.hi != NULL): no LM head in the pass; its
-  // operand rows and row scales go here, for one LM head over several passes
+  // operand rows and row scales go here, for the caller's LM head over them
   ActOut lm_rows_x;
   float *lm_rows_scale;
 };
@@ -90,7 +90,7 @@ struct prism_ctx {
   ActOut xfc;                       // FC operand planes [R, H + feat_max]
   float *u = nullptr, *r1 = nullptr;  // residual stream rows [R, H]
   ActOut ug, r1g, hg;               // (x * gain) operand planes [R, H]
-  ActOut lmr_x;                     // bf16: LM-head operand rows of a tree-scoring group [LMR_MAX_ROWS, H]
+  ActOut lmr_x;                     // bf16: LM-head operand rows of a tree-scoring pass [LMR_MAX_ROWS, H]
   float *lmr_scale = nullptr;       // and their row scales
   float *ss_u = nullptr, *ss_r1 = nullptr, *ss_h = nullptr;  // [parts <= H/16][R]
   float *sc_u = nullptr, *sc_r1 = nullptr, *sc_h = nullptr;  // row scales [R]
@@ -703,7 +703,7 @@ static void enqueue_back(prism_ctx *c, const Pass &p, const KvArgs &kv, const fl
   }
   gemm_go(c, g, s);
   const int parts_h = gemm_ss_parts(g);
-  if (p.lm_rows_x.hi) {   // the caller runs the LM head over several passes' rows
+  if (p.lm_rows_x.hi) {   // the caller runs the LM head over these rows
     launch_rowscale(R, c->ss_h, parts_h, H, c->cfg.rms_eps, p.lm_rows_scale, s);
     return;
   }
