@@ -308,6 +308,12 @@ def test_tree_parity_small():
     run_tree_parity(SMALL_BF16_TREE)
 
 
+def test_tree_parity_small_f32():
+    """fp32 weights and KV: ungrouped tree attention (the VALU kernel), fp32
+    products and LM head."""
+    run_tree_parity(SMALL_BF16_TREE.with_(name="small_f32_tree", dtype="f32"))
+
+
 # Head geometries of the grouped tree attention (a workgroup takes the
 # largest divisor of w whose rows x query heads fit 16 score columns): 6 rows
 # of 2 heads, 2 rows of 8 heads, 4 rows of 4 heads at head_dim 128, and a

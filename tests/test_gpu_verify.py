@@ -225,6 +225,14 @@ def test_score_tree_and_verify_small_two_groups():
     assert len(lens) == 13
 
 
+def test_score_tree_and_verify_small_f32():
+    """fp32: 4 trees x 21 rows = 84 rows in passes of up to 64 rows (64, then
+    20, the second one's nodes attending to KV the first one wrote), each pass
+    with its own LM head; the attention ungrouped."""
+    lens = run_score_tree(SMALL_BF16_TREE.with_(name="small_f32_tree_b4", dtype="f32", batch=4))
+    assert len(lens) == 4
+
+
 def test_score_tree_and_verify_small_h480():
     """Hidden size 480: 15 k-blocks per row (odd, so the LM head's single K
     slice ends with a k-block of zero activations), 30 output tiles in the
