@@ -315,10 +315,9 @@ prism_status prism_draft_tree(prism_ctx *ctx, const prism_batch *batch,
  * [B, n_nodes] as prism_draft_tree writes them (node order: every parent
  * before its children).  Writes d_logits [B, n_nodes + 1, V] fp32 (row 0:
  * the token after the root; row 1 + j: after node j) and the KV slots
- * L_b .. L_b + n_nodes.  The rows run in tree order: bf16 contexts whose
- * hidden size is a multiple of 64 take passes of whole trees, up to 256 rows
- * each; other contexts take passes of up to max_batch * max(1, tree_width)
- * rows (at most 64).  n_nodes <= 63.  A
+ * L_b .. L_b + n_nodes.  The rows run in tree order: bf16 contexts take
+ * passes of whole trees, up to 256 rows each; fp32 contexts take passes of
+ * up to max_batch * max(1, tree_width) rows (at most 64).  n_nodes <= 63.  A
  * depth outside 1..n_nodes, or a mask without the node's own bit or naming a
  * later node, is clamped and raises PRISM_ERR_INVALID_ARG in
  * prism_device_status. */
