@@ -605,6 +605,64 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   }
 }
 
+// The same merge for passes of at most CMBW_MAX_CHUNKS chunks per row and
+// head dims up to 256, by one wave per (row, query head), 4 per workgroup:
+// lane c holds chunk c's statistics, two wave reductions (fixed order)
+// replace the workgroup's barriers, and lane l adds, in chunk order, the
+// partial outputs of dims l, l + 64, ...  (A workgroup per (row, head) with
+// block reductions spent most of its time in its barriers when a row has 2-5
+// chunks: 7808 workgroups for a 244-row scoring pass.)
+constexpr int CMBW_MAX_CHUNKS = 8;
+template <typename T>
+__global__ __launch_bounds__(256) void k_attn_combine_w(AttnArgs a) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int h = blockIdx.x * 4 + wave, r = blockIdx.y;
+  if (h >= a.nq) return;                      // whole waves; no barriers below
+  int b, L, prefix, total;
+  uint64_t bits;
+  row_range(a, r, b, L, prefix, total, bits);
+  const int span = ATT_S * a.nsub;
+  if (total > a.nch * span && h == 0 && lane == 0) atomicOr(a.err, ERRF_CAPACITY);
+  const int nch = min((total + span - 1) / span, a.nch);   // <= CMBW_MAX_CHUNKS (launcher)
+  const size_t base = ((size_t)r * a.nq + h) * a.nch;
+  const int d = a.d;
+  // the partial outputs first, then the statistics they are weighted by
+  float po[CMBW_MAX_CHUNKS][4];
+#pragma unroll
+  for (int c = 0; c < CMBW_MAX_CHUNKS; ++c)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int dim = lane + 64 * j;
+      po[c][j] = c < nch && dim < d ? a.po[(base + c) * d + dim] : 0.f;
+    }
+  const float l = lane < nch ? a.pl[base + lane] : 0.f;
+  const float mc = lane < nch ? a.pm[base + lane] : -INFINITY;
+  const float M = wave_max(l > 0.f ? mc : -INFINITY);
+  const float w = l > 0.f ? expf(mc - M) : 0.f;
+  const float lsum = wave_sum(l * w);
+  float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < CMBW_MAX_CHUNKS; ++c) {
+    const float wc = readlane_f32(w, c);      // 0 past nch
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] += po[c][j] * wc;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int dim = lane + 64 * j;
+    if (dim >= d) break;
+    const float v = lsum > 0.f ? o[j] / lsum : 0.f;
+    const size_t i = (size_t)r * a.o.ld + (size_t)h * d + dim;
+    if constexpr (sizeof(T) == 2) {
+      const uint32_t hb = f2bf(v);
+      ((bf16_t *)a.o.hi)[i] = (bf16_t)hb;
+      ((bf16_t *)a.o.lo)[i] = (bf16_t)f2bf(v - bf2f(hb));
+    } else {
+      ((float *)a.o.hi)[i] = v;
+    }
+  }
+}
+
 void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, const RowsIn &in,
                       const KvArgs &kv, int max_slots, int grp, int rps, float *pm, float *pl,
                       float *po, ActOut o, uint32_t *err, hipStream_t s) {
@@ -638,6 +696,9 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
   // chunk index slowest: every row's first chunks are dispatched before any
   // row's later ones, so the last workgroups to start are the short tails
   dim3 g1(nkv, units, a.nch), g2(nq, R);
+  // few chunks per row: the merge by one wave per (row, head)
+  const bool small = a.nch <= CMBW_MAX_CHUNKS && d <= 256;
+  const dim3 g2w((nq + 3) / 4, R);
   // K/V that one pass requests at capacity (R rows of max_slots slots):
   // beyond 1.5 times the 256 MiB infinity cache the rows are streamed with
   // nontemporal loads (70B batch 32, 539 MB: 5.917 -> 5.847 ms); below it
@@ -662,10 +723,12 @@ void launch_attention(bool bf16, int R, int nq, int nkv, int d, const float *q, 
     } else {
       hipLaunchKernelGGL(k_attn_partial<bf16_t>, g1, dim3(256), 0, s, a);
     }
-    hipLaunchKernelGGL(k_attn_combine<bf16_t>, g2, dim3(256), 0, s, a);
+    if (small) hipLaunchKernelGGL(k_attn_combine_w<bf16_t>, g2w, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_attn_combine<bf16_t>, g2, dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL(k_attn_partial<float>, g1, dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_attn_combine<float>, g2, dim3(256), 0, s, a);
+    if (small) hipLaunchKernelGGL(k_attn_combine_w<float>, g2w, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_attn_combine<float>, g2, dim3(256), 0, s, a);
   }
 }
 
