@@ -233,6 +233,17 @@ def test_score_tree_and_verify_small_f32():
     assert len(lens) == 4
 
 
+@pytest.mark.parametrize("nodes", [1, 2])
+def test_score_tree_and_verify_one_tiny_tree(nodes):
+    """One tree of 1 or 2 nodes: a scoring pass of 2 or 3 rows (the 2-row
+    one on the GEMV products), an attention group smaller than its 4-row
+    group size, and the LM head over a partial row tile."""
+    cfg = SMALL_BF16_TREE.with_(name="small_bf16_tree_v%d" % nodes, batch=1, n_steps=2,
+                                tree_width=2, tree_nodes=nodes)
+    lens = run_score_tree(cfg)
+    assert len(lens) == 1
+
+
 def test_score_tree_and_verify_small_h480():
     """Hidden size 480: 15 k-blocks per row (odd, so the LM head's single K
     slice ends with a k-block of zero activations), 30 output tiles in the
