@@ -158,6 +158,30 @@ inline ProductPlan plan_product(int n_tiles, int nkb, int K, int K_full, int R, 
   return p;
 }
 
+// fp32 words of the K-slice partial sums ([split][rows][N]) that any
+// batched product of an [N = 16 n_tiles, K] matrix (nkb k-blocks) writes at
+// GEMV_MAX_ROWS + 1 .. rows_max rows.  The slices depend on the row count
+// and the tiles per wave and do not shrink as K grows, so the full K bounds
+// the fusion FC's feature-column products too.
+inline size_t product_partial_floats(int n_tiles, int nkb, int K, int rows_max) {
+  size_t most = 0;
+  const size_t N = (size_t)16 * n_tiles;
+  for (int rr = GEMV_MAX_ROWS + 1; rr <= rows_max; ++rr) {
+    int sp = 0;
+    if (rr > MAX_ROWS) {
+      sp = rowgrp_split(n_tiles, nkb, rr);
+    } else {
+      for (int nt = 1; nt <= 8; nt *= 2) {
+        if (n_tiles % nt) continue;
+        const int s = batched_split(n_tiles, nt, nkb, K, rr);
+        if (s > sp) sp = s;
+      }
+    }
+    if ((size_t)rr * sp * N > most) most = (size_t)rr * sp * N;
+  }
+  return most;
+}
+
 // Whether a plan's workgroup fits the instantiation it launches (the
 // launcher refuses a plan that does not).
 inline bool plan_fits(const ProductPlan &p, int R) {

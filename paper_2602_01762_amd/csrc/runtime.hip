@@ -309,20 +309,9 @@ prism_status prism_create(const prism_config *cfg, prism_ctx **out) {
   add((void **)&c->hid[1], R * c->H * 4);
   if ((int)RF > GEMV_MAX_ROWS) {   // batched products: K-slice partial sums [split][rows][N]
     size_t pn = 0;
-    // the slices depend on the row count and tiles per wave, and grow with
-    // K: every count, every tile count, the full K of each matrix
     auto upd = [&](int N, int K) {
       const TiledMat t = make_tiled(N, K, bf16);
-      for (int rr = GEMV_MAX_ROWS + 1; rr <= (int)RF; ++rr) {
-        int sp = 0;
-        if (rr > MAX_ROWS) {
-          sp = rowgrp_split(t.n_tiles, t.nkb, rr);
-        } else {
-          for (int nt = 1; nt <= 8; nt *= 2)
-            if (t.n_tiles % nt == 0) sp = std::max(sp, batched_split(t.n_tiles, nt, t.nkb, t.K, rr));
-        }
-        pn = std::max(pn, (size_t)rr * sp * N);
-      }
+      pn = std::max(pn, product_partial_floats(t.n_tiles, t.nkb, t.K, (int)RF));
     };
     upd(c->H, c->H + k.feat_width);
     upd(c->H, 2 * c->H);

@@ -83,6 +83,10 @@ int main() {
       std::scanf("%d %d %d %d %d", &rm, &gp, &gp2, &nkv, &ms);
       const long p = attention_partial_rows(rm, gp, gp2, nkv, ms, mc);
       std::printf("%ld %d\n", p, mc);
+    } else if (!std::strcmp(cmd, "pfl")) {    // n_tiles nkb K rows_max
+      int nt, nkb, K, rm;
+      std::scanf("%d %d %d %d", &nt, &nkb, &K, &rm);
+      std::printf("%zu\n", product_partial_floats(nt, nkb, K, rm));
     } else if (!std::strcmp(cmd, "sgrp")) {   // bf16 nq nkv d
       int bf, nq, nkv, d;
       std::scanf("%d %d %d %d", &bf, &nq, &nkv, &d);
@@ -329,3 +333,30 @@ def test_scoring_attention_groups(driver, bf, nq, nkv, d, want):
     assert gs == want
     if gs > 1:
         assert gs * (nq // nkv) <= 16 < (gs + 1) * (nq // nkv)
+
+
+def test_partial_buffer_holds_every_plan(driver):
+    """The K-slice partial buffer (sized at creation by
+    product_partial_floats over the full K of each matrix) holds split x rows
+    x N floats for the plan of every product at every batched row count: up
+    to 256 rows for bf16 (tree-scoring passes), 64 for fp32, the fusion FC
+    planned over its feature columns only."""
+    cfgs = list(CONFIGS.values()) + [SMALL_BF16_CHAIN, SMALL_BF16_TREE, SMALL_F32_CHAIN,
+                                     SMALL_BF16_CHAIN.with_(ffn=6400),
+                                     SMALL_BF16_CHAIN.with_(hidden=480, feat_width=1440)]
+    for cfg in cfgs:
+        bf = 1 if cfg.dtype == "bf16" else 0
+        kq = 32 if bf else 16
+        rows_max = 256 if bf else 64
+        prods = _products(cfg)
+        sizes = driver("".join("pfl %d %d %d %d\n" % (nt, Kf // kq, Kf, rows_max)
+                               for (nt, nkb, K, Kf, qkv) in prods))
+        size = max(int(x) for x in sizes if x)
+        lines, cases = [], []
+        for (nt, nkb, K, Kf, qkv), R in itertools.product(prods, range(3, rows_max + 1)):
+            lines.append("plan %d %d %d %d %d %d %d 163840" % (nt, nkb, K, Kf, R, qkv, bf))
+            cases.append((nt, R))
+        out = driver("\n".join(lines) + "\n")
+        for (nt, R), o in zip(cases, out):
+            split = int(o.split()[2])
+            assert split * R * 16 * nt <= size, (cfg.name, nt, R, split, size)
