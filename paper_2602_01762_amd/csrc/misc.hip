@@ -554,10 +554,68 @@ void launch_lm_topk(const LmTopkArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(k_lm_topk, dim3(a.n_wg, a.R), dim3(256), 0, s, a);
 }
 
+// The same merge for at most 64 partial lists per row (the tree levels'
+// top-k pass), one wave per row, 4 rows per workgroup: lane l holds list l
+// and its (max, sum of exp); two wave reductions give the log-sum-exp and k
+// rounds of a wave arg-max over the list heads the top-k, with no barriers.
+// (A workgroup per row left 7 of 8 threads idle and paid the block
+// reductions' barriers.)
+template <int KB>
+__global__ __launch_bounds__(256) void k_lm_combine_w(LmCombArgs a) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + wave;
+  if (r >= a.R) return;                       // whole waves; no barriers below
+  const int k = a.topk;
+  const bool has = lane < a.n_wg;             // n_wg <= 64 (launcher)
+  const int wc = has ? lane : 0;
+  const float *pv = a.pval + ((size_t)r * a.n_wg + wc) * k;
+  const int *pi = a.pid + ((size_t)r * a.n_wg + wc) * k;
+  const uint64_t none = cand_key(-INFINITY, 0x7fffffff);
+  uint64_t lk[KB];                            // the lane's list, best first
+#pragma unroll
+  for (int j = 0; j < KB; ++j) {
+    const int jc = j < k ? j : 0;
+    const float v = pv[jc];
+    const int id = pi[jc];
+    lk[j] = has && j < k ? cand_key(v, id) : none;
+  }
+  const float m = has ? a.pmax[(size_t)r * a.n_wg + wc] : -INFINITY;
+  const float sl = has ? a.psum[(size_t)r * a.n_wg + wc] : 0.f;
+  const float M = wave_max(m);
+  const float S = wave_sum(m == -INFINITY ? 0.f : sl * expf(m - M));
+  const float lse = M + logf(S);
+  for (int j = 0; j < k; ++j) {
+    uint64_t b[1] = {lk[0]};
+    wave_max_key_n<1>(b);
+    const bool win = lk[0] == b[0];           // keys are distinct: one owner (or all spent)
+#pragma unroll
+    for (int q = 0; q + 1 < KB; ++q) lk[q] = win ? lk[q + 1] : lk[q];
+    lk[KB - 1] = win ? none : lk[KB - 1];
+    if (lane == 0) {
+      const int id = key_id(b[0]);
+      if (j == 0 && id == NO_TOKEN) atomicOr(a.err, ERRF_NONFINITE);
+      a.ids[(size_t)r * k + j] = id;
+      if (a.logp) a.logp[(size_t)r * k + j] = key_value(b[0]) - lse;
+      if (j == 0) {
+        if (a.tok_a) a.tok_a[r] = id;
+        if (a.tok_b) a.tok_b[(size_t)r * a.ld_b] = id;
+      }
+    }
+  }
+}
+
 void launch_lm_combine(int R, int n_wg, int topk, int V, const float *pmax, const float *psum,
                        const float *pval, const int *pid, int *ids, float *logp, int *tok_a,
                        int *tok_b, int ld_b, uint32_t *err, hipStream_t s) {
   LmCombArgs a{R, n_wg, topk, V, pmax, psum, pval, pid, ids, logp, tok_a, tok_b, ld_b, err};
+  if (n_wg <= 64 && topk > 1) {   // few lists per row (the tree's top-k pass): a wave per row
+    const dim3 g((R + 3) / 4);
+    if (topk <= 2) hipLaunchKernelGGL(k_lm_combine_w<2>, g, dim3(256), 0, s, a);
+    else if (topk <= 4) hipLaunchKernelGGL(k_lm_combine_w<4>, g, dim3(256), 0, s, a);
+    else if (topk <= 8) hipLaunchKernelGGL(k_lm_combine_w<8>, g, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_lm_combine_w<16>, g, dim3(256), 0, s, a);
+    return;
+  }
   if (topk <= 1) hipLaunchKernelGGL(k_lm_combine<1>, dim3(R), dim3(256), 0, s, a);
   else if (topk <= 2) hipLaunchKernelGGL(k_lm_combine<2>, dim3(R), dim3(256), 0, s, a);
   else if (topk <= 4) hipLaunchKernelGGL(k_lm_combine<4>, dim3(R), dim3(256), 0, s, a);
