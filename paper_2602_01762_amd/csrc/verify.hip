@@ -9,8 +9,9 @@
 // Logits rows are V-wide fp32 (0.5 MB at V = 128256), so the work is a
 // stream over them: k_rows_stats splits each row over VSPLIT workgroups,
 // each reducing its slice to (max z, sum exp(z - max), arg-max of the raw
-// logits), z = logit / T; one workgroup per sequence then merges the slices
-// in order and takes the decisions.  Draws use the drafter's inverse CDF
+// logits), z = logit / T (greedy verification: the arg-max only); one
+// workgroup per sequence then merges the slices in order and takes the
+// decisions.  Draws use the drafter's inverse CDF
 // in token-id order.
 #include <cstdarg>
 #include <cstdio>
@@ -36,6 +37,9 @@ __device__ __forceinline__ void slice_of(int V, int part, int &lo, int &hi) {
   hi = min(V, lo + per);
 }
 
+// SOFT = false (greedy verification, which reads only the arg-max): no
+// exponentials, and the statistics stored as (-inf, 0).
+template <bool SOFT>
 __global__ __launch_bounds__(256) void k_rows_stats(const float *__restrict__ x, int V,
                                                     float inv_t, RowStat *out) {
   __shared__ float shv[8];
@@ -48,6 +52,7 @@ __global__ __launch_bounds__(256) void k_rows_stats(const float *__restrict__ x,
   int bi = 0x7fffffff;
   auto take = [&](float v, int i) {
     if (better(v, i, bv, bi)) { bv = v; bi = i; }
+    if (!SOFT) return;
     const float z = v * inv_t;            // online max / sum of exp(z - max)
     if (z > mz) {
       s = s * expf(mz - z) + 1.f;
@@ -72,8 +77,11 @@ __global__ __launch_bounds__(256) void k_rows_stats(const float *__restrict__ x,
         if (i + q < hi) take(v[u][q], i + q);
     }
   }
-  const float M = block_max(mz, shv);
-  const float S = block_sum(mz == -INFINITY ? 0.f : s * expf(mz - M), shv);
+  float M = -INFINITY, S = 0.f;
+  if constexpr (SOFT) {
+    M = block_max(mz, shv);
+    S = block_sum(mz == -INFINITY ? 0.f : s * expf(mz - M), shv);
+  }
   block_argmax(bv, bi, shv, shi);
   if (tid == 0) out[(size_t)row * VSPLIT + part] = RowStat{M, S, bv, bi};
 }
@@ -420,9 +428,12 @@ void launch_verify_chain(int B, int K, int V, float inv_t, const float *tl, cons
   RowStat *ts = (RowStat *)stats;
   RowStat *ds = ts + (size_t)B * (K + 1) * VSPLIT;
   const float it = inv_t > 0.f ? inv_t : 1.f;
-  hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * (K + 1)), dim3(256), 0, s, tl, V, it, ts);
-  if (inv_t > 0.f)
-    hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * K), dim3(256), 0, s, dl, V, it, ds);
+  if (inv_t > 0.f) {   // sampled: the target and draft rows' softmax statistics
+    hipLaunchKernelGGL(k_rows_stats<true>, dim3(VSPLIT, B * (K + 1)), dim3(256), 0, s, tl, V, it, ts);
+    hipLaunchKernelGGL(k_rows_stats<true>, dim3(VSPLIT, B * K), dim3(256), 0, s, dl, V, it, ds);
+  } else {             // greedy: the target rows' arg-max only
+    hipLaunchKernelGGL(k_rows_stats<false>, dim3(VSPLIT, B * (K + 1)), dim3(256), 0, s, tl, V, it, ts);
+  }
   VerifyChainArgs a{K, V, inv_t, tl, dl, ts, ds, drafts, u, n_acc, next, err};
   hipLaunchKernelGGL(k_verify_chain, dim3(B), dim3(DRAW_THREADS), 0, s, a);
 }
@@ -431,7 +442,7 @@ void launch_verify_tree(int B, int nodes, int V, const float *tl, const int32_t 
                         const int32_t *parent, int32_t *n_acc, int32_t *path, int32_t *next,
                         void *stats, hipStream_t s) {
   RowStat *ts = (RowStat *)stats;
-  hipLaunchKernelGGL(k_rows_stats, dim3(VSPLIT, B * (nodes + 1)), dim3(256), 0, s, tl, V, 1.f, ts);
+  hipLaunchKernelGGL(k_rows_stats<false>, dim3(VSPLIT, B * (nodes + 1)), dim3(256), 0, s, tl, V, 1.f, ts);
   VerifyTreeArgs a{nodes, V, ts, tokens, parent, n_acc, path, next};
   hipLaunchKernelGGL(k_verify_tree, dim3(B), dim3(64), 0, s, a);
 }
