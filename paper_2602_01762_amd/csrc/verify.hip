@@ -108,90 +108,130 @@ __device__ __forceinline__ RowSum merge_row(const RowStat *st) {
 // order).  Ids go in blocks of 256 (lane l of a wave holds ids 4l..4l+3 of a
 // block, one 16-byte load per row); wave w owns a contiguous run of blocks.
 // Pass 1 sums each wave's run; an in-order prefix over the waves finds the
-// run holding u * total; pass 2 walks that run block by block with a lane
-// prefix sum (lane order = id order) to the id.  Rounding that leaves no
-// crossing takes the highest id of positive weight.  W(base, v[4]) gives the
-// 4 weights of ids base..base+3 (ids >= V weigh 0).
+// run holding u * total.  Pass 2 splits that run over the waves again (a
+// share of a few blocks each, all loaded at once), and a second in-order
+// prefix finds the share; pass 3 walks the share block by block with a lane
+// prefix sum (lane order = id order) to the id.  (One wave walking the whole
+// run waited on one block's load after another.)  Rounding that leaves no
+// crossing takes the highest id of positive weight of the run.  W(base, v[4])
+// gives the 4 weights of ids base..base+3 (ids >= V weigh 0).  s_wave holds
+// DRAW_SHARED floats, s_pick 3 ints.
 constexpr int DRAW_THREADS = 1024;
 constexpr int DRAW_WAVES = DRAW_THREADS / 64;
+constexpr int DRAW_SHARED = 2 * DRAW_WAVES + 4;
+
+// the first of n in-order sums that carries the running total (from base)
+// past goal: its index and the total before it; none (rounding): the last
+// positive one, with the goal moved to +inf
+__device__ __forceinline__ void pick_in_order(const float *sums, int n, float base, float goal,
+                                              int &pick, float &at, float &g) {
+  float run = base;
+  pick = -1;
+  at = base;
+  g = goal;
+  for (int i = 0; i < n; ++i) {
+    if (sums[i] > 0.f && run + sums[i] > goal) { pick = i; at = run; return; }
+    run += sums[i];
+  }
+  for (int i = n - 1; i >= 0; --i)
+    if (sums[i] > 0.f) { pick = i; break; }
+  g = INFINITY;
+}
 
 template <typename W>
 __device__ int draw_ids(int V, float u, W w4, float *s_wave, int *s_pick) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int nblk = (V + 255) / 256;
-  const int b0 = (int)((long)wave * nblk / DRAW_WAVES), b1 = (int)((long)(wave + 1) * nblk / DRAW_WAVES);
-  float acc = 0.f;
-  for (int blk = b0; blk < b1; ++blk) {
-    float v[4];
-    w4(blk * 256 + 4 * lane, v);
-    acc += (v[0] + v[1]) + (v[2] + v[3]);
+  {   // pass 1: each wave's run
+    const int r0 = (int)((long)wave * nblk / DRAW_WAVES), r1 = (int)((long)(wave + 1) * nblk / DRAW_WAVES);
+    float acc = 0.f;
+    for (int blk = r0; blk < r1; ++blk) {
+      float v[4];
+      w4(blk * 256 + 4 * lane, v);
+      acc += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) s_wave[wave] = acc;
   }
-  acc = wave_sum(acc);
-  if (lane == 0) s_wave[wave] = acc;
   __syncthreads();
   if (tid == 0) {
-    float run = 0.f;
-    for (int i = 0; i < DRAW_WAVES; ++i) run += s_wave[i];
-    const float goal = fminf(fmaxf(u, 0.f), 1.f) * run;
-    int pick = -1;
-    float base = 0.f;
-    run = 0.f;
-    for (int i = 0; i < DRAW_WAVES; ++i) {
-      if (s_wave[i] > 0.f && run + s_wave[i] > goal) { pick = i; base = run; break; }
-      run += s_wave[i];
-    }
-    float g2 = goal;
-    if (pick < 0) {   // past the end by rounding: the last id of positive weight,
-                      // which pass 2 returns when nothing crosses (goal = +inf)
-      for (int i = DRAW_WAVES - 1; i >= 0; --i)
-        if (s_wave[i] > 0.f) { pick = i; break; }
-      g2 = INFINITY;
-    }
+    float total = 0.f;
+    for (int i = 0; i < DRAW_WAVES; ++i) total += s_wave[i];
+    int pick;
+    float at, g;
+    pick_in_order(s_wave, DRAW_WAVES, 0.f, fminf(fmaxf(u, 0.f), 1.f) * total, pick, at, g);
     s_pick[0] = pick;
-    s_wave[DRAW_WAVES] = base;
-    s_wave[DRAW_WAVES + 1] = g2;
+    s_wave[2 * DRAW_WAVES] = at;
+    s_wave[2 * DRAW_WAVES + 1] = g;
     s_pick[1] = -1;
   }
   __syncthreads();
-  if (wave == s_pick[0]) {
-    float run = s_wave[DRAW_WAVES];
-    const float goal = s_wave[DRAW_WAVES + 1];
-    int found = -1, last = -1;
-    for (int blk = b0; blk < b1 && found < 0; ++blk) {
+  const int run_w = s_pick[0];
+  if (run_w >= 0) {   // uniform
+    // pass 2: the run's blocks split over the waves
+    const int p0 = (int)((long)run_w * nblk / DRAW_WAVES), p1 = (int)((long)(run_w + 1) * nblk / DRAW_WAVES);
+    const int b0 = p0 + (int)((long)wave * (p1 - p0) / DRAW_WAVES);
+    const int b1 = p0 + (int)((long)(wave + 1) * (p1 - p0) / DRAW_WAVES);
+    float acc = 0.f;
+    for (int blk = b0; blk < b1; ++blk) {
       float v[4];
       w4(blk * 256 + 4 * lane, v);
-      const float ls = (v[0] + v[1]) + (v[2] + v[3]);
-      float x = ls;   // inclusive prefix over the lanes, fixed order
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const float t = __shfl_up(x, o, 64);
-        if (lane >= o) x += t;
-      }
-      const unsigned long long hit = __ballot(ls > 0.f && run + x > goal);
-      const unsigned long long nz = __ballot(ls > 0.f);
-      if (nz) {
-        const int l = 63 - __clzll((long long)nz);
-        const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
-                             __shfl(v[3], l, 64)};
-        for (int q = 3; q >= 0; --q)
-          if (vl[q] > 0.f) { last = blk * 256 + 4 * l + q; break; }
-      }
-      if (hit) {
-        const int l = __ffsll((long long)hit) - 1;
-        float r = run + __shfl(x, l, 64) - __shfl(ls, l, 64);   // prefix before lane l
-        const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
-                             __shfl(v[3], l, 64)};
-        int id = -1, lastl = -1;
-        for (int q = 0; q < 4; ++q) {
-          if (vl[q] > 0.f) lastl = blk * 256 + 4 * l + q;
-          if (vl[q] > 0.f && r + vl[q] > goal) { id = blk * 256 + 4 * l + q; break; }
-          r += vl[q];
-        }
-        found = id >= 0 ? id : lastl;
-      }
-      run += __shfl(x, 63, 64);
+      acc += (v[0] + v[1]) + (v[2] + v[3]);
     }
-    if (lane == 0) s_pick[1] = found >= 0 ? found : last;
+    acc = wave_sum(acc);
+    if (lane == 0) s_wave[DRAW_WAVES + wave] = acc;
+    __syncthreads();
+    if (tid == 0) {
+      int pick;
+      float at, g;
+      pick_in_order(s_wave + DRAW_WAVES, DRAW_WAVES, s_wave[2 * DRAW_WAVES], s_wave[2 * DRAW_WAVES + 1],
+                    pick, at, g);
+      s_pick[2] = pick;
+      s_wave[2 * DRAW_WAVES + 2] = at;
+      s_wave[2 * DRAW_WAVES + 3] = g;
+    }
+    __syncthreads();
+    // pass 3: the share that holds the goal, walked by its wave
+    if (wave == s_pick[2]) {
+      float run = s_wave[2 * DRAW_WAVES + 2];
+      const float goal = s_wave[2 * DRAW_WAVES + 3];
+      int found = -1, last = -1;
+      for (int blk = b0; blk < b1 && found < 0; ++blk) {
+        float v[4];
+        w4(blk * 256 + 4 * lane, v);
+        const float ls = (v[0] + v[1]) + (v[2] + v[3]);
+        float x = ls;   // inclusive prefix over the lanes, fixed order
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const float t = __shfl_up(x, o, 64);
+          if (lane >= o) x += t;
+        }
+        const unsigned long long hit = __ballot(ls > 0.f && run + x > goal);
+        const unsigned long long nz = __ballot(ls > 0.f);
+        if (nz) {
+          const int l = 63 - __clzll((long long)nz);
+          const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
+                               __shfl(v[3], l, 64)};
+          for (int q = 3; q >= 0; --q)
+            if (vl[q] > 0.f) { last = blk * 256 + 4 * l + q; break; }
+        }
+        if (hit) {
+          const int l = __ffsll((long long)hit) - 1;
+          float r = run + __shfl(x, l, 64) - __shfl(ls, l, 64);   // prefix before lane l
+          const float vl[4] = {__shfl(v[0], l, 64), __shfl(v[1], l, 64), __shfl(v[2], l, 64),
+                               __shfl(v[3], l, 64)};
+          int id = -1, lastl = -1;
+          for (int q = 0; q < 4; ++q) {
+            if (vl[q] > 0.f) lastl = blk * 256 + 4 * l + q;
+            if (vl[q] > 0.f && r + vl[q] > goal) { id = blk * 256 + 4 * l + q; break; }
+            r += vl[q];
+          }
+          found = id >= 0 ? id : lastl;
+        }
+        run += __shfl(x, 63, 64);
+      }
+      if (lane == 0) s_pick[1] = found >= 0 ? found : last;
+    }
   }
   __syncthreads();
   return s_pick[1];
@@ -211,8 +251,8 @@ struct VerifyChainArgs {
 constexpr int VER_MAXK = 64;     // drafts per sequence (max_steps <= 63)
 
 __global__ __launch_bounds__(DRAW_THREADS) void k_verify_chain(VerifyChainArgs a) {
-  __shared__ float s_wave[DRAW_WAVES + 2];
-  __shared__ int s_pick[2];
+  __shared__ float s_wave[DRAW_SHARED];
+  __shared__ int s_pick[3];
   __shared__ RowSum s_t[VER_MAXK + 1], s_d[VER_MAXK];
   __shared__ int s_x[VER_MAXK];
   __shared__ float s_lt[VER_MAXK], s_ld[VER_MAXK];
