@@ -113,12 +113,38 @@ __device__ __forceinline__ RowSum merge_row(const RowStat *st) {
 // prefix finds the share; pass 3 walks the share block by block with a lane
 // prefix sum (lane order = id order) to the id.  (One wave walking the whole
 // run waited on one block's load after another.)  Rounding that leaves no
-// crossing takes the highest id of positive weight of the run.  W(base, v[4])
-// gives the 4 weights of ids base..base+3 (ids >= V weigh 0).  s_wave holds
-// DRAW_SHARED floats, s_pick 3 ints.
+// crossing takes the highest id of positive weight of the run.  L(base)
+// loads the raw values of ids base..base+3 (unconditionally) and
+// W(raw, base, v[4]) gives their 4 weights (ids >= V weigh 0); the passes
+// load a batch of DRAW_BATCH blocks before weighing them, so that the loads
+// are in flight together.  s_wave holds DRAW_SHARED floats, s_pick 3 ints.
 constexpr int DRAW_THREADS = 1024;
 constexpr int DRAW_WAVES = DRAW_THREADS / 64;
 constexpr int DRAW_SHARED = 2 * DRAW_WAVES + 4;
+constexpr int DRAW_BATCH = 8;
+struct DrawRaw {
+  f32x4 x, y;          // the target row's values (and the draft row's, for the residual)
+};
+
+// sum of the weights of blocks [b0, b1) in this lane's columns, loaded a
+// batch at a time
+template <typename L, typename W>
+__device__ __forceinline__ float lane_sum(int b0, int b1, int lane, L ld, W wg) {
+  float acc = 0.f;
+  for (int blk = b0; blk < b1; blk += DRAW_BATCH) {
+    DrawRaw raw[DRAW_BATCH];
+#pragma unroll
+    for (int j = 0; j < DRAW_BATCH; ++j) raw[j] = ld(min(blk + j, b1 - 1) * 256 + 4 * lane);
+#pragma unroll
+    for (int j = 0; j < DRAW_BATCH; ++j) {
+      if (blk + j >= b1) break;
+      float v[4];
+      wg(raw[j], (blk + j) * 256 + 4 * lane, v);
+      acc += (v[0] + v[1]) + (v[2] + v[3]);
+    }
+  }
+  return acc;
+}
 
 // the first of n in-order sums that carries the running total (from base)
 // past goal: its index and the total before it; none (rounding): the last
@@ -138,19 +164,13 @@ __device__ __forceinline__ void pick_in_order(const float *sums, int n, float ba
   g = INFINITY;
 }
 
-template <typename W>
-__device__ int draw_ids(int V, float u, W w4, float *s_wave, int *s_pick) {
+template <typename L, typename W>
+__device__ int draw_ids(int V, float u, L ld, W wg, float *s_wave, int *s_pick) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int nblk = (V + 255) / 256;
   {   // pass 1: each wave's run
     const int r0 = (int)((long)wave * nblk / DRAW_WAVES), r1 = (int)((long)(wave + 1) * nblk / DRAW_WAVES);
-    float acc = 0.f;
-    for (int blk = r0; blk < r1; ++blk) {
-      float v[4];
-      w4(blk * 256 + 4 * lane, v);
-      acc += (v[0] + v[1]) + (v[2] + v[3]);
-    }
-    acc = wave_sum(acc);
+    const float acc = wave_sum(r1 > r0 ? lane_sum(r0, r1, lane, ld, wg) : 0.f);
     if (lane == 0) s_wave[wave] = acc;
   }
   __syncthreads();
@@ -172,13 +192,7 @@ __device__ int draw_ids(int V, float u, W w4, float *s_wave, int *s_pick) {
     const int p0 = (int)((long)run_w * nblk / DRAW_WAVES), p1 = (int)((long)(run_w + 1) * nblk / DRAW_WAVES);
     const int b0 = p0 + (int)((long)wave * (p1 - p0) / DRAW_WAVES);
     const int b1 = p0 + (int)((long)(wave + 1) * (p1 - p0) / DRAW_WAVES);
-    float acc = 0.f;
-    for (int blk = b0; blk < b1; ++blk) {
-      float v[4];
-      w4(blk * 256 + 4 * lane, v);
-      acc += (v[0] + v[1]) + (v[2] + v[3]);
-    }
-    acc = wave_sum(acc);
+    const float acc = wave_sum(b1 > b0 ? lane_sum(b0, b1, lane, ld, wg) : 0.f);
     if (lane == 0) s_wave[DRAW_WAVES + wave] = acc;
     __syncthreads();
     if (tid == 0) {
@@ -198,7 +212,7 @@ __device__ int draw_ids(int V, float u, W w4, float *s_wave, int *s_pick) {
       int found = -1, last = -1;
       for (int blk = b0; blk < b1 && found < 0; ++blk) {
         float v[4];
-        w4(blk * 256 + 4 * lane, v);
+        wg(ld(blk * 256 + 4 * lane), blk * 256 + 4 * lane, v);
         const float ls = (v[0] + v[1]) + (v[2] + v[3]);
         float x = ls;   // inclusive prefix over the lanes, fixed order
 #pragma unroll
@@ -300,38 +314,40 @@ __global__ __launch_bounds__(DRAW_THREADS) void k_verify_chain(VerifyChainArgs a
     const float it = a.inv_t, u = a.u[(size_t)b * (K + 1) + K];
     const RowSum t = s_t[n];
     const float *trow = a.tl + ((size_t)b * (K + 1) + n) * V;
-    auto wt = [&](int i0, float (&v)[4]) {   // p_target up to its normaliser
-      if (i0 + 3 < V) {
-        const f32x4 x = *(const f32x4 *)(trow + i0);
-        v[0] = expf(x.x * it - t.M); v[1] = expf(x.y * it - t.M);
-        v[2] = expf(x.z * it - t.M); v[3] = expf(x.w * it - t.M);
-      } else {
-        for (int q = 0; q < 4; ++q) v[q] = i0 + q < V ? expf(trow[i0 + q] * it - t.M) : 0.f;
-      }
+    // V is a multiple of 16, so ids i0..i0+3 are all inside or all past the
+    // row; the loads are unconditional (clamped to id 0, masked), so that a
+    // batch of blocks keeps its loads in flight together
+    auto lt = [&](int i0) {   // the target row's values (clamped past the row)
+      DrawRaw r;
+      r.x = *(const f32x4 *)(trow + (i0 < V ? i0 : 0));
+      r.y = r.x;
+      return r;
+    };
+    auto wt = [&](const DrawRaw &r, int i0, float (&v)[4]) {   // p_target up to its normaliser
+      const bool in = i0 < V;
+      v[0] = in ? expf(r.x.x * it - t.M) : 0.f; v[1] = in ? expf(r.x.y * it - t.M) : 0.f;
+      v[2] = in ? expf(r.x.z * it - t.M) : 0.f; v[3] = in ? expf(r.x.w * it - t.M) : 0.f;
     };
     if (s_mode == 1) {   // max(0, p_target - p_draft) at the rejected position
       const RowSum d = s_d[n];
       const float *drow = a.dl + ((size_t)b * K + n) * V;
       const float ist = 1.f / t.S, isd = 1.f / d.S;
-      auto wr = [&](int i0, float (&v)[4]) {
-        float p[4], q4[4];
-        if (i0 + 3 < V) {
-          const f32x4 x = *(const f32x4 *)(trow + i0), y = *(const f32x4 *)(drow + i0);
-          p[0] = x.x; p[1] = x.y; p[2] = x.z; p[3] = x.w;
-          q4[0] = y.x; q4[1] = y.y; q4[2] = y.z; q4[3] = y.w;
-        } else {
-          for (int q = 0; q < 4; ++q) {
-            p[q] = i0 + q < V ? trow[i0 + q] : -INFINITY;
-            q4[q] = i0 + q < V ? drow[i0 + q] : -INFINITY;
-          }
-        }
-        for (int q = 0; q < 4; ++q)
-          v[q] = fmaxf(0.f, expf(p[q] * it - t.M) * ist - expf(q4[q] * it - d.M) * isd);
+      auto lr = [&](int i0) {   // both rows' values (clamped past the row)
+        DrawRaw r;
+        r.x = *(const f32x4 *)(trow + (i0 < V ? i0 : 0));
+        r.y = *(const f32x4 *)(drow + (i0 < V ? i0 : 0));
+        return r;
       };
-      next = draw_ids(V, u, wr, s_wave, s_pick);
-      if (next < 0) next = draw_ids(V, u, wt, s_wave, s_pick);   // identical distributions
+      auto wr = [&](const DrawRaw &r, int i0, float (&v)[4]) {
+        const bool in = i0 < V;
+        const float p[4] = {r.x.x, r.x.y, r.x.z, r.x.w}, q4[4] = {r.y.x, r.y.y, r.y.z, r.y.w};
+        for (int q = 0; q < 4; ++q)
+          v[q] = in ? fmaxf(0.f, expf(p[q] * it - t.M) * ist - expf(q4[q] * it - d.M) * isd) : 0.f;
+      };
+      next = draw_ids(V, u, lr, wr, s_wave, s_pick);
+      if (next < 0) next = draw_ids(V, u, lt, wt, s_wave, s_pick);   // identical distributions
     } else {
-      next = draw_ids(V, u, wt, s_wave, s_pick);
+      next = draw_ids(V, u, lt, wt, s_wave, s_pick);
     }
   }
   if (tid == 0) {
