@@ -263,6 +263,43 @@ def test_score_tree_and_verify_small_mha():
     assert len(lens) == 5
 
 
+def test_score_tree_graph_replay_reads_new_tokens():
+    """A second scoring call on the same buffers replays the captured graph;
+    with new token ids written into the tree buffers in place, its logits
+    follow the new tokens (the oracle scores the changed tree), and the
+    call count of captured graphs does not grow."""
+    from oracle import Oracle
+    from paper_2602_01762_amd import Drafter
+    cfg = SMALL_BF16_TREE.with_(name="small_bf16_tree_b4_replay", batch=4)
+    dr, w, inp = gpu_setup(cfg)
+    tr = dr.tree(inp, debug=False)
+    tcfg = scoring_target(cfg)
+    wt = make_weights(tcfg.with_(seed=7), "cuda")
+    it = make_inputs(tcfg, "cuda")
+    it.features.zero_()
+    tdr = Drafter(tcfg, max_batch=64)
+    tdr.load(wt)
+    lg = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"])
+    torch.cuda.synchronize()
+    from paper_2602_01762_amd import binding as B
+    n_graphs = B.prism_graph_cache(tdr.ctx)[0]
+    tr["tokens"].copy_((tr["tokens"] * 7 + 3) % cfg.vocab)     # a valid tree with other tokens
+    lg2 = tdr.score_tree(it, tr["tokens"], tr["depth"], tr["mask"], out=lg)
+    torch.cuda.synchronize()
+    assert tdr.device_status() == 0
+    assert B.prism_graph_cache(tdr.ctx)[0] == n_graphs
+    seqs = list(range(cfg.batch))
+    ref = Oracle(tcfg, host_weights(wt)).score_tree(
+        host_inputs(it, tcfg, seqs), tr["tokens"].cpu().numpy(), tr["depth"].cpu().numpy(),
+        tr["mask"].cpu().numpy(), seqs)
+    g = lg2.cpu().numpy().astype(np.float64)
+    for b in seqs:
+        e = float(np.max(np.abs(g[b] - ref["logits"][b])))
+        assert e <= LOGIT_TOL[cfg.dtype], "seq %d: logits max-abs %.3g" % (b, e)
+    tdr.close()
+    dr.close()
+
+
 def test_score_tree_rows_are_checked():
     """A mask that names a later node or lacks the node's own bit, and a
     depth out of range, are clamped to well-formed rows and reported."""
