@@ -360,3 +360,36 @@ def test_partial_buffer_holds_every_plan(driver):
         for (nt, R), o in zip(cases, out):
             split = int(o.split()[2])
             assert split * R * 16 * nt <= size, (cfg.name, nt, R, split, size)
+
+
+def test_plans_on_random_shapes(driver):
+    """Seeded random product shapes (tile counts, k-block counts, rows up to
+    256, both dtypes, with and without a feature-column range): every plan
+    fits its kernel, row-group plans appear exactly above 64 rows (bf16),
+    every slice count leaves each slice at least one k-block, and the
+    partial buffer sized for the shape holds split x rows x N."""
+    import numpy as np
+    rng = np.random.default_rng(1234)
+    lines, cases = [], []
+    for _ in range(300):
+        bf = int(rng.integers(0, 2))
+        kq = 32 if bf else 16
+        nt = int(rng.integers(1, 2049))
+        nkb_full = int(rng.integers(1, 900))
+        lo = int(rng.integers(0, nkb_full)) if rng.random() < 0.3 else 0
+        nkb = nkb_full - lo
+        R = int(rng.integers(3, 257 if bf else 65))
+        qkv = int(rng.random() < 0.2)
+        lines.append("plan %d %d %d %d %d %d %d 163840" % (nt, nkb, nkb * kq, nkb_full * kq, R, qkv, bf))
+        lines.append("pfl %d %d %d %d" % (nt, nkb_full, nkb_full * kq, 256 if bf else 64))
+        cases.append((bf, nt, nkb, R))
+    out = [o for o in driver("\n".join(lines) + "\n") if o]
+    assert len(out) == 2 * len(cases)
+    for i, (bf, nt, nkb, R) in enumerate(cases):
+        kw, tiles, split, gemv, fits, maxw, rowgrp = (int(x) for x in out[2 * i].split())
+        size = int(out[2 * i + 1])
+        assert fits == 1, (bf, nt, nkb, R, out[2 * i])
+        assert rowgrp == (1 if bf and R > 64 else 0), (bf, nt, nkb, R, out[2 * i])
+        if split > 0:
+            assert split <= nkb, (bf, nt, nkb, R, split)
+            assert split * R * 16 * nt <= size, (bf, nt, nkb, R, split, size)
