@@ -376,6 +376,10 @@ def sub_result(cfg, m):
 
 
 def tree_cycle_bench(args):
+    print(json.dumps(tree_cycle_measure(args)), flush=True)
+
+
+def tree_cycle_measure(args):
     """One tree speculation cycle on the 8B shapes: the drafter's tree call
     (batch 4, D 6, w 8, v 60), the target model's pass over the root and the
     60 nodes of each tree under the tree mask (one transformer layer of the
@@ -445,7 +449,9 @@ def tree_cycle_bench(args):
            "score_mfma_frac_executed": round(4 * rows * score_params / (t["score"] * 1e-6) / 1e12
                                              / BF16_PEAK_TFLOPS, 4),
            "score_bytes_per_call": score_bytes}
-    print(json.dumps(res), flush=True)
+    dr.close()
+    tdr.close()
+    return res
 
 
 def main():
@@ -528,6 +534,15 @@ def main():
         inp70 = make_inputs(L3_70B_BS32, "cuda")
         res["llama3_70b_bs32"] = sub_result(L3_70B_BS32, measure(L3_70B_BS32, w70, inp70, args,
                                                                  gemm=True))
+        del w70, inp70
+        torch.cuda.empty_cache()
+        # the tree speculation cycle (draft tree, target scoring, verification)
+        t = tree_cycle_measure(args)
+        res["tree_cycle"] = {"workload": t["config"]["workload"], "us_per_cycle": t["value"],
+                             "part_us": t["part_us"],
+                             "score_mfma_frac_executed": t["score_mfma_frac_executed"],
+                             "target_rows": t["config"]["target_rows"],
+                             "target_passes": t["config"]["target_passes"]}
     print(json.dumps(res), flush=True)
 
 
