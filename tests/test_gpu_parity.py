@@ -329,6 +329,13 @@ def test_tree_parity_head_geometries(cfg):
     run_tree_parity(cfg)
 
 
+# The most rows a tree level takes in one pass: batch 8 x width 8 = 64 rows
+# (four 16-row tiles in every batched product and in the LM head).
+def test_tree_parity_max_rows():
+    run_tree_parity(SMALL_BF16_TREE.with_(name="small_bf16_tree_b8_w8", batch=8, tree_width=8,
+                                          n_steps=3, tree_nodes=20, ctx_range=(40, 200)))
+
+
 def test_tree_width_one_equals_chain():
     tcfg = SMALL_BF16_TREE.with_(tree_width=1, tree_nodes=SMALL_BF16_TREE.n_steps)
     dr, w, inp = gpu_setup(tcfg)
